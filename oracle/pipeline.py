@@ -1,0 +1,38 @@
+"""Oracle for the whole pruning stage -- test infrastructure.
+
+Score (Eq. (3)), select (top-K0, basis, Eq. (4)), restore the original order
+and gather the kept rows with their positional indices (section
+"Inference-Time Token Pruning").
+"""
+from dataclasses import dataclass
+
+import numpy as np
+
+from .predictor import predicted_attention
+from .select import greedy_select
+
+
+@dataclass
+class PruneResult:
+    p_hat: np.ndarray      # [B, N] float64
+    idx: np.ndarray        # [B, K] ascending original indices
+    order: np.ndarray      # [B, K] selection order
+    V_out: np.ndarray      # [B, K, D] kept rows (same dtype as the V given)
+    pos_out: np.ndarray    # [B, K] positional indices of the kept rows
+
+
+def prune(V, T, t_off, pos_v, pos_t, w: dict, K: int, K0: int, tau: float = 1e-2,
+          theta: float = 10000.0) -> PruneResult:
+    V = np.asarray(V)
+    B, N, D = V.shape
+    p = np.empty((B, N))
+    idx = np.empty((B, K), np.int64)
+    order = np.empty((B, K), np.int64)
+    for b in range(B):
+        lo, hi = int(t_off[b]), int(t_off[b + 1])
+        p[b] = predicted_attention(V[b], T[lo:hi], pos_v[b], pos_t[lo:hi], w, theta)
+        r = greedy_select(p[b], V[b], K, K0, tau)
+        idx[b], order[b] = r.idx, r.order
+    V_out = np.take_along_axis(V, idx[:, :, None], axis=1)
+    pos_out = np.take_along_axis(np.asarray(pos_v), idx, axis=1)
+    return PruneResult(p, idx, order, V_out, pos_out)
