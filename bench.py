@@ -1,0 +1,163 @@
+"""Benchmark of the fused MAP pruning stage (map_prune) on one MI355X.
+
+Workload: the LLaVA-NeXT-7B shape -- one image of 2880 visual tokens x 4096
+(bf16), a 64-token question, keep 160 (K0 = 80) -- from the seeded synthetic
+generator (random-init predictor weights).  A step is one map_prune call:
+predictor scoring, cosine similarity, selection and gather, inputs resident
+in HBM.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "pruned images/sec + µs/image at N=2880,d=4096,K=160; % MFMA/HBM roofline"
+PEAK_MFMA_BF16 = 2500.0   # TFLOP/s, dense
+PEAK_MFMA_F32 = 157.3     # TFLOP/s
+PEAK_HBM = 8000.0         # GB/s
+
+
+def algorithmic_work(cfg, sumM):
+    """Per-launch algorithmic work of each kernel: (bound, amount, unit)."""
+    B, N, K = cfg.B, cfg.N, cfg.K
+    D, H, dp = cfg.pred.D, cfg.pred.D_h, cfg.pred.d_p
+    el = 2 if cfg.dtype == "bf16" else 4
+    rows = B * N + sumM
+    return {
+        # layer 1 of f_V and f_T, and the unique half (with the diagonal) of each Gram matrix
+        "gemm_layer1_gram": ("mfma", 2.0 * rows * D * H + B * N * (N + 1) * D, "flop"),
+        "gemm_layer2": ("mfma", 2.0 * rows * H * H, "flop"),
+        "gemm_proj_rope": ("mfma", 2.0 * rows * H * dp, "flop"),
+        # read V, write norms, 1/norms and the cos/sin table
+        "prep": ("hbm", B * N * D * el + 8.0 * B * N + 8.0 * rows * dp / 2, "byte"),
+        # read the kept rows and write them out
+        "gather": ("hbm", 2.0 * B * K * D * el + 8.0 * B * K, "byte"),
+    }
+
+
+def cpu_baseline(x, cfg):
+    """The oracle as it stands, timed on this host on one image."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    names = ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")
+    w = {n: x[n + "_f32"] for n in names}
+    lo, hi = int(x["t_off"][0]), int(x["t_off"][1])
+    t0 = time.perf_counter()
+    r = oracle.prune(x["V_f32"][:1], x["T_f32"][lo:hi], np.array([0, hi - lo]), x["pos_v"][:1],
+                     x["pos_t"][lo:hi], w, cfg.K, cfg.K0, cfg.tau, cfg.pred.rope_theta)
+    dt = time.perf_counter() - t0
+    threads = sum(i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas")
+    return {"value": 1.0 / dt, "unit": "images/s", "cores": int(threads or 1), "kind": "oracle",
+            "sample": f"1 image of the workload (N={cfg.N}, D={cfg.pred.D}, M={hi - lo}, K={cfg.K}, "
+                      f"K0={cfg.K0}): float64 predictor, literal Eq. (4) greedy, gather; "
+                      f"{dt:.2f} s on {os.cpu_count()} visible CPUs"}, r
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llava_next")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the pruning stage is per image with no exchange, "
+              "and this build runs on a single MI355X (use --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_06411_amd as mp
+    from workloads import get_config, make_inputs
+
+    cfg = get_config(args.workload)
+    x = make_inputs(cfg)
+    dev = torch.device("cuda:0")
+
+    def to_dev(a):
+        if cfg.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    names = ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")
+    w = mp.PredictorWeights(**{n: to_dev(x[n + "_store"]) for n in names}, rope_theta=cfg.pred.rope_theta)
+    V, T = to_dev(x["V_store"]), to_dev(x["T_store"])
+    pos_v, pos_t = torch.from_numpy(x["pos_v"]).to(dev), torch.from_numpy(x["pos_t"]).to(dev)
+    t_off = x["t_off"]
+    ws = mp.PruneWorkspace(w, V, t_off, cfg.K)
+    out = mp.map_prune(w, V, pos_v, T, pos_t, t_off, cfg.K, cfg.K0, cfg.tau, workspace=ws)
+
+    def step():
+        mp.map_prune(w, V, pos_v, T, pos_t, t_off, cfg.K, cfg.K0, cfg.tau, out=out, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = e0.elapsed_time(e1) / args.steps
+
+    # Per-kernel durations, measured with HIP events on the launch stream
+    # (the library brackets each of its launches while timing is enabled).
+    mp.timing_reset()
+    mp.timing_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    per_kernel = mp.timing_read()
+    mp.timing_enable(False)
+    mp.timing_reset()
+
+    sumM = int(t_off[-1])
+    work = algorithmic_work(cfg, sumM)
+    kern = {k: {"avg_us": 1e3 * v[0] / v[1], "launches_per_step": v[1] / args.steps}
+            for k, v in per_kernel.items()}
+    dominant = max(kern, key=lambda k: kern[k]["avg_us"] * kern[k]["launches_per_step"])
+    roof_kernel = dominant if dominant in work else max(
+        (k for k in kern if k in work), key=lambda k: kern[k]["avg_us"])
+    bound, amount, unit = work[roof_kernel]
+    avg_s = kern[roof_kernel]["avg_us"] * 1e-6
+    if bound == "mfma":
+        achieved = amount / avg_s / 1e12
+        peak = PEAK_MFMA_BF16 if cfg.dtype == "bf16" else PEAK_MFMA_F32
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s"}
+    else:
+        achieved = amount / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM, "unit": "GB/s"}
+    roof.update({"frac": roof["achieved"] / roof["peak"], "traffic": None, "kernel": roof_kernel,
+                 "avg_us": kern[roof_kernel]["avg_us"], "algorithmic_per_launch": amount,
+                 "algorithmic_unit": unit})
+
+    line = {
+        "metric": METRIC, "value": cfg.B * 1000.0 / ms, "unit": "images/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "us_per_image": 1000.0 * ms / cfg.B, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic (seeded mixture, random-init predictor)",
+        "config": {"workload": f"{cfg.name}: B={cfg.B} N={cfg.N} D={cfg.pred.D} M={sumM} K={cfg.K} "
+                               f"K0={cfg.K0} tau={cfg.tau} D_h={cfg.pred.D_h} d_p={cfg.pred.d_p} {cfg.dtype}",
+                   "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "single GPU"},
+        "wall_s_timed": wall, "kernels": kern, "dominant_kernel": dominant, "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"], _ = cpu_baseline(x, cfg)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

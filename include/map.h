@@ -1,0 +1,179 @@
+/*
+ * map.h -- C ABI of the MAP visual-token pruning stage on MI355X (gfx950).
+ *
+ * The stage runs in front of the first language-model layer of a multimodal
+ * LLM and keeps K of the N visual tokens of each image ("Learning to Predict
+ * Middle-Layer Attention in MLLMs for Visual Token Pruning", section
+ * "Inference-Time Token Pruning"):
+ *
+ *   map_score       visual + question tokens -> predicted attention p_hat
+ *                   (Eq. (3), section "Cross-Modal Attention Distillation")
+ *   map_similarity  visual tokens -> row norms and cosine similarity, the
+ *                   pairwise quantities the diversity term of Eq. (4) needs
+ *   map_select      p_hat + similarity + K -> retained token indices
+ *                   (top-K0 initial set, orthonormal basis, greedy Eq. (4),
+ *                   original order restored)
+ *   map_prune       all of the above fused, plus the gather of the kept rows
+ *                   and of their positional indices
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers.  Every tensor argument is a DEVICE pointer into memory the caller
+ *   owns (allocated with hipMalloc or by a framework); the library never
+ *   allocates, frees or retains it.  Host pointers are named *_host.
+ * Layout.  Row-major and contiguous.  Batched tensors put the image index
+ *   first.  Weight matrices use the W[out][in] layout.
+ * Types.  map_dtype selects the storage type of V, T, the weights and V_out:
+ *   MAP_F32 (float) or MAP_BF16 (bfloat16 bits).  Scores, norms, similarity
+ *   and gains are always float32; indices and positions int32.
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  All work
+ *   is enqueued on it; a call returns without waiting, and outputs are valid
+ *   once the stream has been synchronised.  Calls on one stream are ordered.
+ * Workspace.  Scratch memory comes from the caller: `ws` must be a device
+ *   buffer of at least map_*_workspace() bytes, 256-byte aligned, not used by
+ *   anything else until the stream has passed the call.  Calls that run at
+ *   the same time need separate workspaces.
+ * Errors.  Arguments are checked on the host before anything is enqueued;
+ *   on failure the call returns a non-zero map_status and enqueues nothing.
+ *   MAP_ERR_HIP means the HIP runtime rejected a launch (the stream may then
+ *   hold part of the work).  No exception crosses this interface.
+ * Determinism.  Identical inputs give bitwise identical outputs.
+ * Limits.  1 <= B <= MAP_MAX_BATCH, 1 <= N <= MAP_MAX_N,
+ *   1 <= K <= min(N, MAP_MAX_K), 0 <= K0 <= K, D % 8 == 0, D_h % 8 == 0,
+ *   d_p a multiple of 4 and <= 128, 1 <= question length <= 8192.
+ */
+#ifndef MAP_H
+#define MAP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MAP_MAX_BATCH 64
+#define MAP_MAX_N 16384
+#define MAP_MAX_K 1024
+
+typedef enum {
+  MAP_OK = 0,
+  MAP_ERR_INVALID_ARG = 1,  /* a size, pointer or parameter is out of range */
+  MAP_ERR_UNSUPPORTED = 2,  /* valid request the library does not implement */
+  MAP_ERR_WORKSPACE = 3,    /* ws is NULL, misaligned or smaller than needed */
+  MAP_ERR_HIP = 4           /* the HIP runtime reported an error            */
+} map_status;
+
+typedef enum { MAP_F32 = 0, MAP_BF16 = 1 } map_dtype;
+
+/* Predictor parameters (section "Cross-Modal Attention Distillation").
+ * f_V, f_T: Linear(D -> D_h) + bias, GELU (erf form), Linear(D_h -> D_h) +
+ * bias.  W_K, W_Q: Linear(D_h -> d_p), no bias.  RoPE with rotate-half
+ * pairing (i, i + d_p/2) and frequencies rope_theta^(-2i/d_p) is applied to
+ * the projected keys and queries.  All pointers are device pointers of the
+ * call's dtype:  w1_* [D_h][D], b1_* [D_h], w2_* [D_h][D_h], b2_* [D_h],
+ * w_k and w_q [d_p][D_h]. */
+typedef struct {
+  const void *w1_v, *b1_v, *w2_v, *b2_v, *w_k;
+  const void *w1_t, *b1_t, *w2_t, *b2_t, *w_q;
+  int32_t D, D_h, d_p;
+  float rope_theta;
+} map_weights;
+
+/* Selection parameters (section "Inference-Time Token Pruning").
+ * K: tokens kept per image.  K0: size of the top-K0 initial retained set
+ * (K0 == K gives plain top-K by p_hat; K0 == 0 starts the greedy rule from
+ * an empty basis).  tau: rank-deficiency threshold; a token whose residual
+ * against the current basis is at most tau times its own norm adds no basis
+ * vector and scores 0 in Eq. (4).  Ties go to the higher p_hat, then to the
+ * lower index; when every remaining candidate scores 0 the candidate with the
+ * highest p_hat is taken. */
+typedef struct {
+  int32_t K;
+  int32_t K0;
+  float tau;
+} map_select_params;
+
+/* Human-readable text of a status code (static storage). */
+const char* map_status_string(int status);
+
+/* Library interface version (major * 10000 + minor * 100 + patch). */
+int map_version(void);
+
+/* Workspace bytes of each call for the given sizes (0 if the sizes are
+ * invalid).  sum_M is the total number of question tokens in the batch. */
+size_t map_score_workspace(map_dtype dt, int B, int N, int sum_M, const map_weights* w);
+size_t map_similarity_workspace(map_dtype dt, int B, int N, int D);
+size_t map_select_workspace(int B, int N, int K);
+size_t map_prune_workspace(map_dtype dt, int B, int N, int sum_M, const map_weights* w, int K);
+
+/* map_score -- predicted attention, Eq. (3):
+ *   p_hat[b][n] = (1/M_b) sum_m softmax_n( <q_m, k_n> / sqrt(d_p) ),
+ *   k_n = RoPE(W_K f_V(v_n), pos_v[b][n]),  q_m = RoPE(W_Q f_T(t_m), pos_t[m]).
+ * V      [B][N][D]   visual tokens (projector output), dtype dt
+ * pos_v  [B][N]      positional index of each visual token
+ * T      [sum_M][D]  question tokens of all images, back to back, dtype dt
+ * pos_t  [sum_M]     positional index of each question token
+ * t_off_host [B+1]   HOST array; image b owns T rows [t_off[b], t_off[b+1]);
+ *                    t_off[0] == 0, strictly increasing, t_off[B] == sum_M
+ * p_out  [B][N]      float32 output; each row sums to 1.
+ * Hidden activations are stored in dt (bf16 in bf16 calls), accumulation is
+ * float32, keys and queries are float32. */
+map_status map_score(const map_weights* w, map_dtype dt, int B, int N,
+                     const void* V, const int32_t* pos_v,
+                     const void* T, const int32_t* pos_t, const int32_t* t_off_host,
+                     float* p_out, void* ws, size_t ws_bytes, void* stream);
+
+/* map_similarity -- row norms and cosine similarity of the visual tokens:
+ *   norms[b][i] = ||v_i||,  S[b][i][j] = <v_i, v_j> / (norms_i norms_j)
+ * (a zero row has norm 0 and a zero row and column in S).  The residual of
+ * Eq. (4) is evaluated from S and the norms.
+ * V [B][N][D] dtype dt;  S_out [B][N][N] float32;  norms_out [B][N] float32. */
+map_status map_similarity(map_dtype dt, int B, int N, int D, const void* V,
+                          float* S_out, float* norms_out,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/* map_select -- diversity-aware selection, Eq. (4), for each image:
+ * R0 = the K0 tokens with the highest p; the basis is built from R0 in
+ * descending p order; then, until K tokens are kept, the candidate with the
+ * largest p_i * ||v_i - B B^T v_i|| is added and its normalised residual
+ * appended to the basis.  The residual is evaluated as
+ * norms_i * sqrt(1 - sum_t c_ti^2) from the cosine similarity S.
+ * p      [B][N]     float32 importance, finite and >= 0
+ * S      [B][N][N]  float32 cosine similarity (as map_similarity writes it)
+ * norms  [B][N]     float32 row norms
+ * idx_out   [B][K]  int32 kept token indices, ascending (original order)
+ * order_out [B][K]  int32 selection order (R0 first) or NULL
+ * gain_out  [B][K]  float32: p of the R0 picks, then the Eq. (4) score of
+ *                   each greedy pick (non-increasing); or NULL */
+map_status map_select(int B, int N, const float* p, const float* S, const float* norms,
+                      map_select_params sp, int32_t* idx_out, int32_t* order_out,
+                      float* gain_out, void* ws, size_t ws_bytes, void* stream);
+
+/* map_prune -- map_score, map_similarity and map_select fused, then the
+ * gather of the kept tokens in their original order:
+ *   V_out[b][k][:] = V[b][idx[b][k]][:] (byte-exact copy, dtype dt)
+ *   pos_out[b][k]  = pos_v[b][idx[b][k]]
+ * Arguments as in the calls above; p_out, order_out and gain_out may be NULL. */
+map_status map_prune(const map_weights* w, map_dtype dt, int B, int N,
+                     const void* V, const int32_t* pos_v,
+                     const void* T, const int32_t* pos_t, const int32_t* t_off_host,
+                     map_select_params sp, int32_t* idx_out, void* V_out, int32_t* pos_out,
+                     float* p_out, int32_t* order_out, float* gain_out,
+                     void* ws, size_t ws_bytes, void* stream);
+
+/* Per-kernel timing for measurement.  While enabled, every kernel the
+ * library launches is bracketed by a pair of HIP events recorded on the
+ * launch stream.  map_timing_read() waits for those events, accumulates the
+ * elapsed time per kernel name and fills up to `cap` entries (names point to
+ * static strings); it returns the number of kernel names seen.
+ * map_timing_reset() drops everything recorded so far. */
+map_status map_timing_enable(int enable);
+int map_timing_read(const char** names, double* total_ms, int* launches, int cap);
+void map_timing_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MAP_H */

@@ -1,0 +1,17 @@
+"""MAP (Middle-layer Attention Prediction) visual-token pruning on MI355X.
+
+The pruning stage of "Learning to Predict Middle-Layer Attention in MLLMs for
+Visual Token Pruning" -- predictor scoring (Eq. (3)), cosine similarity of
+the visual tokens, diversity-aware selection (Eq. (4)) and the gather of the
+kept tokens -- as hand-written HIP kernels for gfx950 behind a C ABI
+(include/map.h).  This package is the Python binding of that library.
+"""
+from .binding import (EXPORTS, MAP_BF16, MAP_F32, MapError, PredictorWeights, PruneWorkspace,
+                      lib, map_prune, map_score, map_select, map_similarity, timing_enable,
+                      timing_read, timing_reset)
+
+__all__ = [
+    "EXPORTS", "MAP_BF16", "MAP_F32", "MapError", "PredictorWeights", "PruneWorkspace", "lib",
+    "map_prune", "map_score", "map_select", "map_similarity", "timing_enable", "timing_read",
+    "timing_reset",
+]

@@ -1,0 +1,278 @@
+"""ctypes binding of libmap (include/map.h): argument marshalling only.
+
+Every function takes and returns torch tensors that live on a ROCm device;
+all arithmetic happens in the library's HIP kernels, enqueued on the current
+torch stream.  There is no CPU fallback: if libmap.so is missing or a call
+fails, an exception is raised.
+"""
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmap.so")
+
+MAP_OK, MAP_ERR_INVALID_ARG, MAP_ERR_UNSUPPORTED, MAP_ERR_WORKSPACE, MAP_ERR_HIP = range(5)
+MAP_F32, MAP_BF16 = 0, 1
+MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
+
+# Every symbol include/map.h declares.
+EXPORTS = (
+    "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
+    "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
+    "map_prune", "map_timing_enable", "map_timing_read", "map_timing_reset",
+)
+
+
+class map_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")] + \
+               [("D", ctypes.c_int32), ("D_h", ctypes.c_int32), ("d_p", ctypes.c_int32),
+                ("rope_theta", ctypes.c_float)]
+
+
+class map_select_params(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int32), ("K0", ctypes.c_int32), ("tau", ctypes.c_float)]
+
+
+_P, _I, _SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+_SIGS = {
+    "map_status_string": (ctypes.c_char_p, [_I]),
+    "map_version": (_I, []),
+    "map_score_workspace": (_SZ, [_I, _I, _I, _I, ctypes.POINTER(map_weights)]),
+    "map_similarity_workspace": (_SZ, [_I, _I, _I, _I]),
+    "map_select_workspace": (_SZ, [_I, _I, _I]),
+    "map_prune_workspace": (_SZ, [_I, _I, _I, _I, ctypes.POINTER(map_weights), _I]),
+    "map_score": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "map_similarity": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),
+    "map_select": (_I, [_I, _I, _P, _P, _P, map_select_params, _P, _P, _P, _P, _SZ, _P]),
+    "map_prune": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
+                       map_select_params, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "map_timing_enable": (_I, [_I]),
+    "map_timing_read": (_I, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
+                             ctypes.POINTER(ctypes.c_int), _I]),
+    "map_timing_reset": (None, []),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libmap (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_06411_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(handle, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = handle
+    return _lib
+
+
+class MapError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        msg = lib().map_status_string(status).decode()
+        super().__init__(f"{where}: {msg} (status {status})")
+        self.status = status
+
+
+def _check(status: int, where: str):
+    if status != MAP_OK:
+        raise MapError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return MAP_BF16
+    if t.dtype == torch.float32:
+        return MAP_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; use torch.float32 or torch.bfloat16")
+
+
+def _need(t: torch.Tensor, name: str, shape, dtype, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device != device or t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)} on {device}, got "
+                         f"{t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return None
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + nbytes]
+
+
+@dataclass
+class PredictorWeights:
+    """Predictor parameters on the device (torch.nn.Linear layout)."""
+    w1_v: torch.Tensor
+    b1_v: torch.Tensor
+    w2_v: torch.Tensor
+    b2_v: torch.Tensor
+    w_k: torch.Tensor
+    w1_t: torch.Tensor
+    b1_t: torch.Tensor
+    w2_t: torch.Tensor
+    b2_t: torch.Tensor
+    w_q: torch.Tensor
+    rope_theta: float = 10000.0
+
+    @property
+    def D(self):
+        return self.w1_v.shape[1]
+
+    @property
+    def D_h(self):
+        return self.w1_v.shape[0]
+
+    @property
+    def d_p(self):
+        return self.w_k.shape[0]
+
+    @property
+    def dtype(self):
+        return self.w1_v.dtype
+
+    def struct(self) -> map_weights:
+        s = map_weights()
+        for n in ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q"):
+            t = getattr(self, n)
+            if not t.is_contiguous() or t.dtype != self.dtype:
+                raise ValueError(f"weight {n} must be contiguous {self.dtype}")
+            setattr(s, n, t.data_ptr())
+        s.D, s.D_h, s.d_p, s.rope_theta = self.D, self.D_h, self.d_p, float(self.rope_theta)
+        return s
+
+
+def _offsets(t_off) -> (ctypes.Array, int):
+    vals = [int(x) for x in (t_off.tolist() if hasattr(t_off, "tolist") else t_off)]
+    arr = (ctypes.c_int32 * len(vals))(*vals)
+    return arr, vals[-1]
+
+
+def map_score(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torch.Tensor,
+              pos_t: torch.Tensor, t_off: Sequence[int], p_out: Optional[torch.Tensor] = None):
+    """Predicted attention p_hat [B, N] (Eq. (3))."""
+    B, N, D = V.shape
+    dev = V.device
+    offs, sumM = _offsets(t_off)
+    if len(offs) != B + 1:
+        raise ValueError("t_off needs B + 1 entries")
+    if p_out is None:
+        p_out = torch.empty(B, N, dtype=torch.float32, device=dev)
+    ws_struct = w.struct()
+    dt = _dtype_code(V)
+    nbytes = lib().map_score_workspace(dt, B, N, sumM, ctypes.byref(ws_struct))
+    if nbytes == 0:
+        raise MapError(MAP_ERR_INVALID_ARG, "map_score_workspace")
+    ws = _workspace(nbytes, dev)
+    _check(lib().map_score(ctypes.byref(ws_struct), dt, B, N, _ptr(V), _ptr(pos_v), _ptr(T),
+                           _ptr(pos_t), offs, _ptr(p_out), _ptr(ws), nbytes, _stream(dev)),
+           "map_score")
+    return p_out
+
+
+def map_similarity(V: torch.Tensor, S_out: Optional[torch.Tensor] = None,
+                   norms_out: Optional[torch.Tensor] = None):
+    """Cosine similarity S [B, N, N] and row norms [B, N] of the visual tokens."""
+    B, N, D = V.shape
+    dev = V.device
+    if S_out is None:
+        S_out = torch.empty(B, N, N, dtype=torch.float32, device=dev)
+    if norms_out is None:
+        norms_out = torch.empty(B, N, dtype=torch.float32, device=dev)
+    dt = _dtype_code(V)
+    nbytes = lib().map_similarity_workspace(dt, B, N, D)
+    ws = _workspace(nbytes, dev)
+    _check(lib().map_similarity(dt, B, N, D, _ptr(V), _ptr(S_out), _ptr(norms_out), _ptr(ws),
+                                nbytes, _stream(dev)), "map_similarity")
+    return S_out, norms_out
+
+
+def map_select(p: torch.Tensor, S: torch.Tensor, norms: torch.Tensor, K: int, K0: int,
+               tau: float = 1e-2, idx_out=None, order_out=None, gain_out=None):
+    """Diversity-aware selection (Eq. (4)): returns (idx ascending, order, gain), each [B, K]."""
+    B, N = p.shape
+    dev = p.device
+    idx_out = torch.empty(B, K, dtype=torch.int32, device=dev) if idx_out is None else idx_out
+    order_out = torch.empty(B, K, dtype=torch.int32, device=dev) if order_out is None else order_out
+    gain_out = torch.empty(B, K, dtype=torch.float32, device=dev) if gain_out is None else gain_out
+    nbytes = lib().map_select_workspace(B, N, K)
+    ws = _workspace(nbytes, dev)
+    sp = map_select_params(K, K0, tau)
+    _check(lib().map_select(B, N, _ptr(p), _ptr(S), _ptr(norms), sp, _ptr(idx_out), _ptr(order_out),
+                            _ptr(gain_out), _ptr(ws), nbytes, _stream(dev)), "map_select")
+    return idx_out, order_out, gain_out
+
+
+class PruneWorkspace:
+    """Reusable workspace for repeated map_prune calls of one shape."""
+
+    def __init__(self, w: PredictorWeights, V: torch.Tensor, t_off, K: int):
+        B, N, _ = V.shape
+        offs, sumM = _offsets(t_off)
+        self.nbytes = lib().map_prune_workspace(_dtype_code(V), B, N, sumM, ctypes.byref(w.struct()), K)
+        if self.nbytes == 0:
+            raise MapError(MAP_ERR_INVALID_ARG, "map_prune_workspace")
+        self.buf = _workspace(self.nbytes, V.device)
+
+
+def map_prune(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torch.Tensor,
+              pos_t: torch.Tensor, t_off: Sequence[int], K: int, K0: int, tau: float = 1e-2,
+              out: Optional[dict] = None, workspace: Optional[PruneWorkspace] = None):
+    """Fused score + similarity + selection + gather.  Returns a dict with
+    idx, V_out, pos_out, p, order and gain (the given `out` tensors are
+    filled in place)."""
+    B, N, D = V.shape
+    dev = V.device
+    offs, sumM = _offsets(t_off)
+    o = dict(out or {})
+    o.setdefault("idx", torch.empty(B, K, dtype=torch.int32, device=dev))
+    o.setdefault("V_out", torch.empty(B, K, D, dtype=V.dtype, device=dev))
+    o.setdefault("pos_out", torch.empty(B, K, dtype=torch.int32, device=dev))
+    o.setdefault("p", torch.empty(B, N, dtype=torch.float32, device=dev))
+    o.setdefault("order", torch.empty(B, K, dtype=torch.int32, device=dev))
+    o.setdefault("gain", torch.empty(B, K, dtype=torch.float32, device=dev))
+    if workspace is None:
+        workspace = PruneWorkspace(w, V, t_off, K)
+    ws_struct = w.struct()
+    sp = map_select_params(K, K0, tau)
+    _check(lib().map_prune(ctypes.byref(ws_struct), _dtype_code(V), B, N, _ptr(V), _ptr(pos_v),
+                           _ptr(T), _ptr(pos_t), offs, sp, _ptr(o["idx"]), _ptr(o["V_out"]),
+                           _ptr(o["pos_out"]), _ptr(o["p"]), _ptr(o["order"]), _ptr(o["gain"]),
+                           _ptr(workspace.buf), workspace.nbytes, _stream(dev)), "map_prune")
+    return o
+
+
+def timing_enable(on: bool = True):
+    _check(lib().map_timing_enable(1 if on else 0), "map_timing_enable")
+
+
+def timing_reset():
+    lib().map_timing_reset()
+
+
+def timing_read(cap: int = 32) -> dict:
+    """{kernel name: (total ms, launches)} for the launches recorded so far."""
+    names = (ctypes.c_char_p * cap)()
+    ms = (ctypes.c_double * cap)()
+    cnt = (ctypes.c_int * cap)()
+    n = lib().map_timing_read(names, ms, cnt, cap)
+    return {names[i].decode(): (ms[i], cnt[i]) for i in range(min(n, cap))}

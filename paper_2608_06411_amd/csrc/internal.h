@@ -1,0 +1,147 @@
+// Internal declarations shared by the host dispatch and the HIP kernels of
+// libmap.  Nothing here is part of the public ABI (include/map.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "map.h"
+
+namespace mapk {
+
+// ---------------------------------------------------------------- bf16
+// Storage type of a bfloat16 value: its 16 raw bits.
+typedef uint16_t bf16_t;
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// float -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16_t>(bf16_t v) { return bf16_to_f32(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
+
+// ---------------------------------------------------------------- timing
+// Kernel launch bracketing for map_timing_* (no-op unless enabled).
+struct TimedLaunch {
+  TimedLaunch(const char* name, hipStream_t s);
+  ~TimedLaunch();
+  const char* name_;
+  hipStream_t s_;
+  int slot_;
+};
+
+// ---------------------------------------------------------------- GEMM
+// C = epilogue(A * B^T): A [M][K] and B [N][K] row-major (K contiguous),
+// float32 accumulation on the matrix cores.  Several independent problems
+// share one launch; each may be batched.
+enum EpiMode : int {
+  EPI_BIAS_GELU = 0,  // C[m][n] = GELU(acc + bias[n]), stored as T
+  EPI_BIAS = 1,       // C[m][n] = acc + bias[n], stored as T
+  EPI_COSINE = 2,     // S[m][n] = acc * rs[m] * rs[n] (float32), mirrored; A == B
+  EPI_ROPE = 3,       // out[m][:] = RoPE(acc[m][:]) (float32) with the row's cos/sin
+};
+
+struct GemmProblem {
+  const void* A;
+  const void* B;
+  void* C;
+  long long strideA, strideB, strideC;  // per batch item, in elements
+  int M, N, K, lda, ldb, ldc;
+  int batch;
+  int epi;
+  const void* bias;        // EPI_BIAS*: [N], element type T
+  const float* rs;         // EPI_COSINE: [batch][M] reciprocal norms
+  const float2* rope_cs;   // EPI_ROPE: [M][N/2] (cos, sin) per row and pair
+  int triangular;          // EPI_COSINE: only tiles with tile_n >= tile_m
+  // filled by the host helper
+  int tiles_m, tiles_n, tiles_per_batch, tile_begin;
+};
+
+constexpr int kMaxGemmProblems = 4;
+struct GemmBatch {
+  GemmProblem p[kMaxGemmProblems];
+  int count;
+  int total_tiles;
+};
+
+void gemm_finalize(GemmBatch& g);  // computes the tile counts
+hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s);
+
+// ---------------------------------------------------------------- prep
+// Row norms of the visual tokens (and their reciprocals) plus the RoPE
+// cos/sin table of every visual and question token.
+struct PrepArgs {
+  const void* V;          // [rowsV][D]
+  int rowsV, D;
+  float* norms;           // [rowsV]
+  float* ninv;            // [rowsV]
+  const int32_t* pos_v;   // [rowsV] (may be null when the table is not needed)
+  const int32_t* pos_t;   // [rowsT]
+  int rowsT;
+  int half;               // d_p / 2
+  float2* cs_v;           // [rowsV][half]
+  float2* cs_t;           // [rowsT][half]
+  double inv_freq[64];    // theta^(-2i/d_p), computed on the host in float64
+};
+hipError_t launch_prep(map_dtype dt, const PrepArgs& a, bool norms, bool table, hipStream_t s);
+
+// ---------------------------------------------------------------- score
+struct ScoreArgs {
+  const float* q;         // [sum_M][d_p] (after RoPE)
+  const float* k;         // [B][N][d_p]  (after RoPE)
+  float* logits;          // [sum_M][N]
+  float2* partial;        // [sum_M][nblk] (running max, sum of exp) per key block
+  float* p_out;           // [B][N]
+  int B, N, d_p, nblk;
+  int t_off[MAP_MAX_BATCH + 1];
+};
+hipError_t launch_score(const ScoreArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- select
+struct SelectArgs {
+  const float* p;        // [B][N]
+  const float* S;        // [B][N][N]
+  const float* norms;    // [B][N]
+  int32_t* R0;           // [B][K0]   top-K0 in descending p order
+  float* C;              // [B][N][Kp] basis coefficients, Ct[i][t] = c_{t,i}
+  float* r2;             // [B][N]    squared unit residuals
+  uint64_t* pub;         // [B][2][G][kPub+1] published keys
+  unsigned int* bar;     // [B] barrier counters
+  int32_t* err;          // [1] set when a barrier wait gives up
+  int32_t* order;        // [B][K]
+  float* gain;           // [B][K]
+  int32_t* idx_out;      // [B][K] ascending
+  int B, N, K, K0, G, ch, pcap;
+  float tau2;
+};
+constexpr int kPub = 8;  // keys each workgroup publishes per round
+hipError_t launch_topk(const SelectArgs& a, hipStream_t s);
+hipError_t launch_select(SelectArgs& a, hipStream_t s);
+hipError_t launch_restore(const SelectArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- gather
+struct GatherArgs {
+  const void* V;           // [B][N][D]
+  const int32_t* pos_v;    // [B][N]
+  const int32_t* idx;      // [B][K] ascending
+  void* V_out;             // [B][K][D]
+  int32_t* pos_out;        // [B][K]
+  int B, N, K, row_bytes;
+};
+hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
+
+}  // namespace mapk

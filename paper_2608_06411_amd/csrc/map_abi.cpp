@@ -1,0 +1,520 @@
+// Host side of the C ABI in include/map.h: argument checks, workspace
+// layout, and the order in which the HIP kernels are enqueued.
+//
+//   map_score:      prep (RoPE table) -> GEMM layer 1 (f_V, f_T) -> GEMM layer 2
+//                   -> GEMM projections + RoPE -> logits -> softmax-mean
+//   map_similarity: prep (norms) -> GEMM (cosine Gram, upper tiles mirrored)
+//   map_select:     top-K0 -> cooperative selection -> restore order
+//   map_prune:      prep (norms + table) -> GEMM layer 1 together with the
+//                   Gram matrix (one launch, both stream V) -> layer 2 ->
+//                   projections -> logits -> softmax-mean -> top-K0 ->
+//                   selection -> restore order -> gather
+#include <math.h>
+#include <string.h>
+
+#include <mutex>
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+using namespace mapk;
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+size_t elem_size(map_dtype dt) { return dt == MAP_BF16 ? 2 : 4; }
+
+// Sequential carve-up of the caller's workspace.
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* p) : base(static_cast<char*>(p)) {}
+  template <typename T> T* take(size_t count) {
+    T* r = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += align_up(count * sizeof(T));
+    return r;
+  }
+  void* take_bytes(size_t bytes) {
+    void* r = base ? base + off : nullptr;
+    off += align_up(bytes);
+    return r;
+  }
+};
+
+bool valid_dtype(map_dtype dt) { return dt == MAP_F32 || dt == MAP_BF16; }
+
+bool valid_weights(const map_weights* w) {
+  if (!w) return false;
+  const void* ptrs[] = {w->w1_v, w->b1_v, w->w2_v, w->b2_v, w->w_k,
+                        w->w1_t, w->b1_t, w->w2_t, w->b2_t, w->w_q};
+  for (const void* p : ptrs)
+    if (!p) return false;
+  return w->D > 0 && w->D % 8 == 0 && w->D_h > 0 && w->D_h % 8 == 0 && w->d_p >= 4 &&
+         w->d_p <= 128 && w->d_p % 4 == 0 && isfinite(w->rope_theta) && w->rope_theta > 0.0f;
+}
+
+bool valid_bn(int B, int N) { return B >= 1 && B <= MAP_MAX_BATCH && N >= 1 && N <= MAP_MAX_N; }
+
+constexpr int kMaxQuestion = 8192;
+
+bool valid_offsets(const int32_t* t_off, int B) {
+  if (!t_off || t_off[0] != 0) return false;
+  for (int b = 0; b < B; ++b) {
+    const int m = t_off[b + 1] - t_off[b];
+    if (m < 1 || m > kMaxQuestion) return false;
+  }
+  return true;
+}
+
+bool valid_select(const map_select_params& sp, int N) {
+  return sp.K >= 1 && sp.K <= N && sp.K <= MAP_MAX_K && sp.K0 >= 0 && sp.K0 <= sp.K &&
+         isfinite(sp.tau) && sp.tau >= 0.0f;
+}
+
+map_status check_ws(void* ws, size_t have, size_t need) {
+  if (need == 0) return MAP_OK;
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) & (kAlign - 1)) || have < need) return MAP_ERR_WORKSPACE;
+  return MAP_OK;
+}
+
+// ------------------------------------------------------------ layouts
+struct ScoreWs {
+  float2 *cs_v, *cs_t;
+  void *h1_v, *h2_v, *h1_t, *h2_t;
+  float *k, *q, *logits;
+  float2* partial;
+};
+
+ScoreWs carve_score(Carver& c, map_dtype dt, int B, int N, int sumM, const map_weights& w) {
+  ScoreWs s;
+  const int half = w.d_p / 2, nblk = (N + 63) / 64;
+  const size_t rowsV = (size_t)B * N;
+  s.cs_v = c.take<float2>(rowsV * half);
+  s.cs_t = c.take<float2>((size_t)sumM * half);
+  s.h1_v = c.take_bytes(rowsV * w.D_h * elem_size(dt));
+  s.h2_v = c.take_bytes(rowsV * w.D_h * elem_size(dt));
+  s.h1_t = c.take_bytes((size_t)sumM * w.D_h * elem_size(dt));
+  s.h2_t = c.take_bytes((size_t)sumM * w.D_h * elem_size(dt));
+  s.k = c.take<float>(rowsV * w.d_p);
+  s.q = c.take<float>((size_t)sumM * w.d_p);
+  s.logits = c.take<float>((size_t)sumM * N);
+  s.partial = c.take<float2>((size_t)sumM * nblk);
+  return s;
+}
+
+struct SelectWs {
+  float* C;
+  float* r2;
+  uint64_t* pub;
+  unsigned int* bar;
+  int32_t* err;
+  int32_t* R0;
+  int32_t* order;
+  float* gain;
+};
+
+SelectWs carve_select(Carver& c, int B, int N, int K) {
+  SelectWs s;
+  s.C = c.take<float>((size_t)B * N * ((K + 3) & ~3));  // token-major, rows of K rounded up to 4
+  s.r2 = c.take<float>((size_t)B * N);
+  s.pub = c.take<uint64_t>((size_t)B * 2 * 128 * (kPub + 1));
+  s.bar = c.take<unsigned int>(B);
+  s.err = c.take<int32_t>(4);
+  s.R0 = c.take<int32_t>((size_t)B * K);
+  s.order = c.take<int32_t>((size_t)B * K);
+  s.gain = c.take<float>((size_t)B * K);
+  return s;
+}
+
+void fill_inv_freq(PrepArgs& pa, const map_weights& w) {
+  const int half = w.d_p / 2;
+  for (int i = 0; i < 64; ++i)
+    pa.inv_freq[i] = i < half ? pow(static_cast<double>(w.rope_theta), -2.0 * i / w.d_p) : 0.0;
+  pa.half = half;
+}
+
+GemmProblem linear(const void* A, int M, const void* W, const void* bias, void* C, int N, int K, int epi) {
+  GemmProblem p;
+  memset(&p, 0, sizeof(p));
+  p.A = A;
+  p.B = W;
+  p.C = C;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.lda = K;
+  p.ldb = K;
+  p.ldc = N;
+  p.batch = 1;
+  p.epi = epi;
+  p.bias = bias;
+  return p;
+}
+
+GemmProblem gram(const void* V, int B, int N, int D, float* S, const float* ninv) {
+  GemmProblem p;
+  memset(&p, 0, sizeof(p));
+  p.A = V;
+  p.B = V;
+  p.C = S;
+  p.M = N;
+  p.N = N;
+  p.K = D;
+  p.lda = D;
+  p.ldb = D;
+  p.ldc = N;
+  p.batch = B;
+  p.strideA = (long long)N * D;
+  p.strideB = (long long)N * D;
+  p.strideC = (long long)N * N;
+  p.epi = EPI_COSINE;
+  p.rs = ninv;
+  p.triangular = 1;
+  return p;
+}
+
+hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const void* V,
+                         const int32_t* pos_v, const void* T, const int32_t* pos_t,
+                         const int32_t* t_off, float* p_out, const ScoreWs& s,
+                         const GemmProblem* extra_l1, float* norms, float* ninv, hipStream_t st) {
+  const int sumM = t_off[B], rowsV = B * N;
+  PrepArgs pa;
+  memset(&pa, 0, sizeof(pa));
+  pa.V = V;
+  pa.rowsV = rowsV;
+  pa.D = w.D;
+  pa.norms = norms;
+  pa.ninv = ninv;
+  pa.pos_v = pos_v;
+  pa.pos_t = pos_t;
+  pa.rowsT = sumM;
+  pa.cs_v = s.cs_v;
+  pa.cs_t = s.cs_t;
+  fill_inv_freq(pa, w);
+  hipError_t e = launch_prep(dt, pa, norms != nullptr, true, st);
+  if (e != hipSuccess) return e;
+
+  GemmBatch g1;
+  memset(&g1, 0, sizeof(g1));
+  g1.p[0] = linear(V, rowsV, w.w1_v, w.b1_v, s.h1_v, w.D_h, w.D, EPI_BIAS_GELU);
+  g1.p[1] = linear(T, sumM, w.w1_t, w.b1_t, s.h1_t, w.D_h, w.D, EPI_BIAS_GELU);
+  g1.count = 2;
+  if (extra_l1) g1.p[g1.count++] = *extra_l1;
+  gemm_finalize(g1);
+  if ((e = launch_gemm(dt, g1, extra_l1 ? "gemm_layer1_gram" : "gemm_layer1", st)) != hipSuccess) return e;
+
+  GemmBatch g2;
+  memset(&g2, 0, sizeof(g2));
+  g2.p[0] = linear(s.h1_v, rowsV, w.w2_v, w.b2_v, s.h2_v, w.D_h, w.D_h, EPI_BIAS);
+  g2.p[1] = linear(s.h1_t, sumM, w.w2_t, w.b2_t, s.h2_t, w.D_h, w.D_h, EPI_BIAS);
+  g2.count = 2;
+  gemm_finalize(g2);
+  if ((e = launch_gemm(dt, g2, "gemm_layer2", st)) != hipSuccess) return e;
+
+  GemmBatch g3;
+  memset(&g3, 0, sizeof(g3));
+  g3.p[0] = linear(s.h2_v, rowsV, w.w_k, nullptr, s.k, w.d_p, w.D_h, EPI_ROPE);
+  g3.p[0].rope_cs = s.cs_v;
+  g3.p[1] = linear(s.h2_t, sumM, w.w_q, nullptr, s.q, w.d_p, w.D_h, EPI_ROPE);
+  g3.p[1].rope_cs = s.cs_t;
+  g3.count = 2;
+  gemm_finalize(g3);
+  if ((e = launch_gemm(dt, g3, "gemm_proj_rope", st)) != hipSuccess) return e;
+
+  ScoreArgs sa;
+  memset(&sa, 0, sizeof(sa));
+  sa.q = s.q;
+  sa.k = s.k;
+  sa.logits = s.logits;
+  sa.partial = s.partial;
+  sa.p_out = p_out;
+  sa.B = B;
+  sa.N = N;
+  sa.d_p = w.d_p;
+  sa.nblk = (N + 63) / 64;
+  for (int b = 0; b <= B; ++b) sa.t_off[b] = t_off[b];
+  return launch_score(sa, st);
+}
+
+hipError_t enqueue_select(int B, int N, const float* p, const float* S, const float* norms,
+                          const map_select_params& sp, int32_t* idx_out, int32_t* order_out,
+                          float* gain_out, const SelectWs& w, hipStream_t st) {
+  SelectArgs a;
+  memset(&a, 0, sizeof(a));
+  a.p = p;
+  a.S = S;
+  a.norms = norms;
+  a.R0 = w.R0;
+  a.C = w.C;
+  a.r2 = w.r2;
+  a.pub = w.pub;
+  a.bar = w.bar;
+  a.err = w.err;
+  a.order = order_out ? order_out : w.order;
+  a.gain = gain_out ? gain_out : w.gain;
+  a.idx_out = idx_out;
+  a.B = B;
+  a.N = N;
+  a.K = sp.K;
+  a.K0 = sp.K0;
+  a.tau2 = sp.tau * sp.tau;
+  hipError_t e = launch_topk(a, st);
+  if (e != hipSuccess) return e;
+  if ((e = launch_select(a, st)) != hipSuccess) return e;
+  return launch_restore(a, st);
+}
+
+map_status hip_status(hipError_t e) { return e == hipSuccess ? MAP_OK : MAP_ERR_HIP; }
+
+size_t score_ws_bytes(map_dtype dt, int B, int N, int sumM, const map_weights& w) {
+  Carver c(nullptr);
+  carve_score(c, dt, B, N, sumM, w);
+  return c.off;
+}
+
+size_t select_ws_bytes(int B, int N, int K) {
+  Carver c(nullptr);
+  carve_select(c, B, N, K);
+  return c.off;
+}
+
+// ------------------------------------------------------------ timing
+struct TimingRecord {
+  const char* name;
+  hipEvent_t start, stop;
+};
+
+struct TimingState {
+  std::mutex mu;
+  bool enabled = false;
+  std::vector<TimingRecord> pending;
+  std::vector<hipEvent_t> spare;
+  std::vector<const char*> names;
+  std::vector<double> total_ms;
+  std::vector<int> launches;
+};
+
+TimingState& timing() {
+  static TimingState t;
+  return t;
+}
+
+hipEvent_t take_event(TimingState& t) {
+  if (!t.spare.empty()) {
+    hipEvent_t e = t.spare.back();
+    t.spare.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+}  // namespace
+
+namespace mapk {
+
+TimedLaunch::TimedLaunch(const char* name, hipStream_t s) : name_(name), s_(s), slot_(-1) {
+  TimingState& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  if (!t.enabled) return;
+  TimingRecord r{name, take_event(t), take_event(t)};
+  if (!r.start || !r.stop) return;
+  (void)hipEventRecord(r.start, s);
+  t.pending.push_back(r);
+  slot_ = static_cast<int>(t.pending.size()) - 1;
+}
+
+TimedLaunch::~TimedLaunch() {
+  if (slot_ < 0) return;
+  TimingState& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  if (slot_ < static_cast<int>(t.pending.size())) (void)hipEventRecord(t.pending[slot_].stop, s_);
+}
+
+}  // namespace mapk
+
+extern "C" {
+
+const char* map_status_string(int status) {
+  switch (status) {
+    case MAP_OK: return "ok";
+    case MAP_ERR_INVALID_ARG: return "invalid argument";
+    case MAP_ERR_UNSUPPORTED: return "unsupported";
+    case MAP_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case MAP_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int map_version(void) { return 100; }
+
+size_t map_score_workspace(map_dtype dt, int B, int N, int sum_M, const map_weights* w) {
+  if (!valid_dtype(dt) || !valid_bn(B, N) || !valid_weights(w) || sum_M < B) return 0;
+  return score_ws_bytes(dt, B, N, sum_M, *w);
+}
+
+size_t map_similarity_workspace(map_dtype dt, int B, int N, int D) {
+  if (!valid_dtype(dt) || !valid_bn(B, N) || D <= 0 || D % 8) return 0;
+  return align_up((size_t)B * N * sizeof(float));
+}
+
+size_t map_select_workspace(int B, int N, int K) {
+  if (!valid_bn(B, N) || K < 1 || K > N || K > MAP_MAX_K) return 0;
+  return select_ws_bytes(B, N, K);
+}
+
+size_t map_prune_workspace(map_dtype dt, int B, int N, int sum_M, const map_weights* w, int K) {
+  if (!valid_dtype(dt) || !valid_bn(B, N) || !valid_weights(w) || sum_M < B || K < 1 || K > N ||
+      K > MAP_MAX_K)
+    return 0;
+  return score_ws_bytes(dt, B, N, sum_M, *w) + select_ws_bytes(B, N, K) +
+         align_up((size_t)B * N * N * sizeof(float)) + 3 * align_up((size_t)B * N * sizeof(float));
+}
+
+map_status map_score(const map_weights* w, map_dtype dt, int B, int N, const void* V,
+                     const int32_t* pos_v, const void* T, const int32_t* pos_t,
+                     const int32_t* t_off_host, float* p_out, void* ws, size_t ws_bytes,
+                     void* stream) {
+  if (!valid_dtype(dt) || !valid_bn(B, N) || !valid_weights(w) || !V || !pos_v || !T || !pos_t ||
+      !p_out || !valid_offsets(t_off_host, B))
+    return MAP_ERR_INVALID_ARG;
+  const int sumM = t_off_host[B];
+  const map_status ws_ok = check_ws(ws, ws_bytes, score_ws_bytes(dt, B, N, sumM, *w));
+  if (ws_ok != MAP_OK) return ws_ok;
+  Carver c(ws);
+  const ScoreWs s = carve_score(c, dt, B, N, sumM, *w);
+  return hip_status(enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p_out, s, nullptr,
+                                  nullptr, nullptr, static_cast<hipStream_t>(stream)));
+}
+
+map_status map_similarity(map_dtype dt, int B, int N, int D, const void* V, float* S_out,
+                          float* norms_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!valid_dtype(dt) || !valid_bn(B, N) || D <= 0 || D % 8 || !V || !S_out || !norms_out)
+    return MAP_ERR_INVALID_ARG;
+  const map_status ws_ok = check_ws(ws, ws_bytes, map_similarity_workspace(dt, B, N, D));
+  if (ws_ok != MAP_OK) return ws_ok;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Carver c(ws);
+  float* ninv = c.take<float>((size_t)B * N);
+  PrepArgs pa;
+  memset(&pa, 0, sizeof(pa));
+  pa.V = V;
+  pa.rowsV = B * N;
+  pa.D = D;
+  pa.norms = norms_out;
+  pa.ninv = ninv;
+  hipError_t e = launch_prep(dt, pa, true, false, st);
+  if (e != hipSuccess) return MAP_ERR_HIP;
+  GemmBatch g;
+  memset(&g, 0, sizeof(g));
+  g.p[0] = gram(V, B, N, D, S_out, ninv);
+  g.count = 1;
+  gemm_finalize(g);
+  return hip_status(launch_gemm(dt, g, "gemm_gram", st));
+}
+
+map_status map_select(int B, int N, const float* p, const float* S, const float* norms,
+                      map_select_params sp, int32_t* idx_out, int32_t* order_out, float* gain_out,
+                      void* ws, size_t ws_bytes, void* stream) {
+  if (!valid_bn(B, N) || !p || !S || !norms || !idx_out || !valid_select(sp, N))
+    return MAP_ERR_INVALID_ARG;
+  const map_status ws_ok = check_ws(ws, ws_bytes, select_ws_bytes(B, N, sp.K));
+  if (ws_ok != MAP_OK) return ws_ok;
+  Carver c(ws);
+  const SelectWs w = carve_select(c, B, N, sp.K);
+  return hip_status(enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, w,
+                                   static_cast<hipStream_t>(stream)));
+}
+
+map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const void* V,
+                     const int32_t* pos_v, const void* T, const int32_t* pos_t,
+                     const int32_t* t_off_host, map_select_params sp, int32_t* idx_out, void* V_out,
+                     int32_t* pos_out, float* p_out, int32_t* order_out, float* gain_out, void* ws,
+                     size_t ws_bytes, void* stream) {
+  if (!valid_dtype(dt) || !valid_bn(B, N) || !valid_weights(w) || !V || !pos_v || !T || !pos_t ||
+      !idx_out || !V_out || !pos_out || !valid_offsets(t_off_host, B) || !valid_select(sp, N))
+    return MAP_ERR_INVALID_ARG;
+  const int sumM = t_off_host[B];
+  const map_status ws_ok = check_ws(ws, ws_bytes, map_prune_workspace(dt, B, N, sumM, w, sp.K));
+  if (ws_ok != MAP_OK) return ws_ok;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  Carver c(ws);
+  const ScoreWs s = carve_score(c, dt, B, N, sumM, *w);
+  const SelectWs sw = carve_select(c, B, N, sp.K);
+  float* S = c.take<float>((size_t)B * N * N);
+  float* norms = c.take<float>((size_t)B * N);
+  float* ninv = c.take<float>((size_t)B * N);
+  float* p = p_out ? p_out : c.take<float>((size_t)B * N);
+  const GemmProblem g = gram(V, B, N, w->D, S, ninv);
+  hipError_t e = enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, &g, norms, ninv, st);
+  if (e != hipSuccess) return MAP_ERR_HIP;
+  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st);
+  if (e != hipSuccess) return MAP_ERR_HIP;
+  GatherArgs ga;
+  ga.V = V;
+  ga.pos_v = pos_v;
+  ga.idx = idx_out;
+  ga.V_out = V_out;
+  ga.pos_out = pos_out;
+  ga.B = B;
+  ga.N = N;
+  ga.K = sp.K;
+  ga.row_bytes = static_cast<int>(w->D * elem_size(dt));
+  return hip_status(launch_gather(ga, st));
+}
+
+map_status map_timing_enable(int enable) {
+  TimingState& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  t.enabled = enable != 0;
+  return MAP_OK;
+}
+
+int map_timing_read(const char** names, double* total_ms, int* launches, int cap) {
+  TimingState& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  for (const TimingRecord& r : t.pending) {
+    float ms = 0.0f;
+    if (hipEventSynchronize(r.stop) == hipSuccess && hipEventElapsedTime(&ms, r.start, r.stop) == hipSuccess) {
+      size_t k = 0;
+      while (k < t.names.size() && strcmp(t.names[k], r.name) != 0) ++k;
+      if (k == t.names.size()) {
+        t.names.push_back(r.name);
+        t.total_ms.push_back(0.0);
+        t.launches.push_back(0);
+      }
+      t.total_ms[k] += ms;
+      t.launches[k] += 1;
+    }
+    t.spare.push_back(r.start);
+    t.spare.push_back(r.stop);
+  }
+  t.pending.clear();
+  const int n = static_cast<int>(t.names.size());
+  for (int i = 0; i < n && i < cap; ++i) {
+    if (names) names[i] = t.names[i];
+    if (total_ms) total_ms[i] = t.total_ms[i];
+    if (launches) launches[i] = t.launches[i];
+  }
+  return n;
+}
+
+void map_timing_reset(void) {
+  TimingState& t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  for (const TimingRecord& r : t.pending) {
+    (void)hipEventSynchronize(r.stop);
+    t.spare.push_back(r.start);
+    t.spare.push_back(r.stop);
+  }
+  t.pending.clear();
+  t.names.clear();
+  t.total_ms.clear();
+  t.launches.clear();
+}
+
+}  // extern "C"

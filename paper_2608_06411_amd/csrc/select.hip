@@ -1,0 +1,893 @@
+// Diversity-aware selection (section "Inference-Time Token Pruning", Eq. (4)).
+//
+// The residual of Eq. (4) is evaluated from the cosine similarity S and the
+// row norms n: with v^_i = v_i / n_i, b_t the orthonormal basis in pick order
+// and c_{t,i} = <b_t, v^_i>,
+//     c_{t,i} = (S[i_t][i] - sum_{l<t} c_{l,i_t} c_{l,i}) / r_{i_t},
+//     r_i^2   = 1 - sum_t c_{t,i}^2,
+//     ||v_i - B B^T v_i|| = n_i r_i,
+// so the score p_i ||v_i - B B^T v_i|| is p_i n_i r_i.  A pick whose r_i is
+// at most tau adds no basis vector (its row of C is zero).
+//
+// One cooperative launch runs the whole selection of every image.  An image
+// is served by G workgroups; workgroup w owns `ch` consecutive tokens (their
+// r^2 and their columns of C, kept token-major in global memory).  Work
+// proceeds in rounds separated by one barrier across the image's workgroups:
+//
+//   pool     Every workgroup builds the same candidate pool and replays the
+//            round's picks on it, redundantly and deterministically, so no
+//            second barrier is needed to agree on them.  The first rounds
+//            place R0 (forced picks in descending p).  Afterwards the pool is
+//            the top of the keys the workgroups published in the previous
+//            round, and the greedy rule runs on it while the best pool key
+//            exceeds beta, an upper bound of every key outside the pool.
+//            Scores never increase as the basis grows, so a pool key above
+//            beta is the true argmax over all candidates: the picks are
+//            exactly those of the step-by-step rule.  The pool keeps its
+//            residual Gram matrix Rm = S - C^T C in LDS, so a pick costs one
+//            rank-one update and one workgroup barrier.
+//   update   Every workgroup applies the round's new basis rows to its own
+//            tokens (a dense product over the rows of earlier rounds, then a
+//            right-looking triangular solve over this round's rows), updates
+//            their keys and publishes its top kPub keys plus its (kPub+1)-th
+//            key as a bound.
+//
+// Keys order candidates as the rule does: positive scores first (by score),
+// then zero scores by p, ties to the lower index; selected tokens key 0.
+#include "internal.h"
+
+namespace mapk {
+
+namespace {
+
+constexpr int NT = 256;
+constexpr int kTopkThreads = 1024;
+constexpr unsigned kSpinLimit = 1u << 22;
+constexpr int kMaxPool = 128;  // two pool members per lane of the picking wave
+
+__device__ __forceinline__ uint32_t ordered_bits(float f) {
+  // non-negative finite floats order like their bits; everything else -> 0
+  return (f > 0.0f && f <= 3.402823466e38f) ? __float_as_uint(f) : 0u;
+}
+
+__device__ __forceinline__ uint64_t make_key(float r2, float qn, float p, int i, float tau2) {
+  uint32_t hi = ordered_bits(p);
+  if (r2 > tau2 && qn > 0.0f) {
+    const float s = qn * sqrtf(r2);
+    if (s > 0.0f) hi = 0x80000000u | ordered_bits(s);
+  }
+  return (static_cast<uint64_t>(hi) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
+}
+
+__device__ __forceinline__ int key_index(uint64_t k) {
+  return static_cast<int>(0xffffffffu - static_cast<uint32_t>(k));
+}
+
+__device__ __forceinline__ float key_score(uint64_t k) {
+  const uint32_t hi = static_cast<uint32_t>(k >> 32);
+  return (hi & 0x80000000u) ? __uint_as_float(hi & 0x7fffffffu) : 0.0f;
+}
+
+// ---- wave64 reductions on the DPP network (row shifts, then row broadcasts)
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_umax(uint32_t v) {
+  const uint32_t o = __builtin_amdgcn_update_dpp(0u, v, CTRL, ROW_MASK, 0xf, false);
+  return o > v ? o : v;
+}
+
+__device__ __forceinline__ uint32_t wave_umax32(uint32_t v) {
+  v = dpp_umax<0x111, 0xf>(v);  // row_shr:1
+  v = dpp_umax<0x112, 0xf>(v);  // row_shr:2
+  v = dpp_umax<0x114, 0xf>(v);  // row_shr:4
+  v = dpp_umax<0x118, 0xf>(v);  // row_shr:8   -> lane 15 of each row holds the row maximum
+  v = dpp_umax<0x142, 0xa>(v);  // row_bcast:15
+  v = dpp_umax<0x143, 0xc>(v);  // row_bcast:31 -> lane 63 holds the wave maximum
+  return __builtin_amdgcn_readlane(v, 63);
+}
+
+// Largest 64-bit key of the wave (0 if every lane holds 0).
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
+  const uint32_t hi = static_cast<uint32_t>(k >> 32);
+  const uint32_t mhi = wave_umax32(hi);
+  const uint32_t mlo = wave_umax32(hi == mhi ? static_cast<uint32_t>(k) : 0u);
+  return (static_cast<uint64_t>(mhi) << 32) | mlo;
+}
+
+__host__ __device__ __forceinline__ int pow2_at_least(int n) {
+  int p = 64;
+  while (p < n) p <<= 1;
+  return p;
+}
+
+// Descending bitonic sort of n keys in LDS (n a power of two), one pair per
+// thread and stage; used only on rare fallback paths.
+__device__ void lds_sort_desc(uint64_t* keys, int n) {
+  __syncthreads();
+  for (int k = 2; k <= n; k <<= 1)
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int q = threadIdx.x; q < n / 2; q += blockDim.x) {
+        const int i = 2 * q - (q & (j - 1));  // lower element of pair q
+        const uint64_t a = keys[i], b = keys[i + j];
+        const bool desc = (i & k) == 0;
+        if (desc == (a < b)) {
+          keys[i] = b;
+          keys[i + j] = a;
+        }
+      }
+      __syncthreads();
+    }
+}
+
+// ------------------------------------------------------------------ top-K0
+// One block per image.  Radix select (4 passes of 8 bits) finds the p bits
+// of the K0-th largest p; the keys at or above it are collected and ranked
+// (p, then lower index first).  Also clears the image's barrier counter and
+// the error flag for the selection launch that follows on the same stream.
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(const SelectArgs a) {
+  extern __shared__ uint64_t cand[];  // [pow2(N)] collected keys
+  __shared__ unsigned hist[256];
+  __shared__ unsigned misc[4];
+  constexpr int MAXE = MAP_MAX_N / kTopkThreads;
+  const int b = blockIdx.x, N = a.N, K0 = a.K0, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const float* p = a.p + (long long)b * N;
+  if (tid == 0) {
+    a.bar[b] = 0u;
+    if (b == 0) *a.err = 0;
+  }
+  if (K0 == 0) return;
+  uint32_t hv[MAXE];
+#pragma unroll
+  for (int r = 0; r < MAXE; ++r) {
+    const int i = r * kTopkThreads + tid;
+    hv[r] = i < N ? ordered_bits(p[i]) : 0u;
+  }
+  uint32_t prefix = 0;
+  unsigned need = static_cast<unsigned>(K0);
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    const uint32_t hmask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
+    if (tid < 256) hist[tid] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < MAXE; ++r) {
+      const int i = r * kTopkThreads + tid;
+      if (i < N && (hv[r] & hmask) == (prefix & hmask)) atomicAdd(&hist[(hv[r] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      // lane l covers digits 255 - 4l .. 252 - 4l (descending)
+      unsigned c[4], s = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        c[q] = hist[255 - 4 * lane - q];
+        s += c[q];
+      }
+      // inclusive prefix over lanes (descending digit order)
+      unsigned incl = s;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const unsigned o = __shfl_up(incl, off);
+        if (lane >= off) incl += o;
+      }
+      const unsigned excl = incl - s;
+      const bool here = excl < need && incl >= need;
+      const unsigned long long bal = __ballot(here);
+      const int src = __builtin_ctzll(bal);
+      if (lane == src) {
+        unsigned run = excl;
+        int d = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (run + c[q] >= need) {
+            d = 255 - 4 * lane - q;
+            break;
+          }
+          run += c[q];
+        }
+        misc[0] = static_cast<unsigned>(d);
+        misc[1] = need - run;
+      }
+    }
+    __syncthreads();
+    prefix |= misc[0] << shift;
+    need = misc[1];
+  }
+  // prefix = p bits of the K0-th largest; collect every key with p bits >= prefix
+  if (tid == 0) misc[2] = 0;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < MAXE; ++r) {
+    const int i = r * kTopkThreads + tid;
+    if (i < N && hv[r] >= prefix) {
+      const unsigned slot = atomicAdd(&misc[2], 1u);
+      cand[slot] = (static_cast<uint64_t>(hv[r]) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
+    }
+  }
+  __syncthreads();
+  const int nc = static_cast<int>(misc[2]);
+  int32_t* out = a.R0 + (long long)b * K0;
+  if (nc <= kTopkThreads) {
+    // rank by count: keys are distinct
+    if (tid < nc) {
+      const uint64_t x = cand[tid];
+      int rank = 0;
+      for (int j = 0; j < nc; ++j) rank += cand[j] > x;
+      if (rank < K0) out[rank] = key_index(x);
+    }
+  } else {  // many equal p values: sort everything collected
+    const int n2 = pow2_at_least(nc);
+    for (int j = nc + tid; j < n2; j += kTopkThreads) cand[j] = 0ull;
+    lds_sort_desc(cand, n2);
+    for (int j = tid; j < K0; j += kTopkThreads) out[j] = key_index(cand[j]);
+  }
+}
+
+// ------------------------------------------------------------------ selection
+// LDS row stride (floats) of the coefficient columns: 4 times an odd number,
+// so float4 reads of 16 consecutive rows hit 16 different bank groups.
+__host__ __device__ inline int col_stride(int K) { return ((K + 31) & ~31) + 4; }
+
+struct Lds {
+  // byte offsets into the dynamic LDS block
+  int midx, mp, mn, mqn, mr2, pslot, pr, pgain, pcol, U, RW, merge, bnd, misc;
+  int bytes;
+  int cs, us, rs, ws;
+};
+
+// RW holds the pool's residual Gram matrix during the picks and the own
+// tokens' new rows (W) during the update; the two never live together.
+__host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap) {
+  Lds L;
+  int o = 0;
+  auto take = [&](int bytes) { const int r = o; o += (bytes + 15) & ~15; return r; };
+  L.cs = col_stride(K);
+  L.us = pcap + 4 + ((pcap / 4) % 2 == 0 ? 4 : 0);  // 4 times an odd number
+  L.rs = pcap + 1;
+  L.ws = ch + 4;
+  L.midx = take(4 * pcap);
+  L.mp = take(4 * pcap);
+  L.mn = take(4 * pcap);
+  L.mqn = take(4 * pcap);
+  L.mr2 = take(4 * pcap);
+  L.pslot = take(4 * pcap);
+  L.pr = take(4 * pcap);
+  L.pgain = take(4 * pcap);
+  L.pcol = take(4 * pcap * L.cs);
+  L.U = take(4 * pcap * L.us);
+  const int rbytes = 4 * pcap * L.rs, wbytes = 4 * pcap * L.ws;
+  L.RW = take(rbytes > wbytes ? rbytes : wbytes);
+  L.merge = take(8 * G * kPub);
+  L.bnd = take(8 * ((kPub + 1) * (NT / 64)));
+  L.misc = take(64);
+  L.bytes = o;
+  return L;
+}
+
+__device__ void image_barrier(unsigned int* ctr, unsigned int target, int32_t* err, int* abort_flag) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    atomicAdd(ctr, 1u);
+    unsigned spins = 0;
+    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      __builtin_amdgcn_s_sleep(1);
+      if (++spins > kSpinLimit) {
+        atomicExch(err, 1);
+        *abort_flag = 1;
+        break;
+      }
+    }
+    __threadfence();
+  }
+  __syncthreads();
+}
+
+// Global C is token-major: Ct[i][l] = c_{l,i}, rows of Kp floats (Kp = K
+// rounded up to 4), so one token's coefficients are contiguous.
+__global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_begin) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  const int G = a.G, ch = a.ch, pcap = a.pcap, K = a.K, K0 = a.K0, N = a.N;
+  const int Kp = (K + 3) & ~3;
+  const int b = b_begin + blockIdx.x / G, w = blockIdx.x % G;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const Lds L = lds_layout(K, G, ch, pcap);
+  int* midx = reinterpret_cast<int*>(lds + L.midx);
+  float* mp = reinterpret_cast<float*>(lds + L.mp);
+  float* mn = reinterpret_cast<float*>(lds + L.mn);
+  float* mqn = reinterpret_cast<float*>(lds + L.mqn);
+  float* mr2 = reinterpret_cast<float*>(lds + L.mr2);
+  int* pslot = reinterpret_cast<int*>(lds + L.pslot);
+  float* prr = reinterpret_cast<float*>(lds + L.pr);
+  float* pgain = reinterpret_cast<float*>(lds + L.pgain);
+  float* pcol = reinterpret_cast<float*>(lds + L.pcol);
+  float* U = reinterpret_cast<float*>(lds + L.U);
+  float* Rm = reinterpret_cast<float*>(lds + L.RW);
+  float* W = reinterpret_cast<float*>(lds + L.RW);
+  uint64_t* merge = reinterpret_cast<uint64_t*>(lds + L.merge);
+  uint64_t* bndk = reinterpret_cast<uint64_t*>(lds + L.bnd);
+  int* misc = reinterpret_cast<int*>(lds + L.misc);
+  const int cs = L.cs, us = L.us, rs = L.rs, wsd = L.ws;
+
+  const float* p = a.p + (long long)b * N;
+  const float* nrm = a.norms + (long long)b * N;
+  const float* S = a.S + (long long)b * N * N;
+  float* Ct = a.C + (long long)b * N * Kp;
+  float* r2g = a.r2 + (long long)b * N;
+  const int32_t* R0 = a.R0 + (long long)b * K0;
+
+  // ---- own tokens [c0, c0 + cnt); thread tid < ch keeps token c0 + tid
+  const int c0 = w * ch;
+  const int cnt = max(0, min(ch, N - c0));
+  const int my_i = c0 + tid;
+  // state: 0 candidate, 1 reserved (in R0, not yet placed), 2 selected
+  int my_state = 2;
+  float my_r2 = 0.0f, my_qn = 0.0f, my_p = 0.0f;
+  if (tid < cnt) {
+    const float pi = p[my_i];
+    const float ni = nrm[my_i];
+    my_p = (pi > 0.0f && pi <= 3.402823466e38f) ? pi : 0.0f;
+    my_qn = my_p * ni;
+    my_r2 = ni > 0.0f ? 1.0f : 0.0f;
+    my_state = 0;
+  }
+  {  // mark the own tokens that belong to R0 (W's memory serves as flags)
+    int* flag = reinterpret_cast<int*>(W);
+    for (int i = tid; i < ch; i += NT) flag[i] = 0;
+    if (tid == 0) misc[0] = 0;  // abort flag
+    __syncthreads();
+    for (int j = tid; j < K0; j += NT) {
+      const int r = R0[j];
+      if (r >= c0 && r < c0 + cnt) flag[r - c0] = 1;
+    }
+    __syncthreads();
+    if (tid < cnt && flag[tid]) my_state = 1;  // reserved: placed by a forced round
+    __syncthreads();
+  }
+
+  int t = 0, fq = 0, round = 0;
+  while (t < K) {
+    // ============================================================ pool
+    const bool forced = fq < K0;
+    uint64_t beta = 0;
+    int pn = 0;
+    if (forced) {
+      pn = min(pcap, K0 - fq);
+      for (int m = tid; m < pn; m += NT) midx[m] = R0[fq + m];
+    } else if (round > 0) {  // keys exist once an update phase has run
+      // Each workgroup published its top kPub keys (descending) and its
+      // (kPub+1)-th key.  beta0 = the largest of those bounds; every key
+      // above it is ranked by counting, list by list, the keys above it.
+      const uint64_t* pub = a.pub + ((long long)b * 2 + ((round - 1) & 1)) * G * (kPub + 1);
+      const int nk = G * kPub;
+      for (int e = tid; e < nk; e += NT) {
+        const int ww = e >> 3, q = e & 7;  // kPub == 8
+        merge[e] = __hip_atomic_load(pub + ww * (kPub + 1) + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      uint64_t bmax = 0;
+      for (int ww = tid; ww < G; ww += NT) {
+        const uint64_t k = __hip_atomic_load(pub + ww * (kPub + 1) + kPub, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+        bmax = k > bmax ? k : bmax;
+      }
+      bmax = wave_max_key(bmax);
+      if (lane == 0) bndk[wave] = bmax;
+      if (tid == 0) misc[2] = 0;  // pool size
+      __syncthreads();
+      uint64_t beta0 = bndk[0];
+      for (int q = 1; q < NT / 64; ++q) beta0 = bndk[q] > beta0 ? bndk[q] : beta0;
+      uint64_t nextk = 0;  // the largest key left out of the pool by the cap
+      for (int e = tid; e < nk; e += NT) {
+        const uint64_t x = merge[e];
+        if (x <= beta0) continue;
+        int rank = e & 7;
+        const int own_list = e >> 3;
+        for (int ww = 0; ww < G; ++ww) {
+          if (ww == own_list) continue;
+          const uint64_t* lst = merge + 8 * ww;  // descending
+          int c = lst[3] > x ? 4 : 0;
+          c += lst[c + 1] > x ? 2 : 0;
+          c += lst[c] > x ? 1 : 0;
+          c += (c == 7 && lst[7] > x) ? 1 : 0;
+          rank += c;
+        }
+        if (rank < pcap) {
+          const int i = key_index(x);
+          midx[rank] = (i >= 0 && i < N) ? i : 0;
+          atomicAdd(&misc[2], 1);
+        } else if (rank == pcap) {
+          nextk = x;
+        }
+      }
+      nextk = wave_max_key(nextk);
+      if (lane == 0) bndk[NT / 64 + wave] = nextk;
+      __syncthreads();
+      pn = misc[2];
+      beta = beta0;
+      for (int q = 0; q < NT / 64; ++q) beta = bndk[NT / 64 + q] > beta ? bndk[NT / 64 + q] : beta;
+    }
+    __syncthreads();
+    // members: state, columns (rows < t, written by their owners before the
+    // barrier) and their block of S; loads batched before use
+    for (int m = tid; m < pn; m += NT) {
+      const int i = midx[m];
+      const float pi = p[i], ni = nrm[i];
+      const float r2 = t == 0 ? (ni > 0.0f ? 1.0f : 0.0f)
+                              : __hip_atomic_load(r2g + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const float pc = (pi > 0.0f && pi <= 3.402823466e38f) ? pi : 0.0f;
+      mp[m] = pc;
+      mn[m] = ni;
+      mqn[m] = pc * ni;
+      mr2[m] = r2;
+    }
+    if (t > 0) {  // columns: pn rows of tq float4 each; a wave per member, lanes along it
+      const int tq = (t + 3) >> 2;
+      for (int m0 = 0; m0 < pn; m0 += 4 * (NT / 64)) {
+        float4 v[4][2];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int m = m0 + wave + 4 * u, q = lane + 64 * h;
+            v[u][h] = (m < pn && q < tq) ? *reinterpret_cast<const float4*>(Ct + (long long)midx[m] * Kp + 4 * q)
+                                         : make_float4(0.f, 0.f, 0.f, 0.f);
+          }
+        for (int q2 = 128; q2 < tq; q2 += 64) {  // columns longer than 512 floats
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int m = m0 + wave + 4 * u, q = q2 + lane;
+            if (m < pn && q < tq)
+              *reinterpret_cast<float4*>(pcol + m * cs + 4 * q) =
+                  *reinterpret_cast<const float4*>(Ct + (long long)midx[m] * Kp + 4 * q);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int m = m0 + wave + 4 * u, q = lane + 64 * h;
+            if (m < pn && q < tq) *reinterpret_cast<float4*>(pcol + m * cs + 4 * q) = v[u][h];
+          }
+      }
+    }
+    // Rm = S among the members (gathered): rows by wave, columns by lane
+    for (int m1 = wave; m1 < pn; m1 += 4 * (NT / 64)) {
+      float v[4][2];
+      long long base[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) base[u] = (long long)midx[min(m1 + 4 * u, pn - 1)] * N;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int m2 = lane + 64 * h;
+          v[u][h] = (m1 + 4 * u < pn && m2 < pn) ? S[base[u] + midx[m2]] : 0.0f;
+        }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int m2 = lane + 64 * h;
+          if (m1 + 4 * u < pn && m2 < pn) Rm[(m1 + 4 * u) * rs + m2] = v[u][h];
+        }
+    }
+    __syncthreads();
+    // Rm -= P P^T over the t rows so far.  Thread (bi, bj) owns rows
+    // bi + 16 x and columns bj + 16 y: the 16 lanes that share bj read 16
+    // consecutive rows (distinct bank groups) and the rest is broadcast.
+    if (t > 0) {
+      const int t4 = t & ~3;
+      const int nbb = (pn + 63) >> 6;  // 64 x 64 super-blocks per side
+      for (int sb = 0; sb < nbb * nbb; ++sb) {
+        const int sr = (sb / nbb) * 64, sc = (sb % nbb) * 64;
+        const int bi = lane & 15, bj = (lane >> 4) + 4 * wave;
+        float acc[4][4] = {};
+        const float* pa[4];
+        const float* pb[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          pa[x] = pcol + min(sr + bi + 16 * x, pn - 1) * cs;
+          pb[x] = pcol + min(sc + bj + 16 * x, pn - 1) * cs;
+        }
+        for (int l = 0; l < t4; l += 4) {
+          float4 xa[4], xb[4];
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            xa[x] = *reinterpret_cast<const float4*>(pa[x] + l);
+            xb[x] = *reinterpret_cast<const float4*>(pb[x] + l);
+          }
+#pragma unroll
+          for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) {
+              acc[x][y] = fmaf(xa[x].x, xb[y].x, acc[x][y]);
+              acc[x][y] = fmaf(xa[x].y, xb[y].y, acc[x][y]);
+              acc[x][y] = fmaf(xa[x].z, xb[y].z, acc[x][y]);
+              acc[x][y] = fmaf(xa[x].w, xb[y].w, acc[x][y]);
+            }
+        }
+        for (int l = t4; l < t; ++l)
+#pragma unroll
+          for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) acc[x][y] = fmaf(pa[x][l], pb[y][l], acc[x][y]);
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+          for (int y = 0; y < 4; ++y) {
+            const int m1 = sr + bi + 16 * x, m2 = sc + bj + 16 * y;
+            if (m1 < pn && m2 < pn) Rm[m1 * rs + m2] -= acc[x][y];
+          }
+      }
+    }
+    __syncthreads();
+
+    // ============================================================ picks
+    // Wave 0 alone, without barriers.  Lane m holds members m and m + 64
+    // (r^2, active flag and key in registers).  For the k-th pick s,
+    //   c_m = (Rm[s][m] - sum_{k'<k} U[s][k'] U[m][k']) / r_s
+    // where U[m][k'] is member m's coefficient on the k'-th basis vector of
+    // this round; each lane writes only its own rows of U, and reads the
+    // pick's row, which the same wave wrote in earlier steps.
+    const int t0 = t;
+    int np = 0;
+    if (wave == 0) {
+      float r2v[2];
+      bool actv[2];
+      uint64_t kk[2] = {0ull, 0ull};
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int m = lane + 64 * h;
+        r2v[h] = m < pn ? mr2[m] : 0.0f;
+        actv[h] = m < pn;
+      }
+      while (t < K) {
+        int s;
+        uint64_t best = 0;
+        if (forced) {
+          s = np < pn ? np : -1;
+        } else {
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int m = lane + 64 * h;
+            kk[h] = actv[h] ? make_key(r2v[h], mqn[m], mp[m], midx[m], a.tau2) : 0ull;
+          }
+          const uint64_t kl = kk[0] > kk[1] ? kk[0] : kk[1];
+          best = wave_max_key(kl);
+          s = -1;
+          if (best > beta) {  // keys are distinct: exactly one member holds `best`
+            const int l = static_cast<int>(__builtin_ctzll(__ballot(kl == best)));
+            const int second = __builtin_amdgcn_readlane(kk[0] == best ? 0 : 1, l);
+            s = l + 64 * second;
+          }
+        }
+        if (s < 0) break;
+        const int sl = s & 63, sh = s >> 6;
+        const float r2s = __builtin_bit_cast(
+            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sh ? r2v[1] : r2v[0]), sl));
+        // no basis vector when the unit residual is at most tau (or the row is zero)
+        const bool skip = !(r2s > a.tau2 && mn[s] > 0.0f);
+        const float r = skip ? 0.0f : sqrtf(r2s);
+        const float rinv = skip ? 0.0f : 1.0f / r;
+        if (lane == 0) {
+          pslot[np] = s;
+          prr[np] = r;
+          pgain[np] = forced ? mp[s] : key_score(best);
+        }
+        const float* us_row = U + s * us;
+        const int k4 = np & ~3;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int m = lane + 64 * h;
+          if (m < pn) {
+            float c;
+            if (m == s) {
+              c = r;
+              actv[h] = false;
+            } else {
+              const float* um = U + m * us;
+              float d0 = 0.0f, d1 = 0.0f;
+              for (int k = 0; k < k4; k += 4) {
+                const float4 x = *reinterpret_cast<const float4*>(us_row + k);
+                const float4 y = *reinterpret_cast<const float4*>(um + k);
+                d0 = fmaf(x.x, y.x, d0);
+                d1 = fmaf(x.y, y.y, d1);
+                d0 = fmaf(x.z, y.z, d0);
+                d1 = fmaf(x.w, y.w, d1);
+              }
+              for (int k = k4; k < np; ++k) d0 = fmaf(us_row[k], um[k], d0);
+              c = (Rm[s * rs + m] - (d0 + d1)) * rinv;
+              if (!skip) r2v[h] = r2v[h] - c * c;
+            }
+            U[m * us + np] = c;
+          }
+        }
+        ++t;
+        ++np;
+      }
+      if (lane == 0) misc[3] = np;
+    }
+    __syncthreads();
+    np = misc[3];
+    t = t0 + np;
+    if (w == 0)  // the selection order and gains of this round
+      for (int k = tid; k < np; k += NT) {
+        a.order[(long long)b * K + t0 + k] = midx[pslot[k]];
+        a.gain[(long long)b * K + t0 + k] = pgain[k];
+      }
+    if (forced) fq += np;
+    if (t >= K) break;
+
+    // ============================================================ update
+    // The round's new rows t0 .. t-1 on the own tokens:
+    //   W_k     = S[pick_k][i] - sum_{l<t0} c_{l,pick_k} c_{l,i}            (dense)
+    //   c_{k,i} = (W_k - sum_{k'<k} U[pick_k][k'] c_{k',i}) / r_k           (triangular)
+    for (int k = 0; k < np; ++k)
+      if (tid < cnt && midx[pslot[k]] == my_i) my_state = 2;
+    // W rows: S rows of the picks at the own tokens (rows by wave, tokens by lane)
+    for (int j0 = wave; j0 < np; j0 += 4 * (NT / 64)) {
+      float v[4][4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int j = j0 + 4 * u;
+        const long long base = (long long)midx[pslot[min(j, np - 1)]] * N + c0;
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const int c = lane + 64 * h;
+          v[u][h] = (j < np && c < cnt) ? S[base + c] : 0.0f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+          const int j = j0 + 4 * u, c = lane + 64 * h;
+          if (j < np && c < cnt) W[j * wsd + c] = v[u][h];
+        }
+    }
+    __syncthreads();
+    if (t0 > 0) {
+      // dense part: 4 picks x 4 own tokens per thread; own columns stream
+      // from global memory (next chunk prefetched), pick columns from LDS
+      const int nbj = (np + 3) >> 2, nbc = (cnt + 3) >> 2;
+      const int t4 = t0 & ~3;
+      for (int blk = tid; blk < nbj * nbc; blk += NT) {
+        const int bj = blk / nbc, bc = blk - bj * nbc;
+        float acc[4][4] = {};
+        const float* pj[4];
+        const float* oc[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          pj[x] = pcol + pslot[min(4 * bj + x, np - 1)] * cs;
+          oc[x] = Ct + (long long)(c0 + min(4 * bc + x, cnt - 1)) * Kp;
+        }
+        float4 xo[4], xn[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          xo[x] = t4 > 0 ? *reinterpret_cast<const float4*>(oc[x]) : make_float4(0.f, 0.f, 0.f, 0.f);
+          xn[x] = xo[x];
+        }
+        for (int l = 0; l < t4; l += 4) {
+          if (l + 4 < t4) {
+#pragma unroll
+            for (int x = 0; x < 4; ++x) xn[x] = *reinterpret_cast<const float4*>(oc[x] + l + 4);
+          }
+          float4 xj[4];
+#pragma unroll
+          for (int x = 0; x < 4; ++x) xj[x] = *reinterpret_cast<const float4*>(pj[x] + l);
+#pragma unroll
+          for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) {
+              acc[x][y] = fmaf(xj[x].x, xo[y].x, acc[x][y]);
+              acc[x][y] = fmaf(xj[x].y, xo[y].y, acc[x][y]);
+              acc[x][y] = fmaf(xj[x].z, xo[y].z, acc[x][y]);
+              acc[x][y] = fmaf(xj[x].w, xo[y].w, acc[x][y]);
+            }
+#pragma unroll
+          for (int x = 0; x < 4; ++x) xo[x] = xn[x];
+        }
+        for (int l = t4; l < t0; ++l)
+#pragma unroll
+          for (int x = 0; x < 4; ++x)
+#pragma unroll
+            for (int y = 0; y < 4; ++y) acc[x][y] = fmaf(pj[x][l], oc[y][l], acc[x][y]);
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+          for (int y = 0; y < 4; ++y) {
+            const int jj = 4 * bj + x, c = 4 * bc + y;
+            if (jj < np && c < cnt) W[jj * wsd + c] -= acc[x][y];
+          }
+      }
+      __syncthreads();
+    }
+    // triangular part in blocks of 8 rows: one thread per own token solves
+    // the block in registers, then every thread updates the later rows
+    constexpr int TB = 8;
+    for (int j0 = 0; j0 < np; j0 += TB) {
+      const int nb = min(TB, np - j0);
+      for (int c = tid; c < cnt; c += NT) {
+        float x[TB];
+#pragma unroll
+        for (int q = 0; q < TB; ++q) x[q] = q < nb ? W[(j0 + q) * wsd + c] : 0.0f;
+#pragma unroll
+        for (int q = 0; q < TB; ++q) {
+          if (q < nb) {
+            const float* lrow = U + pslot[j0 + q] * us + j0;  // coefficients on this block's rows
+            float v = x[q];
+#pragma unroll
+            for (int q2 = 0; q2 < TB; ++q2)
+              if (q2 < q) v = fmaf(-lrow[q2], x[q2], v);
+            const float rj = prr[j0 + q];
+            x[q] = rj > 0.0f ? v / rj : 0.0f;
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < TB; ++q)
+          if (q < nb) W[(j0 + q) * wsd + c] = x[q];
+      }
+      __syncthreads();
+      if (j0 + nb < np) {
+        for (int c = lane; c < cnt; c += 64) {
+          float x[TB];
+#pragma unroll
+          for (int q = 0; q < TB; ++q) x[q] = q < nb ? W[(j0 + q) * wsd + c] : 0.0f;
+          for (int j2 = j0 + nb + wave; j2 < np; j2 += NT / 64) {
+            const float* lrow = U + pslot[j2] * us + j0;
+            float v = W[j2 * wsd + c];
+#pragma unroll
+            for (int q = 0; q < TB; ++q)
+              if (q < nb) v = fmaf(-lrow[q], x[q], v);
+            W[j2 * wsd + c] = v;
+          }
+        }
+        __syncthreads();
+      }
+    }
+    // new rows to global memory (token-major) and the own r2
+    {
+      const int total = np * cnt;
+      for (int e = tid; e < total; e += NT) {
+        const int c = e / np, jj = e - c * np;
+        Ct[(long long)(c0 + c) * Kp + t0 + jj] = W[jj * wsd + c];
+      }
+    }
+    const bool live = tid < cnt && my_state != 2;
+    if (live)
+      for (int jj = 0; jj < np; ++jj) {
+        const float c = W[jj * wsd + tid];
+        my_r2 = my_r2 - c * c;
+      }
+    if (live) __hip_atomic_store(r2g + my_i, my_r2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // keys of the own tokens: each wave extracts the top kPub + 1 of its
+    // tokens, then wave 0 extracts the top kPub + 1 of those
+    {
+      uint64_t k = (tid < cnt && my_state == 0) ? make_key(my_r2, my_qn, my_p, my_i, a.tau2) : 0ull;
+      for (int q = 0; q <= kPub; ++q) {
+        const uint64_t best = wave_max_key(k);
+        if (lane == 0) bndk[wave * (kPub + 1) + q] = best;
+        if (k == best) k = 0ull;
+      }
+      __syncthreads();
+      if (wave == 0) {
+        uint64_t k2 = lane < (NT / 64) * (kPub + 1) ? bndk[lane] : 0ull;
+        uint64_t* pub = a.pub + ((long long)b * 2 + (round & 1)) * G * (kPub + 1) + w * (kPub + 1);
+        for (int q = 0; q <= kPub; ++q) {
+          const uint64_t best = wave_max_key(k2);
+          if (lane == 0) __hip_atomic_store(pub + q, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (k2 == best) k2 = 0ull;
+        }
+      }
+    }
+    ++round;
+    image_barrier(a.bar + b, static_cast<unsigned>(round * G), a.err, misc);
+    if (misc[0]) break;
+  }
+}
+
+// ------------------------------------------------------------------ restore
+// One block per image: the K kept indices in ascending order (rank by count;
+// indices are distinct).
+__global__ __launch_bounds__(NT) void restore_kernel(const SelectArgs a) {
+  extern __shared__ int ord[];
+  const int b = blockIdx.x, K = a.K;
+  for (int i = threadIdx.x; i < K; i += NT) {
+    const int v = a.order[(long long)b * K + i];
+    ord[i] = (v >= 0 && v < a.N) ? v : 0;  // only an aborted selection leaves other values
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < K; i += NT) {
+    const int v = ord[i];
+    int rank = 0;
+    for (int j = 0; j < K; ++j) rank += ord[j] < v;
+    a.idx_out[(long long)b * K + rank] = v;
+  }
+}
+
+struct DeviceInfo {
+  int cus = 0;
+};
+
+DeviceInfo& device_info() {
+  static DeviceInfo info[64];
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  DeviceInfo& d = info[dev & 63];
+  if (d.cus == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess) d.cus = prop.multiProcessorCount;
+  }
+  return d;
+}
+
+}  // namespace
+
+hipError_t launch_topk(const SelectArgs& a, hipStream_t s) {
+  TimedLaunch tl("topk", s);
+  const size_t shm = (size_t)pow2_at_least(a.N) * 8;
+  if (shm > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(topk_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(shm));
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(topk_kernel, dim3(a.B), dim3(kTopkThreads), shm, s, a);
+  return hipGetLastError();
+}
+
+// Picks the tokens per workgroup (hence workgroups per image) and the pool
+// capacity within the LDS budget, then runs the images in as few cooperative
+// launches as the co-residency limit allows.
+hipError_t launch_select(SelectArgs& a, hipStream_t s) {
+  const int K = a.K, N = a.N;
+  constexpr int kMaxLds = 160 * 1024;
+  const int cus = device_info().cus > 0 ? device_info().cus : 1;
+  int chosen_ch = 0, chosen_pcap = 0, chosen_G = 0, chosen_bytes = 0, per_cu = 0;
+  for (int ch : {64, 128, 256}) {
+    const int G = (N + ch - 1) / ch;
+    if (G > 128) continue;
+    int pcap = kMaxPool;
+    while (pcap > 8 && lds_layout(K, G, ch, pcap).bytes > kMaxLds) pcap -= 8;
+    const int bytes = lds_layout(K, G, ch, pcap).bytes;
+    if (bytes > kMaxLds) continue;
+    if (bytes > 65536) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+      if (e != hipSuccess) return e;
+    }
+    int pc = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&pc, select_kernel, NT, bytes);
+    if (e != hipSuccess) return e;
+    if (pc <= 0) continue;
+    chosen_ch = ch;
+    chosen_pcap = pcap;
+    chosen_G = G;
+    chosen_bytes = bytes;
+    per_cu = pc;
+    if ((long long)a.B * G <= (long long)pc * cus) break;  // every image at once
+  }
+  if (per_cu <= 0) return hipErrorInvalidConfiguration;
+  a.ch = chosen_ch;
+  a.G = chosen_G;
+  a.pcap = chosen_pcap;
+  const int per_launch = static_cast<int>(((long long)per_cu * cus) / chosen_G);
+  if (per_launch < 1) return hipErrorInvalidConfiguration;
+  for (int b0 = 0; b0 < a.B; b0 += per_launch) {
+    const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
+    int b_begin = b0;
+    void* params[] = {&a, &b_begin};
+    TimedLaunch tl("select", s);
+    hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(select_kernel), dim3(nb * chosen_G),
+                                              dim3(NT), params, static_cast<unsigned>(chosen_bytes), s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_restore(const SelectArgs& a, hipStream_t s) {
+  TimedLaunch tl("restore", s);
+  hipLaunchKernelGGL(restore_kernel, dim3(a.B), dim3(NT), sizeof(int) * a.K, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace mapk
