@@ -43,7 +43,7 @@ namespace {
 constexpr int NT = 256;
 constexpr int kTopkThreads = 1024;
 constexpr unsigned kSpinLimit = 1u << 22;
-constexpr int kMaxPool = 128;  // two pool members per lane of the picking wave
+constexpr int kMaxPool = 64;  // one pool member per lane of the picking wave
 
 __device__ __forceinline__ uint32_t ordered_bits(float f) {
   // non-negative finite floats order like their bits; everything else -> 0
@@ -230,26 +230,30 @@ __host__ __device__ inline int col_stride(int K) { return ((K + 31) & ~31) + 4; 
 
 struct Lds {
   // byte offsets into the dynamic LDS block
-  int midx, mp, mn, mqn, mr2, pslot, pr, pgain, pcol, U, RW, merge, bnd, misc;
+  int midx, mp, mn, mqn, mr2, mkey, pslot, pr, pgain, pcol, U, RW, merge, bnd, misc;
   int bytes;
   int cs, us, rs, ws;
 };
 
 // RW holds the pool's residual Gram matrix during the picks and the own
 // tokens' new rows (W) during the update; the two never live together.
+// mr2 and mkey are double-buffered by pick parity.
 __host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap) {
   Lds L;
   int o = 0;
   auto take = [&](int bytes) { const int r = o; o += (bytes + 15) & ~15; return r; };
   L.cs = col_stride(K);
-  L.us = pcap + 4 + ((pcap / 4) % 2 == 0 ? 4 : 0);  // 4 times an odd number
+  // U rows hold kMaxPool entries whatever the pool capacity, so the pick
+  // loop's fixed-length dot never leaves its row; 4 times an odd number
+  L.us = kMaxPool + 4 + (((kMaxPool + 4) / 4) % 2 == 0 ? 4 : 0);
   L.rs = pcap + 1;
   L.ws = ch + 4;
   L.midx = take(4 * pcap);
   L.mp = take(4 * pcap);
   L.mn = take(4 * pcap);
   L.mqn = take(4 * pcap);
-  L.mr2 = take(4 * pcap);
+  L.mr2 = take(2 * 4 * pcap);
+  L.mkey = take(2 * 8 * pcap);
   L.pslot = take(4 * pcap);
   L.pr = take(4 * pcap);
   L.pgain = take(4 * pcap);
@@ -296,7 +300,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   float* mp = reinterpret_cast<float*>(lds + L.mp);
   float* mn = reinterpret_cast<float*>(lds + L.mn);
   float* mqn = reinterpret_cast<float*>(lds + L.mqn);
-  float* mr2 = reinterpret_cast<float*>(lds + L.mr2);
+  float* mr2 = reinterpret_cast<float*>(lds + L.mr2);     // [2][pcap]
+  uint64_t* mkey = reinterpret_cast<uint64_t*>(lds + L.mkey);  // [2][pcap]
   int* pslot = reinterpret_cast<int*>(lds + L.pslot);
   float* prr = reinterpret_cast<float*>(lds + L.pr);
   float* pgain = reinterpret_cast<float*>(lds + L.pgain);
@@ -377,26 +382,35 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       uint64_t beta0 = bndk[0];
       for (int q = 1; q < NT / 64; ++q) beta0 = bndk[q] > beta0 ? bndk[q] : beta0;
       uint64_t nextk = 0;  // the largest key left out of the pool by the cap
-      for (int e = tid; e < nk; e += NT) {
-        const uint64_t x = merge[e];
-        if (x <= beta0) continue;
-        int rank = e & 7;
-        const int own_list = e >> 3;
-        for (int ww = 0; ww < G; ++ww) {
-          if (ww == own_list) continue;
-          const uint64_t* lst = merge + 8 * ww;  // descending
-          int c = lst[3] > x ? 4 : 0;
-          c += lst[c + 1] > x ? 2 : 0;
-          c += lst[c] > x ? 1 : 0;
-          c += (c == 7 && lst[7] > x) ? 1 : 0;
-          rank += c;
+      // rank of each key above beta0 = number of published keys above it;
+      // the lists are read in 16-byte pieces that every lane of a wave shares
+      for (int e0 = 0; e0 < nk; e0 += 2 * NT) {
+        uint64_t x[2];
+        int rk[2] = {0, 0};
+#pragma unroll
+        for (int h = 0; h < 2; ++h) x[h] = (e0 + tid + h * NT < nk) ? merge[e0 + tid + h * NT] : 0ull;
+        const bool any = (x[0] > beta0) || (x[1] > beta0);
+        if (__ballot(any) != 0ull) {
+          for (int e = 0; e < nk; e += 8) {
+            const uint64_t* lst = merge + e;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              const uint64_t y = lst[q];
+              rk[0] += y > x[0];
+              rk[1] += y > x[1];
+            }
+          }
         }
-        if (rank < pcap) {
-          const int i = key_index(x);
-          midx[rank] = (i >= 0 && i < N) ? i : 0;
-          atomicAdd(&misc[2], 1);
-        } else if (rank == pcap) {
-          nextk = x;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          if (x[h] <= beta0) continue;
+          if (rk[h] < pcap) {
+            const int i = key_index(x[h]);
+            midx[rk[h]] = (i >= 0 && i < N) ? i : 0;
+            atomicAdd(&misc[2], 1);
+          } else if (rk[h] == pcap) {
+            nextk = x[h];
+          }
         }
       }
       nextk = wave_max_key(nextk);
@@ -450,44 +464,57 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           }
       }
     }
-    // Rm = S among the members (gathered): rows by wave, columns by lane
-    for (int m1 = wave; m1 < pn; m1 += 4 * (NT / 64)) {
-      float v[4][2];
-      long long base[4];
+    // Rm = S among the members (gathered): rows m1 = wave + 4 q, columns
+    // m2 = lane (+64); all loads of a thread issued before the first store
+    {
+      constexpr int QMAX = kMaxPool / 4;
+      float v[QMAX][2];
+      int col[2];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) base[u] = (long long)midx[min(m1 + 4 * u, pn - 1)] * N;
+      for (int h = 0; h < 2; ++h) col[h] = midx[min(lane + 64 * h, pn - 1)];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int m2 = lane + 64 * h;
-          v[u][h] = (m1 + 4 * u < pn && m2 < pn) ? S[base[u] + midx[m2]] : 0.0f;
-        }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int q = 0; q < QMAX; ++q) {
+        const int m1 = wave + 4 * q;
+        const long long base = (long long)midx[min(m1, pn - 1)] * N;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int m2 = lane + 64 * h;
-          if (m1 + 4 * u < pn && m2 < pn) Rm[(m1 + 4 * u) * rs + m2] = v[u][h];
+          v[q][h] = (m1 < pn && m2 < pn) ? S[base + col[h]] : 0.0f;
         }
+      }
+#pragma unroll
+      for (int q = 0; q < QMAX; ++q) {
+        const int m1 = wave + 4 * q;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int m2 = lane + 64 * h;
+          if (m1 < pn && m2 < pn) Rm[m1 * rs + m2] = v[q][h];
+        }
+      }
     }
     __syncthreads();
-    // Rm -= P P^T over the t rows so far.  Thread (bi, bj) owns rows
-    // bi + 16 x and columns bj + 16 y: the 16 lanes that share bj read 16
-    // consecutive rows (distinct bank groups) and the rest is broadcast.
+    // this round's coefficients start at zero, so the pick loop needs no masks
+    for (int e = tid; e < pn * (us / 4); e += NT)
+      reinterpret_cast<float4*>(U)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    // Rm -= P P^T over the t rows so far.  With R = ceil(pn / 4), tile
+    // (bi, bj), bi <= bj, covers rows bi + R x and columns bj + R y; lanes
+    // with consecutive tiles read consecutive rows (distinct bank groups) or
+    // share a row (broadcast).  Off-diagonal tiles also write the mirror.
     if (t > 0) {
+      const int R = (pn + 3) >> 2;
+      const int ntile = R * (R + 1) / 2;
       const int t4 = t & ~3;
-      const int nbb = (pn + 63) >> 6;  // 64 x 64 super-blocks per side
-      for (int sb = 0; sb < nbb * nbb; ++sb) {
-        const int sr = (sb / nbb) * 64, sc = (sb % nbb) * 64;
-        const int bi = lane & 15, bj = (lane >> 4) + 4 * wave;
+      for (int e = tid; e < ntile; e += NT) {
+        int bi = 0, rem = e;
+        while (rem >= R - bi) { rem -= R - bi; ++bi; }
+        const int bj = bi + rem;
         float acc[4][4] = {};
         const float* pa[4];
         const float* pb[4];
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
-          pa[x] = pcol + min(sr + bi + 16 * x, pn - 1) * cs;
-          pb[x] = pcol + min(sc + bj + 16 * x, pn - 1) * cs;
+          pa[x] = pcol + min(bi + R * x, pn - 1) * cs;
+          pb[x] = pcol + min(bj + R * x, pn - 1) * cs;
         }
         for (int l = 0; l < t4; l += 4) {
           float4 xa[4], xb[4];
@@ -515,58 +542,49 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         for (int x = 0; x < 4; ++x)
 #pragma unroll
           for (int y = 0; y < 4; ++y) {
-            const int m1 = sr + bi + 16 * x, m2 = sc + bj + 16 * y;
-            if (m1 < pn && m2 < pn) Rm[m1 * rs + m2] -= acc[x][y];
+            const int m1 = bi + R * x, m2 = bj + R * y;
+            if (m1 < pn && m2 < pn) {
+              Rm[m1 * rs + m2] -= acc[x][y];
+              if (bi != bj) Rm[m2 * rs + m1] -= acc[x][y];
+            }
           }
       }
     }
     __syncthreads();
 
     // ============================================================ picks
-    // Wave 0 alone, without barriers.  Lane m holds members m and m + 64
-    // (r^2, active flag and key in registers).  For the k-th pick s,
-    //   c_m = (Rm[s][m] - sum_{k'<k} U[s][k'] U[m][k']) / r_s
-    // where U[m][k'] is member m's coefficient on the k'-th basis vector of
-    // this round; each lane writes only its own rows of U, and reads the
-    // pick's row, which the same wave wrote in earlier steps.
+    // Wave 0 alone, without barriers; lane m holds pool member m (r^2, key
+    // inputs, active flag in registers).  For the k-th pick s,
+    //   c_m = (Rm[s][m] - sum_{k'<k} U[s][k'] U[m][k']) / r_s,
+    // U[m][k'] being member m's coefficient on the k'-th basis vector of
+    // this round.  Each step issues all its LDS reads (Rm[s][m], row s of U
+    // and the lane's own row of U, whose entries past the live ones are
+    // zero) before using them, so a pick costs about one LDS round trip.
     const int t0 = t;
-    int np = 0;
     if (wave == 0) {
-      float r2v[2];
-      bool actv[2];
-      uint64_t kk[2] = {0ull, 0ull};
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int m = lane + 64 * h;
-        r2v[h] = m < pn ? mr2[m] : 0.0f;
-        actv[h] = m < pn;
-      }
+      int np = 0;
+      const bool in = lane < pn;
+      float r2v = in ? mr2[lane] : 0.0f;
+      const float qnv = in ? mqn[lane] : 0.0f, pv = in ? mp[lane] : 0.0f;
+      const int iv = in ? midx[lane] : 0;
+      bool actv = in;
+      const float* u0 = U + min(lane, pcap - 1) * us;
       while (t < K) {
         int s;
         uint64_t best = 0;
         if (forced) {
           s = np < pn ? np : -1;
         } else {
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int m = lane + 64 * h;
-            kk[h] = actv[h] ? make_key(r2v[h], mqn[m], mp[m], midx[m], a.tau2) : 0ull;
-          }
-          const uint64_t kl = kk[0] > kk[1] ? kk[0] : kk[1];
+          const uint64_t kl = actv ? make_key(r2v, qnv, pv, iv, a.tau2) : 0ull;
           best = wave_max_key(kl);
-          s = -1;
-          if (best > beta) {  // keys are distinct: exactly one member holds `best`
-            const int l = static_cast<int>(__builtin_ctzll(__ballot(kl == best)));
-            const int second = __builtin_amdgcn_readlane(kk[0] == best ? 0 : 1, l);
-            s = l + 64 * second;
-          }
+          // keys are distinct: exactly one member holds `best`
+          s = best > beta ? static_cast<int>(__builtin_ctzll(__ballot(kl == best))) : -1;
         }
         if (s < 0) break;
-        const int sl = s & 63, sh = s >> 6;
-        const float r2s = __builtin_bit_cast(
-            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sh ? r2v[1] : r2v[0]), sl));
+        const float r2s = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, r2v), s));
+        const float ns = mn[s];
         // no basis vector when the unit residual is at most tau (or the row is zero)
-        const bool skip = !(r2s > a.tau2 && mn[s] > 0.0f);
+        const bool skip = !(r2s > a.tau2 && ns > 0.0f);
         const float r = skip ? 0.0f : sqrtf(r2s);
         const float rinv = skip ? 0.0f : 1.0f / r;
         if (lane == 0) {
@@ -574,33 +592,32 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           prr[np] = r;
           pgain[np] = forced ? mp[s] : key_score(best);
         }
-        const float* us_row = U + s * us;
-        const int k4 = np & ~3;
+        const float rm = Rm[s * rs + min(lane, pn - 1)];
+        const float* usr = U + s * us;
+        float4 xs[kMaxPool / 4], y0[kMaxPool / 4];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int m = lane + 64 * h;
-          if (m < pn) {
-            float c;
-            if (m == s) {
-              c = r;
-              actv[h] = false;
-            } else {
-              const float* um = U + m * us;
-              float d0 = 0.0f, d1 = 0.0f;
-              for (int k = 0; k < k4; k += 4) {
-                const float4 x = *reinterpret_cast<const float4*>(us_row + k);
-                const float4 y = *reinterpret_cast<const float4*>(um + k);
-                d0 = fmaf(x.x, y.x, d0);
-                d1 = fmaf(x.y, y.y, d1);
-                d0 = fmaf(x.z, y.z, d0);
-                d1 = fmaf(x.w, y.w, d1);
-              }
-              for (int k = k4; k < np; ++k) d0 = fmaf(us_row[k], um[k], d0);
-              c = (Rm[s * rs + m] - (d0 + d1)) * rinv;
-              if (!skip) r2v[h] = r2v[h] - c * c;
-            }
-            U[m * us + np] = c;
+        for (int q = 0; q < kMaxPool / 4; ++q) {
+          xs[q] = *reinterpret_cast<const float4*>(usr + 4 * q);
+          y0[q] = *reinterpret_cast<const float4*>(u0 + 4 * q);
+        }
+        float d = 0.0f;
+#pragma unroll
+        for (int q = 0; q < kMaxPool / 4; ++q) {
+          d = fmaf(xs[q].x, y0[q].x, d);
+          d = fmaf(xs[q].y, y0[q].y, d);
+          d = fmaf(xs[q].z, y0[q].z, d);
+          d = fmaf(xs[q].w, y0[q].w, d);
+        }
+        if (in) {
+          float c;
+          if (lane == s) {
+            c = r;
+            actv = false;
+          } else {
+            c = (rm - d) * rinv;
+            if (!skip) r2v = r2v - c * c;
           }
+          U[lane * us + np] = c;
         }
         ++t;
         ++np;
@@ -608,7 +625,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       if (lane == 0) misc[3] = np;
     }
     __syncthreads();
-    np = misc[3];
+    const int np = misc[3];
     t = t0 + np;
     if (w == 0)  // the selection order and gains of this round
       for (int k = tid; k < np; k += NT) {
@@ -624,26 +641,24 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     //   c_{k,i} = (W_k - sum_{k'<k} U[pick_k][k'] c_{k',i}) / r_k           (triangular)
     for (int k = 0; k < np; ++k)
       if (tid < cnt && midx[pslot[k]] == my_i) my_state = 2;
-    // W rows: S rows of the picks at the own tokens (rows by wave, tokens by lane)
-    for (int j0 = wave; j0 < np; j0 += 4 * (NT / 64)) {
-      float v[4][4];
+    // W rows: S rows of the picks at the own tokens; row j = wave + 4 u,
+    // token c = lane + 64 h; up to 32 loads in flight per thread
+    {
+      const int nh = (cnt + 63) >> 6;
+      for (int h = 0; h < nh; ++h) {
+        const int c = lane + 64 * h;
+        float v[kMaxPool / 4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int j = j0 + 4 * u;
-        const long long base = (long long)midx[pslot[min(j, np - 1)]] * N + c0;
+        for (int u = 0; u < kMaxPool / 4; ++u) {
+          const int j = wave + 4 * u;
+          v[u] = (j < np && c < cnt) ? S[(long long)midx[pslot[j]] * N + c0 + c] : 0.0f;
+        }
 #pragma unroll
-        for (int h = 0; h < 4; ++h) {
-          const int c = lane + 64 * h;
-          v[u][h] = (j < np && c < cnt) ? S[base + c] : 0.0f;
+        for (int u = 0; u < kMaxPool / 4; ++u) {
+          const int j = wave + 4 * u;
+          if (j < np && c < cnt) W[j * wsd + c] = v[u];
         }
       }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int h = 0; h < 4; ++h) {
-          const int j = j0 + 4 * u, c = lane + 64 * h;
-          if (j < np && c < cnt) W[j * wsd + c] = v[u][h];
-        }
     }
     __syncthreads();
     if (t0 > 0) {
@@ -707,21 +722,27 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     constexpr int TB = 8;
     for (int j0 = 0; j0 < np; j0 += TB) {
       const int nb = min(TB, np - j0);
+      float lblk[TB][TB];  // lblk[q][q2] = coefficient of pick j0+q on row t0+j0+q2
+      float rblk[TB];
+#pragma unroll
+      for (int q = 0; q < TB; ++q) {
+        const float* lr = U + pslot[min(j0 + q, np - 1)] * us + j0;
+        const float4 a0 = *reinterpret_cast<const float4*>(lr);
+        const float4 a1 = *reinterpret_cast<const float4*>(lr + 4);
+        lblk[q][0] = a0.x; lblk[q][1] = a0.y; lblk[q][2] = a0.z; lblk[q][3] = a0.w;
+        lblk[q][4] = a1.x; lblk[q][5] = a1.y; lblk[q][6] = a1.z; lblk[q][7] = a1.w;
+        rblk[q] = prr[min(j0 + q, np - 1)];
+      }
       for (int c = tid; c < cnt; c += NT) {
         float x[TB];
 #pragma unroll
         for (int q = 0; q < TB; ++q) x[q] = q < nb ? W[(j0 + q) * wsd + c] : 0.0f;
 #pragma unroll
         for (int q = 0; q < TB; ++q) {
-          if (q < nb) {
-            const float* lrow = U + pslot[j0 + q] * us + j0;  // coefficients on this block's rows
-            float v = x[q];
+          float v = x[q];
 #pragma unroll
-            for (int q2 = 0; q2 < TB; ++q2)
-              if (q2 < q) v = fmaf(-lrow[q2], x[q2], v);
-            const float rj = prr[j0 + q];
-            x[q] = rj > 0.0f ? v / rj : 0.0f;
-          }
+          for (int q2 = 0; q2 < q; ++q2) v = fmaf(-lblk[q][q2], x[q2], v);
+          x[q] = (q < nb && rblk[q] > 0.0f) ? v / rblk[q] : 0.0f;
         }
 #pragma unroll
         for (int q = 0; q < TB; ++q)
@@ -733,13 +754,27 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           float x[TB];
 #pragma unroll
           for (int q = 0; q < TB; ++q) x[q] = q < nb ? W[(j0 + q) * wsd + c] : 0.0f;
-          for (int j2 = j0 + nb + wave; j2 < np; j2 += NT / 64) {
-            const float* lrow = U + pslot[j2] * us + j0;
-            float v = W[j2 * wsd + c];
+          for (int j2 = j0 + nb + wave; j2 < np; j2 += 4 * (NT / 64)) {
+            float4 l0[4], l1[4];
+            float v[4];
 #pragma unroll
-            for (int q = 0; q < TB; ++q)
-              if (q < nb) v = fmaf(-lrow[q], x[q], v);
-            W[j2 * wsd + c] = v;
+            for (int u = 0; u < 4; ++u) {
+              const int jr = min(j2 + (NT / 64) * u, np - 1);
+              const float* lr = U + pslot[jr] * us + j0;
+              l0[u] = *reinterpret_cast<const float4*>(lr);
+              l1[u] = *reinterpret_cast<const float4*>(lr + 4);
+              v[u] = W[jr * wsd + c];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const float lq[TB] = {l0[u].x, l0[u].y, l0[u].z, l0[u].w, l1[u].x, l1[u].y, l1[u].z, l1[u].w};
+#pragma unroll
+              for (int q = 0; q < TB; ++q)
+                if (q < nb) v[u] = fmaf(-lq[q], x[q], v[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              if (j2 + (NT / 64) * u < np) W[(j2 + (NT / 64) * u) * wsd + c] = v[u];
           }
         }
         __syncthreads();
