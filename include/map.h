@@ -38,6 +38,12 @@
  *   MAP_ERR_HIP means the HIP runtime rejected a launch (the stream may then
  *   hold part of the work).  No exception crosses this interface.
  * Determinism.  Identical inputs give bitwise identical outputs.
+ * Residency.  The selection runs as one persistent launch per group of
+ *   images whose workgroups must all be resident at once (they meet at
+ *   device-wide barriers).  The library sizes each launch to fit the device;
+ *   if other work kept them off the device past a bounded wait (seconds),
+ *   the selection stops and every idx_out entry of the call is -1 (map_prune
+ *   then writes pos_out = -1 and zero rows).  The kernels never hang.
  * Limits.  1 <= B <= MAP_MAX_BATCH, 1 <= N <= MAP_MAX_N,
  *   1 <= K <= min(N, MAP_MAX_K), 0 <= K0 <= K, D % 8 == 0, D_h % 8 == 0,
  *   d_p a multiple of 4 and <= 128, 1 <= question length <= 8192.

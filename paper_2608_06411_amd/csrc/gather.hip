@@ -19,10 +19,10 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
   const int nrows = min(kRows, a.K - k0);
   if (threadIdx.x < nrows) {
     const int k = k0 + threadIdx.x;
-    int i = a.idx[(long long)b * a.K + k];
-    i = (i >= 0 && i < a.N) ? i : 0;
-    rows[threadIdx.x] = i;
-    a.pos_out[(long long)b * a.K + k] = a.pos_v[(long long)b * a.N + i];
+    const int i = a.idx[(long long)b * a.K + k];
+    const bool ok = i >= 0 && i < a.N;  // -1 marks an aborted selection
+    rows[threadIdx.x] = ok ? i : -1;
+    a.pos_out[(long long)b * a.K + k] = ok ? a.pos_v[(long long)b * a.N + i] : -1;
   }
   __syncthreads();
   const uint4* src = static_cast<const uint4*>(a.V) + (long long)b * a.N * chunks;
@@ -34,9 +34,10 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int e = e0 + u * 256;
+      v[u] = make_uint4(0u, 0u, 0u, 0u);
       if (e < total) {
         const int r = e / chunks, c = e - r * chunks;
-        v[u] = src[(long long)rows[r] * chunks + c];
+        if (rows[r] >= 0) v[u] = src[(long long)rows[r] * chunks + c];
       }
     }
 #pragma unroll
@@ -50,9 +51,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
 }  // namespace
 
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
-  TimedLaunch tl("gather", s);
-  hipLaunchKernelGGL(gather_kernel, dim3((a.K + kRows - 1) / kRows, a.B), dim3(256), 0, s, a);
-  return hipGetLastError();
+  return launch_kernel("gather", gather_kernel, dim3((a.K + kRows - 1) / kRows, a.B), dim3(256), 0, s, a);
 }
 
 }  // namespace mapk

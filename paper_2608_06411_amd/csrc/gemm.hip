@@ -293,12 +293,8 @@ void gemm_finalize(GemmBatch& g) {
 
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s) {
   if (g.total_tiles == 0) return hipSuccess;
-  TimedLaunch tl(name, s);
-  if (dt == MAP_BF16)
-    hipLaunchKernelGGL(gemm_kernel<bf16_t>, dim3(g.total_tiles), dim3(NT), 0, s, g);
-  else
-    hipLaunchKernelGGL(gemm_kernel<float>, dim3(g.total_tiles), dim3(NT), 0, s, g);
-  return hipGetLastError();
+  if (dt == MAP_BF16) return launch_kernel(name, gemm_kernel<bf16_t>, dim3(g.total_tiles), dim3(NT), 0, s, g);
+  return launch_kernel(name, gemm_kernel<float>, dim3(g.total_tiles), dim3(NT), 0, s, g);
 }
 
 }  // namespace mapk

@@ -2,9 +2,13 @@
 // libmap.  Nothing here is part of the public ABI (include/map.h).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
+
+#include <tuple>
+#include <utility>
 
 #include "map.h"
 
@@ -34,15 +38,32 @@ template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
 
-// ---------------------------------------------------------------- timing
-// Kernel launch bracketing for map_timing_* (no-op unless enabled).
-struct TimedLaunch {
-  TimedLaunch(const char* name, hipStream_t s);
-  ~TimedLaunch();
-  const char* name_;
-  hipStream_t s_;
-  int slot_;
+// ---------------------------------------------------------------- launch
+// Every kernel goes through launch_kernel.  While map_timing is enabled the
+// registry hands out a pair of events, which the runtime stamps with the
+// dispatch's own start and end (hipExtLaunchKernel); otherwise both are null
+// and the launch is a plain one.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
 };
+LaunchEvents timing_events(const char* name);
+
+template <typename Tuple, size_t... I>
+inline void kernel_argv(void** argv, Tuple& t, std::index_sequence<I...>) {
+  ((argv[I] = static_cast<void*>(&std::get<I>(t))), ...);
+}
+
+template <typename... P, typename... A>
+hipError_t launch_kernel(const char* name, void (*kernel)(P...), dim3 grid, dim3 block, size_t lds_bytes,
+                         hipStream_t s, A... args) {
+  static_assert(sizeof...(P) == sizeof...(A), "kernel argument count");
+  std::tuple<P...> vals{args...};
+  void* argv[sizeof...(P)];
+  kernel_argv(argv, vals, std::index_sequence_for<P...>{});
+  const LaunchEvents ev = timing_events(name);
+  return hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, argv, lds_bytes, s, ev.start,
+                            ev.stop, 0);
+}
 
 // ---------------------------------------------------------------- GEMM
 // C = epilogue(A * B^T): A [M][K] and B [N][K] row-major (K contiguous),

@@ -317,22 +317,17 @@ hipEvent_t take_event(TimingState& t) {
 
 namespace mapk {
 
-TimedLaunch::TimedLaunch(const char* name, hipStream_t s) : name_(name), s_(s), slot_(-1) {
+LaunchEvents timing_events(const char* name) {
   TimingState& t = timing();
   std::lock_guard<std::mutex> g(t.mu);
-  if (!t.enabled) return;
+  LaunchEvents ev;
+  if (!t.enabled) return ev;
   TimingRecord r{name, take_event(t), take_event(t)};
-  if (!r.start || !r.stop) return;
-  (void)hipEventRecord(r.start, s);
+  if (!r.start || !r.stop) return ev;
   t.pending.push_back(r);
-  slot_ = static_cast<int>(t.pending.size()) - 1;
-}
-
-TimedLaunch::~TimedLaunch() {
-  if (slot_ < 0) return;
-  TimingState& t = timing();
-  std::lock_guard<std::mutex> g(t.mu);
-  if (slot_ < static_cast<int>(t.pending.size())) (void)hipEventRecord(t.pending[slot_].stop, s_);
+  ev.start = r.start;
+  ev.stop = r.stop;
+  return ev;
 }
 
 }  // namespace mapk

@@ -63,12 +63,8 @@ hipError_t launch_prep(map_dtype dt, const PrepArgs& a, bool norms, bool table, 
   const long long entries = table ? (long long)(a.rowsV + a.rowsT) * a.half : 0;
   const int tb = static_cast<int>((entries + 255) / 256);
   if (nb + tb == 0) return hipSuccess;
-  TimedLaunch tl("prep", s);
-  if (dt == MAP_BF16)
-    hipLaunchKernelGGL(prep_kernel<bf16_t>, dim3(nb + tb), dim3(256), 0, s, a, nb);
-  else
-    hipLaunchKernelGGL(prep_kernel<float>, dim3(nb + tb), dim3(256), 0, s, a, nb);
-  return hipGetLastError();
+  if (dt == MAP_BF16) return launch_kernel("prep", prep_kernel<bf16_t>, dim3(nb + tb), dim3(256), 0, s, a, nb);
+  return launch_kernel("prep", prep_kernel<float>, dim3(nb + tb), dim3(256), 0, s, a, nb);
 }
 
 }  // namespace mapk

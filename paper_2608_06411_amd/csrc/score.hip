@@ -172,15 +172,9 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
   int maxM = 0;
   for (int b = 0; b < a.B; ++b) maxM = a.t_off[b + 1] - a.t_off[b] > maxM ? a.t_off[b + 1] - a.t_off[b] : maxM;
   const dim3 grid(a.nblk, a.B);
-  {
-    TimedLaunch tl("logits", s);
-    hipLaunchKernelGGL(logits_kernel, grid, dim3(256), 0, s, a);
-  }
-  hipError_t e = hipGetLastError();
+  const hipError_t e = launch_kernel("logits", logits_kernel, grid, dim3(256), 0, s, a);
   if (e != hipSuccess) return e;
-  TimedLaunch tl("softmax_mean", s);
-  hipLaunchKernelGGL(softmax_mean_kernel, grid, dim3(256), sizeof(float2) * maxM, s, a);
-  return hipGetLastError();
+  return launch_kernel("softmax_mean", softmax_mean_kernel, grid, dim3(256), sizeof(float2) * maxM, s, a);
 }
 
 }  // namespace mapk

@@ -823,14 +823,16 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
 
 // ------------------------------------------------------------------ restore
 // One block per image: the K kept indices in ascending order (rank by count;
-// indices are distinct).
+// indices are distinct).  After an aborted selection (error flag set) every
+// index is -1.
 __global__ __launch_bounds__(NT) void restore_kernel(const SelectArgs a) {
   extern __shared__ int ord[];
   const int b = blockIdx.x, K = a.K;
-  for (int i = threadIdx.x; i < K; i += NT) {
-    const int v = a.order[(long long)b * K + i];
-    ord[i] = (v >= 0 && v < a.N) ? v : 0;  // only an aborted selection leaves other values
+  if (__hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+    for (int i = threadIdx.x; i < K; i += NT) a.idx_out[(long long)b * K + i] = -1;
+    return;
   }
+  for (int i = threadIdx.x; i < K; i += NT) ord[i] = a.order[(long long)b * K + i];
   __syncthreads();
   for (int i = threadIdx.x; i < K; i += NT) {
     const int v = ord[i];
@@ -859,20 +861,21 @@ DeviceInfo& device_info() {
 }  // namespace
 
 hipError_t launch_topk(const SelectArgs& a, hipStream_t s) {
-  TimedLaunch tl("topk", s);
   const size_t shm = (size_t)pow2_at_least(a.N) * 8;
   if (shm > 65536) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(topk_kernel),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(shm));
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(topk_kernel, dim3(a.B), dim3(kTopkThreads), shm, s, a);
-  return hipGetLastError();
+  return launch_kernel("topk", topk_kernel, dim3(a.B), dim3(kTopkThreads), shm, s, a);
 }
 
 // Picks the tokens per workgroup (hence workgroups per image) and the pool
-// capacity within the LDS budget, then runs the images in as few cooperative
-// launches as the co-residency limit allows.
+// capacity within the LDS budget, then runs the images in as few launches as
+// keep every launch's workgroups resident at once (the occupancy check
+// below).  The image barriers rely on that residency; if other work on the
+// device ever held them off for longer than their bounded wait, the launch
+// ends early with the error flag set and restore_kernel reports -1 indices.
 hipError_t launch_select(SelectArgs& a, hipStream_t s) {
   const int K = a.K, N = a.N;
   constexpr int kMaxLds = 160 * 1024;
@@ -909,20 +912,15 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
   if (per_launch < 1) return hipErrorInvalidConfiguration;
   for (int b0 = 0; b0 < a.B; b0 += per_launch) {
     const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
-    int b_begin = b0;
-    void* params[] = {&a, &b_begin};
-    TimedLaunch tl("select", s);
-    hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(select_kernel), dim3(nb * chosen_G),
-                                              dim3(NT), params, static_cast<unsigned>(chosen_bytes), s);
+    const hipError_t e = launch_kernel("select", select_kernel, dim3(nb * chosen_G), dim3(NT),
+                                       static_cast<size_t>(chosen_bytes), s, a, b0);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
 hipError_t launch_restore(const SelectArgs& a, hipStream_t s) {
-  TimedLaunch tl("restore", s);
-  hipLaunchKernelGGL(restore_kernel, dim3(a.B), dim3(NT), sizeof(int) * a.K, s, a);
-  return hipGetLastError();
+  return launch_kernel("restore", restore_kernel, dim3(a.B), dim3(NT), sizeof(int) * a.K, s, a);
 }
 
 }  // namespace mapk
