@@ -9,7 +9,7 @@
 // so the score p_i ||v_i - B B^T v_i|| is p_i n_i r_i.  A pick whose r_i is
 // at most tau adds no basis vector (its row of C is zero).
 //
-// One cooperative launch runs the whole selection of every image.  An image
+// One persistent launch runs the whole selection of every image.  An image
 // is served by G workgroups; workgroup w owns `ch` consecutive tokens (their
 // r^2 and their columns of C, kept token-major in global memory).  Work
 // proceeds in rounds separated by one barrier across the image's workgroups:
@@ -24,8 +24,9 @@
 //            Scores never increase as the basis grows, so a pool key above
 //            beta is the true argmax over all candidates: the picks are
 //            exactly those of the step-by-step rule.  The pool keeps its
-//            residual Gram matrix Rm = S - C^T C in LDS, so a pick costs one
-//            rank-one update and one workgroup barrier.
+//            residual Gram matrix Rm = S - C^T C in LDS; one wave makes the
+//            round's picks, each a wave-wide argmax and one dot product per
+//            member against this round's coefficients, with no barrier.
 //   update   Every workgroup applies the round's new basis rows to its own
 //            tokens (a dense product over the rows of earlier rounds, then a
 //            right-looking triangular solve over this round's rows), updates
