@@ -112,27 +112,17 @@ __device__ __forceinline__ void mma_slice<float>(const uint4 (*As)[8], const uin
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 __device__ __forceinline__ int acc_col(int lane) { return lane & 31; }
 
-template <typename T>
-__global__ __launch_bounds__(NT) void gemm_kernel(const GemmBatch args) {
-  // One contiguous 64 KiB block: A slices in [0, 2), B slices in [2, 4); the
-  // RoPE epilogue reuses all of it as a 128 x 128 float tile.
-  __shared__ uint4 smem[4][BM][8];
-  uint4 (*As)[BM][8] = smem;
-  uint4 (*Bs)[BM][8] = smem + 2;
-  constexpr int VEC = Slice<T>::VEC;
-  constexpr int BK = Slice<T>::BK;
-
+// Workgroup -> (problem, batch item, tile row, tile column).
+__device__ __forceinline__ void decode_tile(const GemmBatch& args, int& pi, int& bt, int& tm, int& tn) {
   const int tile = xcd_remap(blockIdx.x, args.total_tiles);
-  int pi = 0;
+  pi = 0;
 #pragma unroll
   for (int q = 1; q < kMaxGemmProblems; ++q)
     if (q < args.count && tile >= args.p[q].tile_begin) pi = q;
   const GemmProblem& P = args.p[pi];
-
   const int local = tile - P.tile_begin;
-  const int bt = local / P.tiles_per_batch;
+  bt = local / P.tiles_per_batch;
   int tt = local - bt * P.tiles_per_batch;
-  int tm, tn;
   if (P.triangular) {  // upper triangle, row by row: row tm holds tiles_n - tm tiles
     tm = 0;
     while (tt >= P.tiles_n - tm) { tt -= P.tiles_n - tm; ++tm; }
@@ -141,59 +131,16 @@ __global__ __launch_bounds__(NT) void gemm_kernel(const GemmBatch args) {
     tm = tt / P.tiles_n;
     tn = tt - tm * P.tiles_n;
   }
-  const int M = P.M, N = P.N, K = P.K;
-  const T* __restrict__ A = static_cast<const T*>(P.A) + bt * P.strideA;
-  const T* __restrict__ B = static_cast<const T*>(P.B) + bt * P.strideB;
+}
+
+// Epilogues on the 128 x 128 accumulator tile.  The RoPE epilogue stages
+// the tile through LDS: rows 0..63 in tile_lo, rows 64..127 in tile_hi
+// (64 x 128 floats each).
+template <typename T>
+__device__ __forceinline__ void epilogue(const GemmProblem& P, int bt, int tm, int tn, f32x16_t (&acc)[2][2],
+                                         float* tile_lo, float* tile_hi, int tid, int lane, int wm, int wn) {
+  const int M = P.M, N = P.N;
   const int m0 = tm * BM, n0 = tn * BN;
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int lv = tid & 7;          // 16-byte chunk this thread moves
-  const int lrow = tid >> 3;       // first row this thread moves (then +32, +64, +96)
-
-  uint4 ra[4], rb[4];
-  auto fetch = [&](int k0) {
-    const int gk = k0 + lv * VEC;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = lrow + 32 * j;
-      const int gm = m0 + r, gn = n0 + r;
-      ra[j] = (gm < M && gk < K) ? *reinterpret_cast<const uint4*>(A + (long long)gm * P.lda + gk)
-                                 : make_uint4(0, 0, 0, 0);
-      rb[j] = (gn < N && gk < K) ? *reinterpret_cast<const uint4*>(B + (long long)gn * P.ldb + gk)
-                                 : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto stash = [&](int buf) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = lrow + 32 * j;
-      As[buf][r][lv ^ (r & 7)] = ra[j];
-      Bs[buf][r][lv ^ (r & 7)] = rb[j];
-    }
-  };
-
-  f32x16_t acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  const int nk = (K + BK - 1) / BK;
-  fetch(0);
-  stash(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const bool more = kt + 1 < nk;
-    if (more) fetch((kt + 1) * BK);
-    mma_slice<T>(As[kt & 1], Bs[kt & 1], wm, wn, lane, acc);
-    if (more) stash((kt + 1) & 1);
-    __syncthreads();
-  }
-
-  // ------------------------------------------------------------ epilogues
   if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS) {
     T* __restrict__ C = static_cast<T*>(P.C) + bt * P.strideC;
     const T* __restrict__ bias = static_cast<const T*>(P.bias);
@@ -250,7 +197,6 @@ __global__ __launch_bounds__(NT) void gemm_kernel(const GemmBatch args) {
         }
     }
   } else {  // EPI_ROPE: stage the tile in LDS so each thread sees both halves of a pair
-    float* tileF = reinterpret_cast<float*>(&smem[0][0][0]);  // 128 x 128 floats = 64 KiB
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -259,21 +205,357 @@ __global__ __launch_bounds__(NT) void gemm_kernel(const GemmBatch args) {
         for (int r = 0; r < 16; ++r) {
           const int rl = wm * 64 + i * 32 + acc_row(r, lane);
           const int cl = wn * 64 + j * 32 + acc_col(lane);
-          tileF[rl * BN + cl] = acc[i][j][r];
+          (rl < 64 ? tile_lo : tile_hi)[(rl & 63) * BN + cl] = acc[i][j][r];
         }
     __syncthreads();
     float* __restrict__ out = static_cast<float*>(P.C) + bt * P.strideC;
     const int half = N >> 1;
+    if ((half & 3) == 0 && (P.ldc & 3) == 0) {
+      // four pairs per item; each thread issues all its cos/sin loads first
+      const int q4 = half >> 2, items = BM * q4;
+      for (int e0 = tid; e0 < items; e0 += 8 * NT) {
+        float4 cs[8][2];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int e = e0 + u * NT, rl = e / q4, c = 4 * (e - rl * q4);
+          const bool ok = e < items && m0 + rl < M;
+          const float4* src = reinterpret_cast<const float4*>(P.rope_cs + (long long)(ok ? m0 + rl : 0) * half + c);
+          cs[u][0] = ok ? src[0] : make_float4(0.f, 0.f, 0.f, 0.f);
+          cs[u][1] = ok ? src[1] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int e = e0 + u * NT, rl = e / q4, c = 4 * (e - rl * q4);
+          const int row = m0 + rl;
+          if (e >= items || row >= M) continue;
+          const float* tr = (rl < 64 ? tile_lo : tile_hi) + (rl & 63) * BN;
+          const float4 a = *reinterpret_cast<const float4*>(tr + c);
+          const float4 b = *reinterpret_cast<const float4*>(tr + c + half);
+          const float4 c0 = cs[u][0], c1 = cs[u][1];  // (cos, sin) of pairs c, c+1 | c+2, c+3
+          float* o = out + (long long)row * P.ldc + c;
+          *reinterpret_cast<float4*>(o) = make_float4(a.x * c0.x - b.x * c0.y, a.y * c0.z - b.y * c0.w,
+                                                      a.z * c1.x - b.z * c1.y, a.w * c1.z - b.w * c1.w);
+          *reinterpret_cast<float4*>(o + half) = make_float4(b.x * c0.x + a.x * c0.y, b.y * c0.z + a.y * c0.w,
+                                                             b.z * c1.x + a.z * c1.y, b.w * c1.z + a.w * c1.w);
+        }
+      }
+      return;
+    }
     for (int e = tid; e < BM * half; e += NT) {
       const int rl = e / half, c = e - rl * half;
       const int row = m0 + rl;
       if (row >= M) continue;
-      const float a = tileF[rl * BN + c], b = tileF[rl * BN + c + half];
+      const float* tr = (rl < 64 ? tile_lo : tile_hi) + (rl & 63) * BN;
+      const float a = tr[c], b = tr[c + half];
       const float2 cs = P.rope_cs[(long long)row * half + c];
       out[(long long)row * P.ldc + c] = a * cs.x - b * cs.y;
       out[(long long)row * P.ldc + c + half] = b * cs.x + a * cs.y;
     }
   }
+}
+
+template <typename T>
+__global__ __launch_bounds__(NT) void gemm_kernel(const GemmBatch args) {
+  // One contiguous 64 KiB block: A slices in [0, 2), B slices in [2, 4); the
+  // RoPE epilogue reuses all of it as a 128 x 128 float tile.
+  __shared__ uint4 smem[4][BM][8];
+  uint4 (*As)[BM][8] = smem;
+  uint4 (*Bs)[BM][8] = smem + 2;
+  constexpr int VEC = Slice<T>::VEC;
+  constexpr int BK = Slice<T>::BK;
+
+  int pi, bt, tm, tn;
+  decode_tile(args, pi, bt, tm, tn);
+  const GemmProblem& P = args.p[pi];
+  const int M = P.M, N = P.N, K = P.K;
+  const T* __restrict__ A = static_cast<const T*>(P.A) + bt * P.strideA;
+  const T* __restrict__ B = static_cast<const T*>(P.B) + bt * P.strideB;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lv = tid & 7;          // 16-byte chunk this thread moves
+  const int lrow = tid >> 3;       // first row this thread moves (then +32, +64, +96)
+
+  uint4 ra[4], rb[4];
+  auto fetch = [&](int k0) {
+    const int gk = k0 + lv * VEC;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = lrow + 32 * j;
+      const int gm = m0 + r, gn = n0 + r;
+      ra[j] = (gm < M && gk < K) ? *reinterpret_cast<const uint4*>(A + (long long)gm * P.lda + gk)
+                                 : make_uint4(0, 0, 0, 0);
+      rb[j] = (gn < N && gk < K) ? *reinterpret_cast<const uint4*>(B + (long long)gn * P.ldb + gk)
+                                 : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = lrow + 32 * j;
+      As[buf][r][lv ^ (r & 7)] = ra[j];
+      Bs[buf][r][lv ^ (r & 7)] = rb[j];
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = (K + BK - 1) / BK;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const bool more = kt + 1 < nk;
+    if (more) fetch((kt + 1) * BK);
+    mma_slice<T>(As[kt & 1], Bs[kt & 1], wm, wn, lane, acc);
+    if (more) stash((kt + 1) & 1);
+    __syncthreads();
+  }
+
+  __syncthreads();  // the RoPE epilogue reuses the LDS tiles
+  epilogue<T>(P, bt, tm, tn, acc, reinterpret_cast<float*>(&smem[0][0][0]),
+              reinterpret_cast<float*>(&smem[2][0][0]), tid, lane, wm, wn);
+}
+
+// Staged epilogues of the direct-load kernel.  After the main loop the four
+// 32 KiB stage arrays are free; the finished tile goes through them so that
+// every global store moves 16 bytes per lane along a row.
+//   q0, q1: the tile in row-major order (rows 0..63 in q0, 64..127 in q1),
+//           128 floats per row;
+//   t0, t1: the tile transposed (tile columns 0..63 in t0, 64..127 in t1),
+//           one tile column per 128-float row whose 16-byte chunks are
+//           XOR-swizzled by the column (chunk r/4 at position r/4 ^ (c & 31)),
+//           so both the staging writes and the row reads avoid bank conflicts.
+struct StagedTile {
+  float* q0;
+  float* q1;
+  float* t0;
+  float* t1;
+  __device__ float* row(int r) const { return (r < 64 ? q0 : q1) + (r & 63) * BN; }
+  // chunk holding tile entries (4 ch .. 4 ch + 3, c), i.e. rows 4 ch .. of column c
+  __device__ float* col_chunk(int c, int ch) const { return (c < 64 ? t0 : t1) + (c & 63) * BM + 4 * (ch ^ (c & 31)); }
+};
+
+// Bias (+ GELU) in float32, bf16 output.
+__device__ __forceinline__ void epi_bias_staged(const GemmProblem& P, int bt, int m0, int n0,
+                                                f32x16_t (&acc)[2][2], const StagedTile& L, int tid,
+                                                int lane, int wm, int wn) {
+  const int M = P.M, N = P.N;
+  const bf16_t* __restrict__ bias = static_cast<const bf16_t*>(P.bias);
+  const bool gelu = P.epi == EPI_BIAS_GELU;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int cl = wn * 64 + j * 32 + acc_col(lane);
+    const float bv = n0 + cl < N ? bf16_to_f32(bias[n0 + cl]) : 0.0f;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = acc[i][j][r] + bv;
+        if (gelu) v = gelu_erf(v);
+        L.row(wm * 64 + i * 32 + acc_row(r, lane))[cl] = v;
+      }
+  }
+  __syncthreads();
+  bf16_t* __restrict__ C = static_cast<bf16_t*>(P.C) + bt * P.strideC;
+  const bool vec = (P.ldc & 7) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
+#pragma unroll 2
+  for (int e = tid; e < BM * (BN / 8); e += NT) {  // 8 columns per item
+    const int r = e >> 4, c8 = (e & 15) * 8;
+    const int row = m0 + r, col = n0 + c8;
+    if (row >= M || col >= N) continue;
+    const float4 x = *reinterpret_cast<const float4*>(L.row(r) + c8);
+    const float4 y = *reinterpret_cast<const float4*>(L.row(r) + c8 + 4);
+    const float f[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+    bf16_t* dst = C + (long long)row * P.ldc + col;
+    if (vec && col + 8 <= N) {
+      uint4 o;
+      o.x = f32_to_bf16(f[0]) | (static_cast<uint32_t>(f32_to_bf16(f[1])) << 16);
+      o.y = f32_to_bf16(f[2]) | (static_cast<uint32_t>(f32_to_bf16(f[3])) << 16);
+      o.z = f32_to_bf16(f[4]) | (static_cast<uint32_t>(f32_to_bf16(f[5])) << 16);
+      o.w = f32_to_bf16(f[6]) | (static_cast<uint32_t>(f32_to_bf16(f[7])) << 16);
+      *reinterpret_cast<uint4*>(dst) = o;
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (col + k < N) dst[k] = f32_to_bf16(f[k]);
+    }
+  }
+}
+
+// Cosine: S[row][col] = acc * rs[row] * rs[col] (float32), written to both
+// (row, col) and (col, row) from the same float, so S is bitwise symmetric.
+// A diagonal tile takes the entries below its diagonal from the transposed
+// copy (the mirror of the entries above it).
+__device__ __forceinline__ void epi_cosine_staged(const GemmProblem& P, int bt, int tm, int tn,
+                                                  f32x16_t (&acc)[2][2], const StagedTile& L,
+                                                  const float* rs_rows, const float* rs_cols, int tid,
+                                                  int lane, int wm, int wn) {
+  const int M = P.M, N = P.N, m0 = tm * BM, n0 = tn * BN;
+  const bool diag = tm == tn;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int cl = wn * 64 + j * 32 + acc_col(lane);
+    const float sc = rs_cols[cl];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int rl0 = wm * 64 + i * 32 + 8 * q + 4 * (lane >> 5);
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] = acc[i][j][4 * q + e] * (rs_rows[rl0 + e] * sc);
+          L.row(rl0 + e)[cl] = v[e];
+        }
+        *reinterpret_cast<float4*>(L.col_chunk(cl, rl0 >> 2)) = make_float4(v[0], v[1], v[2], v[3]);
+      }
+  }
+  __syncthreads();
+  float* __restrict__ S = static_cast<float*>(P.C) + bt * P.strideC;
+  const bool vec = (P.ldc & 3) == 0;
+  // S[m0 + r][n0 + 4 ch ..]: row r of the tile (the mirror below a diagonal tile's diagonal)
+  for (int e = tid; e < BM * (BN / 4); e += NT) {
+    const int r = e >> 5, ch = e & 31;
+    const int row = m0 + r, col = n0 + 4 * ch;
+    if (row >= M || col >= N) continue;
+    float4 x = *reinterpret_cast<const float4*>(L.row(r) + 4 * ch);
+    if (diag) {  // entry (r, c) with c < r is tile entry (c, r): rows 4 ch .. of column r
+      const float4 t = *reinterpret_cast<const float4*>(L.col_chunk(r, ch));
+      if (4 * ch + 0 < r) x.x = t.x;
+      if (4 * ch + 1 < r) x.y = t.y;
+      if (4 * ch + 2 < r) x.z = t.z;
+      if (4 * ch + 3 < r) x.w = t.w;
+    }
+    float* dst = S + (long long)row * P.ldc + col;
+    if (vec && col + 4 <= N) {
+      *reinterpret_cast<float4*>(dst) = x;
+    } else {
+      const float f[4] = {x.x, x.y, x.z, x.w};
+      for (int k = 0; k < 4 && col + k < N; ++k) dst[k] = f[k];
+    }
+  }
+  if (diag) return;
+  // S[n0 + c][m0 + 4 ch ..]: column c of the tile
+  for (int e = tid; e < BN * (BM / 4); e += NT) {
+    const int c = e >> 5, ch = e & 31;
+    const int row = n0 + c, col = m0 + 4 * ch;
+    if (row >= N || col >= M) continue;
+    const float4 x = *reinterpret_cast<const float4*>(L.col_chunk(c, ch));
+    float* dst = S + (long long)row * P.ldc + col;
+    if (vec && col + 4 <= M) {
+      *reinterpret_cast<float4*>(dst) = x;
+    } else {
+      const float f[4] = {x.x, x.y, x.z, x.w};
+      for (int k = 0; k < 4 && col + k < M; ++k) dst[k] = f[k];
+    }
+  }
+}
+
+// bf16 variant with a four-stage LDS ring filled by direct global->LDS loads
+// (global_load_lds_dwordx4): three K slices are in flight while the matrix
+// cores consume the fourth, with no register staging.  Each wave moves 32
+// rows of A and 32 rows of B per slice, one instruction per 8 rows: lane l
+// lands at row 8j + l/8, chunk position l%8 of its instruction's 1 KiB, and
+// fetches the chunk the XOR swizzle puts there.  The stages are separate LDS
+// arrays addressed with compile-time stage numbers, so the only waits on
+// those loads are the explicit counted ones before each barrier.
+// Requirements (checked by the host): K % 256 == 0, lda and ldb multiples of
+// 8, A and B 16-byte aligned.
+constexpr int kStages = 4;
+
+__device__ __forceinline__ void wait_vm_lgkm0(int outstanding) {
+  // s_waitcnt encoding: vmcnt in bits [3:0] and [15:14], expcnt [6:4]
+  // (7 = no wait), lgkmcnt [11:8]; here vmcnt = outstanding (0, 8 or 16)
+  // and lgkmcnt = 0
+  if (outstanding >= 16) __builtin_amdgcn_s_waitcnt(0x4070);
+  else if (outstanding >= 8) __builtin_amdgcn_s_waitcnt(0x0078);
+  else __builtin_amdgcn_s_waitcnt(0x0070);
+}
+
+__global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
+  __shared__ uint4 st0[2][BM][8], st1[2][BM][8], st2[2][BM][8], st3[2][BM][8];  // 4 x 32 KiB
+  __shared__ float rs_tile[BM + BN];  // cosine epilogue: reciprocal norms of the tile's rows, columns
+  int pi, bt, tm, tn;
+  decode_tile(args, pi, bt, tm, tn);
+  const GemmProblem& P = args.p[pi];
+  const int M = P.M, N = P.N;
+  const bf16_t* __restrict__ A = static_cast<const bf16_t*>(P.A) + bt * P.strideA;
+  const bf16_t* __restrict__ B = static_cast<const bf16_t*>(P.B) + bt * P.strideB;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int nk = P.K / 64;
+  if (P.epi == EPI_COSINE) {  // read before the loop, visible after its barriers
+    const float* rs = P.rs + (long long)bt * M;
+    const int k = tid < BM ? m0 + tid : n0 + tid - BM;
+    rs_tile[tid] = k < (tid < BM ? M : N) ? rs[k] : 0.0f;
+  }
+
+  // Per-lane global row pointers of this wave's 4 A rows and 4 B rows
+  // (rows past the matrix read its last row; they are never stored).
+  const int v = (lane & 7) ^ (lane >> 3);
+  const bf16_t* ga[4];
+  const bf16_t* gb[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = 32 * wave + 8 * j + (lane >> 3);
+    ga[j] = A + (long long)min(m0 + r, M - 1) * P.lda + 8 * v;
+    gb[j] = B + (long long)min(n0 + r, N - 1) * P.ldb + 8 * v;
+  }
+  auto issue = [&](uint4 (*dst)[BM][8], int kt) {
+    const int k0 = kt * 64;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      __builtin_amdgcn_global_load_lds(ga[j] + k0, &dst[0][32 * wave + 8 * j][0], 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(gb[j] + k0, &dst[1][32 * wave + 8 * j][0], 16, 0, 0);
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  // A step waits for its slice (this wave's loads, then every wave's at the
+  // barrier), refills the stage every wave finished reading in the previous
+  // step with the slice three ahead, and runs the matrix cores on its stage.
+  // nk is a multiple of 4, so the stage of every step is a compile-time
+  // constant and the code stays straight-line.
+  auto mma = [&](uint4 (*cur)[BM][8]) { mma_slice<bf16_t>(cur[0], cur[1], wm, wn, lane, acc); };
+  issue(st0, 0);
+  issue(st1, 1);
+  issue(st2, 2);
+  int kt = 0;
+  for (; kt + 4 < nk; kt += 4) {
+    wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st3, kt + 3); mma(st0);
+    wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st0, kt + 4); mma(st1);
+    wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st1, kt + 5); mma(st2);
+    wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st2, kt + 6); mma(st3);
+  }
+  wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st3, kt + 3); mma(st0);
+  wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); mma(st1);
+  wait_vm_lgkm0(8); __builtin_amdgcn_s_barrier(); mma(st2);
+  wait_vm_lgkm0(0); __builtin_amdgcn_s_barrier(); mma(st3);
+  __syncthreads();  // the epilogues reuse the stage arrays
+  const StagedTile L{reinterpret_cast<float*>(&st0[0][0][0]), reinterpret_cast<float*>(&st1[0][0][0]),
+                     reinterpret_cast<float*>(&st2[0][0][0]), reinterpret_cast<float*>(&st3[0][0][0])};
+  if (P.epi == EPI_COSINE)
+    epi_cosine_staged(P, bt, tm, tn, acc, L, rs_tile, rs_tile + BM, tid, lane, wm, wn);
+  else if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS)
+    epi_bias_staged(P, bt, m0, n0, acc, L, tid, lane, wm, wn);
+  else
+    epilogue<bf16_t>(P, bt, tm, tn, acc, L.q0, L.q1, tid, lane, wm, wn);
 }
 
 }  // namespace
@@ -293,7 +575,17 @@ void gemm_finalize(GemmBatch& g) {
 
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s) {
   if (g.total_tiles == 0) return hipSuccess;
-  if (dt == MAP_BF16) return launch_kernel(name, gemm_kernel<bf16_t>, dim3(g.total_tiles), dim3(NT), 0, s, g);
+  if (dt == MAP_BF16) {
+    bool dma = true;  // every problem meets the direct-load requirements
+    for (int i = 0; i < g.count; ++i) {
+      const GemmProblem& p = g.p[i];
+      dma = dma && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+            (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
+            p.strideA % 8 == 0 && p.strideB % 8 == 0;
+    }
+    if (dma) return launch_kernel(name, gemm_dma_kernel, dim3(g.total_tiles), dim3(NT), 0, s, g);
+    return launch_kernel(name, gemm_kernel<bf16_t>, dim3(g.total_tiles), dim3(NT), 0, s, g);
+  }
   return launch_kernel(name, gemm_kernel<float>, dim3(g.total_tiles), dim3(NT), 0, s, g);
 }
 
