@@ -45,6 +45,9 @@ constexpr int NT = 256;
 constexpr int kTopkThreads = 1024;
 constexpr unsigned kSpinLimit = 1u << 22;
 constexpr int kMaxPool = 64;  // one pool member per lane of the picking wave
+constexpr int kRing = 16;     // loaded rows the pipelined update buffers ahead
+
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 
 __device__ __forceinline__ uint32_t ordered_bits(float f) {
   // non-negative finite floats order like their bits; everything else -> 0
@@ -232,14 +235,15 @@ __host__ __device__ inline int col_stride(int K) { return ((K + 31) & ~31) + 4; 
 struct Lds {
   // byte offsets into the dynamic LDS block
   int midx, mp, mn, mqn, mr2, mkey, pslot, pr, pgain, pcol, U, RW, merge, bnd, misc;
+  int ownC, D, flags;  // pipelined update only
   int bytes;
-  int cs, us, rs, ws;
+  int cs, us, rs, ws, ocs;
 };
 
 // RW holds the pool's residual Gram matrix during the picks and the own
 // tokens' new rows (W) during the update; the two never live together.
 // mr2 and mkey are double-buffered by pick parity.
-__host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap) {
+__host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap, bool pipe) {
   Lds L;
   int o = 0;
   auto take = [&](int bytes) { const int r = o; o += (bytes + 15) & ~15; return r; };
@@ -258,13 +262,23 @@ __host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap) {
   L.pslot = take(4 * pcap);
   L.pr = take(4 * pcap);
   L.pgain = take(4 * pcap);
-  L.pcol = take(4 * pcap * L.cs);
+  // pipelined: after the round-start product the same space holds this
+  // round's coefficients of the own tokens [ch][us] and the ring of loaded
+  // rows [kRing][ws]
+  L.pcol = take(4 * (pipe ? max(pcap * L.cs, ch * L.us + kRing * L.ws) : pcap * L.cs));
   L.U = take(4 * pcap * L.us);
   const int rbytes = 4 * pcap * L.rs, wbytes = 4 * pcap * L.ws;
   L.RW = take(rbytes > wbytes ? rbytes : wbytes);
   L.merge = take(8 * G * kPub);
   L.bnd = take(8 * ((kPub + 1) * (NT / 64)));
   L.misc = take(64);
+  // pipelined update: the own tokens' coefficient rows of earlier rounds
+  // (token-major, stride 4 times an odd number), the earlier rounds' part of
+  // every pool member's row at the own tokens (D) and the stage counters
+  L.ocs = ((K + 3) & ~3) + 4 + ((((K + 3) & ~3) / 4 + 1) % 2 == 0 ? 4 : 0);
+  L.ownC = pipe ? take(4 * ch * L.ocs) : 0;
+  L.D = pipe ? take(4 * pcap * L.ws) : 0;
+  L.flags = pipe ? take(32) : 0;
   L.bytes = o;
   return L;
 }
@@ -290,13 +304,14 @@ __device__ void image_barrier(unsigned int* ctr, unsigned int target, int32_t* e
 
 // Global C is token-major: Ct[i][l] = c_{l,i}, rows of Kp floats (Kp = K
 // rounded up to 4), so one token's coefficients are contiguous.
+template <bool PIPE>
 __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_begin) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   const int G = a.G, ch = a.ch, pcap = a.pcap, K = a.K, K0 = a.K0, N = a.N;
   const int Kp = (K + 3) & ~3;
   const int b = b_begin + blockIdx.x / G, w = blockIdx.x % G;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const Lds L = lds_layout(K, G, ch, pcap);
+  const Lds L = lds_layout(K, G, ch, pcap, PIPE);
   int* midx = reinterpret_cast<int*>(lds + L.midx);
   float* mp = reinterpret_cast<float*>(lds + L.mp);
   float* mn = reinterpret_cast<float*>(lds + L.mn);
@@ -313,7 +328,15 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   uint64_t* merge = reinterpret_cast<uint64_t*>(lds + L.merge);
   uint64_t* bndk = reinterpret_cast<uint64_t*>(lds + L.bnd);
   int* misc = reinterpret_cast<int*>(lds + L.misc);
-  const int cs = L.cs, us = L.us, rs = L.rs, wsd = L.ws;
+  const int cs = L.cs, us = L.us, rs = L.rs, wsd = L.ws, ocs = L.ocs;
+  float* ownC = reinterpret_cast<float*>(lds + L.ownC);  // PIPE: [ch][ocs] own rows, earlier rounds
+  float* Dm = reinterpret_cast<float*>(lds + L.D);       // PIPE: [pcap][wsd] earlier rounds' part
+  float* crow = pcol;                                    // PIPE, picks: [ch][us] this round's own rows
+  float* ring = pcol + ch * us;                          // PIPE, picks: [kRing][wsd] loaded rows
+  int* npub = reinterpret_cast<int*>(lds + L.flags);     // PIPE: picks published this round
+  int* nload = npub + 1;                                 // rows loaded into the ring
+  int* ntri = npub + 2;                                  // rows finished
+  int* pdone = npub + 3;                                 // round tag once the picks are over
 
   const float* p = a.p + (long long)b * N;
   const float* nrm = a.norms + (long long)b * N;
@@ -341,6 +364,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     int* flag = reinterpret_cast<int*>(W);
     for (int i = tid; i < ch; i += NT) flag[i] = 0;
     if (tid == 0) misc[0] = 0;  // abort flag
+    if (PIPE && tid < 4) npub[tid] = 0;
     __syncthreads();
     for (int j = tid; j < K0; j += NT) {
       const int r = R0[j];
@@ -497,11 +521,71 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     // this round's coefficients start at zero, so the pick loop needs no masks
     for (int e = tid; e < pn * (us / 4); e += NT)
       reinterpret_cast<float4*>(U)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (PIPE && tid < 3) npub[tid] = 0;  // npub, nload, ntri
+    if (PIPE && t > 0 && pn > 0) {
+      // One float32 matrix-core product over the t rows so far, the pool's
+      // columns against the pool's columns and the own tokens' rows:
+      //   Rm[m][j] -= sum_l c_{l,m} c_{l,j}   (pool member j)
+      //   D[m][i]   = sum_l c_{l,m} c_{l,i}   (own token i)
+      // Wave w computes rows 32 (w >> 1) .. and columns 64 (w & 1) .. of the
+      // 64 x 128 result as two 32 x 32 tiles; in a step of eight rows l the
+      // lanes of half h supply rows l0 + 4 h .. l0 + 4 h + 3.
+      const int tr = wave >> 1, jh = wave & 1, r = lane & 31, h = lane >> 5;
+      const float* arow = pcol + min(32 * tr + r, pn - 1) * cs;
+      const float* brow[2];
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = 64 * jh + 32 * jj + r;
+        brow[jj] = j < 64 ? pcol + min(j, pn - 1) * cs : ownC + min(j - 64, cnt - 1) * ocs;
+      }
+      f32x16_t acc[2];
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[jj][e] = 0.0f;
+      for (int l0 = 0; l0 < t; l0 += 8) {
+        const int lb = l0 + 4 * h;
+        float4 a = *reinterpret_cast<const float4*>(arow + lb);
+        float4 bv[2];
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) bv[jj] = *reinterpret_cast<const float4*>(brow[jj] + lb);
+        if (lb + 4 > t) {  // rows at or past t hold stale values: zero both operands
+          const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (lb >= t) { a = z; bv[0] = z; bv[1] = z; }
+          else {
+            if (lb + 1 >= t) { a.y = 0.f; bv[0].y = 0.f; bv[1].y = 0.f; }
+            if (lb + 2 >= t) { a.z = 0.f; bv[0].z = 0.f; bv[1].z = 0.f; }
+            a.w = 0.f; bv[0].w = 0.f; bv[1].w = 0.f;
+          }
+        }
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj) {
+          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.x, bv[jj].x, acc[jj], 0, 0, 0);
+          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.y, bv[jj].y, acc[jj], 0, 0, 0);
+          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.z, bv[jj].z, acc[jj], 0, 0, 0);
+          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.w, bv[jj].w, acc[jj], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = 32 * tr + 8 * (e >> 2) + 4 * h + (e & 3);
+          const int j = 64 * jh + 32 * jj + r;
+          if (m < pn) {
+            if (j < 64) {
+              if (j < pn) Rm[m * rs + j] -= acc[jj][e];
+            } else {
+              Dm[m * wsd + j - 64] = acc[jj][e];
+            }
+          }
+        }
+    }
     // Rm -= P P^T over the t rows so far.  With R = ceil(pn / 4), tile
     // (bi, bj), bi <= bj, covers rows bi + R x and columns bj + R y; lanes
     // with consecutive tiles read consecutive rows (distinct bank groups) or
     // share a row (broadcast).  Off-diagonal tiles also write the mirror.
-    if (t > 0) {
+    if (!PIPE && t > 0) {
       const int R = (pn + 3) >> 2;
       const int ntile = R * (R + 1) / 2;
       const int t4 = t & ~3;
@@ -552,6 +636,11 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
     }
     __syncthreads();
+    if (PIPE) {  // this round's own rows start at zero: the finishing dot needs no masks
+      for (int e = tid; e < ch * (us / 4); e += NT)
+        reinterpret_cast<float4*>(crow)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+      __syncthreads();
+    }
 
     // ============================================================ picks
     // Wave 0 alone, without barriers; lane m holds pool member m (r^2, key
@@ -620,10 +709,86 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           }
           U[lane * us + np] = c;
         }
+        if (PIPE) __hip_atomic_store(npub, np + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         ++t;
         ++np;
       }
       if (lane == 0) misc[3] = np;
+      if (PIPE) __hip_atomic_store(pdone, round + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    } else if (PIPE && wave != 2) {
+      // The own tokens are brought up to date while wave 0 picks (lane i
+      // serves own token i), in pick order:
+      //   wave 3  loads W_k[i] = S[pick_k][i] - D[pick_k][i] (the earlier
+      //           rounds' part came from the round-start product) for every
+      //           published pick, many rows in flight, into a ring of kRing;
+      //   wave 1  finishes c_{k,i} = (W_k[i] - sum_{k'<k} U[pick_k][k'] c_{k',i}) / r_k.
+      // Each stage publishes how many rows it has handled; the loader stays
+      // less than kRing rows ahead of the finisher.  A stage stops once the
+      // picks are over and it has handled every one of them, or when this
+      // round completes the selection (its update is then never used).
+      const int rtag = round + 1;
+      int k = 0;
+      while (true) {
+        bool over = false;
+        int n = 0;
+        while (true) {
+          if (__hip_atomic_load(pdone, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == rtag) {
+            const int fin = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            over = fin <= k || t0 + fin >= K;
+          }
+          if (over) break;
+          if (wave == 3) {
+            const int avail = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            const int room = __hip_atomic_load(ntri, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) + kRing;
+            n = min(min(avail, room) - k, kRing);
+          } else {
+            n = __hip_atomic_load(nload, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) - k;
+          }
+          if (n > 0) break;
+          __builtin_amdgcn_s_sleep(1);
+        }
+        if (over) break;
+        if (wave == 3) {
+          float v[kRing];
+          const int col = c0 + min(lane, cnt - 1);
+#pragma unroll
+          for (int u = 0; u < kRing; ++u)  // unconditional loads of valid rows
+            v[u] = S[(long long)midx[pslot[k + min(u, n - 1)]] * N + col];
+#pragma unroll
+          for (int u = 0; u < kRing; ++u)
+            if (u < n) {
+              const float dv = t0 > 0 ? Dm[pslot[k + u] * wsd + lane] : 0.0f;
+              ring[((k + u) & (kRing - 1)) * wsd + lane] = v[u] - dv;
+            }
+          k += n;
+          __hip_atomic_store(nload, k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        } else {
+          const float* ur = U + pslot[k] * us;
+          float* cr = crow + lane * us;  // zero past the finished rows
+          const float rk = prr[k];
+          const float w0 = ring[(k & (kRing - 1)) * wsd + lane];
+          float e4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int g = 0; g < kMaxPool / 16; ++g) {
+            if (16 * g >= k) break;
+            float4 u4[4], c4[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              u4[j] = *reinterpret_cast<const float4*>(ur + 16 * g + 4 * j);
+              c4[j] = *reinterpret_cast<const float4*>(cr + 16 * g + 4 * j);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              e4[0] = fmaf(u4[j].x, c4[j].x, e4[0]); e4[1] = fmaf(u4[j].y, c4[j].y, e4[1]);
+              e4[2] = fmaf(u4[j].z, c4[j].z, e4[2]); e4[3] = fmaf(u4[j].w, c4[j].w, e4[3]);
+            }
+          }
+          const float v = w0 - ((e4[0] + e4[1]) + (e4[2] + e4[3]));
+          cr[k] = rk > 0.0f ? v / rk : 0.0f;
+          ++k;
+          __hip_atomic_store(ntri, k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+      }
     }
     __syncthreads();
     const int np = misc[3];
@@ -642,6 +807,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     //   c_{k,i} = (W_k - sum_{k'<k} U[pick_k][k'] c_{k',i}) / r_k           (triangular)
     for (int k = 0; k < np; ++k)
       if (tid < cnt && midx[pslot[k]] == my_i) my_state = 2;
+    if (!PIPE) {
     // W rows: S rows of the picks at the own tokens; row j = wave + 4 u,
     // token c = lane + 64 h; up to 32 loads in flight per thread
     {
@@ -781,18 +947,22 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         __syncthreads();
       }
     }
-    // new rows to global memory (token-major) and the own r2
+    }  // !PIPE
+    // new rows to global memory (token-major), to the own rows in LDS when
+    // pipelined, and the own r2
     {
       const int total = np * cnt;
       for (int e = tid; e < total; e += NT) {
         const int c = e / np, jj = e - c * np;
-        Ct[(long long)(c0 + c) * Kp + t0 + jj] = W[jj * wsd + c];
+        const float v = PIPE ? crow[c * us + jj] : W[jj * wsd + c];
+        if (PIPE) ownC[c * ocs + t0 + jj] = v;
+        Ct[(long long)(c0 + c) * Kp + t0 + jj] = v;
       }
     }
     const bool live = tid < cnt && my_state != 2;
     if (live)
       for (int jj = 0; jj < np; ++jj) {
-        const float c = W[jj * wsd + tid];
+        const float c = PIPE ? crow[tid * us + jj] : W[jj * wsd + tid];
         my_r2 = my_r2 - c * c;
       }
     if (live) __hip_atomic_store(r2g + my_i, my_r2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -880,28 +1050,39 @@ hipError_t launch_topk(const SelectArgs& a, hipStream_t s) {
 hipError_t launch_select(SelectArgs& a, hipStream_t s) {
   const int K = a.K, N = a.N;
   constexpr int kMaxLds = 160 * 1024;
+  constexpr int kMinPipePool = 48;  // below this the pipelined variant loses more to extra rounds
   const int cus = device_info().cus > 0 ? device_info().cus : 1;
   int chosen_ch = 0, chosen_pcap = 0, chosen_G = 0, chosen_bytes = 0, per_cu = 0;
+  bool chosen_pipe = false;
   for (int ch : {64, 128, 256}) {
     const int G = (N + ch - 1) / ch;
     if (G > 128) continue;
+    bool pipe = ch == 64;
     int pcap = kMaxPool;
-    while (pcap > 8 && lds_layout(K, G, ch, pcap).bytes > kMaxLds) pcap -= 8;
-    const int bytes = lds_layout(K, G, ch, pcap).bytes;
+    while (pcap > 8 && lds_layout(K, G, ch, pcap, pipe).bytes > kMaxLds) pcap -= 8;
+    if (pipe && pcap < kMinPipePool) {
+      pipe = false;
+      pcap = kMaxPool;
+      while (pcap > 8 && lds_layout(K, G, ch, pcap, false).bytes > kMaxLds) pcap -= 8;
+    }
+    const int bytes = lds_layout(K, G, ch, pcap, pipe).bytes;
     if (bytes > kMaxLds) continue;
+    const void* fn = pipe ? reinterpret_cast<const void*>(select_kernel<true>)
+                          : reinterpret_cast<const void*>(select_kernel<false>);
     if (bytes > 65536) {
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+      hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
       if (e != hipSuccess) return e;
     }
     int pc = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&pc, select_kernel, NT, bytes);
+    hipError_t e = pipe ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&pc, select_kernel<true>, NT, bytes)
+                        : hipOccupancyMaxActiveBlocksPerMultiprocessor(&pc, select_kernel<false>, NT, bytes);
     if (e != hipSuccess) return e;
     if (pc <= 0) continue;
     chosen_ch = ch;
     chosen_pcap = pcap;
     chosen_G = G;
     chosen_bytes = bytes;
+    chosen_pipe = pipe;
     per_cu = pc;
     if ((long long)a.B * G <= (long long)pc * cus) break;  // every image at once
   }
@@ -913,8 +1094,11 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
   if (per_launch < 1) return hipErrorInvalidConfiguration;
   for (int b0 = 0; b0 < a.B; b0 += per_launch) {
     const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
-    const hipError_t e = launch_kernel("select", select_kernel, dim3(nb * chosen_G), dim3(NT),
-                                       static_cast<size_t>(chosen_bytes), s, a, b0);
+    const hipError_t e =
+        chosen_pipe ? launch_kernel("select", select_kernel<true>, dim3(nb * chosen_G), dim3(NT),
+                                    static_cast<size_t>(chosen_bytes), s, a, b0)
+                    : launch_kernel("select", select_kernel<false>, dim3(nb * chosen_G), dim3(NT),
+                                    static_cast<size_t>(chosen_bytes), s, a, b0);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
