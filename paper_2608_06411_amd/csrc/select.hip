@@ -57,7 +57,7 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
 __device__ __forceinline__ uint64_t make_key(float r2, float qn, float p, int i, float tau2) {
   uint32_t hi = ordered_bits(p);
   if (r2 > tau2 && qn > 0.0f) {
-    const float s = qn * sqrtf(r2);
+    const float s = qn * __builtin_amdgcn_sqrtf(r2);  // hardware square root (1 ulp)
     if (s > 0.0f) hi = 0x80000000u | ordered_bits(s);
   }
   return (static_cast<uint64_t>(hi) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
@@ -269,7 +269,7 @@ __host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap, bool p
   L.U = take(4 * pcap * L.us);
   const int rbytes = 4 * pcap * L.rs, wbytes = 4 * pcap * L.ws;
   L.RW = take(rbytes > wbytes ? rbytes : wbytes);
-  L.merge = take(8 * G * kPub);
+  L.merge = take(max(8 * G * kPub, 4 * ch));  // also the picked-token flags
   L.bnd = take(8 * ((kPub + 1) * (NT / 64)));
   L.misc = take(64);
   // pipelined update: the own tokens' coefficient rows of earlier rounds
@@ -675,8 +675,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         const float ns = mn[s];
         // no basis vector when the unit residual is at most tau (or the row is zero)
         const bool skip = !(r2s > a.tau2 && ns > 0.0f);
-        const float r = skip ? 0.0f : sqrtf(r2s);
-        const float rinv = skip ? 0.0f : 1.0f / r;
+        const float r = skip ? 0.0f : __builtin_amdgcn_sqrtf(r2s);
+        const float rinv = skip ? 0.0f : __builtin_amdgcn_rcpf(r);  // hardware reciprocal (1 ulp)
         if (lane == 0) {
           pslot[np] = s;
           prr[np] = r;
@@ -805,8 +805,17 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     // The round's new rows t0 .. t-1 on the own tokens:
     //   W_k     = S[pick_k][i] - sum_{l<t0} c_{l,pick_k} c_{l,i}            (dense)
     //   c_{k,i} = (W_k - sum_{k'<k} U[pick_k][k'] c_{k',i}) / r_k           (triangular)
-    for (int k = 0; k < np; ++k)
-      if (tid < cnt && midx[pslot[k]] == my_i) my_state = 2;
+    {  // own tokens picked this round (the merge buffer is free here)
+      int* picked = reinterpret_cast<int*>(merge);
+      for (int i = tid; i < ch; i += NT) picked[i] = 0;
+      __syncthreads();
+      for (int k = tid; k < np; k += NT) {
+        const int i = midx[pslot[k]] - c0;
+        if (i >= 0 && i < cnt) picked[i] = 1;
+      }
+      __syncthreads();
+      if (tid < cnt && picked[tid]) my_state = 2;
+    }
     if (!PIPE) {
     // W rows: S rows of the picks at the own tokens; row j = wave + 4 u,
     // token c = lane + 64 h; up to 32 loads in flight per thread
