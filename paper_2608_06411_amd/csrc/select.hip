@@ -386,13 +386,20 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       for (int m = tid; m < pn; m += NT) midx[m] = R0[fq + m];
     } else if (round > 0) {  // keys exist once an update phase has run
       // Each workgroup published its top kPub keys (descending) and its
-      // (kPub+1)-th key.  beta0 = the largest of those bounds; every key
-      // above it is ranked by counting, list by list, the keys above it.
+      // (kPub+1)-th key.  beta0 = the largest of those bounds; the keys above
+      // it are compacted (in any order) and each is ranked by counting the
+      // compacted keys above it.  Ranks are unique, so every workgroup builds
+      // the same pool in the same order.
       const uint64_t* pub = a.pub + ((long long)b * 2 + ((round - 1) & 1)) * G * (kPub + 1);
-      const int nk = G * kPub;
-      for (int e = tid; e < nk; e += NT) {
-        const int ww = e >> 3, q = e & 7;  // kPub == 8
-        merge[e] = __hip_atomic_load(pub + ww * (kPub + 1) + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int nk = G * kPub;  // at most 128 x 8 = 4 NT
+      constexpr int XK = 4;
+      uint64_t x[XK];
+#pragma unroll
+      for (int h = 0; h < XK; ++h) {
+        const int e = tid + h * NT;
+        x[h] = e < nk ? __hip_atomic_load(pub + (e >> 3) * (kPub + 1) + (e & 7), __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT)
+                      : 0ull;  // kPub == 8
       }
       uint64_t bmax = 0;
       for (int ww = tid; ww < G; ww += NT) {
@@ -402,119 +409,88 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
       bmax = wave_max_key(bmax);
       if (lane == 0) bndk[wave] = bmax;
-      if (tid == 0) misc[2] = 0;  // pool size
+      if (tid == 0) misc[2] = 0;  // candidates above beta0
       __syncthreads();
       uint64_t beta0 = bndk[0];
       for (int q = 1; q < NT / 64; ++q) beta0 = bndk[q] > beta0 ? bndk[q] : beta0;
+      uint64_t* cand = merge;
+#pragma unroll
+      for (int h = 0; h < XK; ++h)
+        if (x[h] > beta0) cand[atomicAdd(&misc[2], 1)] = x[h];
+      __syncthreads();
+      const int nc = misc[2];
       uint64_t nextk = 0;  // the largest key left out of the pool by the cap
-      // rank of each key above beta0 = number of published keys above it;
-      // the lists are read in 16-byte pieces that every lane of a wave shares
-      for (int e0 = 0; e0 < nk; e0 += 2 * NT) {
-        uint64_t x[2];
-        int rk[2] = {0, 0};
 #pragma unroll
-        for (int h = 0; h < 2; ++h) x[h] = (e0 + tid + h * NT < nk) ? merge[e0 + tid + h * NT] : 0ull;
-        const bool any = (x[0] > beta0) || (x[1] > beta0);
-        if (__ballot(any) != 0ull) {
-          for (int e = 0; e < nk; e += 8) {
-            const uint64_t* lst = merge + e;
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-              const uint64_t y = lst[q];
-              rk[0] += y > x[0];
-              rk[1] += y > x[1];
-            }
-          }
-        }
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          if (x[h] <= beta0) continue;
-          if (rk[h] < pcap) {
-            const int i = key_index(x[h]);
-            midx[rk[h]] = (i >= 0 && i < N) ? i : 0;
-            atomicAdd(&misc[2], 1);
-          } else if (rk[h] == pcap) {
-            nextk = x[h];
-          }
+      for (int h = 0; h < XK; ++h) {
+        if (x[h] <= beta0) continue;
+        int rk = 0;
+        for (int j = 0; j < nc; ++j) rk += cand[j] > x[h];
+        if (rk < pcap) {
+          const int i = key_index(x[h]);
+          midx[rk] = (i >= 0 && i < N) ? i : 0;
+        } else if (rk == pcap) {
+          nextk = x[h];
         }
       }
       nextk = wave_max_key(nextk);
       if (lane == 0) bndk[NT / 64 + wave] = nextk;
       __syncthreads();
-      pn = misc[2];
+      pn = min(nc, pcap);
       beta = beta0;
       for (int q = 0; q < NT / 64; ++q) beta = bndk[NT / 64 + q] > beta ? bndk[NT / 64 + q] : beta;
     }
     __syncthreads();
     // members: state, columns (rows < t, written by their owners before the
-    // barrier) and their block of S; loads batched before use
-    for (int m = tid; m < pn; m += NT) {
-      const int i = midx[m];
-      const float pi = p[i], ni = nrm[i];
-      const float r2 = t == 0 ? (ni > 0.0f ? 1.0f : 0.0f)
-                              : __hip_atomic_load(r2g + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const float pc = (pi > 0.0f && pi <= 3.402823466e38f) ? pi : 0.0f;
-      mp[m] = pc;
-      mn[m] = ni;
-      mqn[m] = pc * ni;
-      mr2[m] = r2;
-    }
-    if (t > 0) {  // columns: pn rows of tq float4 each; a wave per member, lanes along it
-      const int tq = (t + 3) >> 2;
-      for (int m0 = 0; m0 < pn; m0 += 4 * (NT / 64)) {
-        float4 v[4][2];
+    // barrier) and their block of S.  Every global load of a thread is issued,
+    // at clamped (valid) addresses, before its first LDS store, so the phase
+    // costs about one memory round trip.
+    if (pn > 0) {
+      constexpr int CB = 12;  // column pieces per thread per batch
+      const int tq = (t + 3) >> 2, pieces = pn * tq;
+      // scalars of member tid
+      const int ms = min(tid, pn - 1), is = midx[ms];
+      const float pi = p[is], ni = nrm[is];
+      const float r2m = t == 0 ? 0.0f : __hip_atomic_load(r2g + is, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // first batch of column pieces: piece e = tid + NT u is float4 q of member m
+      float4 cv[CB];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int m = m0 + wave + 4 * u, q = lane + 64 * h;
-            v[u][h] = (m < pn && q < tq) ? *reinterpret_cast<const float4*>(Ct + (long long)midx[m] * Kp + 4 * q)
-                                         : make_float4(0.f, 0.f, 0.f, 0.f);
-          }
-        for (int q2 = 128; q2 < tq; q2 += 64) {  // columns longer than 512 floats
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int m = m0 + wave + 4 * u, q = q2 + lane;
-            if (m < pn && q < tq)
-              *reinterpret_cast<float4*>(pcol + m * cs + 4 * q) =
-                  *reinterpret_cast<const float4*>(Ct + (long long)midx[m] * Kp + 4 * q);
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int m = m0 + wave + 4 * u, q = lane + 64 * h;
-            if (m < pn && q < tq) *reinterpret_cast<float4*>(pcol + m * cs + 4 * q) = v[u][h];
-          }
+      for (int u = 0; u < CB; ++u) {
+        const int e = min(tid + NT * u, max(pieces - 1, 0));
+        const int m = tq > 0 ? e / tq : 0, q = e - m * tq;
+        cv[u] = tq > 0 ? *reinterpret_cast<const float4*>(Ct + (long long)midx[m] * Kp + 4 * q)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
       }
-    }
-    // Rm = S among the members (gathered): rows m1 = wave + 4 q, columns
-    // m2 = lane (+64); all loads of a thread issued before the first store
-    {
+      // S among the members: rows m1 = wave + 4 q, column m2 = lane
       constexpr int QMAX = kMaxPool / 4;
-      float v[QMAX][2];
-      int col[2];
+      float sv[QMAX];
+      const long long colS = midx[min(lane, pn - 1)];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) col[h] = midx[min(lane + 64 * h, pn - 1)];
+      for (int q = 0; q < QMAX; ++q) sv[q] = S[(long long)midx[min(wave + 4 * q, pn - 1)] * N + colS];
+      // stores
+      if (tid < pn) {
+        const float pc = (pi > 0.0f && pi <= 3.402823466e38f) ? pi : 0.0f;
+        mp[tid] = pc;
+        mn[tid] = ni;
+        mqn[tid] = pc * ni;
+        mr2[tid] = t == 0 ? (ni > 0.0f ? 1.0f : 0.0f) : r2m;
+      }
 #pragma unroll
-      for (int q = 0; q < QMAX; ++q) {
-        const int m1 = wave + 4 * q;
-        const long long base = (long long)midx[min(m1, pn - 1)] * N;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int m2 = lane + 64 * h;
-          v[q][h] = (m1 < pn && m2 < pn) ? S[base + col[h]] : 0.0f;
+      for (int u = 0; u < CB; ++u) {
+        const int e = tid + NT * u;
+        if (e < pieces) {
+          const int m = e / tq, q = e - m * tq;
+          *reinterpret_cast<float4*>(pcol + m * cs + 4 * q) = cv[u];
         }
+      }
+      for (int e = tid + NT * CB; e < pieces; e += NT) {  // long columns: the rest, piece by piece
+        const int m = e / tq, q = e - m * tq;
+        *reinterpret_cast<float4*>(pcol + m * cs + 4 * q) =
+            *reinterpret_cast<const float4*>(Ct + (long long)midx[m] * Kp + 4 * q);
       }
 #pragma unroll
       for (int q = 0; q < QMAX; ++q) {
         const int m1 = wave + 4 * q;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int m2 = lane + 64 * h;
-          if (m1 < pn && m2 < pn) Rm[m1 * rs + m2] = v[q][h];
-        }
+        if (m1 < pn && lane < pn) Rm[m1 * rs + lane] = sv[q];
       }
     }
     __syncthreads();
