@@ -625,16 +625,17 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     // U[m][k'] being member m's coefficient on the k'-th basis vector of
     // this round.  Each step issues all its LDS reads (Rm[s][m], row s of U
     // and the lane's own row of U, whose entries past the live ones are
-    // zero) before using them, so a pick costs about one LDS round trip.
+    // zero) before using them, so a pick costs about one LDS round trip; the
+    // products are only formed for the groups of 16 picks made so far.
     const int t0 = t;
     if (wave == 0) {
       int np = 0;
       const bool in = lane < pn;
       float r2v = in ? mr2[lane] : 0.0f;
-      const float qnv = in ? mqn[lane] : 0.0f, pv = in ? mp[lane] : 0.0f;
+      const float qnv = in ? mqn[lane] : 0.0f, pv = in ? mp[lane] : 0.0f, nv = in ? mn[lane] : 0.0f;
       const int iv = in ? midx[lane] : 0;
       bool actv = in;
-      const float* u0 = U + min(lane, pcap - 1) * us;
+      const float* u0 = U + min(lane, pcap - 1) * us;  // member `lane`'s row (zero past np)
       while (t < K) {
         int s;
         uint64_t best = 0;
@@ -647,17 +648,6 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           s = best > beta ? static_cast<int>(__builtin_ctzll(__ballot(kl == best))) : -1;
         }
         if (s < 0) break;
-        const float r2s = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, r2v), s));
-        const float ns = mn[s];
-        // no basis vector when the unit residual is at most tau (or the row is zero)
-        const bool skip = !(r2s > a.tau2 && ns > 0.0f);
-        const float r = skip ? 0.0f : __builtin_amdgcn_sqrtf(r2s);
-        const float rinv = skip ? 0.0f : __builtin_amdgcn_rcpf(r);  // hardware reciprocal (1 ulp)
-        if (lane == 0) {
-          pslot[np] = s;
-          prr[np] = r;
-          pgain[np] = forced ? mp[s] : key_score(best);
-        }
         const float rm = Rm[s * rs + min(lane, pn - 1)];
         const float* usr = U + s * us;
         float4 xs[kMaxPool / 4], y0[kMaxPool / 4];
@@ -666,14 +656,32 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           xs[q] = *reinterpret_cast<const float4*>(usr + 4 * q);
           y0[q] = *reinterpret_cast<const float4*>(u0 + 4 * q);
         }
-        float d = 0.0f;
-#pragma unroll
-        for (int q = 0; q < kMaxPool / 4; ++q) {
-          d = fmaf(xs[q].x, y0[q].x, d);
-          d = fmaf(xs[q].y, y0[q].y, d);
-          d = fmaf(xs[q].z, y0[q].z, d);
-          d = fmaf(xs[q].w, y0[q].w, d);
+        const float r2s = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, r2v), s));
+        const float ns = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, nv), s));
+        // no basis vector when the unit residual is at most tau (or the row is zero)
+        const bool skip = !(r2s > a.tau2 && ns > 0.0f);
+        const float r = skip ? 0.0f : __builtin_amdgcn_sqrtf(r2s);
+        const float rinv = skip ? 0.0f : __builtin_amdgcn_rcpf(r);  // hardware reciprocal (1 ulp)
+        if (lane == 0) {
+          pslot[np] = s;
+          prr[np] = r;
+          pgain[np] = forced ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pv), s))
+                             : key_score(best);
         }
+        // dot over the picks so far, in groups of 16 (entries past np are zero)
+        float d4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int g = 0; g < kMaxPool / 16; ++g) {
+          if (16 * g >= np) break;
+#pragma unroll
+          for (int q = 4 * g; q < 4 * g + 4; ++q) {
+            d4[0] = fmaf(xs[q].x, y0[q].x, d4[0]);
+            d4[1] = fmaf(xs[q].y, y0[q].y, d4[1]);
+            d4[2] = fmaf(xs[q].z, y0[q].z, d4[2]);
+            d4[3] = fmaf(xs[q].w, y0[q].w, d4[3]);
+          }
+        }
+        const float d = (d4[0] + d4[1]) + (d4[2] + d4[3]);
         if (in) {
           float c;
           if (lane == s) {
