@@ -712,26 +712,29 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       // round completes the selection (its update is then never used).
       const int rtag = round + 1;
       int k = 0;
+      int ready = 0;  // rows known to be available to this stage
       while (true) {
         bool over = false;
-        int n = 0;
-        while (true) {
-          if (__hip_atomic_load(pdone, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == rtag) {
-            const int fin = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
-            over = fin <= k || t0 + fin >= K;
+        if (k >= ready || (k & 7) == 0) {  // poll (and look for the end now and then)
+          while (true) {
+            if (__hip_atomic_load(pdone, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == rtag) {
+              const int fin = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+              over = fin <= k || t0 + fin >= K;
+            }
+            if (over) break;
+            if (wave == 3) {
+              const int avail = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+              const int room = __hip_atomic_load(ntri, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) + kRing;
+              ready = min(avail, room);
+            } else {
+              ready = __hip_atomic_load(nload, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+            if (ready > k) break;
+            __builtin_amdgcn_s_sleep(1);
           }
           if (over) break;
-          if (wave == 3) {
-            const int avail = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
-            const int room = __hip_atomic_load(ntri, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) + kRing;
-            n = min(min(avail, room) - k, kRing);
-          } else {
-            n = __hip_atomic_load(nload, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) - k;
-          }
-          if (n > 0) break;
-          __builtin_amdgcn_s_sleep(1);
         }
-        if (over) break;
+        const int n = min(ready - k, kRing);
         if (wave == 3) {
           float v[kRing];
           const int col = c0 + min(lane, cnt - 1);
@@ -751,26 +754,30 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           float* cr = crow + lane * us;  // zero past the finished rows
           const float rk = prr[k];
           const float w0 = ring[(k & (kRing - 1)) * wsd + lane];
+          // all reads first (one LDS round trip), products only for the
+          // groups of 16 rows finished so far
+          float4 u4[kMaxPool / 4], c4[kMaxPool / 4];
+#pragma unroll
+          for (int j = 0; j < kMaxPool / 4; ++j) {
+            u4[j] = *reinterpret_cast<const float4*>(ur + 4 * j);
+            c4[j] = *reinterpret_cast<const float4*>(cr + 4 * j);
+          }
           float e4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
           for (int g = 0; g < kMaxPool / 16; ++g) {
             if (16 * g >= k) break;
-            float4 u4[4], c4[4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              u4[j] = *reinterpret_cast<const float4*>(ur + 16 * g + 4 * j);
-              c4[j] = *reinterpret_cast<const float4*>(cr + 16 * g + 4 * j);
-            }
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 4 * g; j < 4 * g + 4; ++j) {
               e4[0] = fmaf(u4[j].x, c4[j].x, e4[0]); e4[1] = fmaf(u4[j].y, c4[j].y, e4[1]);
               e4[2] = fmaf(u4[j].z, c4[j].z, e4[2]); e4[3] = fmaf(u4[j].w, c4[j].w, e4[3]);
             }
           }
           const float v = w0 - ((e4[0] + e4[1]) + (e4[2] + e4[3]));
-          cr[k] = rk > 0.0f ? v / rk : 0.0f;
+          cr[k] = rk > 0.0f ? v * __builtin_amdgcn_rcpf(rk) : 0.0f;
           ++k;
-          __hip_atomic_store(ntri, k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+          // progress for the loader's ring, every fourth row (the ring holds kRing)
+          if ((k & 3) == 0 || k >= ready)
+            __hip_atomic_store(ntri, k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
       }
     }
