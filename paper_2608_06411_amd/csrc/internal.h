@@ -158,7 +158,9 @@ hipError_t launch_restore(const SelectArgs& a, hipStream_t s);
 struct GatherArgs {
   const void* V;           // [B][N][D]
   const int32_t* pos_v;    // [B][N]
-  const int32_t* idx;      // [B][K] ascending
+  const int32_t* order;    // [B][K] selection order (distinct indices)
+  const int32_t* err;      // selection error flag (set: every index is -1)
+  int32_t* idx_out;        // [B][K] kept indices, ascending (written here)
   void* V_out;             // [B][K][D]
   int32_t* pos_out;        // [B][K]
   int B, N, K, row_bytes;

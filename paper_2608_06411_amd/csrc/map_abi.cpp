@@ -239,9 +239,11 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   return launch_score(sa, st);
 }
 
+// with_restore = false leaves idx_out to the caller's next kernel (the fused
+// gather of map_prune ranks the selection order itself)
 hipError_t enqueue_select(int B, int N, const float* p, const float* S, const float* norms,
                           const map_select_params& sp, int32_t* idx_out, int32_t* order_out,
-                          float* gain_out, const SelectWs& w, hipStream_t st) {
+                          float* gain_out, const SelectWs& w, hipStream_t st, bool with_restore = true) {
   SelectArgs a;
   memset(&a, 0, sizeof(a));
   a.p = p;
@@ -264,7 +266,7 @@ hipError_t enqueue_select(int B, int N, const float* p, const float* S, const fl
   hipError_t e = launch_topk(a, st);
   if (e != hipSuccess) return e;
   if ((e = launch_select(a, st)) != hipSuccess) return e;
-  return launch_restore(a, st);
+  return with_restore ? launch_restore(a, st) : hipSuccess;
 }
 
 map_status hip_status(hipError_t e) { return e == hipSuccess ? MAP_OK : MAP_ERR_HIP; }
@@ -447,12 +449,14 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   const GemmProblem g = gram(V, B, N, w->D, S, ninv);
   hipError_t e = enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, &g, norms, ninv, st);
   if (e != hipSuccess) return MAP_ERR_HIP;
-  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st);
+  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st, false);
   if (e != hipSuccess) return MAP_ERR_HIP;
   GatherArgs ga;
   ga.V = V;
   ga.pos_v = pos_v;
-  ga.idx = idx_out;
+  ga.order = order_out ? order_out : sw.order;
+  ga.err = sw.err;
+  ga.idx_out = idx_out;
   ga.V_out = V_out;
   ga.pos_out = pos_out;
   ga.B = B;

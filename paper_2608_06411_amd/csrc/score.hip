@@ -1,16 +1,18 @@
 // Predicted attention, Eq. (3): logits, softmax over the visual tokens and
 // the mean over the question tokens.
 //
-// logits_kernel: one workgroup per (block of 64 visual tokens, image).  The
-// block's keys and, chunk by chunk, the image's queries sit in LDS; each
-// thread forms a 4x4 patch of q.k / sqrt(d_p) in float32 and the workgroup
-// also emits, per question token, the running (max, sum of exp) of its 64
-// logits, so that no pass over a whole logits row is needed later.
+// logits_kernel: one workgroup per (block of 64 visual tokens, chunk of 16
+// question tokens, image).  The block's keys and the chunk's queries sit in
+// LDS; each thread forms q.k / sqrt(d_p) in float32 for one query and four
+// keys, and the 16 lanes that share a query also emit the running (max, sum
+// of exp) of its 64 logits, so that no pass over a whole logits row is needed
+// later.
 //
-// softmax_mean_kernel: same grid.  Each workgroup folds the per-block
-// partials of its image into the row statistics (max_m, sum_m), then for its
-// 64 tokens averages exp(l_mn - max_m) / sum_m over m.  The sums run in a
-// fixed order, so the result is bitwise reproducible.
+// softmax_mean_kernel: one workgroup per (block of 64 visual tokens, image).
+// Each workgroup folds the per-block partials of its image into the row
+// statistics (max_m, sum_m), four threads per row with all loads in flight,
+// then for its 64 tokens averages exp(l_mn - max_m) / sum_m over m.  The sums
+// run in a fixed order, so the result is bitwise reproducible.
 #include "internal.h"
 
 namespace mapk {
@@ -18,100 +20,85 @@ namespace mapk {
 namespace {
 
 constexpr int KB = 64;    // visual tokens per workgroup
-constexpr int QB = 64;    // question tokens per LDS chunk
+constexpr int QB = 16;    // question tokens per workgroup
 constexpr int DPAD = 129; // padded LDS row (d_p <= 128)
 
 __global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
   __shared__ float ks[KB][DPAD];
   __shared__ float qs[QB][DPAD];
-  const int blk = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+  const int blk = blockIdx.x, q0 = blockIdx.y * QB, b = blockIdx.z, tid = threadIdx.x;
   const int n0 = blk * KB, dp = a.d_p;
   const int mb = a.t_off[b], M = a.t_off[b + 1] - mb;
+  if (q0 >= M) return;
   const float scale = 1.0f / sqrtf(static_cast<float>(dp));
-  // stage the keys: float4 loads, all issued before the LDS stores
-  {
-    const int q4 = dp >> 2, total = KB * q4;
-    for (int e0 = tid; e0 < total; e0 += 8 * 256) {
-      float4 v[8];
+  const int q4 = dp >> 2;
+  {  // keys and queries: float4 loads at clamped addresses, all issued before the LDS stores
+    constexpr int U = (KB + QB) * 32 / 256;  // pieces per thread for d_p = 128
+    float4 v[U];
+    const int kt = KB * q4, total = (KB + QB) * q4;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int e = e0 + u * 256, r = e / q4, d4 = e - r * q4;
-        v[u] = (e < total && n0 + r < a.N)
-                   ? *reinterpret_cast<const float4*>(a.k + ((long long)b * a.N + n0 + r) * dp + 4 * d4)
-                   : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
+    for (int u = 0; u < U; ++u) {
+      const int e = min(tid + u * 256, total - 1);
+      const bool key = e < kt;
+      const int r = key ? e / q4 : (e - kt) / q4, d4 = key ? e - r * q4 : (e - kt) - r * q4;
+      const float* src = key ? a.k + ((long long)b * a.N + min(n0 + r, a.N - 1)) * dp
+                             : a.q + (long long)(mb + min(q0 + r, M - 1)) * dp;
+      v[u] = *reinterpret_cast<const float4*>(src + 4 * d4);
+    }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int e = e0 + u * 256, r = e / q4, d4 = e - r * q4;
-        if (e < total) {
-          ks[r][4 * d4] = v[u].x; ks[r][4 * d4 + 1] = v[u].y;
-          ks[r][4 * d4 + 2] = v[u].z; ks[r][4 * d4 + 3] = v[u].w;
-        }
-      }
+    for (int u = 0; u < U; ++u) {
+      const int e = tid + u * 256;
+      if (e >= total) continue;
+      const bool key = e < kt;
+      const int r = key ? e / q4 : (e - kt) / q4, d4 = key ? e - r * q4 : (e - kt) - r * q4;
+      float* dst = key ? &ks[r][4 * d4] : &qs[r][4 * d4];
+      dst[0] = v[u].x; dst[1] = v[u].y; dst[2] = v[u].z; dst[3] = v[u].w;
+    }
+    for (int e = tid + U * 256; e < total; e += 256) {  // (not reached for d_p <= 128)
+      const bool key = e < kt;
+      const int r = key ? e / q4 : (e - kt) / q4, d4 = key ? e - r * q4 : (e - kt) - r * q4;
+      const float* src = key ? a.k + ((long long)b * a.N + min(n0 + r, a.N - 1)) * dp
+                             : a.q + (long long)(mb + min(q0 + r, M - 1)) * dp;
+      const float4 x = *reinterpret_cast<const float4*>(src + 4 * d4);
+      float* dst = key ? &ks[r][4 * d4] : &qs[r][4 * d4];
+      dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
     }
   }
-  const int tm = tid >> 4, tn = tid & 15;  // rows 4 tm .. 4 tm + 3, keys 4 tn .. 4 tn + 3
-  for (int q0 = 0; q0 < M; q0 += QB) {
-    __syncthreads();
-    {
-      const int q4 = dp >> 2, total = QB * q4;
-      for (int e0 = tid; e0 < total; e0 += 8 * 256) {
-        float4 v[8];
+  __syncthreads();
+  const int tm = tid >> 4, tn = tid & 15;  // query q0 + tm, keys 4 tn .. 4 tn + 3
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int d = 0; d < dp; ++d) {
+    const float qv = qs[tm][d];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int e = e0 + u * 256, r = e / q4, d4 = e - r * q4;
-          v[u] = (e < total && q0 + r < M)
-                     ? *reinterpret_cast<const float4*>(a.q + (long long)(mb + q0 + r) * dp + 4 * d4)
-                     : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+    for (int j = 0; j < 4; ++j) acc[j] = fmaf(qv, ks[4 * tn + j][d], acc[j]);
+  }
+  const int m = q0 + tm;
+  float mx = -INFINITY;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int e = e0 + u * 256, r = e / q4, d4 = e - r * q4;
-          if (e < total) {
-            qs[r][4 * d4] = v[u].x; qs[r][4 * d4 + 1] = v[u].y;
-            qs[r][4 * d4 + 2] = v[u].z; qs[r][4 * d4 + 3] = v[u].w;
-          }
-        }
-      }
-    }
-    __syncthreads();
-    float acc[4][4] = {};
-    for (int d = 0; d < dp; ++d) {
-      float qv[4], kv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) qv[i] = qs[4 * tm + i][d];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kv[j] = ks[4 * tn + j][d];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(qv[i], kv[j], acc[i][j]);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = q0 + 4 * tm + i;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int n = n0 + 4 * tn + j;
-        acc[i][j] *= scale;
-        if (n < a.N) {
-          mx = fmaxf(mx, acc[i][j]);
-          if (m < M) a.logits[(long long)(mb + m) * a.N + n] = acc[i][j];
-        }
-      }
-      // the 16 threads sharing tm are 16 consecutive lanes
-#pragma unroll
-      for (int off = 8; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 16));
-      float sm = 0.0f;
+  for (int j = 0; j < 4; ++j) {
+    acc[j] *= scale;
+    if (n0 + 4 * tn + j < a.N) mx = fmaxf(mx, acc[j]);
+  }
+  if (m < M) {
+    float* row = a.logits + (long long)(mb + m) * a.N + n0 + 4 * tn;
+    if ((a.N & 3) == 0 && n0 + 4 * tn + 3 < a.N) {
+      *reinterpret_cast<float4*>(row) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    } else {
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        if (n0 + 4 * tn + j < a.N) sm += expf(acc[i][j] - mx);
-#pragma unroll
-      for (int off = 8; off > 0; off >>= 1) sm += __shfl_xor(sm, off, 16);
-      if (tn == 0 && m < M) a.partial[(long long)(mb + m) * a.nblk + blk] = make_float2(mx, sm);
+        if (n0 + 4 * tn + j < a.N) row[j] = acc[j];
     }
   }
+  // the 16 lanes sharing tm are 16 consecutive lanes
+#pragma unroll
+  for (int off = 8; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 16));
+  float sm = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (n0 + 4 * tn + j < a.N) sm += expf(acc[j] - mx);
+#pragma unroll
+  for (int off = 8; off > 0; off >>= 1) sm += __shfl_xor(sm, off, 16);
+  if (tn == 0 && m < M) a.partial[(long long)(mb + m) * a.nblk + blk] = make_float2(mx, sm);
 }
 
 __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
@@ -119,24 +106,40 @@ __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
   __shared__ float part[4][KB];
   const int blk = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int mb = a.t_off[b], M = a.t_off[b + 1] - mb;
-  // row statistics from the per-block partials (independent loads batched)
-  for (int m = tid; m < M; m += 256) {
-    const float2* pr = a.partial + (long long)(mb + m) * a.nblk;
+  // row statistics from the per-block partials: four threads per row, each
+  // folding every fourth block (all loads in flight), then the four
+  // (max, sum) pairs combined in a fixed order
+  constexpr int PU = 16;
+  const int qtr = tid & 3;
+  for (int m0 = 0; m0 < M; m0 += 64) {
+    const int m = m0 + (tid >> 2);
+    const float2* pr = a.partial + (long long)(mb + min(m, M - 1)) * a.nblk;
     float mx = -INFINITY, sm = 0.0f;
-    for (int j0 = 0; j0 < a.nblk; j0 += 16) {
-      float2 v[16];
+    for (int j0 = qtr; j0 < a.nblk; j0 += 4 * PU) {
+      float2 v[PU];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = j0 + u < a.nblk ? pr[j0 + u] : make_float2(-INFINITY, 0.0f);
+      for (int u = 0; u < PU; ++u) v[u] = pr[min(j0 + 4 * u, a.nblk - 1)];
       float bm = mx;
 #pragma unroll
-      for (int u = 0; u < 16; ++u) bm = fmaxf(bm, v[u].x);
+      for (int u = 0; u < PU; ++u)
+        if (j0 + 4 * u < a.nblk) bm = fmaxf(bm, v[u].x);
       sm = (mx == -INFINITY) ? 0.0f : sm * expf(mx - bm);
 #pragma unroll
-      for (int u = 0; u < 16; ++u)
-        if (j0 + u < a.nblk) sm += v[u].y * expf(v[u].x - bm);
+      for (int u = 0; u < PU; ++u)
+        if (j0 + 4 * u < a.nblk) sm += v[u].y * expf(v[u].x - bm);
       mx = bm;
     }
-    stats[m] = make_float2(mx, 1.0f / sm);
+#pragma unroll
+    for (int off = 1; off < 4; off <<= 1) {
+      const float om = __shfl_xor(mx, off, 4), os = __shfl_xor(sm, off, 4);
+      const float nm = fmaxf(mx, om);
+      // the pair order is fixed by the lane pattern, so all four lanes agree
+      const float a0 = (qtr & off) ? os : sm, m0v = (qtr & off) ? om : mx;
+      const float a1 = (qtr & off) ? sm : os, m1v = (qtr & off) ? mx : om;
+      sm = (m0v == -INFINITY ? 0.0f : a0 * expf(m0v - nm)) + (m1v == -INFINITY ? 0.0f : a1 * expf(m1v - nm));
+      mx = nm;
+    }
+    if (qtr == 0 && m < M) stats[m] = make_float2(mx, 1.0f / sm);
   }
   __syncthreads();
   const int c = tid & (KB - 1), g = tid >> 6;  // token, slice of question tokens
@@ -171,10 +174,11 @@ __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
 hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
   int maxM = 0;
   for (int b = 0; b < a.B; ++b) maxM = a.t_off[b + 1] - a.t_off[b] > maxM ? a.t_off[b + 1] - a.t_off[b] : maxM;
-  const dim3 grid(a.nblk, a.B);
-  const hipError_t e = launch_kernel("logits", logits_kernel, grid, dim3(256), 0, s, a);
+  const hipError_t e =
+      launch_kernel("logits", logits_kernel, dim3(a.nblk, (maxM + QB - 1) / QB, a.B), dim3(256), 0, s, a);
   if (e != hipSuccess) return e;
-  return launch_kernel("softmax_mean", softmax_mean_kernel, grid, dim3(256), sizeof(float2) * maxM, s, a);
+  return launch_kernel("softmax_mean", softmax_mean_kernel, dim3(a.nblk, a.B), dim3(256), sizeof(float2) * maxM, s,
+                       a);
 }
 
 }  // namespace mapk
