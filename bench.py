@@ -39,16 +39,12 @@ def algorithmic_work(cfg, sumM):
         "gemm_proj_rope": ("mfma", 2.0 * rows * H * dp, "flop"),
         # read V, write norms, 1/norms and the cos/sin table
         "prep": ("hbm", B * N * D * el + 8.0 * B * N + 8.0 * rows * dp / 2, "byte"),
-        # read the kept rows and write them out
-        "gather": ("hbm", 2.0 * B * K * D * el + 8.0 * B * K, "byte"),
+        # read the selection order and the kept rows, write the rows, indices and positions
+        "gather": ("hbm", 2.0 * B * K * D * el + 16.0 * B * K, "byte"),
         # read keys and queries, write logits and per-block (max, sum of exp)
         "logits": ("hbm", 4.0 * (B * N + sumM) * dp + 4.0 * sumM * N + 8.0 * sumM * ((N + 63) // 64), "byte"),
         # read logits and partials, write p
         "softmax_mean": ("hbm", 4.0 * sumM * N + 8.0 * sumM * ((N + 63) // 64) + 4.0 * B * N, "byte"),
-        # read p, write the K0 indices
-        "topk": ("hbm", 4.0 * B * N + 4.0 * B * cfg.K0, "byte"),
-        # read the selection order, write the sorted indices
-        "restore": ("hbm", 8.0 * B * K, "byte"),
         # Eq. (4) consumes p, the norms and the K similarity rows of the
         # selected tokens, and emits order, gain and indices
         "select": ("hbm", B * (8.0 * N + 4.0 * K * N + 12.0 * K), "byte"),
@@ -64,9 +60,7 @@ KERNEL_SOURCES = {
     "gemm_proj_rope": ("gemm.hip", "internal.h"),
     "logits": ("score.hip", "internal.h"),
     "softmax_mean": ("score.hip", "internal.h"),
-    "topk": ("select.hip", "internal.h"),
     "select": ("select.hip", "internal.h"),
-    "restore": ("select.hip", "internal.h"),
     "gather": ("gather.hip", "internal.h"),
 }
 

@@ -126,6 +126,8 @@ struct ScoreArgs {
   const float* k;         // [B][N][d_p]  (after RoPE)
   float* logits;          // [sum_M][N]
   float2* partial;        // [sum_M][nblk] (running max, sum of exp) per key block
+  unsigned int* clear_bar; // optional: selection barrier counters [B] to zero
+  int32_t* clear_err;      // optional: selection error flag to zero
   float* p_out;           // [B][N]
   int B, N, d_p, nblk;
   int t_off[MAP_MAX_BATCH + 1];
@@ -137,7 +139,6 @@ struct SelectArgs {
   const float* p;        // [B][N]
   const float* S;        // [B][N][N]
   const float* norms;    // [B][N]
-  int32_t* R0;           // [B][K0]   top-K0 in descending p order
   float* C;              // [B][N][Kp] basis coefficients, Ct[i][t] = c_{t,i}
   float* r2;             // [B][N]    squared unit residuals
   uint64_t* pub;         // [B][2][G][kPub+1] published keys
@@ -150,7 +151,7 @@ struct SelectArgs {
   float tau2;
 };
 constexpr int kPub = 8;  // keys each workgroup publishes per round
-hipError_t launch_topk(const SelectArgs& a, hipStream_t s);
+hipError_t launch_select_clear(const SelectArgs& a, hipStream_t s);
 hipError_t launch_select(SelectArgs& a, hipStream_t s);
 hipError_t launch_restore(const SelectArgs& a, hipStream_t s);
 

@@ -111,7 +111,6 @@ struct SelectWs {
   uint64_t* pub;
   unsigned int* bar;
   int32_t* err;
-  int32_t* R0;
   int32_t* order;
   float* gain;
 };
@@ -123,7 +122,6 @@ SelectWs carve_select(Carver& c, int B, int N, int K) {
   s.pub = c.take<uint64_t>((size_t)B * 2 * 128 * (kPub + 1));
   s.bar = c.take<unsigned int>(B);
   s.err = c.take<int32_t>(4);
-  s.R0 = c.take<int32_t>((size_t)B * K);
   s.order = c.take<int32_t>((size_t)B * K);
   s.gain = c.take<float>((size_t)B * K);
   return s;
@@ -179,7 +177,8 @@ GemmProblem gram(const void* V, int B, int N, int D, float* S, const float* ninv
 hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const void* V,
                          const int32_t* pos_v, const void* T, const int32_t* pos_t,
                          const int32_t* t_off, float* p_out, const ScoreWs& s,
-                         const GemmProblem* extra_l1, float* norms, float* ninv, hipStream_t st) {
+                         const GemmProblem* extra_l1, float* norms, float* ninv, hipStream_t st,
+                         unsigned int* clear_bar = nullptr, int32_t* clear_err = nullptr) {
   const int sumM = t_off[B], rowsV = B * N;
   PrepArgs pa;
   memset(&pa, 0, sizeof(pa));
@@ -230,6 +229,8 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   sa.k = s.k;
   sa.logits = s.logits;
   sa.partial = s.partial;
+  sa.clear_bar = clear_bar;
+  sa.clear_err = clear_err;
   sa.p_out = p_out;
   sa.B = B;
   sa.N = N;
@@ -239,17 +240,16 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   return launch_score(sa, st);
 }
 
-// with_restore = false leaves idx_out to the caller's next kernel (the fused
-// gather of map_prune ranks the selection order itself)
+// Inside map_prune (fused = true) the scoring kernel has already cleared the
+// selection's counters and the gather ranks the selection order itself.
 hipError_t enqueue_select(int B, int N, const float* p, const float* S, const float* norms,
                           const map_select_params& sp, int32_t* idx_out, int32_t* order_out,
-                          float* gain_out, const SelectWs& w, hipStream_t st, bool with_restore = true) {
+                          float* gain_out, const SelectWs& w, hipStream_t st, bool fused = false) {
   SelectArgs a;
   memset(&a, 0, sizeof(a));
   a.p = p;
   a.S = S;
   a.norms = norms;
-  a.R0 = w.R0;
   a.C = w.C;
   a.r2 = w.r2;
   a.pub = w.pub;
@@ -263,10 +263,10 @@ hipError_t enqueue_select(int B, int N, const float* p, const float* S, const fl
   a.K = sp.K;
   a.K0 = sp.K0;
   a.tau2 = sp.tau * sp.tau;
-  hipError_t e = launch_topk(a, st);
+  hipError_t e = fused ? hipSuccess : launch_select_clear(a, st);
   if (e != hipSuccess) return e;
   if ((e = launch_select(a, st)) != hipSuccess) return e;
-  return with_restore ? launch_restore(a, st) : hipSuccess;
+  return fused ? hipSuccess : launch_restore(a, st);
 }
 
 map_status hip_status(hipError_t e) { return e == hipSuccess ? MAP_OK : MAP_ERR_HIP; }
@@ -447,9 +447,10 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   float* ninv = c.take<float>((size_t)B * N);
   float* p = p_out ? p_out : c.take<float>((size_t)B * N);
   const GemmProblem g = gram(V, B, N, w->D, S, ninv);
-  hipError_t e = enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, &g, norms, ninv, st);
+  hipError_t e =
+      enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, &g, norms, ninv, st, sw.bar, sw.err);
   if (e != hipSuccess) return MAP_ERR_HIP;
-  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st, false);
+  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st, true);
   if (e != hipSuccess) return MAP_ERR_HIP;
   GatherArgs ga;
   ga.V = V;

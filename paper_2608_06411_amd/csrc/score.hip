@@ -106,6 +106,10 @@ __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
   __shared__ float part[4][KB];
   const int blk = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int mb = a.t_off[b], M = a.t_off[b + 1] - mb;
+  if (a.clear_bar && blk == 0 && b == 0) {  // the selection that follows starts from zero
+    for (int i = tid; i < a.B; i += 256) a.clear_bar[i] = 0u;
+    if (tid == 0) *a.clear_err = 0;
+  }
   // row statistics from the per-block partials: four threads per row, each
   // folding every fourth block (all loads in flight), then the four
   // (max, sum) pairs combined in a fixed order

@@ -42,7 +42,6 @@ namespace mapk {
 namespace {
 
 constexpr int NT = 256;
-constexpr int kTopkThreads = 1024;
 constexpr unsigned kSpinLimit = 1u << 22;
 constexpr int kMaxPool = 64;  // one pool member per lane of the picking wave
 constexpr int kRing = 16;     // loaded rows the pipelined update buffers ahead
@@ -97,134 +96,12 @@ __device__ __forceinline__ uint64_t wave_max_key(uint64_t k) {
   return (static_cast<uint64_t>(mhi) << 32) | mlo;
 }
 
-__host__ __device__ __forceinline__ int pow2_at_least(int n) {
-  int p = 64;
-  while (p < n) p <<= 1;
-  return p;
-}
-
-// Descending bitonic sort of n keys in LDS (n a power of two), one pair per
-// thread and stage; used only on rare fallback paths.
-__device__ void lds_sort_desc(uint64_t* keys, int n) {
-  __syncthreads();
-  for (int k = 2; k <= n; k <<= 1)
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int q = threadIdx.x; q < n / 2; q += blockDim.x) {
-        const int i = 2 * q - (q & (j - 1));  // lower element of pair q
-        const uint64_t a = keys[i], b = keys[i + j];
-        const bool desc = (i & k) == 0;
-        if (desc == (a < b)) {
-          keys[i] = b;
-          keys[i + j] = a;
-        }
-      }
-      __syncthreads();
-    }
-}
-
-// ------------------------------------------------------------------ top-K0
-// One block per image.  Radix select (4 passes of 8 bits) finds the p bits
-// of the K0-th largest p; the keys at or above it are collected and ranked
-// (p, then lower index first).  Also clears the image's barrier counter and
-// the error flag for the selection launch that follows on the same stream.
-__global__ __launch_bounds__(kTopkThreads) void topk_kernel(const SelectArgs a) {
-  extern __shared__ uint64_t cand[];  // [pow2(N)] collected keys
-  __shared__ unsigned hist[256];
-  __shared__ unsigned misc[4];
-  constexpr int MAXE = MAP_MAX_N / kTopkThreads;
-  const int b = blockIdx.x, N = a.N, K0 = a.K0, tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
-  const float* p = a.p + (long long)b * N;
-  if (tid == 0) {
-    a.bar[b] = 0u;
-    if (b == 0) *a.err = 0;
-  }
-  if (K0 == 0) return;
-  uint32_t hv[MAXE];
-#pragma unroll
-  for (int r = 0; r < MAXE; ++r) {
-    const int i = r * kTopkThreads + tid;
-    hv[r] = i < N ? ordered_bits(p[i]) : 0u;
-  }
-  uint32_t prefix = 0;
-  unsigned need = static_cast<unsigned>(K0);
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    const uint32_t hmask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
-    if (tid < 256) hist[tid] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < MAXE; ++r) {
-      const int i = r * kTopkThreads + tid;
-      if (i < N && (hv[r] & hmask) == (prefix & hmask)) atomicAdd(&hist[(hv[r] >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    if (wave == 0) {
-      // lane l covers digits 255 - 4l .. 252 - 4l (descending)
-      unsigned c[4], s = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        c[q] = hist[255 - 4 * lane - q];
-        s += c[q];
-      }
-      // inclusive prefix over lanes (descending digit order)
-      unsigned incl = s;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const unsigned o = __shfl_up(incl, off);
-        if (lane >= off) incl += o;
-      }
-      const unsigned excl = incl - s;
-      const bool here = excl < need && incl >= need;
-      const unsigned long long bal = __ballot(here);
-      const int src = __builtin_ctzll(bal);
-      if (lane == src) {
-        unsigned run = excl;
-        int d = 0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (run + c[q] >= need) {
-            d = 255 - 4 * lane - q;
-            break;
-          }
-          run += c[q];
-        }
-        misc[0] = static_cast<unsigned>(d);
-        misc[1] = need - run;
-      }
-    }
-    __syncthreads();
-    prefix |= misc[0] << shift;
-    need = misc[1];
-  }
-  // prefix = p bits of the K0-th largest; collect every key with p bits >= prefix
-  if (tid == 0) misc[2] = 0;
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < MAXE; ++r) {
-    const int i = r * kTopkThreads + tid;
-    if (i < N && hv[r] >= prefix) {
-      const unsigned slot = atomicAdd(&misc[2], 1u);
-      cand[slot] = (static_cast<uint64_t>(hv[r]) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
-    }
-  }
-  __syncthreads();
-  const int nc = static_cast<int>(misc[2]);
-  int32_t* out = a.R0 + (long long)b * K0;
-  if (nc <= kTopkThreads) {
-    // rank by count: keys are distinct
-    if (tid < nc) {
-      const uint64_t x = cand[tid];
-      int rank = 0;
-      for (int j = 0; j < nc; ++j) rank += cand[j] > x;
-      if (rank < K0) out[rank] = key_index(x);
-    }
-  } else {  // many equal p values: sort everything collected
-    const int n2 = pow2_at_least(nc);
-    for (int j = nc + tid; j < n2; j += kTopkThreads) cand[j] = 0ull;
-    lds_sort_desc(cand, n2);
-    for (int j = tid; j < K0; j += kTopkThreads) out[j] = key_index(cand[j]);
-  }
+// ------------------------------------------------------------------ clear
+// Zeroes the image barrier counters and the error flag before a selection
+// launch (map_prune clears them in its scoring kernel instead).
+__global__ __launch_bounds__(64) void select_clear_kernel(const SelectArgs a) {
+  for (int i = threadIdx.x; i < a.B; i += 64) a.bar[i] = 0u;
+  if (threadIdx.x == 0) *a.err = 0;
 }
 
 // ------------------------------------------------------------------ selection
@@ -269,7 +146,7 @@ __host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap, bool p
   L.U = take(4 * pcap * L.us);
   const int rbytes = 4 * pcap * L.rs, wbytes = 4 * pcap * L.ws;
   L.RW = take(rbytes > wbytes ? rbytes : wbytes);
-  L.merge = take(max(8 * G * kPub, 4 * ch));  // also the picked-token flags
+  L.merge = take(max(8 * (G * kPub + 2), 4 * ch));  // also the picked-token flags
   L.bnd = take(8 * ((kPub + 1) * (NT / 64)));
   L.misc = take(64);
   // pipelined update: the own tokens' coefficient rows of earlier rounds
@@ -343,13 +220,12 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   const float* S = a.S + (long long)b * N * N;
   float* Ct = a.C + (long long)b * N * Kp;
   float* r2g = a.r2 + (long long)b * N;
-  const int32_t* R0 = a.R0 + (long long)b * K0;
 
   // ---- own tokens [c0, c0 + cnt); thread tid < ch keeps token c0 + tid
   const int c0 = w * ch;
   const int cnt = max(0, min(ch, N - c0));
   const int my_i = c0 + tid;
-  // state: 0 candidate, 1 reserved (in R0, not yet placed), 2 selected
+  // state: 0 candidate, 2 selected
   int my_state = 2;
   float my_r2 = 0.0f, my_qn = 0.0f, my_p = 0.0f;
   if (tid < cnt) {
@@ -360,31 +236,46 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     my_r2 = ni > 0.0f ? 1.0f : 0.0f;
     my_state = 0;
   }
-  {  // mark the own tokens that belong to R0 (W's memory serves as flags)
-    int* flag = reinterpret_cast<int*>(W);
-    for (int i = tid; i < ch; i += NT) flag[i] = 0;
-    if (tid == 0) misc[0] = 0;  // abort flag
-    if (PIPE && tid < 4) npub[tid] = 0;
-    __syncthreads();
-    for (int j = tid; j < K0; j += NT) {
-      const int r = R0[j];
-      if (r >= c0 && r < c0 + cnt) flag[r - c0] = 1;
+  // Publishes the top kPub + 1 keys of the own candidates into slot `slot`:
+  // each wave extracts the top kPub + 1 of its tokens, then wave 0 the top
+  // kPub + 1 of those.  While R0 is being placed the keys order by p alone
+  // (descending p, then lower index), so the pools of those rounds are the
+  // top of p; afterwards they order by the Eq. (4) score.
+  auto publish = [&](int slot, bool by_p) {
+    uint64_t k = 0ull;
+    if (tid < cnt && my_state == 0)
+      k = by_p ? ((static_cast<uint64_t>(ordered_bits(my_p)) << 32) | (0xffffffffu - static_cast<uint32_t>(my_i)))
+               : make_key(my_r2, my_qn, my_p, my_i, a.tau2);
+    for (int q = 0; q <= kPub; ++q) {
+      const uint64_t best = wave_max_key(k);
+      if (lane == 0) bndk[wave * (kPub + 1) + q] = best;
+      if (k == best) k = 0ull;
     }
     __syncthreads();
-    if (tid < cnt && flag[tid]) my_state = 1;  // reserved: placed by a forced round
-    __syncthreads();
-  }
+    if (wave == 0) {
+      uint64_t k2 = lane < (NT / 64) * (kPub + 1) ? bndk[lane] : 0ull;
+      uint64_t* pub = a.pub + ((long long)b * 2 + slot) * G * (kPub + 1) + w * (kPub + 1);
+      for (int q = 0; q <= kPub; ++q) {
+        const uint64_t best = wave_max_key(k2);
+        if (lane == 0) __hip_atomic_store(pub + q, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (k2 == best) k2 = 0ull;
+      }
+    }
+  };
+  if (tid == 0) misc[0] = 0;  // abort flag
+  if (PIPE && tid < 4) npub[tid] = 0;
+  __syncthreads();
+  publish(1, K0 > 0);  // the keys the first round merges
+  image_barrier(a.bar + b, static_cast<unsigned>(G), a.err, misc);
+  if (misc[0]) return;
 
   int t = 0, fq = 0, round = 0;
   while (t < K) {
     // ============================================================ pool
-    const bool forced = fq < K0;
+    const bool forced = fq < K0;  // this round places members of R0
     uint64_t beta = 0;
     int pn = 0;
-    if (forced) {
-      pn = min(pcap, K0 - fq);
-      for (int m = tid; m < pn; m += NT) midx[m] = R0[fq + m];
-    } else if (round > 0) {  // keys exist once an update phase has run
+    {
       // Each workgroup published its top kPub keys (descending) and its
       // (kPub+1)-th key.  beta0 = the largest of those bounds; the keys above
       // it are compacted (in any order) and each is ranked by counting the
@@ -419,17 +310,21 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         if (x[h] > beta0) cand[atomicAdd(&misc[2], 1)] = x[h];
       __syncthreads();
       const int nc = misc[2];
+      if ((nc & 1) && tid == 0) cand[nc] = 0ull;  // pad to whole 16-byte pairs (the buffer holds nk + 1)
+      __syncthreads();
       uint64_t nextk = 0;  // the largest key left out of the pool by the cap
-#pragma unroll
-      for (int h = 0; h < XK; ++h) {
-        if (x[h] <= beta0) continue;
+      for (int c = tid; c < nc; c += NT) {  // candidate c: its rank = number of candidates above it
+        const uint64_t xc = cand[c];
         int rk = 0;
-        for (int j = 0; j < nc; ++j) rk += cand[j] > x[h];
+        for (int j = 0; j < nc; j += 2) {
+          const ulonglong2 y = *reinterpret_cast<const ulonglong2*>(cand + j);
+          rk += (y.x > xc) + (y.y > xc);
+        }
         if (rk < pcap) {
-          const int i = key_index(x[h]);
+          const int i = key_index(xc);
           midx[rk] = (i >= 0 && i < N) ? i : 0;
         } else if (rk == pcap) {
-          nextk = x[h];
+          nextk = xc;
         }
       }
       nextk = wave_max_key(nextk);
@@ -639,8 +534,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       while (t < K) {
         int s;
         uint64_t best = 0;
-        if (forced) {
-          s = np < pn ? np : -1;
+        if (forced) {  // the pool is the top of p in descending order
+          s = np < min(pn, K0 - fq) ? np : -1;
         } else {
           const uint64_t kl = actv ? make_key(r2v, qnv, pv, iv, a.tau2) : 0ull;
           best = wave_max_key(kl);
@@ -966,28 +861,9 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         my_r2 = my_r2 - c * c;
       }
     if (live) __hip_atomic_store(r2g + my_i, my_r2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // keys of the own tokens: each wave extracts the top kPub + 1 of its
-    // tokens, then wave 0 extracts the top kPub + 1 of those
-    {
-      uint64_t k = (tid < cnt && my_state == 0) ? make_key(my_r2, my_qn, my_p, my_i, a.tau2) : 0ull;
-      for (int q = 0; q <= kPub; ++q) {
-        const uint64_t best = wave_max_key(k);
-        if (lane == 0) bndk[wave * (kPub + 1) + q] = best;
-        if (k == best) k = 0ull;
-      }
-      __syncthreads();
-      if (wave == 0) {
-        uint64_t k2 = lane < (NT / 64) * (kPub + 1) ? bndk[lane] : 0ull;
-        uint64_t* pub = a.pub + ((long long)b * 2 + (round & 1)) * G * (kPub + 1) + w * (kPub + 1);
-        for (int q = 0; q <= kPub; ++q) {
-          const uint64_t best = wave_max_key(k2);
-          if (lane == 0) __hip_atomic_store(pub + q, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          if (k2 == best) k2 = 0ull;
-        }
-      }
-    }
+    publish(round & 1, fq < K0);
     ++round;
-    image_barrier(a.bar + b, static_cast<unsigned>(round * G), a.err, misc);
+    image_barrier(a.bar + b, static_cast<unsigned>((round + 1) * G), a.err, misc);
     if (misc[0]) break;
   }
 }
@@ -1031,14 +907,8 @@ DeviceInfo& device_info() {
 
 }  // namespace
 
-hipError_t launch_topk(const SelectArgs& a, hipStream_t s) {
-  const size_t shm = (size_t)pow2_at_least(a.N) * 8;
-  if (shm > 65536) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(topk_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(shm));
-    if (e != hipSuccess) return e;
-  }
-  return launch_kernel("topk", topk_kernel, dim3(a.B), dim3(kTopkThreads), shm, s, a);
+hipError_t launch_select_clear(const SelectArgs& a, hipStream_t s) {
+  return launch_kernel("select_clear", select_clear_kernel, dim3(1), dim3(64), 0, s, a);
 }
 
 // Picks the tokens per workgroup (hence workgroups per image) and the pool
