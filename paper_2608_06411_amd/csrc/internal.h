@@ -147,6 +147,7 @@ struct SelectArgs {
   int32_t* order;        // [B][K]
   float* gain;           // [B][K]
   int32_t* idx_out;      // [B][K] ascending
+  int32_t* r0flag;       // [B] 1 where R0 was placed by one factorisation
   int B, N, K, K0, G, ch, pcap;
   float tau2;
 };

@@ -113,6 +113,7 @@ struct SelectWs {
   int32_t* err;
   int32_t* order;
   float* gain;
+  int32_t* r0flag;
 };
 
 SelectWs carve_select(Carver& c, int B, int N, int K) {
@@ -124,6 +125,7 @@ SelectWs carve_select(Carver& c, int B, int N, int K) {
   s.err = c.take<int32_t>(4);
   s.order = c.take<int32_t>((size_t)B * K);
   s.gain = c.take<float>((size_t)B * K);
+  s.r0flag = c.take<int32_t>(B);
   return s;
 }
 
@@ -258,6 +260,7 @@ hipError_t enqueue_select(int B, int N, const float* p, const float* S, const fl
   a.order = order_out ? order_out : w.order;
   a.gain = gain_out ? gain_out : w.gain;
   a.idx_out = idx_out;
+  a.r0flag = w.r0flag;
   a.B = B;
   a.N = N;
   a.K = sp.K;

@@ -71,6 +71,26 @@ __device__ __forceinline__ float key_score(uint64_t k) {
   return (hi & 0x80000000u) ? __uint_as_float(hi & 0x7fffffffu) : 0.0f;
 }
 
+// Ranking by counting compares keys as doubles: hi * 2^14 + (16383 - index)
+// is exact (hi < 2^32, index < 2^14) and orders like the key, and a key y
+// exceeds x exactly when x - y (exact) is negative, so a count is a sum of
+// sign bits, with no compare masks.
+__device__ __forceinline__ double key_rank_value(uint64_t k) {
+  return static_cast<double>(static_cast<uint32_t>(k >> 32)) * 16384.0 + static_cast<double>(16383 - key_index(k));
+}
+__device__ __forceinline__ int above(double x, double y) {  // 1 when y > x
+  return static_cast<int>(__builtin_bit_cast(uint64_t, x - y) >> 63);
+}
+__device__ __forceinline__ int rank_value_index(double v) {  // the index a rank value encodes
+  const double hi = __builtin_floor(v * (1.0 / 16384.0));
+  return 16383 - static_cast<int>(v - hi * 16384.0);
+}
+__device__ __forceinline__ uint64_t rank_value_key(double v) {
+  const double hi = __builtin_floor(v * (1.0 / 16384.0));
+  const int i = 16383 - static_cast<int>(v - hi * 16384.0);
+  return (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
+}
+
 // ---- wave64 reductions on the DPP network (row shifts, then row broadcasts)
 template <int CTRL, int ROW_MASK>
 __device__ __forceinline__ uint32_t dpp_umax(uint32_t v) {
@@ -86,6 +106,24 @@ __device__ __forceinline__ uint32_t wave_umax32(uint32_t v) {
   v = dpp_umax<0x142, 0xa>(v);  // row_bcast:15
   v = dpp_umax<0x143, 0xc>(v);  // row_bcast:31 -> lane 63 holds the wave maximum
   return __builtin_amdgcn_readlane(v, 63);
+}
+
+// Lane n of each row of 16 lanes, broadcast to its row (DPP row_newbcast).
+template <int N_>
+__device__ __forceinline__ float row_bcast_c(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x150 + N_, 0xf, 0xf, false));
+}
+__device__ __forceinline__ float row_bcast(float v, int n) {  // n a constant after unrolling
+  switch (n) {
+    case 0: return row_bcast_c<0>(v);   case 1: return row_bcast_c<1>(v);
+    case 2: return row_bcast_c<2>(v);   case 3: return row_bcast_c<3>(v);
+    case 4: return row_bcast_c<4>(v);   case 5: return row_bcast_c<5>(v);
+    case 6: return row_bcast_c<6>(v);   case 7: return row_bcast_c<7>(v);
+    case 8: return row_bcast_c<8>(v);   case 9: return row_bcast_c<9>(v);
+    case 10: return row_bcast_c<10>(v); case 11: return row_bcast_c<11>(v);
+    case 12: return row_bcast_c<12>(v); case 13: return row_bcast_c<13>(v);
+    case 14: return row_bcast_c<14>(v); default: return row_bcast_c<15>(v);
+  }
 }
 
 // Largest 64-bit key of the wave (0 if every lane holds 0).
@@ -179,6 +217,376 @@ __device__ void image_barrier(unsigned int* ctr, unsigned int target, int32_t* e
   __syncthreads();
 }
 
+// ------------------------------------------------------------------ R0 in one pass
+// R0 is known from p alone, so its K0 picks need no argmax: their coefficients
+// are the rows of one triangular factorisation,
+//     c_{k,i} = (S[r_k][i] - sum_{l<k} c_{l,r_k} c_{l,i}) / r_k,
+// over the pivots r_0 .. r_{K0-1} (descending p).  Every workgroup finds R0
+// itself, loads X = [S among R0 ; S between R0 and its own tokens] (rows are
+// tokens, columns pivots, the R0 diagonal set to 1, or 0 for a zero row) and
+// factors it left-looking in column blocks of 16 (its own kernel: the
+// selection kernel's registers and LDS are laid out for the rounds):
+//   update  X[r][J] -= X[r][0:J0] X[J][0:J0]^T     (matrix cores, every row r at or past J)
+//   pivot   the 16 x 16 diagonal block in one wave's registers; a pivot whose
+//           unit residual is at most tau gets r = 0 and a zero column
+//   panel   X[r][J] solved against the diagonal block, one thread per row
+// The own rows end as the own tokens' coefficients, the R0 rows as the
+// factor.  Workgroup w of an image owns tokens [64 w, 64 w + 64).
+constexpr int kR0Max = 128;   // largest K0 placed this way (larger: by pool rounds)
+constexpr int kR0Cand = 1024; // keys the top-K0 ranking holds
+
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
+__host__ __device__ inline bool r0_by_factor(int K0) { return K0 > 0 && K0 <= kR0Max; }
+
+struct R0Lds {
+  int X, r0, ri, cand, kmax, misc, bytes;
+  int K0p, xs, xrows;
+};
+
+__host__ __device__ inline R0Lds r0_layout(int K0) {
+  R0Lds L;
+  int o = 0;
+  auto take = [&](int bytes) { const int r = o; o += (bytes + 15) & ~15; return r; };
+  L.K0p = (K0 + 15) & ~15;
+  L.xs = L.K0p + 4;  // 4 times an odd number: float4 reads of 16 rows hit 16 bank groups
+  L.xrows = 64 * ((L.K0p + 64 + 63) / 64);  // R0 rows, then 64 own rows, in whole blocks of 64
+  L.X = take(4 * L.xrows * L.xs);
+  L.r0 = take(4 * L.K0p);
+  L.ri = take(4 * L.K0p);
+  L.cand = take(8 * (kR0Cand + 8));
+  L.kmax = take(8 * NT);
+  L.misc = take(16);
+  L.bytes = o;
+  return L;
+}
+
+// Places R0 for image blockIdx.y: the own tokens' coefficient rows on the
+// K0 pivots (global C) and their r^2 (global r2), and (workgroup 0) the
+// selection order and gains of the first K0 picks and the image's flag
+// r0flag = 1.  When more than kR0Cand keys tie with or exceed the threads'
+// K0-th largest maximum it writes nothing but r0flag = 0: the selection
+// kernel then places R0 by pool rounds.
+__global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  const int N = a.N, K0 = a.K0, K = a.K, Kp = (K + 3) & ~3;
+  const int b = blockIdx.y, w = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* p = a.p + (long long)b * N;
+  const float* nrm = a.norms + (long long)b * N;
+  const float* S = a.S + (long long)b * N * N;
+  float* Ct = a.C + (long long)b * N * Kp;
+  float* r2g = a.r2 + (long long)b * N;
+  const int c0 = 64 * w, cnt = min(64, N - c0);
+  const R0Lds R = r0_layout(K0);
+  float* X = reinterpret_cast<float*>(lds + R.X);
+  int* r0 = reinterpret_cast<int*>(lds + R.r0);
+  float* riv = reinterpret_cast<float*>(lds + R.ri);
+  double* cand = reinterpret_cast<double*>(lds + R.cand);  // rank values
+  double* kmax = reinterpret_cast<double*>(lds + R.kmax);
+  int* ncand = reinterpret_cast<int*>(lds + R.misc);
+  uint64_t* T0p = reinterpret_cast<uint64_t*>(lds + R.misc + 8);
+  const int K0p = R.K0p, xs = R.xs, nb = K0p / 16;
+
+  // ---- R0 = the K0 largest keys.  Thread u sees tokens u, u + NT, ...; the
+  // K0-th largest of the threads' maxima, T0, is at most the K0-th largest
+  // key, so the keys >= T0 hold R0; each of them is ranked by counting.
+  // The first PC tokens of each thread stay in registers for the second pass.
+  constexpr int PC = 16, PB = 8;
+  auto key_of = [](float pv, int i) -> uint64_t {
+    return (static_cast<uint64_t>(ordered_bits(pv)) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
+  };
+  float pc[PC];
+#pragma unroll
+  for (int u = 0; u < PC; ++u) pc[u] = p[min(tid + u * NT, N - 1)];
+  uint64_t mx = 0;
+#pragma unroll
+  for (int u = 0; u < PC; ++u) {
+    const int i = tid + u * NT;
+    const uint64_t k = key_of(pc[u], i);
+    mx = (i < N && k > mx) ? k : mx;
+  }
+  for (int i0 = tid + PC * NT; i0 < N; i0 += PB * NT) {
+    float pv[PB];
+#pragma unroll
+    for (int u = 0; u < PB; ++u) pv[u] = p[min(i0 + u * NT, N - 1)];
+#pragma unroll
+    for (int u = 0; u < PB; ++u) {
+      const int i = i0 + u * NT;
+      const uint64_t k = key_of(pv[u], i);
+      mx = (i < N && k > mx) ? k : mx;
+    }
+  }
+  const double mxv = mx ? key_rank_value(mx) : -1.0;  // threads without tokens rank last
+  kmax[tid] = mxv;
+  if (tid == 0) *ncand = 0;
+  __syncthreads();
+  {
+    const double2* y2 = reinterpret_cast<const double2*>(kmax);
+    int r4[4] = {0, 0, 0, 0};  // independent counters: no serial chain
+    for (int u0 = 0; u0 < NT / 2; u0 += 16) {
+      double2 y[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) y[u] = y2[u0 + u];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) r4[u & 3] += above(mxv, y[u].x) + above(mxv, y[u].y);
+    }
+    // at least K0 threads hold tokens (N >= K0, K0 <= NT); their maxima are
+    // distinct, and the empty threads' zeros rank below them
+    if ((r4[0] + r4[1]) + (r4[2] + r4[3]) == K0 - 1) *T0p = mx;
+  }
+  __syncthreads();
+  const uint64_t T0 = *T0p;
+#pragma unroll
+  for (int u = 0; u < PC; ++u) {
+    const int i = tid + u * NT;
+    const uint64_t k = key_of(pc[u], i);
+    if (i < N && k >= T0) {
+      const int o = atomicAdd(ncand, 1);
+      if (o < kR0Cand) cand[o] = key_rank_value(k);
+    }
+  }
+  for (int i0 = tid + PC * NT; i0 < N; i0 += PB * NT) {
+    float pv[PB];
+#pragma unroll
+    for (int u = 0; u < PB; ++u) pv[u] = p[min(i0 + u * NT, N - 1)];
+#pragma unroll
+    for (int u = 0; u < PB; ++u) {
+      const int i = i0 + u * NT;
+      const uint64_t k = key_of(pv[u], i);
+      if (i < N && k >= T0) {
+        const int o = atomicAdd(ncand, 1);
+        if (o < kR0Cand) cand[o] = key_rank_value(k);
+      }
+    }
+  }
+  __syncthreads();
+  const int nc = *ncand;
+  if (nc > kR0Cand) {  // the same on every workgroup of the image
+    if (w == 0 && tid == 0) a.r0flag[b] = 0;
+    return;
+  }
+  if (tid < 8) cand[nc + tid] = -1.0;  // whole groups of 8 for the ranking loop
+  __syncthreads();
+  for (int c = tid; c < nc; c += NT) {
+    const double x = cand[c];
+    int r4[4] = {0, 0, 0, 0};
+    const double2* y2 = reinterpret_cast<const double2*>(cand);
+    for (int j = 0; j < nc; j += 8) {
+      const double2 y0 = y2[j / 2], y1 = y2[j / 2 + 1], y2v = y2[j / 2 + 2], y3 = y2[j / 2 + 3];
+      r4[0] += above(x, y0.x) + above(x, y0.y);
+      r4[1] += above(x, y1.x) + above(x, y1.y);
+      r4[2] += above(x, y2v.x) + above(x, y2v.y);
+      r4[3] += above(x, y3.x) + above(x, y3.y);
+    }
+    const int rk = (r4[0] + r4[1]) + (r4[2] + r4[3]);
+    if (rk < K0) r0[rk] = rank_value_index(x);
+  }
+  __syncthreads();
+  const int rlast = r0[K0 - 1];  // own tokens with keys >= klast are in R0
+  const uint64_t klast = key_of(p[rlast], rlast);
+  const int rmine = r0[min(tid, K0 - 1)];
+  const float pmine = p[rmine];  // gain of pick tid (workgroup 0 writes it below)
+
+  // ---- the factorisation
+  {
+    const bool first = true;
+    const int ocnt = cnt;
+    // X[row][c] = S[r0[c]][token(row)]: lane = row within a block of 64 rows,
+    // wave w takes columns w, w + 4, ...  R0 rows load only their strictly
+    // lower part (the factorisation never reads above the diagonal), own rows
+    // the K0 columns; every load (lanes with nothing to load read one shared
+    // address) is issued before the first store, and the stores are
+    // branch-free selects over whole row blocks
+    {
+      constexpr int QB = kR0Max / 4;  // columns per wave at most
+      const int nq = K0p / 4, nh = R.xrows / 64;
+      int rc[QB];
+#pragma unroll
+      for (int q = 0; q < QB; ++q) rc[q] = r0[min(wave + 4 * q, K0 - 1)];
+      int tok[3], lim[3];
+      float dg[3];
+#pragma unroll
+      for (int h = 0; h < 3; ++h) {
+        const int row = 64 * h + lane;
+        const bool isr0 = row < K0p;
+        const bool valid = isr0 ? row < K0 : row - K0p < ocnt;
+        tok[h] = valid ? (isr0 ? r0[min(row, K0 - 1)] : c0 + min(row - K0p, ocnt - 1)) : c0;
+        lim[h] = !valid ? 0 : isr0 ? row : K0;
+        dg[h] = (isr0 && valid) ? nrm[tok[h]] : 0.0f;  // the diagonal: 1 for a nonzero row (below)
+      }
+      float v[3][QB];
+#pragma unroll
+      for (int qc = 0; qc < QB / 4; ++qc)
+        if (4 * qc < nq) {
+#pragma unroll
+          for (int h = 0; h < 3; ++h)
+            if (h < nh) {
+#pragma unroll
+              for (int qq = 0; qq < 4; ++qq) {
+                const int q = 4 * qc + qq, c = wave + 4 * q;
+                v[h][q] = S[(long long)rc[q] * N + (c < lim[h] ? tok[h] : c0)];
+              }
+            }
+        }
+#pragma unroll
+      for (int qc = 0; qc < QB / 4; ++qc)
+        if (4 * qc < nq) {
+#pragma unroll
+          for (int h = 0; h < 3; ++h)
+            if (h < nh) {
+              const int row = 64 * h + lane;
+#pragma unroll
+              for (int qq = 0; qq < 4; ++qq) {
+                const int q = 4 * qc + qq, c = wave + 4 * q;
+                X[row * xs + c] = c < lim[h] ? v[h][q] : (c == row && dg[h] > 0.0f ? 1.0f : 0.0f);
+              }
+            }
+        }
+    }
+    if (w == 0) {  // the first K0 picks of the selection order
+      if (tid == 0) a.r0flag[b] = 1;
+      if (tid < K0) {
+        a.order[(long long)b * K + tid] = rmine;
+        a.gain[(long long)b * K + tid] = (pmine > 0.0f && pmine <= 3.402823466e38f) ? pmine : 0.0f;
+      }
+    }
+    __syncthreads();
+    for (int jb = 0; jb < nb; ++jb) {
+      const int J0 = 16 * jb;
+      if (jb > 0) {
+        // update: 16-row tiles, the R0 rows at or past J0 (pass 0) and the own
+        // rows; lane group g supplies k = 16 s + 4 g + e to the e-th product
+        // of step s.  The diagonal block's columns (B) are read once per wave.
+        constexpr int KS = kR0Max / 16;
+        const int nr = first ? nb - jb : 0;
+        const int nown = (ocnt + 15) >> 4;
+        const float* brow = X + (J0 + (lane & 15)) * xs + 4 * (lane >> 4);
+        f32x4_t bv[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+          if (s < jb) bv[s] = *reinterpret_cast<const f32x4_t*>(brow + 16 * s);
+        for (int tile = wave; tile < nr + nown; tile += NT / 64) {
+          const int rbase = tile < nr ? J0 + 16 * tile : K0p + 16 * (tile - nr);
+          const float* arow = X + (rbase + (lane & 15)) * xs + 4 * (lane >> 4);
+          float* drow = X + (rbase + 4 * (lane >> 4)) * xs + J0 + (lane & 15);
+          float cur[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cur[e] = drow[e * xs];
+          f32x4_t av[KS];
+#pragma unroll
+          for (int s = 0; s < KS; ++s)
+            if (s < jb) av[s] = *reinterpret_cast<const f32x4_t*>(arow + 16 * s);
+          f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int s = 0; s < KS; ++s)
+            if (s < jb) {
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].x, bv[s].x, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].y, bv[s].y, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].z, bv[s].z, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].w, bv[s].w, acc, 0, 0, 0);
+            }
+          // result row 4 (lane >> 4) + e, column lane & 15
+#pragma unroll
+          for (int e = 0; e < 4; ++e) drow[e * xs] = cur[e] - acc[e];
+        }
+      }
+      __syncthreads();
+      if (first && wave == 0) {
+        // pivot: lane j (and its copies j + 16, ...) holds diagonal-block row
+        // J0 + j; straight-line code (selects, no branches) so the updates of
+        // later columns overlap the next pivot's reciprocal square root
+        const int j = lane & 15;
+        float* xr = X + (J0 + j) * xs + J0;
+        float x[16];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x4_t v = *reinterpret_cast<const f32x4_t*>(xr + 4 * q);
+          x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+        }
+        // step k: every lane of the row of 16 gets the pivot and the column
+        // entries it needs by DPP broadcast within the row
+        float myri = 0.0f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const float d = row_bcast(x[k], k);
+          const float rinv = d > a.tau2 ? __builtin_amdgcn_rsqf(d) : 0.0f;  // hardware reciprocal square root (1 ulp)
+          const float lj = j > k ? x[k] * rinv : 0.0f;  // L[j][k] below the pivot, zero at and above it
+          myri = j == k ? rinv : myri;
+          x[k] = j == k ? d * rinv : (j > k ? lj : x[k]);
+#pragma unroll
+          for (int j2 = k + 1; j2 < 16; ++j2) x[j2] = fmaf(-lj, row_bcast(lj, j2), x[j2]);
+        }
+        if (lane < 16) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4_t v = {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
+            *reinterpret_cast<f32x4_t*>(xr + 4 * q) = v;
+          }
+          riv[J0 + lane] = myri;
+        }
+      }
+      __syncthreads();
+      {
+        // panel: rows past the diagonal block, one thread each
+        const int np = first ? K0p - J0 - 16 : 0;
+        for (int u = tid; u < np + ocnt; u += NT) {
+          const int row = u < np ? J0 + 16 + u : K0p + (u - np);
+          float* xr = X + row * xs + J0;
+          float x[16];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4_t v = *reinterpret_cast<const f32x4_t*>(xr + 4 * q);
+            x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+          }
+#pragma unroll
+          for (int jj = 0; jj < 16; ++jj) {
+            const float* lr = X + (J0 + jj) * xs + J0;
+            float v = x[jj];
+#pragma unroll
+            for (int q = 0; q < (jj + 3) / 4; ++q) {
+              const f32x4_t l4 = *reinterpret_cast<const f32x4_t*>(lr + 4 * q);
+              if (4 * q + 0 < jj) v = fmaf(-l4.x, x[4 * q + 0], v);
+              if (4 * q + 1 < jj) v = fmaf(-l4.y, x[4 * q + 1], v);
+              if (4 * q + 2 < jj) v = fmaf(-l4.z, x[4 * q + 2], v);
+              if (4 * q + 3 < jj) v = fmaf(-l4.w, x[4 * q + 3], v);
+            }
+            x[jj] = v * riv[J0 + jj];
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4_t v = {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
+            *reinterpret_cast<f32x4_t*>(xr + 4 * q) = v;
+          }
+        }
+      }
+      __syncthreads();
+    }
+    // own rows out: piece e = (own row e >> 5, float4 e & 31)
+    const int K0q = (K0 + 3) >> 2;  // at most 32; columns K0 .. 4 K0q - 1 are zero
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + NT * u, i = e >> 5, q = e & 31;
+      if (i < ocnt && q < K0q)
+        *reinterpret_cast<f32x4_t*>(Ct + (long long)(c0 + i) * Kp + 4 * q) =
+            *reinterpret_cast<const f32x4_t*>(X + (K0p + i) * xs + 4 * q);
+    }
+    if (tid < ocnt) {  // R0 members get a NaN r^2: the selection kernel reads them as selected
+      const float* xr = X + (K0p + tid) * xs;
+      f32x4_t s4 = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int q = 0; q < kR0Max / 4; ++q)
+        if (q < K0q) {
+          const f32x4_t v = *reinterpret_cast<const f32x4_t*>(xr + 4 * q);
+          s4 += v * v;
+        }
+      const int i = c0 + tid;
+      const uint64_t ki = (static_cast<uint64_t>(ordered_bits(p[i])) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
+      r2g[i] = ki >= klast ? __builtin_nanf("") : (nrm[i] > 0.0f ? 1.0f : 0.0f) - ((s4.x + s4.y) + (s4.z + s4.w));
+    }
+  }
+}
+
 // Global C is token-major: Ct[i][l] = c_{l,i}, rows of Kp floats (Kp = K
 // rounded up to 4), so one token's coefficients are contiguous.
 template <bool PIPE>
@@ -246,6 +654,17 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     if (tid < cnt && my_state == 0)
       k = by_p ? ((static_cast<uint64_t>(ordered_bits(my_p)) << 32) | (0xffffffffu - static_cast<uint32_t>(my_i)))
                : make_key(my_r2, my_qn, my_p, my_i, a.tau2);
+    if (ch <= 64) {  // the own tokens are wave 0's lanes: its top keys are the workgroup's
+      if (wave == 0) {
+        uint64_t* pub = a.pub + ((long long)b * 2 + slot) * G * (kPub + 1) + w * (kPub + 1);
+        for (int q = 0; q <= kPub; ++q) {
+          const uint64_t best = wave_max_key(k);
+          if (lane == 0) __hip_atomic_store(pub + q, best, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          if (k == best) k = 0ull;
+        }
+      }
+      return;
+    }
     for (int q = 0; q <= kPub; ++q) {
       const uint64_t best = wave_max_key(k);
       if (lane == 0) bndk[wave * (kPub + 1) + q] = best;
@@ -262,14 +681,46 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
     }
   };
+  // R0 placed by r0_kernel (when it fits and did not give up): take over the
+  // own tokens' state and coefficient rows; otherwise the first rounds place it
+  bool r0_done = false;
+  if (r0_by_factor(K0)) {
+    // the flag, the own r^2 and the own rows are loaded together (the rows
+    // are used only when the flag is set)
+    const int K0q = (K0 + 3) >> 2;
+    float4 rows[8];
+    if (PIPE) {  // piece e = (own token e >> 5, float4 e & 31): at most 64 x 32
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = tid + NT * u, i = min(e >> 5, cnt - 1), q = min(e & 31, K0q - 1);
+        rows[u] = *reinterpret_cast<const float4*>(Ct + (long long)(c0 + i) * Kp + 4 * q);
+      }
+    }
+    const float r2v = r2g[c0 + min(tid, cnt - 1)];
+    r0_done = a.r0flag[b] != 0;
+    if (r0_done) {
+      if (K0 >= K) return;
+      if (tid < cnt) {
+        if (r2v != r2v) my_state = 2;  // NaN: a member of R0
+        else my_r2 = r2v;
+      }
+      if (PIPE) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int e = tid + NT * u, i = e >> 5, q = e & 31;
+          if (i < cnt && q < K0q) *reinterpret_cast<float4*>(ownC + i * ocs + 4 * q) = rows[u];
+        }
+      }
+    }
+  }
   if (tid == 0) misc[0] = 0;  // abort flag
   if (PIPE && tid < 4) npub[tid] = 0;
   __syncthreads();
-  publish(1, K0 > 0);  // the keys the first round merges
+  publish(1, K0 > 0 && !r0_done);  // the keys the first round merges
   image_barrier(a.bar + b, static_cast<unsigned>(G), a.err, misc);
   if (misc[0]) return;
 
-  int t = 0, fq = 0, round = 0;
+  int t = r0_done ? K0 : 0, fq = r0_done ? K0 : 0, round = 0;
   while (t < K) {
     // ============================================================ pool
     const bool forced = fq < K0;  // this round places members of R0
@@ -304,27 +755,39 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       __syncthreads();
       uint64_t beta0 = bndk[0];
       for (int q = 1; q < NT / 64; ++q) beta0 = bndk[q] > beta0 ? bndk[q] : beta0;
-      uint64_t* cand = merge;
+      double* cand = reinterpret_cast<double*>(merge);  // rank values of the keys above beta0
 #pragma unroll
       for (int h = 0; h < XK; ++h)
-        if (x[h] > beta0) cand[atomicAdd(&misc[2], 1)] = x[h];
+        if (x[h] > beta0) cand[atomicAdd(&misc[2], 1)] = key_rank_value(x[h]);
       __syncthreads();
       const int nc = misc[2];
-      if ((nc & 1) && tid == 0) cand[nc] = 0ull;  // pad to whole 16-byte pairs (the buffer holds nk + 1)
+      if ((nc & 1) && tid == 0) cand[nc] = -1.0;  // pad to whole pairs (the buffer holds nk + 2)
       __syncthreads();
       uint64_t nextk = 0;  // the largest key left out of the pool by the cap
       for (int c = tid; c < nc; c += NT) {  // candidate c: its rank = number of candidates above it
-        const uint64_t xc = cand[c];
-        int rk = 0;
-        for (int j = 0; j < nc; j += 2) {
-          const ulonglong2 y = *reinterpret_cast<const ulonglong2*>(cand + j);
-          rk += (y.x > xc) + (y.y > xc);
+        const double xc = cand[c];
+        int r4[4] = {0, 0, 0, 0};
+        int j = 0;
+        for (; j + 8 <= nc; j += 8) {
+          const double2 y0 = *reinterpret_cast<const double2*>(cand + j);
+          const double2 y1 = *reinterpret_cast<const double2*>(cand + j + 2);
+          const double2 y2 = *reinterpret_cast<const double2*>(cand + j + 4);
+          const double2 y3 = *reinterpret_cast<const double2*>(cand + j + 6);
+          r4[0] += above(xc, y0.x) + above(xc, y0.y);
+          r4[1] += above(xc, y1.x) + above(xc, y1.y);
+          r4[2] += above(xc, y2.x) + above(xc, y2.y);
+          r4[3] += above(xc, y3.x) + above(xc, y3.y);
         }
+        for (; j < nc; j += 2) {
+          const double2 y = *reinterpret_cast<const double2*>(cand + j);
+          r4[0] += above(xc, y.x) + above(xc, y.y);
+        }
+        const int rk = (r4[0] + r4[1]) + (r4[2] + r4[3]);
         if (rk < pcap) {
-          const int i = key_index(xc);
+          const int i = rank_value_index(xc);
           midx[rk] = (i >= 0 && i < N) ? i : 0;
         } else if (rk == pcap) {
-          nextk = xc;
+          nextk = rank_value_key(xc);
         }
       }
       nextk = wave_max_key(nextk);
@@ -962,6 +1425,17 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
   a.pcap = chosen_pcap;
   const int per_launch = static_cast<int>(((long long)per_cu * cus) / chosen_G);
   if (per_launch < 1) return hipErrorInvalidConfiguration;
+  if (r0_by_factor(a.K0)) {
+    const int rb = r0_layout(a.K0).bytes;
+    if (rb > 65536) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(r0_kernel),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, rb);
+      if (e != hipSuccess) return e;
+    }
+    const hipError_t e = launch_kernel("select_r0", r0_kernel, dim3((a.N + 63) / 64, a.B), dim3(NT),
+                                       static_cast<size_t>(rb), s, a);
+    if (e != hipSuccess) return e;
+  }
   for (int b0 = 0; b0 < a.B; b0 += per_launch) {
     const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
     const hipError_t e =

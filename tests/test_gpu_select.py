@@ -73,6 +73,8 @@ CASES = [
     (1, 1, 16, 1, 1, "bf16", "flat", {}),              # N = 1
     (1, 600, 128, 500, 50, "bf16", "flat", {}),        # large K: small pool, many rounds
     (1, 5000, 64, 64, 32, "bf16", "peaked", {}),       # many workgroups per image
+    (1, 9000, 64, 150, 100, "bf16", "flat", {}),       # more than 64 own tokens per workgroup
+    (1, 2000, 256, 300, 200, "bf16", "peaked", {}),    # K0 beyond the one-pass R0: pool rounds
 ]
 
 
@@ -109,3 +111,18 @@ def test_select_is_deterministic():
     b = _select(store, "bf16", p, 120, 60)
     for x, y in zip(a, b):
         np.testing.assert_array_equal(x, y)
+
+
+def test_select_r0_candidate_overflow():
+    """p arranged so that very many keys reach the threads' K0-th largest
+    maximum (token i is seen by thread i mod 256): R0 falls back to pool
+    rounds and must still be the top K0 of p, placed in order."""
+    N, K, K0 = 2560, 160, 128
+    V, store = _tokens(11, 1, N, 64, "f32")
+    i = np.arange(N)
+    p = (1.0 + 1e-3 * (i % 256) + 1e-6 * (i // 256))[None, :]
+    p = (p / p.sum()).astype(np.float32)
+    idx, order, gain = _select(store, "f32", p, K, K0)
+    want = np.lexsort((i, -p[0].astype(np.float64)))[:K0]
+    np.testing.assert_array_equal(order[0][:K0], want)
+    _check(V, p, K, K0, idx, order, gain)
