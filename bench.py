@@ -26,9 +26,13 @@ PEAK_MFMA_F32 = 157.3     # TFLOP/s
 PEAK_HBM = 8000.0         # GB/s
 
 
+R0_FACTOR_MAX = 128  # largest K0 the selection places by one factorisation (its own kernel)
+
+
 def algorithmic_work(cfg, sumM):
     """Per-launch algorithmic work of each kernel: (bound, amount, unit)."""
-    B, N, K = cfg.B, cfg.N, cfg.K
+    B, N, K, K0 = cfg.B, cfg.N, cfg.K, cfg.K0
+    K0f = K0 if 0 < K0 <= R0_FACTOR_MAX else 0  # picks placed by the R0 kernel
     D, H, dp = cfg.pred.D, cfg.pred.D_h, cfg.pred.d_p
     el = 2 if cfg.dtype == "bf16" else 4
     rows = B * N + sumM
@@ -45,9 +49,12 @@ def algorithmic_work(cfg, sumM):
         "logits": ("hbm", 4.0 * (B * N + sumM) * dp + 4.0 * sumM * N + 8.0 * sumM * ((N + 63) // 64), "byte"),
         # read logits and partials, write p
         "softmax_mean": ("hbm", 4.0 * sumM * N + 8.0 * sumM * ((N + 63) // 64) + 4.0 * B * N, "byte"),
-        # Eq. (4) consumes p, the norms and the K similarity rows of the
-        # selected tokens, and emits order, gain and indices
-        "select": ("hbm", B * (8.0 * N + 4.0 * K * N + 12.0 * K), "byte"),
+        # R0 (K0 <= 128): p, the norms and the K0 similarity rows of R0 in; the
+        # K0 coefficient rows of every token, r^2, order and gain out
+        "select_r0": ("hbm", B * (12.0 * N + 8.0 * K0 * N + 8.0 * K0), "byte"),
+        # the greedy picks of Eq. (4): p, the norms, r^2 and the coefficient rows
+        # so far in, the similarity rows of the picks; order, gain and indices out
+        "select": ("hbm", B * (12.0 * N + 4.0 * K0f * N + 4.0 * (K - K0f) * N + 12.0 * (K - K0f)), "byte"),
     }
 
 
@@ -60,6 +67,7 @@ KERNEL_SOURCES = {
     "gemm_proj_rope": ("gemm.hip", "internal.h"),
     "logits": ("score.hip", "internal.h"),
     "softmax_mean": ("score.hip", "internal.h"),
+    "select_r0": ("select.hip", "internal.h"),
     "select": ("select.hip", "internal.h"),
     "gather": ("gather.hip", "internal.h"),
 }
@@ -203,9 +211,10 @@ def main():
     gemm = max((k for k in kern if work.get(k, ("",))[0] == "mfma"), key=lambda k: kern[k]["avg_us"])
     roof_mfma = roofline(gemm, work, kern, cfg, args.workload)
     if dominant == "select":
-        # a chain of K dependent picks: per-pick latency, not bandwidth, sets its time
-        roof["note"] = (f"latency-bound: {cfg.K} sequential picks, "
-                        f"{kern[dominant]['avg_us'] / cfg.K:.2f} us per pick")
+        # a chain of dependent picks: per-pick latency, not bandwidth, sets its time
+        greedy = cfg.K - (cfg.K0 if 0 < cfg.K0 <= R0_FACTOR_MAX else 0)
+        roof["note"] = (f"latency-bound: {greedy} sequential greedy picks, "
+                        f"{kern[dominant]['avg_us'] / max(greedy, 1):.2f} us per pick")
 
     line = {
         "metric": METRIC, "value": cfg.B * 1000.0 / ms, "unit": "images/s", "n_gpus": 1,

@@ -150,7 +150,7 @@ __host__ __device__ inline int col_stride(int K) { return ((K + 31) & ~31) + 4; 
 struct Lds {
   // byte offsets into the dynamic LDS block
   int midx, mp, mn, mqn, mr2, mkey, pslot, pr, pgain, pcol, U, RW, merge, bnd, misc;
-  int ownC, D, flags;  // pipelined update only
+  int ownC, D, flags, r2acc;  // pipelined update only
   int bytes;
   int cs, us, rs, ws, ocs;
 };
@@ -194,6 +194,7 @@ __host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap, bool p
   L.ownC = pipe ? take(4 * ch * L.ocs) : 0;
   L.D = pipe ? take(4 * pcap * L.ws) : 0;
   L.flags = pipe ? take(32) : 0;
+  L.r2acc = pipe ? take(4 * 64) : 0;
   L.bytes = o;
   return L;
 }
@@ -587,6 +588,40 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
   }
 }
 
+// One 32 x 32 float32 tile, acc[e] = sum over l < tk of A[row][l] B[col][l]
+// for row 8 (e >> 2) + 4 h + (e & 3) and column lane & 31 (h = lane >> 5),
+// with arow and brow pointing at this lane's row and column plus 4 h; tk is
+// a multiple of 8 and the entries up to tk are valid (zero past the data).
+// Odd and even steps of eight accumulate separately and each step's
+// operands are read before the previous step's products issue.
+__device__ __forceinline__ void tile_product(const float* arow, const float* brow, int tk, f32x16_t& out) {
+  f32x16_t acc[2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[x][e] = 0.0f;
+  auto step = [&](int x, const f32x4_t& av, const f32x4_t& bv) {
+    acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(av.x, bv.x, acc[x], 0, 0, 0);
+    acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(av.y, bv.y, acc[x], 0, 0, 0);
+    acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(av.z, bv.z, acc[x], 0, 0, 0);
+    acc[x] = __builtin_amdgcn_mfma_f32_32x32x2f32(av.w, bv.w, acc[x], 0, 0, 0);
+  };
+  f32x4_t a = *reinterpret_cast<const f32x4_t*>(arow);
+  f32x4_t b = *reinterpret_cast<const f32x4_t*>(brow);
+  int l0 = 0;
+  for (; l0 + 16 <= tk; l0 += 16) {
+    const f32x4_t a2 = *reinterpret_cast<const f32x4_t*>(arow + l0 + 8);
+    const f32x4_t b2 = *reinterpret_cast<const f32x4_t*>(brow + l0 + 8);
+    step(0, a, b);
+    const int ln = min(l0 + 16, tk - 8);  // the next step's rows (a valid read at the end)
+    a = *reinterpret_cast<const f32x4_t*>(arow + ln);
+    b = *reinterpret_cast<const f32x4_t*>(brow + ln);
+    step(1, a2, b2);
+  }
+  if (l0 < tk) step(0, a, b);  // an odd last step
+  out = acc[0] + acc[1];
+}
+
 // Global C is token-major: Ct[i][l] = c_{l,i}, rows of Kp floats (Kp = K
 // rounded up to 4), so one token's coefficients are contiguous.
 template <bool PIPE>
@@ -622,6 +657,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   int* nload = npub + 1;                                 // rows loaded into the ring
   int* ntri = npub + 2;                                  // rows finished
   int* pdone = npub + 3;                                 // round tag once the picks are over
+  int* dready = npub + 4;                                // waves done with their D tiles
+  float* r2acc = reinterpret_cast<float*>(lds + L.r2acc);  // PIPE: finisher's sums of squares
 
   const float* p = a.p + (long long)b * N;
   const float* nrm = a.norms + (long long)b * N;
@@ -804,26 +841,33 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     // costs about one memory round trip.
     if (pn > 0) {
       constexpr int CB = 12;  // column pieces per thread per batch
-      const int tq = (t + 3) >> 2, pieces = pn * tq;
+      // member (tid >> 2) is loaded by four threads, float4 pieces q = (tid & 3) + 4 u;
+      // pieces up to column tk = t rounded up to 8 are written, with the
+      // columns at or past t set to zero (the round-start product then needs
+      // no masks)
+      const int tq = (t + 3) >> 2, tk4 = ((t + 7) & ~7) >> 2;
       // scalars of member tid
       const int ms = min(tid, pn - 1), is = midx[ms];
       const float pi = p[is], ni = nrm[is];
       const float r2m = t == 0 ? 0.0f : __hip_atomic_load(r2g + is, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      // first batch of column pieces: piece e = tid + NT u is float4 q of member m
-      float4 cv[CB];
+      const int mq = tid >> 2;
+      const float* csrc = Ct + (long long)midx[min(mq, pn - 1)] * Kp;
+      f32x4_t cv[CB];
 #pragma unroll
-      for (int u = 0; u < CB; ++u) {
-        const int e = min(tid + NT * u, max(pieces - 1, 0));
-        const int m = tq > 0 ? e / tq : 0, q = e - m * tq;
-        cv[u] = tq > 0 ? *reinterpret_cast<const float4*>(Ct + (long long)midx[m] * Kp + 4 * q)
-                       : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-      // S among the members: rows m1 = wave + 4 q, column m2 = lane
+      for (int u = 0; u < CB; ++u)
+        cv[u] = *reinterpret_cast<const f32x4_t*>(csrc + 4 * min((tid & 3) + 4 * u, max(tq - 1, 0)));
+      // S among the members: rows m1 = 16 wave + q, column m2 = lane
       constexpr int QMAX = kMaxPool / 4;
       float sv[QMAX];
       const long long colS = midx[min(lane, pn - 1)];
+      // S is symmetric: entries below the diagonal come from the mirror, and
+      // lanes with nothing to load read the row's diagonal (one shared line)
 #pragma unroll
-      for (int q = 0; q < QMAX; ++q) sv[q] = S[(long long)midx[min(wave + 4 * q, pn - 1)] * N + colS];
+      for (int q = 0; q < QMAX; ++q) {
+        const int m1 = min(QMAX * wave + q, pn - 1);
+        const long long row = midx[m1];
+        sv[q] = S[row * N + (lane >= m1 ? colS : row)];
+      }
       // stores
       if (tid < pn) {
         const float pc = (pi > 0.0f && pi <= 3.402823466e38f) ? pi : 0.0f;
@@ -832,88 +876,61 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         mqn[tid] = pc * ni;
         mr2[tid] = t == 0 ? (ni > 0.0f ? 1.0f : 0.0f) : r2m;
       }
+      if (mq < pn) {
+        auto put = [&](int q, f32x4_t v) {  // piece q, zero at and past column t
+          const int l = 4 * q;
+          v.x = l < t ? v.x : 0.0f;
+          v.y = l + 1 < t ? v.y : 0.0f;
+          v.z = l + 2 < t ? v.z : 0.0f;
+          v.w = l + 3 < t ? v.w : 0.0f;
+          *reinterpret_cast<f32x4_t*>(pcol + mq * cs + l) = v;
+        };
 #pragma unroll
-      for (int u = 0; u < CB; ++u) {
-        const int e = tid + NT * u;
-        if (e < pieces) {
-          const int m = e / tq, q = e - m * tq;
-          *reinterpret_cast<float4*>(pcol + m * cs + 4 * q) = cv[u];
+        for (int u = 0; u < CB; ++u) {
+          const int q = (tid & 3) + 4 * u;
+          if (q < tk4) put(q, cv[u]);
         }
+        for (int q = (tid & 3) + 4 * CB; q < tk4; q += 4)  // long columns: the rest
+          put(q, *reinterpret_cast<const f32x4_t*>(csrc + 4 * min(q, tq - 1)));
       }
-      for (int e = tid + NT * CB; e < pieces; e += NT) {  // long columns: the rest, piece by piece
-        const int m = e / tq, q = e - m * tq;
-        *reinterpret_cast<float4*>(pcol + m * cs + 4 * q) =
-            *reinterpret_cast<const float4*>(Ct + (long long)midx[m] * Kp + 4 * q);
-      }
+      if (PIPE && t > 0)  // the own rows' columns t .. tk - 1 are zero too
+        for (int e = tid; e < cnt * 8; e += NT) {
+          const int i = e >> 3, l = t + (e & 7);
+          if (l < 4 * tk4) ownC[i * ocs + l] = 0.0f;
+        }
 #pragma unroll
       for (int q = 0; q < QMAX; ++q) {
-        const int m1 = wave + 4 * q;
-        if (m1 < pn && lane < pn) Rm[m1 * rs + lane] = sv[q];
+        const int m1 = QMAX * wave + q;
+        if (m1 < pn && lane < pn && lane >= m1) {
+          Rm[m1 * rs + lane] = sv[q];
+          Rm[lane * rs + m1] = sv[q];
+        }
       }
     }
     __syncthreads();
     // this round's coefficients start at zero, so the pick loop needs no masks
     for (int e = tid; e < pn * (us / 4); e += NT)
       reinterpret_cast<float4*>(U)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (PIPE && tid < 3) npub[tid] = 0;  // npub, nload, ntri
+    if (PIPE && tid < 5 && tid != 3) npub[tid] = 0;  // npub, nload, ntri, dready
     if (PIPE && t > 0 && pn > 0) {
-      // One float32 matrix-core product over the t rows so far, the pool's
-      // columns against the pool's columns and the own tokens' rows:
-      //   Rm[m][j] -= sum_l c_{l,m} c_{l,j}   (pool member j)
-      //   D[m][i]   = sum_l c_{l,m} c_{l,i}   (own token i)
-      // Wave w computes rows 32 (w >> 1) .. and columns 64 (w & 1) .. of the
-      // 64 x 128 result as two 32 x 32 tiles; in a step of eight rows l the
-      // lanes of half h supply rows l0 + 4 h .. l0 + 4 h + 3.
-      const int tr = wave >> 1, jh = wave & 1, r = lane & 31, h = lane >> 5;
-      const float* arow = pcol + min(32 * tr + r, pn - 1) * cs;
-      const float* brow[2];
+      // The pool's residual Gram matrix, one float32 matrix-core product over
+      // the t rows so far (columns t .. tk - 1 are zero):
+      //   Rm[m][j] -= sum_l c_{l,m} c_{l,j}
+      // Wave w computes the 32 x 32 tile (w >> 1, w & 1); the own tokens'
+      // part (D) is computed by waves 1 to 3 while wave 0 picks.
+      const int tr = wave >> 1, tc = wave & 1, r = lane & 31, h = lane >> 5;
+      float cur[16];  // current entries of this lane's results, read ahead
 #pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        const int j = 64 * jh + 32 * jj + r;
-        brow[jj] = j < 64 ? pcol + min(j, pn - 1) * cs : ownC + min(j - 64, cnt - 1) * ocs;
+      for (int e = 0; e < 16; ++e)
+        cur[e] = Rm[min(32 * tr + 8 * (e >> 2) + 4 * h + (e & 3), pn - 1) * rs + min(32 * tc + r, pn - 1)];
+      f32x16_t acc;
+      tile_product(pcol + min(32 * tr + r, pn - 1) * cs + 4 * h, pcol + min(32 * tc + r, pn - 1) * cs + 4 * h,
+                   (t + 7) & ~7, acc);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = 32 * tr + 8 * (e >> 2) + 4 * h + (e & 3), j = 32 * tc + r;
+        if (m < pn && j < pn) Rm[m * rs + j] = cur[e] - acc[e];
       }
-      f32x16_t acc[2];
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[jj][e] = 0.0f;
-      for (int l0 = 0; l0 < t; l0 += 8) {
-        const int lb = l0 + 4 * h;
-        float4 a = *reinterpret_cast<const float4*>(arow + lb);
-        float4 bv[2];
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) bv[jj] = *reinterpret_cast<const float4*>(brow[jj] + lb);
-        if (lb + 4 > t) {  // rows at or past t hold stale values: zero both operands
-          const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (lb >= t) { a = z; bv[0] = z; bv[1] = z; }
-          else {
-            if (lb + 1 >= t) { a.y = 0.f; bv[0].y = 0.f; bv[1].y = 0.f; }
-            if (lb + 2 >= t) { a.z = 0.f; bv[0].z = 0.f; bv[1].z = 0.f; }
-            a.w = 0.f; bv[0].w = 0.f; bv[1].w = 0.f;
-          }
-        }
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.x, bv[jj].x, acc[jj], 0, 0, 0);
-          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.y, bv[jj].y, acc[jj], 0, 0, 0);
-          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.z, bv[jj].z, acc[jj], 0, 0, 0);
-          acc[jj] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.w, bv[jj].w, acc[jj], 0, 0, 0);
-        }
-      }
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int m = 32 * tr + 8 * (e >> 2) + 4 * h + (e & 3);
-          const int j = 64 * jh + 32 * jj + r;
-          if (m < pn) {
-            if (j < 64) {
-              if (j < pn) Rm[m * rs + j] -= acc[jj][e];
-            } else {
-              Dm[m * wsd + j - 64] = acc[jj][e];
-            }
-          }
-        }
     }
     // Rm -= P P^T over the t rows so far.  With R = ceil(pn / 4), tile
     // (bi, bj), bi <= bj, covers rows bi + R x and columns bj + R y; lanes
@@ -970,11 +987,6 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
     }
     __syncthreads();
-    if (PIPE) {  // this round's own rows start at zero: the finishing dot needs no masks
-      for (int e = tid; e < ch * (us / 4); e += NT)
-        reinterpret_cast<float4*>(crow)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
-      __syncthreads();
-    }
 
     // ============================================================ picks
     // Wave 0 alone, without barriers; lane m holds pool member m (r^2, key
@@ -1001,11 +1013,25 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           s = np < min(pn, K0 - fq) ? np : -1;
         } else {
           const uint64_t kl = actv ? make_key(r2v, qnv, pv, iv, a.tau2) : 0ull;
-          best = wave_max_key(kl);
-          // keys are distinct: exactly one member holds `best`
-          s = best > beta ? static_cast<int>(__builtin_ctzll(__ballot(kl == best))) : -1;
+          // the largest high word nearly always belongs to one member; only
+          // a tie needs the low words (keys are distinct, so one member wins)
+          const uint32_t khi = static_cast<uint32_t>(kl >> 32);
+          const uint32_t mhi = wave_umax32(khi);
+          const uint64_t tied = __ballot(khi == mhi);
+          int sl;
+          if (__builtin_popcountll(tied) == 1) {
+            sl = static_cast<int>(__builtin_ctzll(tied));
+            best = (static_cast<uint64_t>(mhi) << 32) |
+                   static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(kl)), sl));
+          } else {
+            best = wave_max_key(kl);
+            sl = static_cast<int>(__builtin_ctzll(__ballot(kl == best)));
+          }
+          s = best > beta ? sl : -1;
         }
         if (s < 0) break;
+        // a pick among the own tokens (wave 0's lanes when 64 tokens per workgroup)
+        if (PIPE && __builtin_amdgcn_readlane(iv, s) == c0 + lane) my_state = 2;
         const float rm = Rm[s * rs + min(lane, pn - 1)];
         const float* usr = U + s * us;
         float4 xs[kMaxPool / 4], y0[kMaxPool / 4];
@@ -1057,7 +1083,32 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
       if (lane == 0) misc[3] = np;
       if (PIPE) __hip_atomic_store(pdone, round + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-    } else if (PIPE && wave != 2) {
+    } else if (PIPE) {
+      // D[m][i] = sum_{l<t0} c_{l,m} c_{l,i} (pool member m, own token i), four
+      // 32 x 32 tiles: wave 1 tile 0, wave 3 tile 1, wave 2 tiles 2 and 3.  The
+      // member columns share their space with this round's own rows and the
+      // ring, so the stages below start once every D tile is done.
+      if (t0 > 0 && pn > 0) {
+        const int r = lane & 31, h = lane >> 5;
+        for (int q = wave == 1 ? 0 : wave == 3 ? 1 : 2; q < (wave == 2 ? 4 : (wave == 1 ? 1 : 2)); ++q) {
+          const int ti = q >> 1, tj = q & 1;
+          f32x16_t acc;
+          tile_product(pcol + min(32 * ti + r, pn - 1) * cs + 4 * h, ownC + min(32 * tj + r, cnt - 1) * ocs + 4 * h,
+                       (t0 + 7) & ~7, acc);
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int m = 32 * ti + 8 * (e >> 2) + 4 * h + (e & 3);
+            if (m < pn) Dm[m * wsd + 32 * tj + r] = acc[e];
+          }
+        }
+      }
+      if (lane == 0) __hip_atomic_fetch_add(dready, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);  // once per wave
+      if (wave != 2) {
+      while (__hip_atomic_load(dready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 3) __builtin_amdgcn_s_sleep(1);
+      if (wave == 1) {  // this round's own row starts at zero: the finishing dot needs no masks
+        float4* cz = reinterpret_cast<float4*>(crow + lane * us);
+        for (int e = 0; e < us / 4; ++e) cz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
       // The own tokens are brought up to date while wave 0 picks (lane i
       // serves own token i), in pick order:
       //   wave 3  loads W_k[i] = S[pick_k][i] - D[pick_k][i] (the earlier
@@ -1071,6 +1122,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       const int rtag = round + 1;
       int k = 0;
       int ready = 0;  // rows known to be available to this stage
+      float csq = 0.0f;  // finisher: sum of the own token's squared new coefficients
       while (true) {
         bool over = false;
         if (k >= ready || (k & 7) == 0) {  // poll (and look for the end now and then)
@@ -1131,12 +1183,19 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
             }
           }
           const float v = w0 - ((e4[0] + e4[1]) + (e4[2] + e4[3]));
-          cr[k] = rk > 0.0f ? v * __builtin_amdgcn_rcpf(rk) : 0.0f;
+          const float c = rk > 0.0f ? v * __builtin_amdgcn_rcpf(rk) : 0.0f;
+          cr[k] = c;
+          // the finished row goes straight to the own rows in LDS and to C
+          ownC[lane * ocs + t0 + k] = c;
+          if (lane < cnt) Ct[(long long)(c0 + lane) * Kp + t0 + k] = c;
+          csq = fmaf(c, c, csq);
           ++k;
           // progress for the loader's ring, every fourth row (the ring holds kRing)
           if ((k & 3) == 0 || k >= ready)
             __hip_atomic_store(ntri, k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
+      }
+      if (wave == 1) r2acc[lane] = csq;
       }
     }
     __syncthreads();
@@ -1154,7 +1213,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     // The round's new rows t0 .. t-1 on the own tokens:
     //   W_k     = S[pick_k][i] - sum_{l<t0} c_{l,pick_k} c_{l,i}            (dense)
     //   c_{k,i} = (W_k - sum_{k'<k} U[pick_k][k'] c_{k',i}) / r_k           (triangular)
-    {  // own tokens picked this round (the merge buffer is free here)
+    if (!PIPE) {  // own tokens picked this round (the merge buffer is free here)
       int* picked = reinterpret_cast<int*>(merge);
       for (int i = tid; i < ch; i += NT) picked[i] = 0;
       __syncthreads();
@@ -1306,23 +1365,23 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
     }
     }  // !PIPE
-    // new rows to global memory (token-major), to the own rows in LDS when
-    // pipelined, and the own r2
-    {
+    // new rows to global memory (token-major) and the own r2 (pipelined:
+    // the finisher wrote the rows and summed the squares already)
+    const bool live = tid < cnt && my_state != 2;
+    if (PIPE) {
+      if (live) my_r2 = my_r2 - r2acc[tid];
+    } else {
       const int total = np * cnt;
       for (int e = tid; e < total; e += NT) {
         const int c = e / np, jj = e - c * np;
-        const float v = PIPE ? crow[c * us + jj] : W[jj * wsd + c];
-        if (PIPE) ownC[c * ocs + t0 + jj] = v;
-        Ct[(long long)(c0 + c) * Kp + t0 + jj] = v;
+        Ct[(long long)(c0 + c) * Kp + t0 + jj] = W[jj * wsd + c];
       }
+      if (live)
+        for (int jj = 0; jj < np; ++jj) {
+          const float c = W[jj * wsd + tid];
+          my_r2 = my_r2 - c * c;
+        }
     }
-    const bool live = tid < cnt && my_state != 2;
-    if (live)
-      for (int jj = 0; jj < np; ++jj) {
-        const float c = PIPE ? crow[tid * us + jj] : W[jj * wsd + tid];
-        my_r2 = my_r2 - c * c;
-      }
     if (live) __hip_atomic_store(r2g + my_i, my_r2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     publish(round & 1, fq < K0);
     ++round;
