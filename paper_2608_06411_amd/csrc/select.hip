@@ -44,7 +44,6 @@ namespace {
 constexpr int NT = 256;
 constexpr unsigned kSpinLimit = 1u << 22;
 constexpr int kMaxPool = 64;  // one pool member per lane of the picking wave
-constexpr int kRing = 16;     // loaded rows the pipelined update buffers ahead
 
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 
@@ -177,10 +176,9 @@ __host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap, bool p
   L.pslot = take(4 * pcap);
   L.pr = take(4 * pcap);
   L.pgain = take(4 * pcap);
-  // pipelined: after the round-start product the same space holds this
-  // round's coefficients of the own tokens [ch][us] and the ring of loaded
-  // rows [kRing][ws]
-  L.pcol = take(4 * (pipe ? max(pcap * L.cs, ch * L.us + kRing * L.ws) : pcap * L.cs));
+  // pipelined: once the round's products are done the same space holds
+  // this round's coefficients of the own tokens [ch][us]
+  L.pcol = take(4 * (pipe ? max(pcap * L.cs, ch * L.us) : pcap * L.cs));
   L.U = take(4 * pcap * L.us);
   const int rbytes = 4 * pcap * L.rs, wbytes = 4 * pcap * L.ws;
   L.RW = take(rbytes > wbytes ? rbytes : wbytes);
@@ -650,12 +648,9 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   int* misc = reinterpret_cast<int*>(lds + L.misc);
   const int cs = L.cs, us = L.us, rs = L.rs, wsd = L.ws, ocs = L.ocs;
   float* ownC = reinterpret_cast<float*>(lds + L.ownC);  // PIPE: [ch][ocs] own rows, earlier rounds
-  float* Dm = reinterpret_cast<float*>(lds + L.D);       // PIPE: [pcap][wsd] earlier rounds' part
+  float* Dm = reinterpret_cast<float*>(lds + L.D);       // PIPE: [pcap][wsd] pool rows at the own tokens
   float* crow = pcol;                                    // PIPE, picks: [ch][us] this round's own rows
-  float* ring = pcol + ch * us;                          // PIPE, picks: [kRing][wsd] loaded rows
   int* npub = reinterpret_cast<int*>(lds + L.flags);     // PIPE: picks published this round
-  int* nload = npub + 1;                                 // rows loaded into the ring
-  int* ntri = npub + 2;                                  // rows finished
   int* pdone = npub + 3;                                 // round tag once the picks are over
   int* dready = npub + 4;                                // waves done with their D tiles
   float* r2acc = reinterpret_cast<float*>(lds + L.r2acc);  // PIPE: finisher's sums of squares
@@ -911,7 +906,10 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     // this round's coefficients start at zero, so the pick loop needs no masks
     for (int e = tid; e < pn * (us / 4); e += NT)
       reinterpret_cast<float4*>(U)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (PIPE && tid < 5 && tid != 3) npub[tid] = 0;  // npub, nload, ntri, dready
+    if (PIPE && tid == 0) {  // picks published, waves done with their tiles
+      npub[0] = 0;
+      npub[4] = 0;
+    }
     if (PIPE && t > 0 && pn > 0) {
       // The pool's residual Gram matrix, one float32 matrix-core product over
       // the t rows so far (columns t .. tk - 1 are zero):
@@ -1084,86 +1082,68 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       if (lane == 0) misc[3] = np;
       if (PIPE) __hip_atomic_store(pdone, round + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     } else if (PIPE) {
-      // D[m][i] = sum_{l<t0} c_{l,m} c_{l,i} (pool member m, own token i), four
-      // 32 x 32 tiles: wave 1 tile 0, wave 3 tile 1, wave 2 tiles 2 and 3.  The
-      // member columns share their space with this round's own rows and the
-      // ring, so the stages below start once every D tile is done.
-      if (t0 > 0 && pn > 0) {
+      // The own tokens are brought up to date while wave 0 picks (lane i
+      // serves own token i).  First every pool member's row at the own
+      // tokens, with the earlier rounds' part removed:
+      //   W[m][i] = S[m][i] - sum_{l<t0} c_{l,m} c_{l,i},
+      // four 32 x 32 tiles (wave 1 tile 0, wave 3 tile 1, wave 2 tiles 2 and
+      // 3), each tile's entries of S loaded before its products.  The member
+      // columns share their space with this round's own rows, so the
+      // finisher starts once every tile is done.  Then wave 1 finishes, in
+      // pick order, c_{k,i} = (W[pick_k][i] - sum_{k'<k} U[pick_k][k'] c_{k',i}) / r_k.
+      if (pn > 0) {
         const int r = lane & 31, h = lane >> 5;
         for (int q = wave == 1 ? 0 : wave == 3 ? 1 : 2; q < (wave == 2 ? 4 : (wave == 1 ? 1 : 2)); ++q) {
           const int ti = q >> 1, tj = q & 1;
+          const int col = c0 + min(32 * tj + r, cnt - 1);
+          float sv[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            sv[e] = S[(long long)midx[min(32 * ti + 8 * (e >> 2) + 4 * h + (e & 3), pn - 1)] * N + col];
           f32x16_t acc;
-          tile_product(pcol + min(32 * ti + r, pn - 1) * cs + 4 * h, ownC + min(32 * tj + r, cnt - 1) * ocs + 4 * h,
-                       (t0 + 7) & ~7, acc);
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+          if (t0 > 0)
+            tile_product(pcol + min(32 * ti + r, pn - 1) * cs + 4 * h, ownC + min(32 * tj + r, cnt - 1) * ocs + 4 * h,
+                         (t0 + 7) & ~7, acc);
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             const int m = 32 * ti + 8 * (e >> 2) + 4 * h + (e & 3);
-            if (m < pn) Dm[m * wsd + 32 * tj + r] = acc[e];
+            if (m < pn) Dm[m * wsd + 32 * tj + r] = sv[e] - acc[e];
           }
         }
       }
       if (lane == 0) __hip_atomic_fetch_add(dready, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);  // once per wave
-      if (wave != 2) {
-      while (__hip_atomic_load(dready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 3) __builtin_amdgcn_s_sleep(1);
-      if (wave == 1) {  // this round's own row starts at zero: the finishing dot needs no masks
-        float4* cz = reinterpret_cast<float4*>(crow + lane * us);
-        for (int e = 0; e < us / 4; ++e) cz[e] = make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-      // The own tokens are brought up to date while wave 0 picks (lane i
-      // serves own token i), in pick order:
-      //   wave 3  loads W_k[i] = S[pick_k][i] - D[pick_k][i] (the earlier
-      //           rounds' part came from the round-start product) for every
-      //           published pick, many rows in flight, into a ring of kRing;
-      //   wave 1  finishes c_{k,i} = (W_k[i] - sum_{k'<k} U[pick_k][k'] c_{k',i}) / r_k.
-      // Each stage publishes how many rows it has handled; the loader stays
-      // less than kRing rows ahead of the finisher.  A stage stops once the
-      // picks are over and it has handled every one of them, or when this
-      // round completes the selection (its update is then never used).
-      const int rtag = round + 1;
-      int k = 0;
-      int ready = 0;  // rows known to be available to this stage
-      float csq = 0.0f;  // finisher: sum of the own token's squared new coefficients
-      while (true) {
-        bool over = false;
-        if (k >= ready || (k & 7) == 0) {  // poll (and look for the end now and then)
-          while (true) {
-            if (__hip_atomic_load(pdone, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == rtag) {
-              const int fin = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
-              over = fin <= k || t0 + fin >= K;
+      if (wave == 1) {
+        while (__hip_atomic_load(dready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 3) __builtin_amdgcn_s_sleep(1);
+        float* cr = crow + lane * us;  // this round's own row: zero past the finished entries
+        for (int e = 0; e < us / 4; ++e) reinterpret_cast<float4*>(cr)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+        // The finisher stops once the picks are over and it has handled every
+        // one of them, or when this round completes the selection (its update
+        // is then never used).
+        const int rtag = round + 1;
+        int k = 0;
+        int ready = 0;  // picks known to be published
+        float csq = 0.0f;  // sum of the own token's squared new coefficients
+        while (true) {
+          bool over = false;
+          if (k >= ready || (k & 7) == 0) {  // poll (and look for the end now and then)
+            while (true) {
+              if (__hip_atomic_load(pdone, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == rtag) {
+                ready = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                over = ready <= k || t0 + ready >= K;
+              } else {
+                ready = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+              }
+              if (over || ready > k) break;
+              __builtin_amdgcn_s_sleep(1);
             }
             if (over) break;
-            if (wave == 3) {
-              const int avail = __hip_atomic_load(npub, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
-              const int room = __hip_atomic_load(ntri, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) + kRing;
-              ready = min(avail, room);
-            } else {
-              ready = __hip_atomic_load(nload, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
-            }
-            if (ready > k) break;
-            __builtin_amdgcn_s_sleep(1);
           }
-          if (over) break;
-        }
-        const int n = min(ready - k, kRing);
-        if (wave == 3) {
-          float v[kRing];
-          const int col = c0 + min(lane, cnt - 1);
-#pragma unroll
-          for (int u = 0; u < kRing; ++u)  // unconditional loads of valid rows
-            v[u] = S[(long long)midx[pslot[k + min(u, n - 1)]] * N + col];
-#pragma unroll
-          for (int u = 0; u < kRing; ++u)
-            if (u < n) {
-              const float dv = t0 > 0 ? Dm[pslot[k + u] * wsd + lane] : 0.0f;
-              ring[((k + u) & (kRing - 1)) * wsd + lane] = v[u] - dv;
-            }
-          k += n;
-          __hip_atomic_store(nload, k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-        } else {
-          const float* ur = U + pslot[k] * us;
-          float* cr = crow + lane * us;  // zero past the finished rows
+          const int sk = pslot[k];
+          const float* ur = U + sk * us;
           const float rk = prr[k];
-          const float w0 = ring[(k & (kRing - 1)) * wsd + lane];
+          const float w0 = Dm[sk * wsd + lane];
           // all reads first (one LDS round trip), products only for the
           // groups of 16 rows finished so far
           float4 u4[kMaxPool / 4], c4[kMaxPool / 4];
@@ -1190,12 +1170,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           if (lane < cnt) Ct[(long long)(c0 + lane) * Kp + t0 + k] = c;
           csq = fmaf(c, c, csq);
           ++k;
-          // progress for the loader's ring, every fourth row (the ring holds kRing)
-          if ((k & 3) == 0 || k >= ready)
-            __hip_atomic_store(ntri, k, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
-      }
-      if (wave == 1) r2acc[lane] = csq;
+        r2acc[lane] = csq;
       }
     }
     __syncthreads();
