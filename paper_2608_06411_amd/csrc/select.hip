@@ -52,11 +52,13 @@ __device__ __forceinline__ uint32_t ordered_bits(float f) {
   return (f > 0.0f && f <= 3.402823466e38f) ? __float_as_uint(f) : 0u;
 }
 
+// A positive Eq. (4) score p n r is keyed by its square (qn)^2 r^2, which
+// orders the same way and needs no square root per candidate.
 __device__ __forceinline__ uint64_t make_key(float r2, float qn, float p, int i, float tau2) {
   uint32_t hi = ordered_bits(p);
   if (r2 > tau2 && qn > 0.0f) {
-    const float s = qn * __builtin_amdgcn_sqrtf(r2);  // hardware square root (1 ulp)
-    if (s > 0.0f) hi = 0x80000000u | ordered_bits(s);
+    const float s2 = qn * qn * r2;
+    if (s2 > 0.0f) hi = 0x80000000u | ordered_bits(s2);
   }
   return (static_cast<uint64_t>(hi) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
 }
@@ -65,9 +67,9 @@ __device__ __forceinline__ int key_index(uint64_t k) {
   return static_cast<int>(0xffffffffu - static_cast<uint32_t>(k));
 }
 
-__device__ __forceinline__ float key_score(uint64_t k) {
+__device__ __forceinline__ float key_score(uint64_t k) {  // the Eq. (4) score of a key
   const uint32_t hi = static_cast<uint32_t>(k >> 32);
-  return (hi & 0x80000000u) ? __uint_as_float(hi & 0x7fffffffu) : 0.0f;
+  return (hi & 0x80000000u) ? __builtin_amdgcn_sqrtf(__uint_as_float(hi & 0x7fffffffu)) : 0.0f;  // hardware square root (1 ulp)
 }
 
 // Ranking by counting compares keys as doubles: hi * 2^14 + (16383 - index)
@@ -106,6 +108,11 @@ __device__ __forceinline__ uint32_t wave_umax32(uint32_t v) {
   v = dpp_umax<0x143, 0xc>(v);  // row_bcast:31 -> lane 63 holds the wave maximum
   return __builtin_amdgcn_readlane(v, 63);
 }
+
+template <int V>
+struct IntC {  // a compile-time integer argument
+  static constexpr int value = V;
+};
 
 // Lane n of each row of 16 lanes, broadcast to its row (DPP row_newbcast).
 template <int N_>
@@ -637,7 +644,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   float* mr2 = reinterpret_cast<float*>(lds + L.mr2);     // [2][pcap]
   uint64_t* mkey = reinterpret_cast<uint64_t*>(lds + L.mkey);  // [2][pcap]
   int* pslot = reinterpret_cast<int*>(lds + L.pslot);
-  float* prr = reinterpret_cast<float*>(lds + L.pr);
+  float* prr = reinterpret_cast<float*>(lds + L.pr);     // 1 / r of each pick (0: no basis vector)
   float* pgain = reinterpret_cast<float*>(lds + L.pgain);
   float* pcol = reinterpret_cast<float*>(lds + L.pcol);
   float* U = reinterpret_cast<float*>(lds + L.U);
@@ -1004,7 +1011,12 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       const int iv = in ? midx[lane] : 0;
       bool actv = in;
       const float* u0 = U + min(lane, pcap - 1) * us;  // member `lane`'s row (zero past np)
-      while (t < K) {
+      // One pick; NG = the number of groups of 16 picks made so far, so only
+      // those groups of the two U rows are read and multiplied.  Returns
+      // false when the round's picks are over.
+      auto pick = [&](auto ngc) -> bool {
+        constexpr int NG = decltype(ngc)::value;
+        if (t >= K) return false;
         int s;
         uint64_t best = 0;
         if (forced) {  // the pool is the top of p in descending order
@@ -1027,14 +1039,17 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           }
           s = best > beta ? sl : -1;
         }
-        if (s < 0) break;
+        // the previous picks are published here, one pick late, when their
+        // writes have long completed and the release costs no wait
+        if (PIPE && np > 0) __hip_atomic_store(npub, np, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (s < 0) return false;
         // a pick among the own tokens (wave 0's lanes when 64 tokens per workgroup)
         if (PIPE && __builtin_amdgcn_readlane(iv, s) == c0 + lane) my_state = 2;
         const float rm = Rm[s * rs + min(lane, pn - 1)];
         const float* usr = U + s * us;
-        float4 xs[kMaxPool / 4], y0[kMaxPool / 4];
+        float4 xs[4 * NG + 1], y0[4 * NG + 1];
 #pragma unroll
-        for (int q = 0; q < kMaxPool / 4; ++q) {
+        for (int q = 0; q < 4 * NG; ++q) {
           xs[q] = *reinterpret_cast<const float4*>(usr + 4 * q);
           y0[q] = *reinterpret_cast<const float4*>(u0 + 4 * q);
         }
@@ -1042,26 +1057,22 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         const float ns = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, nv), s));
         // no basis vector when the unit residual is at most tau (or the row is zero)
         const bool skip = !(r2s > a.tau2 && ns > 0.0f);
-        const float r = skip ? 0.0f : __builtin_amdgcn_sqrtf(r2s);
-        const float rinv = skip ? 0.0f : __builtin_amdgcn_rcpf(r);  // hardware reciprocal (1 ulp)
+        const float rinv = skip ? 0.0f : __builtin_amdgcn_rsqf(r2s);  // hardware reciprocal square root (1 ulp)
+        const float r = r2s * rinv;
         if (lane == 0) {
           pslot[np] = s;
-          prr[np] = r;
+          prr[np] = rinv;
           pgain[np] = forced ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pv), s))
                              : key_score(best);
         }
-        // dot over the picks so far, in groups of 16 (entries past np are zero)
+        // dot over the picks so far (entries past np are zero)
         float d4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int g = 0; g < kMaxPool / 16; ++g) {
-          if (16 * g >= np) break;
-#pragma unroll
-          for (int q = 4 * g; q < 4 * g + 4; ++q) {
-            d4[0] = fmaf(xs[q].x, y0[q].x, d4[0]);
-            d4[1] = fmaf(xs[q].y, y0[q].y, d4[1]);
-            d4[2] = fmaf(xs[q].z, y0[q].z, d4[2]);
-            d4[3] = fmaf(xs[q].w, y0[q].w, d4[3]);
-          }
+        for (int q = 0; q < 4 * NG; ++q) {
+          d4[0] = fmaf(xs[q].x, y0[q].x, d4[0]);
+          d4[1] = fmaf(xs[q].y, y0[q].y, d4[1]);
+          d4[2] = fmaf(xs[q].z, y0[q].z, d4[2]);
+          d4[3] = fmaf(xs[q].w, y0[q].w, d4[3]);
         }
         const float d = (d4[0] + d4[1]) + (d4[2] + d4[3]);
         if (in) {
@@ -1075,10 +1086,16 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           }
           U[lane * us + np] = c;
         }
-        if (PIPE) __hip_atomic_store(npub, np + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         ++t;
         ++np;
-      }
+        return true;
+      };
+      bool going = pick(IntC<0>{});
+      while (going && np <= 16) going = pick(IntC<1>{});
+      while (going && np <= 32) going = pick(IntC<2>{});
+      while (going && np <= 48) going = pick(IntC<3>{});
+      while (going) going = pick(IntC<4>{});
+      if (PIPE) __hip_atomic_store(npub, np, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
       if (lane == 0) misc[3] = np;
       if (PIPE) __hip_atomic_store(pdone, round + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     } else if (PIPE) {
@@ -1163,7 +1180,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
             }
           }
           const float v = w0 - ((e4[0] + e4[1]) + (e4[2] + e4[3]));
-          const float c = rk > 0.0f ? v * __builtin_amdgcn_rcpf(rk) : 0.0f;
+          const float c = v * rk;  // rk = 1 / r_k, zero when the pick adds no basis vector
           cr[k] = c;
           // the finished row goes straight to the own rows in LDS and to C
           ownC[lane * ocs + t0 + k] = c;
@@ -1302,7 +1319,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           float v = x[q];
 #pragma unroll
           for (int q2 = 0; q2 < q; ++q2) v = fmaf(-lblk[q][q2], x[q2], v);
-          x[q] = (q < nb && rblk[q] > 0.0f) ? v / rblk[q] : 0.0f;
+          x[q] = q < nb ? v * rblk[q] : 0.0f;  // rblk = 1 / r, zero when the pick adds no basis vector
         }
 #pragma unroll
         for (int q = 0; q < TB; ++q)
