@@ -37,12 +37,15 @@ def algorithmic_work(cfg, sumM):
     el = 2 if cfg.dtype == "bf16" else 4
     rows = B * N + sumM
     return {
-        # layer 1 of f_V and f_T, and the unique half (with the diagonal) of each Gram matrix
-        "gemm_layer1_gram": ("mfma", 2.0 * rows * D * H + B * N * (N + 1) * D, "flop"),
-        "gemm_layer2": ("mfma", 2.0 * rows * H * H, "flop"),
+        # layer 1 of f_V and f_T, the folded weights W_K W2 and W_Q W2, and the
+        # unique half (with the diagonal) of each Gram matrix
+        "gemm_layer1_gram": ("mfma", 2.0 * rows * D * H + 2.0 * 2 * dp * H * H + B * N * (N + 1) * D, "flop"),
+        # second layer and projection as one product with the folded weights
         "gemm_proj_rope": ("mfma", 2.0 * rows * H * dp, "flop"),
-        # read V, write norms, 1/norms and the cos/sin table
-        "prep": ("hbm", B * N * D * el + 8.0 * B * N + 8.0 * rows * dp / 2, "byte"),
+        # read V, write norms, 1/norms and the cos/sin table; transpose the two
+        # second-layer weights and fold the biases
+        "prep": ("hbm", B * N * D * el + 8.0 * B * N + 8.0 * rows * dp / 2 + 2 * 2.0 * H * H * el
+                 + 2 * (dp * H + H) * el + 8.0 * dp, "byte"),
         # read the selection order and the kept rows, write the rows, indices and positions
         "gather": ("hbm", 2.0 * B * K * D * el + 16.0 * B * K, "byte"),
         # read keys and queries, write logits and per-block (max, sum of exp)
@@ -63,7 +66,6 @@ def algorithmic_work(cfg, sumM):
 KERNEL_SOURCES = {
     "prep": ("prep.hip", "internal.h"),
     "gemm_layer1_gram": ("gemm.hip", "internal.h"),
-    "gemm_layer2": ("gemm.hip", "internal.h"),
     "gemm_proj_rope": ("gemm.hip", "internal.h"),
     "logits": ("score.hip", "internal.h"),
     "softmax_mean": ("score.hip", "internal.h"),

@@ -124,7 +124,10 @@ size_t map_prune_workspace(map_dtype dt, int B, int N, int sum_M, const map_weig
  *                    t_off[0] == 0, strictly increasing, t_off[B] == sum_M
  * p_out  [B][N]      float32 output; each row sums to 1.
  * Hidden activations are stored in dt (bf16 in bf16 calls), accumulation is
- * float32, keys and queries are float32. */
+ * float32, keys and queries are float32.  The second MLP layer and the
+ * projection are applied as one product: W_K f_V(v) = (W_K W2) h + W_K b2 with
+ * h the first layer's output (likewise W_Q and f_T); the folded weights are
+ * formed inside every call, in dt, from the weights passed. */
 map_status map_score(const map_weights* w, map_dtype dt, int B, int N,
                      const void* V, const int32_t* pos_v,
                      const void* T, const int32_t* pos_t, const int32_t* t_off_host,

@@ -149,7 +149,7 @@ __device__ __forceinline__ void epilogue(const GemmProblem& P, int bt, int tm, i
     for (int j = 0; j < 2; ++j) {
       const int col = n0 + wn * 64 + j * 32 + acc_col(lane);
       if (col >= N) continue;
-      const float bv = to_f32<T>(bias[col]);
+      const float bv = bias ? to_f32<T>(bias[col]) : 0.0f;
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -196,17 +196,19 @@ __device__ __forceinline__ void epilogue(const GemmProblem& P, int bt, int tm, i
           }
         }
     }
-  } else {  // EPI_ROPE: stage the tile in LDS so each thread sees both halves of a pair
+  } else {  // EPI_ROPE: stage the tile (plus the bias) in LDS so each thread sees both halves of a pair
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 2; ++j) {
+      const int cl = wn * 64 + j * 32 + acc_col(lane);
+      const float bv = (P.rope_bias && n0 + cl < N) ? P.rope_bias[n0 + cl] : 0.0f;
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int rl = wm * 64 + i * 32 + acc_row(r, lane);
-          const int cl = wn * 64 + j * 32 + acc_col(lane);
-          (rl < 64 ? tile_lo : tile_hi)[(rl & 63) * BN + cl] = acc[i][j][r];
+          (rl < 64 ? tile_lo : tile_hi)[(rl & 63) * BN + cl] = acc[i][j][r] + bv;
         }
+    }
     __syncthreads();
     float* __restrict__ out = static_cast<float*>(P.C) + bt * P.strideC;
     const int half = N >> 1;
@@ -353,7 +355,7 @@ __device__ __forceinline__ void epi_bias_staged(const GemmProblem& P, int bt, in
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int cl = wn * 64 + j * 32 + acc_col(lane);
-    const float bv = n0 + cl < N ? bf16_to_f32(bias[n0 + cl]) : 0.0f;
+    const float bv = (bias && n0 + cl < N) ? bf16_to_f32(bias[n0 + cl]) : 0.0f;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll

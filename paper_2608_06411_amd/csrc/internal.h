@@ -71,9 +71,9 @@ hipError_t launch_kernel(const char* name, void (*kernel)(P...), dim3 grid, dim3
 // share one launch; each may be batched.
 enum EpiMode : int {
   EPI_BIAS_GELU = 0,  // C[m][n] = GELU(acc + bias[n]), stored as T
-  EPI_BIAS = 1,       // C[m][n] = acc + bias[n], stored as T
+  EPI_BIAS = 1,       // C[m][n] = acc + bias[n] (no bias when null), stored as T
   EPI_COSINE = 2,     // S[m][n] = acc * rs[m] * rs[n] (float32), mirrored; A == B
-  EPI_ROPE = 3,       // out[m][:] = RoPE(acc[m][:]) (float32) with the row's cos/sin
+  EPI_ROPE = 3,       // out[m][:] = RoPE(acc[m][:] + rope_bias) (float32) with the row's cos/sin
 };
 
 struct GemmProblem {
@@ -87,12 +87,13 @@ struct GemmProblem {
   const void* bias;        // EPI_BIAS*: [N], element type T
   const float* rs;         // EPI_COSINE: [batch][M] reciprocal norms
   const float2* rope_cs;   // EPI_ROPE: [M][N/2] (cos, sin) per row and pair
+  const float* rope_bias;  // EPI_ROPE: [N] float32 added before the rotation (may be null)
   int triangular;          // EPI_COSINE: only tiles with tile_n >= tile_m
   // filled by the host helper
   int tiles_m, tiles_n, tiles_per_batch, tile_begin;
 };
 
-constexpr int kMaxGemmProblems = 4;
+constexpr int kMaxGemmProblems = 6;
 struct GemmBatch {
   GemmProblem p[kMaxGemmProblems];
   int count;
@@ -117,8 +118,18 @@ struct PrepArgs {
   float2* cs_v;           // [rowsV][half]
   float2* cs_t;           // [rowsT][half]
   double inv_freq[64];    // theta^(-2i/d_p), computed on the host in float64
+  // the folded second layer and projection (one pair per modality):
+  //   tdst[s] = tsrc[s]^T           (square, tn x tn, element type of the call)
+  //   fout[s][o] = sum_k fw[s][o][k] fb[s][k]   (o < frows, k < fcols, float32)
+  const void* tsrc[2];
+  void* tdst[2];
+  int tn;
+  const void* fw[2];
+  const void* fb[2];
+  float* fout[2];
+  int frows, fcols;
 };
-hipError_t launch_prep(map_dtype dt, const PrepArgs& a, bool norms, bool table, hipStream_t s);
+hipError_t launch_prep(map_dtype dt, const PrepArgs& a, bool norms, bool table, bool fold, hipStream_t s);
 
 // ---------------------------------------------------------------- score
 struct ScoreArgs {

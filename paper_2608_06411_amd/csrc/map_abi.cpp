@@ -83,7 +83,10 @@ map_status check_ws(void* ws, size_t have, size_t need) {
 // ------------------------------------------------------------ layouts
 struct ScoreWs {
   float2 *cs_v, *cs_t;
-  void *h1_v, *h2_v, *h1_t, *h2_t;
+  void *h1_v, *h1_t;
+  void *w2t_v, *w2t_t;  // W2^T of f_V, f_T
+  void *wc_v, *wc_t;    // folded W_K W2, W_Q W2 [d_p][D_h]
+  float *bc_v, *bc_t;   // folded W_K b2, W_Q b2 [d_p]
   float *k, *q, *logits;
   float2* partial;
 };
@@ -95,9 +98,13 @@ ScoreWs carve_score(Carver& c, map_dtype dt, int B, int N, int sumM, const map_w
   s.cs_v = c.take<float2>(rowsV * half);
   s.cs_t = c.take<float2>((size_t)sumM * half);
   s.h1_v = c.take_bytes(rowsV * w.D_h * elem_size(dt));
-  s.h2_v = c.take_bytes(rowsV * w.D_h * elem_size(dt));
   s.h1_t = c.take_bytes((size_t)sumM * w.D_h * elem_size(dt));
-  s.h2_t = c.take_bytes((size_t)sumM * w.D_h * elem_size(dt));
+  s.w2t_v = c.take_bytes((size_t)w.D_h * w.D_h * elem_size(dt));
+  s.w2t_t = c.take_bytes((size_t)w.D_h * w.D_h * elem_size(dt));
+  s.wc_v = c.take_bytes((size_t)w.d_p * w.D_h * elem_size(dt));
+  s.wc_t = c.take_bytes((size_t)w.d_p * w.D_h * elem_size(dt));
+  s.bc_v = c.take<float>(w.d_p);
+  s.bc_t = c.take<float>(w.d_p);
   s.k = c.take<float>(rowsV * w.d_p);
   s.q = c.take<float>((size_t)sumM * w.d_p);
   s.logits = c.take<float>((size_t)sumM * N);
@@ -195,7 +202,23 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   pa.cs_v = s.cs_v;
   pa.cs_t = s.cs_t;
   fill_inv_freq(pa, w);
-  hipError_t e = launch_prep(dt, pa, norms != nullptr, true, st);
+  // the second layer and the projection as one product: W_K (W2 h + b2) =
+  // (W_K W2) h + W_K b2 (and W_Q with f_T's second layer); prep transposes W2
+  // and forms the folded biases, the layer-1 launch forms W_K W2
+  pa.tsrc[0] = w.w2_v;
+  pa.tsrc[1] = w.w2_t;
+  pa.tdst[0] = s.w2t_v;
+  pa.tdst[1] = s.w2t_t;
+  pa.tn = w.D_h;
+  pa.fw[0] = w.w_k;
+  pa.fw[1] = w.w_q;
+  pa.fb[0] = w.b2_v;
+  pa.fb[1] = w.b2_t;
+  pa.fout[0] = s.bc_v;
+  pa.fout[1] = s.bc_t;
+  pa.frows = w.d_p;
+  pa.fcols = w.D_h;
+  hipError_t e = launch_prep(dt, pa, norms != nullptr, true, true, st);
   if (e != hipSuccess) return e;
 
   GemmBatch g1;
@@ -204,23 +227,20 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   g1.p[1] = linear(T, sumM, w.w1_t, w.b1_t, s.h1_t, w.D_h, w.D, EPI_BIAS_GELU);
   g1.count = 2;
   if (extra_l1) g1.p[g1.count++] = *extra_l1;
+  // last, so their few short tiles fill the launch's final wave
+  g1.p[g1.count++] = linear(w.w_k, w.d_p, s.w2t_v, nullptr, s.wc_v, w.D_h, w.D_h, EPI_BIAS);  // W_K W2
+  g1.p[g1.count++] = linear(w.w_q, w.d_p, s.w2t_t, nullptr, s.wc_t, w.D_h, w.D_h, EPI_BIAS);  // W_Q W2
   gemm_finalize(g1);
   if ((e = launch_gemm(dt, g1, extra_l1 ? "gemm_layer1_gram" : "gemm_layer1", st)) != hipSuccess) return e;
 
-  GemmBatch g2;
-  memset(&g2, 0, sizeof(g2));
-  g2.p[0] = linear(s.h1_v, rowsV, w.w2_v, w.b2_v, s.h2_v, w.D_h, w.D_h, EPI_BIAS);
-  g2.p[1] = linear(s.h1_t, sumM, w.w2_t, w.b2_t, s.h2_t, w.D_h, w.D_h, EPI_BIAS);
-  g2.count = 2;
-  gemm_finalize(g2);
-  if ((e = launch_gemm(dt, g2, "gemm_layer2", st)) != hipSuccess) return e;
-
   GemmBatch g3;
   memset(&g3, 0, sizeof(g3));
-  g3.p[0] = linear(s.h2_v, rowsV, w.w_k, nullptr, s.k, w.d_p, w.D_h, EPI_ROPE);
+  g3.p[0] = linear(s.h1_v, rowsV, s.wc_v, nullptr, s.k, w.d_p, w.D_h, EPI_ROPE);
   g3.p[0].rope_cs = s.cs_v;
-  g3.p[1] = linear(s.h2_t, sumM, w.w_q, nullptr, s.q, w.d_p, w.D_h, EPI_ROPE);
+  g3.p[0].rope_bias = s.bc_v;
+  g3.p[1] = linear(s.h1_t, sumM, s.wc_t, nullptr, s.q, w.d_p, w.D_h, EPI_ROPE);
   g3.p[1].rope_cs = s.cs_t;
+  g3.p[1].rope_bias = s.bc_t;
   g3.count = 2;
   gemm_finalize(g3);
   if ((e = launch_gemm(dt, g3, "gemm_proj_rope", st)) != hipSuccess) return e;
@@ -407,7 +427,7 @@ map_status map_similarity(map_dtype dt, int B, int N, int D, const void* V, floa
   pa.D = D;
   pa.norms = norms_out;
   pa.ninv = ninv;
-  hipError_t e = launch_prep(dt, pa, true, false, st);
+  hipError_t e = launch_prep(dt, pa, true, false, false, st);
   if (e != hipSuccess) return MAP_ERR_HIP;
   GemmBatch g;
   memset(&g, 0, sizeof(g));
