@@ -2,8 +2,8 @@
 // indices (section "Inference-Time Token Pruning": the selected tokens are
 // restored to their original order and keep their positions).
 //
-// One workgroup per kept row k: it finds the index of rank k in the
-// selection order (indices are distinct, so the rank of an index is the
+// One workgroup per kept row k: it stages the selection order in LDS, finds
+// the index of rank k (indices are distinct, so the rank of an index is the
 // number of smaller ones), writes it, and copies the row byte-exactly with
 // 16-byte loads and stores, every load of a thread issued before its first
 // store.  After an aborted selection every index is -1, every position -1
@@ -15,18 +15,26 @@ namespace mapk {
 namespace {
 
 __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
+  extern __shared__ int ord[];  // [K rounded up to 8] the selection order (padding: past any index)
   __shared__ int found;
-  const int b = blockIdx.y, k = blockIdx.x, K = a.K;
+  const int b = blockIdx.y, k = blockIdx.x, K = a.K, K8 = (K + 7) & ~7;
   const int chunks = a.row_bytes >> 4;
   if (threadIdx.x == 0) found = -1;
-  __syncthreads();
   const bool aborted = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
-  const int32_t* ord = a.order + (long long)b * K;
+  for (int j = threadIdx.x; j < K8; j += 256) ord[j] = j < K ? a.order[(long long)b * K + j] : 0x7fffffff;
+  __syncthreads();
   for (int j = threadIdx.x; j < K && !aborted; j += 256) {
     const int v = ord[j];
-    int rank = 0;
-    for (int q = 0; q < K; ++q) rank += ord[q] < v;
-    if (rank == k) found = v;
+    int r4[4] = {0, 0, 0, 0};
+    for (int q = 0; q < K8; q += 8) {  // eight LDS broadcasts per step, four counters
+      const int4 x = *reinterpret_cast<const int4*>(ord + q);
+      const int4 y = *reinterpret_cast<const int4*>(ord + q + 4);
+      r4[0] += (x.x < v) + (y.x < v);
+      r4[1] += (x.y < v) + (y.y < v);
+      r4[2] += (x.z < v) + (y.z < v);
+      r4[3] += (x.w < v) + (y.w < v);
+    }
+    if ((r4[0] + r4[1]) + (r4[2] + r4[3]) == k) found = v;
   }
   __syncthreads();
   const int i = found;
@@ -53,7 +61,8 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
 }  // namespace
 
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
-  return launch_kernel("gather", gather_kernel, dim3(a.K, a.B), dim3(256), 0, s, a);
+  return launch_kernel("gather", gather_kernel, dim3(a.K, a.B), dim3(256),
+                       sizeof(int) * static_cast<size_t>((a.K + 7) & ~7), s, a);
 }
 
 }  // namespace mapk

@@ -21,7 +21,7 @@ namespace {
 
 constexpr int KB = 64;    // visual tokens per workgroup
 constexpr int QB = 16;    // question tokens per workgroup
-constexpr int DPAD = 129; // padded LDS row (d_p <= 128)
+constexpr int DPAD = 132; // padded LDS row (d_p <= 128): 4 times an odd number, 16-byte aligned
 
 __global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
   __shared__ float ks[KB][DPAD];
@@ -67,10 +67,17 @@ __global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
   __syncthreads();
   const int tm = tid >> 4, tn = tid & 15;  // query q0 + tm, keys 4 tn .. 4 tn + 3
   float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int d = 0; d < dp; ++d) {
-    const float qv = qs[tm][d];
+#pragma unroll 4
+  for (int d = 0; d < dp; d += 4) {  // d_p is a multiple of 4
+    const float4 qv = *reinterpret_cast<const float4*>(&qs[tm][d]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = fmaf(qv, ks[4 * tn + j][d], acc[j]);
+    for (int j = 0; j < 4; ++j) {
+      const float4 kv = *reinterpret_cast<const float4*>(&ks[4 * tn + j][d]);
+      acc[j] = fmaf(qv.x, kv.x, acc[j]);
+      acc[j] = fmaf(qv.y, kv.y, acc[j]);
+      acc[j] = fmaf(qv.z, kv.z, acc[j]);
+      acc[j] = fmaf(qv.w, kv.w, acc[j]);
+    }
   }
   const int m = q0 + tm;
   float mx = -INFINITY;
