@@ -2,11 +2,10 @@
 // the mean over the question tokens.
 //
 // logits_kernel: one workgroup per (block of 64 visual tokens, chunk of 16
-// question tokens, image).  The block's keys and the chunk's queries sit in
-// LDS; each thread forms q.k / sqrt(d_p) in float32 for one query and four
-// keys, and the 16 lanes that share a query also emit the running (max, sum
-// of exp) of its 64 logits, so that no pass over a whole logits row is needed
-// later.
+// question tokens, image).  Each wave forms a 16 x 16 tile of q.k / sqrt(d_p)
+// on float32 matrix cores from operands read straight from global memory, and
+// the workgroup also emits each query's (max, sum of exp) over its 64 logits,
+// so that no pass over a whole logits row is needed later.
 //
 // softmax_mean_kernel: one workgroup per (block of 64 visual tokens, image).
 // Each workgroup folds the per-block partials of its image into the row
@@ -21,91 +20,86 @@ namespace {
 
 constexpr int KB = 64;    // visual tokens per workgroup
 constexpr int QB = 16;    // question tokens per workgroup
-constexpr int DPAD = 132; // padded LDS row (d_p <= 128): 4 times an odd number, 16-byte aligned
+
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 __global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
-  __shared__ float ks[KB][DPAD];
-  __shared__ float qs[QB][DPAD];
+  __shared__ float wmax[4][QB];
+  __shared__ float wsum[4][QB];
   const int blk = blockIdx.x, q0 = blockIdx.y * QB, b = blockIdx.z, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const int n0 = blk * KB, dp = a.d_p;
   const int mb = a.t_off[b], M = a.t_off[b + 1] - mb;
   if (q0 >= M) return;
+  // Wave w forms the 16 x 16 tile (queries q0 .. q0 + 15) x (keys n0 + 16 w ..)
+  // on float32 16 x 16 x 4 matrix cores.  Lane l supplies query row l & 15
+  // and key row l & 15 at d = 16 t + 4 (l >> 4) + e to the e-th product of
+  // step t, read as one float4 straight from global memory (rows past the
+  // data read the last row; entries past d_p are zero).
+  const int r = lane & 15, g = lane >> 4;
+  const float* qr = a.q + (long long)(mb + min(q0 + r, M - 1)) * dp;
+  const float* kr = a.k + ((long long)b * a.N + min(n0 + 16 * wave + r, a.N - 1)) * dp;
+  constexpr int TS = 8;  // steps of 16 for d_p <= 128
+  f32x4_t qv[TS], kv[TS];
+#pragma unroll
+  for (int t = 0; t < TS; ++t) {  // every load issued before the first product
+    const int d = min(16 * t + 4 * g, dp - 4);
+    qv[t] = *reinterpret_cast<const f32x4_t*>(qr + d);
+    kv[t] = *reinterpret_cast<const f32x4_t*>(kr + d);
+  }
+  __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the products
+  f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int t = 0; t < TS; ++t) {
+    const float in = 16 * t + 4 * g < dp ? 1.0f : 0.0f;  // zero past d_p (the load was clamped)
+    qv[t] *= in;
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[t].x, kv[t].x, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[t].y, kv[t].y, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[t].z, kv[t].z, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qv[t].w, kv[t].w, acc, 0, 0, 0);
+  }
+  // acc[i]: query q0 + 4 g + i, key n0 + 16 w + r
   const float scale = 1.0f / sqrtf(static_cast<float>(dp));
-  const int q4 = dp >> 2;
-  {  // keys and queries: float4 loads at clamped addresses, all issued before the LDS stores
-    constexpr int U = (KB + QB) * 32 / 256;  // pieces per thread for d_p = 128
-    float4 v[U];
-    const int kt = KB * q4, total = (KB + QB) * q4;
+  const int n = n0 + 16 * wave + r;
+  const bool nok = n < a.N;
+  float mx[4];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int e = min(tid + u * 256, total - 1);
-      const bool key = e < kt;
-      const int r = key ? e / q4 : (e - kt) / q4, d4 = key ? e - r * q4 : (e - kt) - r * q4;
-      const float* src = key ? a.k + ((long long)b * a.N + min(n0 + r, a.N - 1)) * dp
-                             : a.q + (long long)(mb + min(q0 + r, M - 1)) * dp;
-      v[u] = *reinterpret_cast<const float4*>(src + 4 * d4);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int e = tid + u * 256;
-      if (e >= total) continue;
-      const bool key = e < kt;
-      const int r = key ? e / q4 : (e - kt) / q4, d4 = key ? e - r * q4 : (e - kt) - r * q4;
-      float* dst = key ? &ks[r][4 * d4] : &qs[r][4 * d4];
-      dst[0] = v[u].x; dst[1] = v[u].y; dst[2] = v[u].z; dst[3] = v[u].w;
-    }
-    for (int e = tid + U * 256; e < total; e += 256) {  // (not reached for d_p <= 128)
-      const bool key = e < kt;
-      const int r = key ? e / q4 : (e - kt) / q4, d4 = key ? e - r * q4 : (e - kt) - r * q4;
-      const float* src = key ? a.k + ((long long)b * a.N + min(n0 + r, a.N - 1)) * dp
-                             : a.q + (long long)(mb + min(q0 + r, M - 1)) * dp;
-      const float4 x = *reinterpret_cast<const float4*>(src + 4 * d4);
-      float* dst = key ? &ks[r][4 * d4] : &qs[r][4 * d4];
-      dst[0] = x.x; dst[1] = x.y; dst[2] = x.z; dst[3] = x.w;
-    }
+  for (int i = 0; i < 4; ++i) {
+    acc[i] *= scale;
+    const int m = q0 + 4 * g + i;
+    if (m < M && nok) a.logits[(long long)(mb + m) * a.N + n] = acc[i];
+    mx[i] = nok ? acc[i] : -INFINITY;
   }
+  // per query: the maximum over the block's 64 keys (the 16 lanes of a group
+  // hold one query's 16 keys of this wave), then the sum of exp in a fixed order
+#pragma unroll
+  for (int off = 8; off > 0; off >>= 1)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mx[i] = fmaxf(mx[i], __shfl_xor(mx[i], off, 16));
+  if (r == 0)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) wmax[wave][4 * g + i] = mx[i];
   __syncthreads();
-  const int tm = tid >> 4, tn = tid & 15;  // query q0 + tm, keys 4 tn .. 4 tn + 3
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll 4
-  for (int d = 0; d < dp; d += 4) {  // d_p is a multiple of 4
-    const float4 qv = *reinterpret_cast<const float4*>(&qs[tm][d]);
+  float sm[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float4 kv = *reinterpret_cast<const float4*>(&ks[4 * tn + j][d]);
-      acc[j] = fmaf(qv.x, kv.x, acc[j]);
-      acc[j] = fmaf(qv.y, kv.y, acc[j]);
-      acc[j] = fmaf(qv.z, kv.z, acc[j]);
-      acc[j] = fmaf(qv.w, kv.w, acc[j]);
-    }
+  for (int i = 0; i < 4; ++i) {
+    const int qi = 4 * g + i;
+    const float bm = fmaxf(fmaxf(wmax[0][qi], wmax[1][qi]), fmaxf(wmax[2][qi], wmax[3][qi]));
+    mx[i] = bm;
+    sm[i] = nok ? expf(acc[i] - bm) : 0.0f;
   }
-  const int m = q0 + tm;
-  float mx = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    acc[j] *= scale;
-    if (n0 + 4 * tn + j < a.N) mx = fmaxf(mx, acc[j]);
-  }
-  if (m < M) {
-    float* row = a.logits + (long long)(mb + m) * a.N + n0 + 4 * tn;
-    if ((a.N & 3) == 0 && n0 + 4 * tn + 3 < a.N) {
-      *reinterpret_cast<float4*>(row) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-    } else {
+  for (int off = 8; off > 0; off >>= 1)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (n0 + 4 * tn + j < a.N) row[j] = acc[j];
-    }
-  }
-  // the 16 lanes sharing tm are 16 consecutive lanes
+    for (int i = 0; i < 4; ++i) sm[i] += __shfl_xor(sm[i], off, 16);
+  if (r == 0)
 #pragma unroll
-  for (int off = 8; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 16));
-  float sm = 0.0f;
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (n0 + 4 * tn + j < a.N) sm += expf(acc[j] - mx);
-#pragma unroll
-  for (int off = 8; off > 0; off >>= 1) sm += __shfl_xor(sm, off, 16);
-  if (tn == 0 && m < M) a.partial[(long long)(mb + m) * a.nblk + blk] = make_float2(mx, sm);
+    for (int i = 0; i < 4; ++i) wsum[wave][4 * g + i] = sm[i];
+  __syncthreads();
+  if (tid < QB && q0 + tid < M)
+    a.partial[(long long)(mb + q0 + tid) * a.nblk + blk] =
+        make_float2(fmaxf(fmaxf(wmax[0][tid], wmax[1][tid]), fmaxf(wmax[2][tid], wmax[3][tid])),
+                    (wsum[0][tid] + wsum[1][tid]) + (wsum[2][tid] + wsum[3][tid]));
 }
 
 __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
@@ -117,6 +111,16 @@ __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
     for (int i = tid; i < a.B; i += 256) a.clear_bar[i] = 0u;
     if (tid == 0) *a.clear_err = 0;
   }
+  // the first LU logits of this thread's token (question tokens g, g + 4,
+  // ...) are loaded now, at clamped addresses, so that they arrive while the
+  // row statistics are formed
+  const int c = tid & (KB - 1), g = tid >> 6;  // token, slice of question tokens
+  const int n = blk * KB + c;
+  constexpr int LU = 16;
+  float l0[LU];
+#pragma unroll
+  for (int u = 0; u < LU; ++u)
+    l0[u] = a.logits[(long long)(mb + min(g + 4 * u, M - 1)) * a.N + min(n, a.N - 1)];
   // row statistics from the per-block partials: four threads per row, each
   // folding every fourth block (all loads in flight), then the four
   // (max, sum) pairs combined in a fixed order
@@ -153,11 +157,17 @@ __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
     if (qtr == 0 && m < M) stats[m] = make_float2(mx, 1.0f / sm);
   }
   __syncthreads();
-  const int c = tid & (KB - 1), g = tid >> 6;  // token, slice of question tokens
-  const int n = blk * KB + c;
   float acc = 0.0f;
-  if (n < a.N)
-    for (int m0 = g; m0 < M; m0 += 4 * 8) {
+  if (n < a.N) {
+#pragma unroll
+    for (int u = 0; u < LU; ++u) {
+      const int m = g + 4 * u;
+      if (m < M) {
+        const float2 st = stats[m];
+        acc += expf(l0[u] - st.x) * st.y;
+      }
+    }
+    for (int m0 = g + 4 * LU; m0 < M; m0 += 4 * 8) {
       float l[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -173,6 +183,7 @@ __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
         }
       }
     }
+  }
   part[g][c] = acc;
   __syncthreads();
   if (g == 0 && n < a.N)
