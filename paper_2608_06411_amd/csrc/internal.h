@@ -102,6 +102,9 @@ struct GemmBatch {
 
 void gemm_finalize(GemmBatch& g);  // computes the tile counts
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s);
+// The projection with the RoPE epilogue (every problem EPI_ROPE, at most two):
+// a K-split kernel for bf16 and N <= 128, else launch_gemm.
+hipError_t launch_proj_rope(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s);
 
 // ---------------------------------------------------------------- prep
 // Row norms of the visual tokens (and their reciprocals) plus the RoPE

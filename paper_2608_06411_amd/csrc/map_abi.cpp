@@ -243,7 +243,7 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   g3.p[1].rope_bias = s.bc_t;
   g3.count = 2;
   gemm_finalize(g3);
-  if ((e = launch_gemm(dt, g3, "gemm_proj_rope", st)) != hipSuccess) return e;
+  if ((e = launch_proj_rope(dt, g3, "gemm_proj_rope", st)) != hipSuccess) return e;
 
   ScoreArgs sa;
   memset(&sa, 0, sizeof(sa));
