@@ -245,8 +245,10 @@ typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
 __host__ __device__ inline bool r0_by_factor(int K0) { return K0 > 0 && K0 <= kR0Max; }
 
+constexpr int kAs = 20;  // row stride of a solve operator: 4 times an odd number
+
 struct R0Lds {
-  int X, r0, ri, cand, kmax, misc, bytes;
+  int X, r0, ainv, cand, kmax, misc, flags, bytes;
   int K0p, xs, xrows;
 };
 
@@ -259,10 +261,11 @@ __host__ __device__ inline R0Lds r0_layout(int K0) {
   L.xrows = 64 * ((L.K0p + 64 + 63) / 64);  // R0 rows, then 64 own rows, in whole blocks of 64
   L.X = take(4 * L.xrows * L.xs);
   L.r0 = take(4 * L.K0p);
-  L.ri = take(4 * L.K0p);
+  L.ainv = take(4 * L.K0p * kAs);  // [K0p / 16][16][kAs]
   L.cand = take(8 * (kR0Cand + 8));
   L.kmax = take(8 * NT);
   L.misc = take(16);
+  L.flags = take(16);
   L.bytes = o;
   return L;
 }
@@ -287,7 +290,8 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
   const R0Lds R = r0_layout(K0);
   float* X = reinterpret_cast<float*>(lds + R.X);
   int* r0 = reinterpret_cast<int*>(lds + R.r0);
-  float* riv = reinterpret_cast<float*>(lds + R.ri);
+  float* Ainv = reinterpret_cast<float*>(lds + R.ainv);
+  int* flg = reinterpret_cast<int*>(lds + R.flags);
   double* cand = reinterpret_cast<double*>(lds + R.cand);  // rank values
   double* kmax = reinterpret_cast<double*>(lds + R.kmax);
   int* ncand = reinterpret_cast<int*>(lds + R.misc);
@@ -396,7 +400,6 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
 
   // ---- the factorisation
   {
-    const bool first = true;
     const int ocnt = cnt;
     // X[row][c] = S[r0[c]][token(row)]: lane = row within a block of 64 rows,
     // wave w takes columns w, w + 4, ...  R0 rows load only their strictly
@@ -457,117 +460,151 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
         a.gain[(long long)b * K + tid] = (pmine > 0.0f && pmine <= 3.402823466e38f) ? pmine : 0.0f;
       }
     }
+    if (tid == 0) {
+      flg[0] = 0;  // pivots done
+      flg[1] = 0;  // row blocks past the diagonal solved by wave 0
+      flg[2] = 1;  // next diagonal block prepared (nothing to prepare for block 1)
+    }
     __syncthreads();
-    for (int jb = 0; jb < nb; ++jb) {
-      const int J0 = 16 * jb;
-      if (jb > 0) {
-        // update: 16-row tiles, the R0 rows at or past J0 (pass 0) and the own
-        // rows; lane group g supplies k = 16 s + 4 g + e to the e-th product
-        // of step s.  The diagonal block's columns (B) are read once per wave.
-        constexpr int KS = kR0Max / 16;
-        const int nr = first ? nb - jb : 0;
-        const int nown = (ocnt + 15) >> 4;
-        const float* brow = X + (J0 + (lane & 15)) * xs + 4 * (lane >> 4);
-        f32x4_t bv[KS];
-#pragma unroll
-        for (int s = 0; s < KS; ++s)
-          if (s < jb) bv[s] = *reinterpret_cast<const f32x4_t*>(brow + 16 * s);
-        for (int tile = wave; tile < nr + nown; tile += NT / 64) {
-          const int rbase = tile < nr ? J0 + 16 * tile : K0p + 16 * (tile - nr);
-          const float* arow = X + (rbase + (lane & 15)) * xs + 4 * (lane >> 4);
-          float* drow = X + (rbase + 4 * (lane >> 4)) * xs + J0 + (lane & 15);
-          float cur[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) cur[e] = drow[e * xs];
-          f32x4_t av[KS];
-#pragma unroll
-          for (int s = 0; s < KS; ++s)
-            if (s < jb) av[s] = *reinterpret_cast<const f32x4_t*>(arow + 16 * s);
-          f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-          for (int s = 0; s < KS; ++s)
-            if (s < jb) {
-              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].x, bv[s].x, acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].y, bv[s].y, acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].z, bv[s].z, acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].w, bv[s].w, acc, 0, 0, 0);
-            }
-          // result row 4 (lane >> 4) + e, column lane & 15
-#pragma unroll
-          for (int e = 0; e < 4; ++e) drow[e * xs] = cur[e] - acc[e];
-        }
+    // Row block R is rows 16 R .. 16 R + 15 of X for R < nb (R0) and own rows
+    // 16 (R - nb) .. for R >= nb.  Column block j is columns 16 j ...
+    //   pivot j   factor the diagonal block (j, j), already brought up to date,
+    //             into its solve operator A_j (A_j b solves L_jj y = b, with
+    //             the entries of skipped pivots zero)
+    //   P(R, j)   X[R][j] = X[R][j] A_j^T (the coefficients on pivots of block j)
+    //   U(R, c)   X[R][c] -= X[R][0:16 c] X[c][0:16 c]^T
+    // Wave 0 runs the chain pivot j, P(j+1, j), the last term of U(j+1, j+1),
+    // pivot j+1, ...; waves 1 to 3 run every other row block (block R on wave
+    // 1 + R % 3): in phase j, P(R, j) and U(R, j+1), and for R = j + 2 also
+    // U(R, R) over the blocks up to j, which wave 0 needs next.  Three LDS
+    // counters order the two sides: pivots done, wave 0's P(j+1, j) stored,
+    // next diagonal block prepared.
+    const int nown = (ocnt + 15) >> 4;
+    auto wait_ge = [&](const int* f, int v) {
+      while (__hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < v) {
       }
-      __syncthreads();
-      if (first && wave == 0) {
-        // pivot: lane j (and its copies j + 16, ...) holds diagonal-block row
-        // J0 + j; straight-line code (selects, no branches) so the updates of
-        // later columns overlap the next pivot's reciprocal square root
-        const int j = lane & 15;
-        float* xr = X + (J0 + j) * xs + J0;
-        float x[16];
+    };
+    auto signal = [&](int* f, int v) {  // after this wave's LDS writes
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      if (lane == 0) __hip_atomic_store(f, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    };
+    // 16 x 16 tile X[rA + i][cC + n] -= sum over k in [16 s0, 16 s1) of
+    // X[rA + i][k] X[rB + n][k] on matrix cores; lane group g supplies
+    // k = 16 s + 4 g + e to the e-th product of step s; result row 4 g + e,
+    // column lane & 15
+    constexpr int KS = kR0Max / 16;
+    auto tile_update = [&](int rA, int rB, int cC, int s0, int s1) {
+      const float* arow = X + (rA + (lane & 15)) * xs + 4 * (lane >> 4);
+      const float* brow = X + (rB + (lane & 15)) * xs + 4 * (lane >> 4);
+      float* drow = X + (rA + 4 * (lane >> 4)) * xs + cC + (lane & 15);
+      float cur[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f32x4_t v = *reinterpret_cast<const f32x4_t*>(xr + 4 * q);
-          x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
+      for (int e = 0; e < 4; ++e) cur[e] = drow[e * xs];
+      f32x4_t av[KS], bv[KS];
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        if (s >= s0 && s < s1) {
+          av[s] = *reinterpret_cast<const f32x4_t*>(arow + 16 * s);
+          bv[s] = *reinterpret_cast<const f32x4_t*>(brow + 16 * s);
         }
-        // step k: every lane of the row of 16 gets the pivot and the column
-        // entries it needs by DPP broadcast within the row
-        float myri = 0.0f;
+      f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        if (s >= s0 && s < s1) {
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].x, bv[s].x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].y, bv[s].y, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].z, bv[s].z, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[s].w, bv[s].w, acc, 0, 0, 0);
+        }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) drow[e * xs] = cur[e] - acc[e];
+    };
+    // P(R, j) for the 16 rows at rbase: X[..][16 j ..] = X[..][16 j ..] A_j^T
+    auto panel = [&](int rbase, int j) {
+      const int J0 = 16 * j;
+      const f32x4_t av = *reinterpret_cast<const f32x4_t*>(X + (rbase + (lane & 15)) * xs + J0 + 4 * (lane >> 4));
+      const f32x4_t bv = *reinterpret_cast<const f32x4_t*>(Ainv + (J0 + (lane & 15)) * kAs + 4 * (lane >> 4));
+      f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.x, bv.x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.y, bv.y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.z, bv.z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av.w, bv.w, acc, 0, 0, 0);
+      float* drow = X + (rbase + 4 * (lane >> 4)) * xs + J0 + (lane & 15);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) drow[e * xs] = acc[e];
+    };
+    if (wave == 0) {
+      const int j = lane & 15, q = lane >> 4;
+      float x[16];  // row j of the current diagonal block
+      auto load_diag = [&](int jb) {
+        const float* xr = X + (16 * jb + j) * xs + 16 * jb;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const f32x4_t v = *reinterpret_cast<const f32x4_t*>(xr + 4 * u);
+          x[4 * u] = v.x; x[4 * u + 1] = v.y; x[4 * u + 2] = v.z; x[4 * u + 3] = v.w;
+        }
+      };
+      load_diag(0);
+      for (int jb = 0; jb < nb; ++jb) {
+        // pivot: straight-line code (selects, no branches); every lane of a
+        // row of 16 gets the pivot and the column entries it needs by DPP
+        // broadcast within the row
+        float myri = 0.0f;  // 1 / r of pivot j (0: no basis vector)
+        float lz[16];       // L[j][k] below the diagonal, zero elsewhere
 #pragma unroll
         for (int k = 0; k < 16; ++k) {
           const float d = row_bcast(x[k], k);
           const float rinv = d > a.tau2 ? __builtin_amdgcn_rsqf(d) : 0.0f;  // hardware reciprocal square root (1 ulp)
-          const float lj = j > k ? x[k] * rinv : 0.0f;  // L[j][k] below the pivot, zero at and above it
+          const float lj = j > k ? x[k] * rinv : 0.0f;
+          lz[k] = lj;
           myri = j == k ? rinv : myri;
-          x[k] = j == k ? d * rinv : (j > k ? lj : x[k]);
 #pragma unroll
           for (int j2 = k + 1; j2 < 16; ++j2) x[j2] = fmaf(-lj, row_bcast(lj, j2), x[j2]);
         }
-        if (lane < 16) {
+        // A_j row by row: A[j] = ri_j (e_j - sum_{k<j} L[j][k] A[k]); copy q
+        // of the row of 16 lanes forms columns q, q + 4, q + 8 and q + 12
+        float bq[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const f32x4_t v = {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
-            *reinterpret_cast<f32x4_t*>(xr + 4 * q) = v;
-          }
-          riv[J0 + lane] = myri;
+        for (int i = 0; i < 4; ++i) bq[i] = q + 4 * i == j ? 1.0f : 0.0f;
+#pragma unroll
+        for (int k = 0; k < 15; ++k) {
+          const float sk = lz[k] * row_bcast(myri, k);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) bq[i] = fmaf(-sk, row_bcast(bq[i], k), bq[i]);
+        }
+        float* ar = Ainv + (16 * jb + j) * kAs + q;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ar[4 * i] = myri * bq[i];
+        signal(flg + 0, jb + 1);
+        if (jb + 1 < nb) {
+          const int r1 = 16 * (jb + 1);
+          wait_ge(flg + 2, jb + 1);  // U(jb+1, jb) and the earlier terms of U(jb+1, jb+1) are in
+          panel(r1, jb);
+          signal(flg + 1, jb + 1);
+          tile_update(r1, r1, r1, jb, jb + 1);  // the last term of U(jb+1, jb+1)
+          load_diag(jb + 1);
         }
       }
-      __syncthreads();
-      {
-        // panel: rows past the diagonal block, one thread each
-        const int np = first ? K0p - J0 - 16 : 0;
-        for (int u = tid; u < np + ocnt; u += NT) {
-          const int row = u < np ? J0 + 16 + u : K0p + (u - np);
-          float* xr = X + row * xs + J0;
-          float x[16];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const f32x4_t v = *reinterpret_cast<const f32x4_t*>(xr + 4 * q);
-            x[4 * q] = v.x; x[4 * q + 1] = v.y; x[4 * q + 2] = v.z; x[4 * q + 3] = v.w;
-          }
-#pragma unroll
-          for (int jj = 0; jj < 16; ++jj) {
-            const float* lr = X + (J0 + jj) * xs + J0;
-            float v = x[jj];
-#pragma unroll
-            for (int q = 0; q < (jj + 3) / 4; ++q) {
-              const f32x4_t l4 = *reinterpret_cast<const f32x4_t*>(lr + 4 * q);
-              if (4 * q + 0 < jj) v = fmaf(-l4.x, x[4 * q + 0], v);
-              if (4 * q + 1 < jj) v = fmaf(-l4.y, x[4 * q + 1], v);
-              if (4 * q + 2 < jj) v = fmaf(-l4.z, x[4 * q + 2], v);
-              if (4 * q + 3 < jj) v = fmaf(-l4.w, x[4 * q + 3], v);
+    } else {
+      for (int jb = 0; jb < nb; ++jb) {
+        for (int R = min(jb + 2, nb); R < nb + nown; ++R) {  // R0 blocks past jb + 1, then the own blocks
+          if (1 + R % 3 != wave) continue;
+          const int rbase = R < nb ? 16 * R : K0p + 16 * (R - nb);
+          wait_ge(flg + 0, jb + 1);
+          panel(rbase, jb);
+          if (jb + 1 < nb) {
+            const int c1 = 16 * (jb + 1);
+            wait_ge(flg + 1, jb + 1);  // row block jb+1 solved up to column block jb
+            tile_update(rbase, c1, c1, 0, jb + 1);  // U(R, jb+1)
+            if (R == jb + 2 && R < nb) {  // the next diagonal block but one
+              tile_update(rbase, rbase, rbase, 0, jb + 1);  // U(R, R) up to column block jb
+              signal(flg + 2, jb + 2);
             }
-            x[jj] = v * riv[J0 + jj];
-          }
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const f32x4_t v = {x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]};
-            *reinterpret_cast<f32x4_t*>(xr + 4 * q) = v;
           }
         }
       }
-      __syncthreads();
     }
+    __syncthreads();
     // own rows out: piece e = (own row e >> 5, float4 e & 31)
     const int K0q = (K0 + 3) >> 2;  // at most 32; columns K0 .. 4 K0q - 1 are zero
 #pragma unroll
