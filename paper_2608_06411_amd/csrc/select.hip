@@ -614,6 +614,7 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
         *reinterpret_cast<f32x4_t*>(Ct + (long long)(c0 + i) * Kp + 4 * q) =
             *reinterpret_cast<const f32x4_t*>(X + (K0p + i) * xs + 4 * q);
     }
+    uint64_t mykey = 0ull;  // own candidate's Eq. (4) key (0: none)
     if (tid < ocnt) {  // R0 members get a NaN r^2: the selection kernel reads them as selected
       const float* xr = X + (K0p + tid) * xs;
       f32x4_t s4 = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -625,7 +626,25 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
         }
       const int i = c0 + tid;
       const uint64_t ki = (static_cast<uint64_t>(ordered_bits(p[i])) << 32) | (0xffffffffu - static_cast<uint32_t>(i));
-      r2g[i] = ki >= klast ? __builtin_nanf("") : (nrm[i] > 0.0f ? 1.0f : 0.0f) - ((s4.x + s4.y) + (s4.z + s4.w));
+      const bool in_r0 = ki >= klast;
+      const float r2v = (nrm[i] > 0.0f ? 1.0f : 0.0f) - ((s4.x + s4.y) + (s4.z + s4.w));
+      r2g[i] = in_r0 ? __builtin_nanf("") : r2v;
+      if (!in_r0) {
+        const float pi = p[i];
+        const float pv = (pi > 0.0f && pi <= 3.402823466e38f) ? pi : 0.0f;
+        mykey = make_key(r2v, pv * nrm[i], pv, i, a.tau2);
+      }
+    }
+    // The keys the selection's first round merges, when its workgroups own
+    // the same 64 tokens: the own candidates' top kPub keys and the next one
+    // as a bound (the kernel boundary orders them before their readers).
+    if (a.ch == 64 && K0 < K && wave == 0) {
+      uint64_t* pub = a.pub + ((long long)b * 2 + 1) * a.G * (kPub + 1) + w * (kPub + 1);
+      for (int q = 0; q <= kPub; ++q) {
+        const uint64_t best = wave_max_key(mykey);
+        if (lane == 0) pub[q] = best;
+        if (mykey == best) mykey = 0ull;
+      }
     }
   }
 }
@@ -792,9 +811,14 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   if (tid == 0) misc[0] = 0;  // abort flag
   if (PIPE && tid < 4) npub[tid] = 0;
   __syncthreads();
-  publish(1, K0 > 0 && !r0_done);  // the keys the first round merges
-  image_barrier(a.bar + b, static_cast<unsigned>(G), a.err, misc);
-  if (misc[0]) return;
+  // the keys the first round merges: published by r0_kernel when it placed
+  // R0 for workgroups of 64 tokens, else here (followed by a barrier)
+  const unsigned bar0 = r0_done && ch == 64 ? 0u : 1u;
+  if (bar0) {
+    publish(1, K0 > 0 && !r0_done);
+    image_barrier(a.bar + b, static_cast<unsigned>(G), a.err, misc);
+    if (misc[0]) return;
+  }
 
   int t = r0_done ? K0 : 0, fq = r0_done ? K0 : 0, round = 0;
   while (t < K) {
@@ -1415,7 +1439,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     if (live) __hip_atomic_store(r2g + my_i, my_r2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     publish(round & 1, fq < K0);
     ++round;
-    image_barrier(a.bar + b, static_cast<unsigned>((round + 1) * G), a.err, misc);
+    image_barrier(a.bar + b, static_cast<unsigned>((round + bar0) * G), a.err, misc);
     if (misc[0]) break;
   }
 }
