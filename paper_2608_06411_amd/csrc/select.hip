@@ -327,33 +327,68 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
       mx = (i < N && k > mx) ? k : mx;
     }
   }
-  const double mxv = mx ? key_rank_value(mx) : -1.0;  // threads without tokens rank last
-  kmax[tid] = mxv;
+  // threads t and t + NT/2 pool their maxima: the NT/2 pair maxima are keys of
+  // disjoint token sets, so the K0-th largest of them (K0 <= NT/2) is still
+  // at most the K0-th largest key
+  uint64_t* kpair = reinterpret_cast<uint64_t*>(kmax);
+  if (tid >= NT / 2) kpair[tid] = mx;
   if (tid == 0) *ncand = 0;
   __syncthreads();
-  {
+  if (tid < NT / 2) {
+    const uint64_t other = kpair[tid + NT / 2];
+    mx = other > mx ? other : mx;
+  }
+  const double mxv = mx ? key_rank_value(mx) : -1.0;  // pairs without tokens rank last
+  __syncthreads();
+  if (tid < NT / 2) kmax[tid] = mxv;
+  __syncthreads();
+  if (tid < NT / 2) {
     const double2* y2 = reinterpret_cast<const double2*>(kmax);
     int r4[4] = {0, 0, 0, 0};  // independent counters: no serial chain
-    for (int u0 = 0; u0 < NT / 2; u0 += 16) {
+    for (int u0 = 0; u0 < NT / 4; u0 += 16) {
       double2 y[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) y[u] = y2[u0 + u];
 #pragma unroll
       for (int u = 0; u < 16; ++u) r4[u & 3] += above(mxv, y[u].x) + above(mxv, y[u].y);
     }
-    // at least K0 threads hold tokens (N >= K0, K0 <= NT); their maxima are
-    // distinct, and the empty threads' zeros rank below them
+    // at least K0 pairs hold tokens (N >= K0, K0 <= NT/2): pair p holds token
+    // p; their maxima are distinct, and the empty pairs' zeros rank below them
     if ((r4[0] + r4[1]) + (r4[2] + r4[3]) == K0 - 1) *T0p = mx;
   }
   __syncthreads();
   const uint64_t T0 = *T0p;
+  // candidates: the register-cached tokens first (a mask, then one LDS atomic
+  // per thread for all of them), the rest one atomic each
+  uint32_t cm = 0u;
 #pragma unroll
   for (int u = 0; u < PC; ++u) {
     const int i = tid + u * NT;
-    const uint64_t k = key_of(pc[u], i);
-    if (i < N && k >= T0) {
-      const int o = atomicAdd(ncand, 1);
-      if (o < kR0Cand) cand[o] = key_rank_value(k);
+    cm |= (i < N && key_of(pc[u], i) >= T0) ? 1u << u : 0u;
+  }
+  {
+    // the wave's exclusive prefix sum of the counts (at most PC = 16, five
+    // bit planes), then one atomic per wave
+    const int c = __builtin_popcount(cm);
+    int pre = 0, tot = 0;
+#pragma unroll
+    for (int bit = 0; bit < 5; ++bit) {
+      const uint64_t m = __ballot((c >> bit) & 1);
+      pre += static_cast<int>(__builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u)))
+             << bit;
+      tot += __builtin_popcountll(m) << bit;
+    }
+    if (tot > 0) {
+      int base = 0;
+      if (lane == 0) base = atomicAdd(ncand, tot);
+      int o = __builtin_amdgcn_readlane(base, 0) + pre;
+#pragma unroll
+      for (int u = 0; u < PC; ++u)
+        if ((cm >> u) & 1u) {
+          if (o < kR0Cand) cand[o] = key_rank_value(key_of(pc[u], tid + u * NT));
+          ++o;
+        }
     }
   }
   for (int i0 = tid + PC * NT; i0 < N; i0 += PB * NT) {
