@@ -38,6 +38,10 @@ CASES = {
                               "pred": PredictorShape(D=512, D_h=136, d_p=64)}, 2e-2),
     "one_token_f32": ("tiny", {"N": 1, "M": (3, 3), "dtype": "f32",
                                "pred": PredictorShape(D=64, D_h=32, d_p=8)}, 1e-6),
+    # d_p not a multiple of 16 and D_h not a multiple of 64: partial steps in
+    # the logits and the projection's K split, an odd number of RoPE pairs
+    "odd_width_bf16": ("sweep", {"B": 2, "N": 131, "M": (2, 17),
+                                 "pred": PredictorShape(D=256, D_h=200, d_p=36)}, 2e-2),
 }
 
 

@@ -75,6 +75,7 @@ CASES = [
     (1, 5000, 64, 64, 32, "bf16", "peaked", {}),       # many workgroups per image
     (1, 9000, 64, 150, 100, "bf16", "flat", {}),       # more than 64 own tokens per workgroup
     (1, 2000, 256, 300, 200, "bf16", "peaked", {}),    # K0 beyond the one-pass R0: pool rounds
+    (1, 1500, 64, 200, 128, "bf16", "peaked", {}),     # the largest one-pass R0 (eight pivot blocks)
 ]
 
 
