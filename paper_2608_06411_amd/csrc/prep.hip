@@ -35,12 +35,24 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepArgs a, int norm_bl
       const T* src = static_cast<const T*>(a.tsrc[s]);
       T* dst = static_cast<T*>(a.tdst[s]);
       const bool whole = a.tn % VEC == 0;
-      for (int e = threadIdx.x; e < TW * (TW / VEC); e += 256) {  // row r, piece c of the source tile
-        const int r = e / (TW / VEC), c = VEC * (e % (TW / VEC)), gr = TW * ti + r, gc = TW * tj + c;
-        if (gr >= a.tn) continue;
-        if (whole && gc + VEC <= a.tn) {
-          *reinterpret_cast<uint4*>(&tile[r][c]) = *reinterpret_cast<const uint4*>(src + (long long)gr * a.tn + gc);
-        } else {
+      constexpr int PP = TW * (TW / VEC) / 256;  // pieces per thread (2 for bf16, 4 for float)
+      if (whole) {  // every piece's load issued before the first LDS store
+        uint4 pv[PP];
+#pragma unroll
+        for (int u = 0; u < PP; ++u) {
+          const int e = threadIdx.x + 256 * u, r = e / (TW / VEC), c = VEC * (e % (TW / VEC));
+          const int gr = min(TW * ti + r, a.tn - 1), gc = min(TW * tj + c, a.tn - VEC);
+          pv[u] = *reinterpret_cast<const uint4*>(src + (long long)gr * a.tn + gc);
+        }
+#pragma unroll
+        for (int u = 0; u < PP; ++u) {
+          const int e = threadIdx.x + 256 * u, r = e / (TW / VEC), c = VEC * (e % (TW / VEC));
+          if (TW * ti + r < a.tn && TW * tj + c + VEC <= a.tn) *reinterpret_cast<uint4*>(&tile[r][c]) = pv[u];
+        }
+      } else {
+        for (int e = threadIdx.x; e < TW * (TW / VEC); e += 256) {  // row r, piece c of the source tile
+          const int r = e / (TW / VEC), c = VEC * (e % (TW / VEC)), gr = TW * ti + r, gc = TW * tj + c;
+          if (gr >= a.tn) continue;
           for (int k = 0; k < VEC && gc + k < a.tn; ++k) tile[r][c + k] = src[(long long)gr * a.tn + gc + k];
         }
       }
@@ -73,7 +85,19 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepArgs a, int norm_bl
     const T* wr = static_cast<const T*>(a.fw[s]) + (long long)o * a.fcols;
     const T* bv = static_cast<const T*>(a.fb[s]);
     float acc = 0.0f;
-    for (int k = lane; k < a.fcols; k += 64) acc = fmaf(to_f32<T>(wr[k]), to_f32<T>(bv[k]), acc);
+    constexpr int U = 8;  // loads in flight per lane
+    for (int k0 = lane; k0 < a.fcols; k0 += 64 * U) {
+      T x[U], y[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = min(k0 + 64 * u, a.fcols - 1);
+        x[u] = wr[k];
+        y[u] = bv[k];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (k0 + 64 * u < a.fcols) acc = fmaf(to_f32<T>(x[u]), to_f32<T>(y[u]), acc);
+    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
     if (lane == 0) a.fout[s][o] = acc;
@@ -86,14 +110,22 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepArgs a, int norm_bl
     constexpr int VEC = 16 / sizeof(T);
     const T* r = static_cast<const T*>(a.V) + (long long)row * a.D;
     float acc = 0.0f;
-    for (int c = lane; c < a.D / VEC; c += 64) {
-      const uint4 u = *reinterpret_cast<const uint4*>(r + c * VEC);
-      const T* e = reinterpret_cast<const T*>(&u);
+    constexpr int U = 8;  // 16-byte loads in flight per lane
+    const int nchunk = a.D / VEC;
+    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+      uint4 uv[U];
 #pragma unroll
-      for (int k = 0; k < VEC; ++k) {
-        const float x = to_f32<T>(e[k]);
-        acc = fmaf(x, x, acc);
-      }
+      for (int u = 0; u < U; ++u) uv[u] = *reinterpret_cast<const uint4*>(r + min(c0 + 64 * u, nchunk - 1) * VEC);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (c0 + 64 * u < nchunk) {
+          const T* e = reinterpret_cast<const T*>(&uv[u]);
+#pragma unroll
+          for (int k = 0; k < VEC; ++k) {
+            const float x = to_f32<T>(e[k]);
+            acc = fmaf(x, x, acc);
+          }
+        }
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
