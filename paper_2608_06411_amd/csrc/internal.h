@@ -162,6 +162,13 @@ struct SelectArgs {
   float* gain;           // [B][K]
   int32_t* idx_out;      // [B][K] ascending
   int32_t* r0flag;       // [B] 1 where R0 was placed by one factorisation
+  // map_prune: the gather of the kept rows at the end of the selection
+  // (gV null: none; launch_select clears it when the order does not fit in LDS)
+  const void* gV;         // [B][N] rows of row_bytes (the visual tokens)
+  const int32_t* gpos;    // [B][N] positions
+  void* gV_out;           // [B][K] rows of row_bytes
+  int32_t* gpos_out;      // [B][K]
+  int row_bytes;
   int B, N, K, K0, G, ch, pcap;
   float tau2;
 };

@@ -264,9 +264,12 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
 
 // Inside map_prune (fused = true) the scoring kernel has already cleared the
 // selection's counters and the gather ranks the selection order itself.
+// With `ga` (map_prune), the selection kernel also gathers the kept rows when
+// its order fits in LDS; *gathered says whether it did.
 hipError_t enqueue_select(int B, int N, const float* p, const float* S, const float* norms,
                           const map_select_params& sp, int32_t* idx_out, int32_t* order_out,
-                          float* gain_out, const SelectWs& w, hipStream_t st, bool fused = false) {
+                          float* gain_out, const SelectWs& w, hipStream_t st, bool fused = false,
+                          const GatherArgs* ga = nullptr, bool* gathered = nullptr) {
   SelectArgs a;
   memset(&a, 0, sizeof(a));
   a.p = p;
@@ -286,9 +289,17 @@ hipError_t enqueue_select(int B, int N, const float* p, const float* S, const fl
   a.K = sp.K;
   a.K0 = sp.K0;
   a.tau2 = sp.tau * sp.tau;
+  if (ga) {
+    a.gV = ga->V;
+    a.gpos = ga->pos_v;
+    a.gV_out = ga->V_out;
+    a.gpos_out = ga->pos_out;
+    a.row_bytes = ga->row_bytes;
+  }
   hipError_t e = fused ? hipSuccess : launch_select_clear(a, st);
   if (e != hipSuccess) return e;
   if ((e = launch_select(a, st)) != hipSuccess) return e;
+  if (gathered) *gathered = a.gV != nullptr;
   return fused ? hipSuccess : launch_restore(a, st);
 }
 
@@ -473,8 +484,6 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   hipError_t e =
       enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, &g, norms, ninv, st, sw.bar, sw.err);
   if (e != hipSuccess) return MAP_ERR_HIP;
-  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st, true);
-  if (e != hipSuccess) return MAP_ERR_HIP;
   GatherArgs ga;
   ga.V = V;
   ga.pos_v = pos_v;
@@ -487,7 +496,10 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   ga.N = N;
   ga.K = sp.K;
   ga.row_bytes = static_cast<int>(w->D * elem_size(dt));
-  return hip_status(launch_gather(ga, st));
+  bool gathered = false;
+  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st, true, &ga, &gathered);
+  if (e != hipSuccess) return MAP_ERR_HIP;
+  return gathered ? MAP_OK : hip_status(launch_gather(ga, st));  // else its own kernel
 }
 
 map_status map_timing_enable(int enable) {

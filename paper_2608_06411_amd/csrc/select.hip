@@ -811,6 +811,68 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
     }
   };
+  // Gather (map_prune): the kept rows and positions in ascending token
+  // order (section "Inference-Time Token Pruning": the kept tokens return
+  // to their original order and keep their positions).  Every workgroup
+  // knows the whole order: the picks of the final round (from t_last) in
+  // LDS, the earlier ones in the order array (written before a barrier).
+  // Workgroup w writes ranks w, w + G, ...; after an abort, or with the
+  // error flag set, its indices and positions are -1 and its rows zero.
+  auto gather_share = [&](bool aborted, int t_last) {
+    if (!a.gV) return;
+    __syncthreads();  // LDS free
+    const bool bad = aborted || __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+    int* ord = reinterpret_cast<int*>(lds + L.RW);  // [K rounded up to 8] (padding: past any index)
+    int* share = reinterpret_cast<int*>(lds + L.merge);  // index of rank w + G s
+    const int K8 = (K + 7) & ~7, nshare = w < K ? (K - w + G - 1) / G : 0;
+    if (!bad) {
+      for (int j = tid; j < K8; j += NT)
+        ord[j] = j >= K ? 0x7fffffff : (j < t_last ? a.order[(long long)b * K + j] : midx[pslot[j - t_last]]);
+      __syncthreads();
+      for (int j = tid; j < K; j += NT) {  // rank = number of smaller indices (they are distinct)
+        const int v = ord[j];
+        int r4[4] = {0, 0, 0, 0};
+        for (int q = 0; q < K8; q += 8) {
+          const int4 x = *reinterpret_cast<const int4*>(ord + q);
+          const int4 y = *reinterpret_cast<const int4*>(ord + q + 4);
+          r4[0] += (x.x < v) + (y.x < v);
+          r4[1] += (x.y < v) + (y.y < v);
+          r4[2] += (x.z < v) + (y.z < v);
+          r4[3] += (x.w < v) + (y.w < v);
+        }
+        const int rk = (r4[0] + r4[1]) + (r4[2] + r4[3]);
+        if (rk % G == w) share[rk / G] = v;
+      }
+      __syncthreads();
+    }
+    for (int sI = tid; sI < nshare; sI += NT) {
+      const int k = w + G * sI, v = bad ? -1 : share[sI];
+      a.idx_out[(long long)b * K + k] = v;
+      a.gpos_out[(long long)b * K + k] = bad ? -1 : a.gpos[(long long)b * N + v];
+    }
+    // rows, 16 bytes per piece; every load of a thread before its first store
+    const int chunks = a.row_bytes >> 4, total = nshare * chunks;
+    const uint4* src = static_cast<const uint4*>(a.gV) + (long long)b * N * chunks;
+    uint4* dst = static_cast<uint4*>(a.gV_out) + (long long)b * K * chunks;
+    constexpr int GU = 4;
+    for (int e0 = tid; e0 < total; e0 += GU * NT) {
+      uint4 v[GU];
+#pragma unroll
+      for (int u = 0; u < GU; ++u) {
+        const int e = min(e0 + u * NT, total - 1), sI = e / chunks;
+        v[u] = src[(long long)(bad ? 0 : share[sI]) * chunks + (e - sI * chunks)];
+      }
+#pragma unroll
+      for (int u = 0; u < GU; ++u) {
+        const int e = e0 + u * NT;
+        if (e < total) {
+          const int sI = e / chunks;
+          dst[(long long)(w + G * sI) * chunks + (e - sI * chunks)] = bad ? make_uint4(0u, 0u, 0u, 0u) : v[u];
+        }
+      }
+    }
+  };
+
   // R0 placed by r0_kernel (when it fits and did not give up): take over the
   // own tokens' state and coefficient rows; otherwise the first rounds place it
   bool r0_done = false;
@@ -829,7 +891,10 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     const float r2v = r2g[c0 + min(tid, cnt - 1)];
     r0_done = a.r0flag[b] != 0;
     if (r0_done) {
-      if (K0 >= K) return;
+      if (K0 >= K) {  // the selection is R0 alone
+        gather_share(false, K);
+        return;
+      }
       if (tid < cnt) {
         if (r2v != r2v) my_state = 2;  // NaN: a member of R0
         else my_r2 = r2v;
@@ -852,7 +917,10 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   if (bar0) {
     publish(1, K0 > 0 && !r0_done);
     image_barrier(a.bar + b, static_cast<unsigned>(G), a.err, misc);
-    if (misc[0]) return;
+    if (misc[0]) {
+      gather_share(true, 0);
+      return;
+    }
   }
 
   int t = r0_done ? K0 : 0, fq = r0_done ? K0 : 0, round = 0;
@@ -1296,7 +1364,10 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         a.gain[(long long)b * K + t0 + k] = pgain[k];
       }
     if (forced) fq += np;
-    if (t >= K) break;
+    if (t >= K) {
+      gather_share(false, t0);
+      break;
+    }
 
     // ============================================================ update
     // The round's new rows t0 .. t-1 on the own tokens:
@@ -1475,7 +1546,10 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     publish(round & 1, fq < K0);
     ++round;
     image_barrier(a.bar + b, static_cast<unsigned>((round + bar0) * G), a.err, misc);
-    if (misc[0]) break;
+    if (misc[0]) {
+      gather_share(true, 0);
+      break;
+    }
   }
 }
 
@@ -1571,6 +1645,11 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
   a.ch = chosen_ch;
   a.G = chosen_G;
   a.pcap = chosen_pcap;
+  if (a.gV) {  // the order must fit where the pool's Gram matrix was
+    const Lds L = lds_layout(K, chosen_G, chosen_ch, chosen_pcap, chosen_pipe);
+    const int rw = 4 * chosen_pcap * (L.rs > L.ws ? L.rs : L.ws);
+    if (4 * ((K + 7) & ~7) > rw || (a.row_bytes & 15) != 0) a.gV = nullptr;
+  }
   const int per_launch = static_cast<int>(((long long)per_cu * cus) / chosen_G);
   if (per_launch < 1) return hipErrorInvalidConfiguration;
   if (r0_by_factor(a.K0)) {
