@@ -29,8 +29,9 @@ PEAK_HBM = 8000.0         # GB/s
 R0_FACTOR_MAX = 128  # largest K0 the selection places by one factorisation (its own kernel)
 
 
-def algorithmic_work(cfg, sumM):
-    """Per-launch algorithmic work of each kernel: (bound, amount, unit)."""
+def algorithmic_work(cfg, sumM, gathered=True):
+    """Per-launch algorithmic work of each kernel: (bound, amount, unit).
+    `gathered`: the selection launch also gathers the kept rows (no gather launch)."""
     B, N, K, K0 = cfg.B, cfg.N, cfg.K, cfg.K0
     K0f = K0 if 0 < K0 <= R0_FACTOR_MAX else 0  # picks placed by the R0 kernel
     D, H, dp = cfg.pred.D, cfg.pred.D_h, cfg.pred.d_p
@@ -56,8 +57,10 @@ def algorithmic_work(cfg, sumM):
         # K0 coefficient rows of every token, r^2, order and gain out
         "select_r0": ("hbm", B * (12.0 * N + 8.0 * K0 * N + 8.0 * K0), "byte"),
         # the greedy picks of Eq. (4): p, the norms, r^2 and the coefficient rows
-        # so far in, the similarity rows of the picks; order, gain and indices out
-        "select": ("hbm", B * (12.0 * N + 4.0 * K0f * N + 4.0 * (K - K0f) * N + 12.0 * (K - K0f)), "byte"),
+        # so far in, the similarity rows of the picks; order, gain and indices
+        # out; and, gathered in the same launch, the kept rows and positions
+        "select": ("hbm", B * (12.0 * N + 4.0 * K0f * N + 4.0 * (K - K0f) * N + 12.0 * (K - K0f))
+                   + (2.0 * B * K * D * el + 16.0 * B * K if gathered else 0.0), "byte"),
     }
 
 
@@ -210,7 +213,7 @@ def main():
     mp.timing_reset()
 
     sumM = int(t_off[-1])
-    work = algorithmic_work(cfg, sumM)
+    work = algorithmic_work(cfg, sumM, gathered="gather" not in per_kernel)
     kern = {k: {"avg_us": 1e3 * v[0] / v[1], "launches_per_step": v[1] / args.steps}
             for k, v in per_kernel.items()}
     dominant = max(kern, key=lambda k: kern[k]["avg_us"] * kern[k]["launches_per_step"])
