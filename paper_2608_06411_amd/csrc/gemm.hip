@@ -10,7 +10,7 @@
 // accumulating in float32.  K advances in 128-byte slices (64 bf16 or 32
 // floats per row) that are staged through LDS with a two-slot ring: the next
 // slice is fetched into registers while the matrix cores consume the current
-// one.  LDS rows are 8 chunks of 16 bytes, XOR-swizzled by (row & 7) so that
+// one.  LDS rows are 8 chunks of 16 bytes, XOR-swizzled by (row >> 1) & 7 so that
 // the 32 rows one MFMA operand read touches land in different banks.
 //
 // Several independent problems (for example the first layer of f_V, the
@@ -37,6 +37,12 @@ template <typename T> struct Slice;
 template <> struct Slice<bf16_t> { static constexpr int VEC = 8; static constexpr int BK = 64; };
 template <> struct Slice<float> { static constexpr int VEC = 4; static constexpr int BK = 32; };
 
+// LDS rows of a K slice are 8 chunks of 16 bytes; chunk c of row r sits at
+// position c ^ swz(r).  Sixteen consecutive rows (the lanes one 16-byte LDS
+// access serves together) then put a given chunk in 16 distinct 16-byte slots
+// of the 256-byte bank window, so the operand reads are free of bank conflicts.
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+
 // Block index -> tile index such that the tiles run by one XCD are contiguous.
 __device__ __forceinline__ int xcd_remap(int b, int total) {
   const int per = total / kXcds, rem = total % kXcds;
@@ -44,8 +50,21 @@ __device__ __forceinline__ int xcd_remap(int b, int total) {
   return x * per + min(x, rem) + local;
 }
 
+// erf by Abramowitz and Stegun, Handbook of Mathematical Functions, formula
+// 7.1.26: for x >= 0, erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) e^(-x^2)
+// with t = 1 / (1 + p x), absolute error at most 1.5e-7 (6e-7 in float32),
+// far below the bfloat16 rounding of the layer's output; erf is odd.  One
+// reciprocal, one exponential and five fused multiply-adds, no branches.
+__device__ __forceinline__ float erf_as(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
+  const float poly =
+      t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f), -0.284496736f), 0.254829592f);
+  return copysignf(fmaf(-poly, __expf(-ax * ax), 1.0f), x);
+}
+
 __device__ __forceinline__ float gelu_erf(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+  return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f));
 }
 
 template <typename T>
@@ -55,28 +74,35 @@ __device__ __forceinline__ void mma_slice(const uint4 (*As)[8], const uint4 (*Bs
 template <>
 __device__ __forceinline__ void mma_slice<bf16_t>(const uint4 (*As)[8], const uint4 (*Bs)[8], int wm,
                                                   int wn, int lane, f32x16_t (&acc)[2][2]) {
+  // The operands of step s + 1 are read into the other register set before
+  // the products of step s issue, so the LDS latency runs under them (the
+  // scheduling barriers keep the two sets apart).
   const int lr = lane & 31, lh = lane >> 5;
-#pragma unroll
-  for (int s = 0; s < 4; ++s) {
+  bf16x8_t a[2][2], b[2][2];
+  auto read = [&](int s, int buf) {
     const int v = 2 * s + lh;  // 16-byte chunk: k = 16 s + 8 lh + (0..7)
-    bf16x8_t a[2], b[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int r = wm * 64 + i * 32 + lr;
-      uint4 t = As[r][v ^ (r & 7)];
-      a[i] = __builtin_bit_cast(bf16x8_t, t);
+      a[buf][i] = __builtin_bit_cast(bf16x8_t, As[r][v ^ swz(r)]);
     }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int r = wn * 64 + j * 32 + lr;
-      uint4 t = Bs[r][v ^ (r & 7)];
-      b[j] = __builtin_bit_cast(bf16x8_t, t);
+      b[buf][j] = __builtin_bit_cast(bf16x8_t, Bs[r][v ^ swz(r)]);
     }
+  };
+  read(0, 0);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if (s < 3) read(s + 1, (s + 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s & 1][i], b[s & 1][j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -91,12 +117,12 @@ __device__ __forceinline__ void mma_slice<float>(const uint4 (*As)[8], const uin
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int r = wm * 64 + i * 32 + lr;
-      a[i] = __builtin_bit_cast(float4, As[r][v ^ (r & 7)]);
+      a[i] = __builtin_bit_cast(float4, As[r][v ^ swz(r)]);
     }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int r = wn * 64 + j * 32 + lr;
-      b[j] = __builtin_bit_cast(float4, Bs[r][v ^ (r & 7)]);
+      b[j] = __builtin_bit_cast(float4, Bs[r][v ^ swz(r)]);
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e)
@@ -113,8 +139,12 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 
 __device__ __forceinline__ int acc_col(int lane) { return lane & 31; }
 
 // Workgroup -> (problem, batch item, tile row, tile column).
+// The tiles of the problems before args.first_tiles run first, each class
+// XCD-contiguous: the launch puts the layer-1 and fold tiles there, so the
+// second wave of workgroups holds only Gram tiles, whose epilogue is shorter.
 __device__ __forceinline__ void decode_tile(const GemmBatch& args, int& pi, int& bt, int& tm, int& tn) {
-  const int tile = xcd_remap(blockIdx.x, args.total_tiles);
+  const int b = blockIdx.x, f = args.first_tiles;
+  const int tile = b < f ? xcd_remap(b, f) : f + xcd_remap(b - f, args.total_tiles - f);
   pi = 0;
 #pragma unroll
   for (int q = 1; q < kMaxGemmProblems; ++q)
@@ -296,8 +326,8 @@ __global__ __launch_bounds__(NT) void gemm_kernel(const GemmBatch args) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = lrow + 32 * j;
-      As[buf][r][lv ^ (r & 7)] = ra[j];
-      Bs[buf][r][lv ^ (r & 7)] = rb[j];
+      As[buf][r][lv ^ swz(r)] = ra[j];
+      Bs[buf][r][lv ^ swz(r)] = rb[j];
     }
   };
 
@@ -503,12 +533,12 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
 
   // Per-lane global row pointers of this wave's 4 A rows and 4 B rows
   // (rows past the matrix read its last row; they are never stored).
-  const int v = (lane & 7) ^ (lane >> 3);
   const bf16_t* ga[4];
   const bf16_t* gb[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = 32 * wave + 8 * j + (lane >> 3);
+    const int v = (lane & 7) ^ swz(r);  // the chunk the swizzle puts at position lane & 7 of row r
     ga[j] = A + (long long)min(m0 + r, M - 1) * P.lda + 8 * v;
     gb[j] = B + (long long)min(n0 + r, N - 1) * P.ldb + 8 * v;
   }
@@ -672,6 +702,8 @@ void gemm_finalize(GemmBatch& g) {
     begin += p.tiles_per_batch * p.batch;
   }
   g.total_tiles = begin;
+  // a trailing cosine problem (the Gram matrix) runs after the others
+  g.first_tiles = g.count > 1 && g.p[g.count - 1].epi == EPI_COSINE ? g.p[g.count - 1].tile_begin : 0;
 }
 
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s) {

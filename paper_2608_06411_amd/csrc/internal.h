@@ -98,6 +98,7 @@ struct GemmBatch {
   GemmProblem p[kMaxGemmProblems];
   int count;
   int total_tiles;
+  int first_tiles;  // tiles dispatched before the rest (0: one class)
 };
 
 void gemm_finalize(GemmBatch& g);  // computes the tile counts

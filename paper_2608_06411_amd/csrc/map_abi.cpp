@@ -226,10 +226,10 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   g1.p[0] = linear(V, rowsV, w.w1_v, w.b1_v, s.h1_v, w.D_h, w.D, EPI_BIAS_GELU);
   g1.p[1] = linear(T, sumM, w.w1_t, w.b1_t, s.h1_t, w.D_h, w.D, EPI_BIAS_GELU);
   g1.count = 2;
-  if (extra_l1) g1.p[g1.count++] = *extra_l1;
-  // last, so their few short tiles fill the launch's final wave
   g1.p[g1.count++] = linear(w.w_k, w.d_p, s.w2t_v, nullptr, s.wc_v, w.D_h, w.D_h, EPI_BIAS);  // W_K W2
   g1.p[g1.count++] = linear(w.w_q, w.d_p, s.w2t_t, nullptr, s.wc_t, w.D_h, w.D_h, EPI_BIAS);  // W_Q W2
+  // the Gram matrix last: its tiles are dispatched after every tile above
+  if (extra_l1) g1.p[g1.count++] = *extra_l1;
   gemm_finalize(g1);
   if ((e = launch_gemm(dt, g1, extra_l1 ? "gemm_layer1_gram" : "gemm_layer1", st)) != hipSuccess) return e;
 
