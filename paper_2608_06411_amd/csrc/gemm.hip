@@ -491,30 +491,48 @@ __device__ __forceinline__ void epi_cosine_staged(const GemmProblem& P, int bt, 
   }
 }
 
-// bf16 variant with a four-stage LDS ring filled by direct global->LDS loads
-// (global_load_lds_dwordx4): three K slices are in flight while the matrix
-// cores consume the fourth, with no register staging.  Each wave moves 32
-// rows of A and 32 rows of B per slice, one instruction per 8 rows: lane l
-// lands at row 8j + l/8, chunk position l%8 of its instruction's 1 KiB, and
-// fetches the chunk the XOR swizzle puts there.  The stages are separate LDS
-// arrays addressed with compile-time stage numbers, so the only waits on
-// those loads are the explicit counted ones before each barrier.
+// bf16 variant with a five-stage LDS ring filled by direct global->LDS loads
+// (global_load_lds_dwordx4): four K slices are in flight while the matrix
+// cores consume the fifth, with no register staging, and the five 32 KiB
+// stages fill gfx950's 160 KiB of LDS.  Each wave moves 32 rows of A and 32
+// rows of B per slice, one instruction per 8 rows: lane l lands at row
+// 8j + l/8, chunk position l%8 of its instruction's 1 KiB, and fetches the
+// chunk the XOR swizzle puts there.  The stages are separate LDS arrays
+// addressed with compile-time stage numbers, so the only waits on those
+// loads are the explicit counted ones before each barrier.
 // Requirements (checked by the host): K % 256 == 0, lda and ldb multiples of
 // 8, A and B 16-byte aligned.
-constexpr int kStages = 4;
+
+// LDS byte address of a __shared__ object (the value M0 takes for a direct load).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
+}
+
+// One global_load_lds_dwordx4: lane l's 16 bytes at gsrc land at byte 16 l
+// of the wave's 1 KiB at LDS address m (wave-uniform, passed in M0).  Issued
+// from inline assembly so that the compiler adds no waits of its own for
+// these loads: it tracks at most four destination arrays of direct loads
+// and otherwise drains all of them before every LDS read.  Every read of a
+// stage is preceded by the explicit counted wait and the barrier.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"  // M0 is written here and nowhere else in the kernel
+__device__ __forceinline__ void dma16(const void* gsrc, uint32_t m) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gsrc), "s"(m) : "memory", "m0");
+}
+#pragma clang diagnostic pop
 
 __device__ __forceinline__ void wait_vm_lgkm0(int outstanding) {
   // s_waitcnt encoding: vmcnt in bits [3:0] and [15:14], expcnt [6:4]
-  // (7 = no wait), lgkmcnt [11:8]; here vmcnt = outstanding (0, 8 or 16)
-  // and lgkmcnt = 0
-  if (outstanding >= 16) __builtin_amdgcn_s_waitcnt(0x4070);
+  // (7 = no wait), lgkmcnt [11:8]; here vmcnt = outstanding (0, 8, 16 or
+  // 24) and lgkmcnt = 0
+  if (outstanding >= 24) __builtin_amdgcn_s_waitcnt(0x4078);
+  else if (outstanding >= 16) __builtin_amdgcn_s_waitcnt(0x4070);
   else if (outstanding >= 8) __builtin_amdgcn_s_waitcnt(0x0078);
   else __builtin_amdgcn_s_waitcnt(0x0070);
 }
 
 __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
-  __shared__ uint4 st0[2][BM][8], st1[2][BM][8], st2[2][BM][8], st3[2][BM][8];  // 4 x 32 KiB
-  __shared__ float rs_tile[BM + BN];  // cosine epilogue: reciprocal norms of the tile's rows, columns
+  __shared__ uint4 st0[2][BM][8], st1[2][BM][8], st2[2][BM][8], st3[2][BM][8], st4[2][BM][8];  // 5 x 32 KiB
   int pi, bt, tm, tn;
   decode_tile(args, pi, bt, tm, tn);
   const GemmProblem& P = args.p[pi];
@@ -525,10 +543,11 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int nk = P.K / 64;
-  if (P.epi == EPI_COSINE) {  // read before the loop, visible after its barriers
+  float rs_mine = 0.0f;  // cosine epilogue: reciprocal norm of tile row tid, or of column tid - BM
+  if (P.epi == EPI_COSINE) {
     const float* rs = P.rs + (long long)bt * M;
     const int k = tid < BM ? m0 + tid : n0 + tid - BM;
-    rs_tile[tid] = k < (tid < BM ? M : N) ? rs[k] : 0.0f;
+    if (k < (tid < BM ? M : N)) rs_mine = rs[k];
   }
 
   // Per-lane global row pointers of this wave's 4 A rows and 4 B rows
@@ -542,12 +561,15 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
     ga[j] = A + (long long)min(m0 + r, M - 1) * P.lda + 8 * v;
     gb[j] = B + (long long)min(n0 + r, N - 1) * P.ldb + 8 * v;
   }
+  // this wave's first destination row inside a stage: 32 wave rows of 128 bytes
+  const uint32_t wrow = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave)) * 32u * 128u;
   auto issue = [&](uint4 (*dst)[BM][8], int kt) {
     const int k0 = kt * 64;
+    const uint32_t m = lds_addr(&dst[0][0][0]) + wrow;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      __builtin_amdgcn_global_load_lds(ga[j] + k0, &dst[0][32 * wave + 8 * j][0], 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(gb[j] + k0, &dst[1][32 * wave + 8 * j][0], 16, 0, 0);
+      dma16(ga[j] + k0, m + 1024u * j);
+      dma16(gb[j] + k0, m + BM * 128u + 1024u * j);
     }
   };
 
@@ -559,27 +581,40 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  // A step waits for its slice (this wave's loads, then every wave's at the
+  // Step kt waits for slice kt (this wave's loads, then every wave's at the
   // barrier), refills the stage every wave finished reading in the previous
-  // step with the slice three ahead, and runs the matrix cores on its stage.
-  // nk is a multiple of 4, so the stage of every step is a compile-time
-  // constant and the code stays straight-line.
+  // step with slice kt + 4, and runs the matrix cores on slice kt.  Slice kt
+  // sits in stage kt % 5, a compile-time constant in the unrolled body; the
+  // early exits are uniform scalar branches.
   auto mma = [&](uint4 (*cur)[BM][8]) { mma_slice<bf16_t>(cur[0], cur[1], wm, wn, lane, acc); };
+  auto step = [&](uint4 (*cur)[BM][8], uint4 (*nxt)[BM][8], int kt) {
+    wait_vm_lgkm0(8 * min(3, nk - 1 - kt));
+    __builtin_amdgcn_s_barrier();
+    if (kt + 4 < nk) issue(nxt, kt + 4);
+    mma(cur);
+  };
   issue(st0, 0);
   issue(st1, 1);
   issue(st2, 2);
-  int kt = 0;
-  for (; kt + 4 < nk; kt += 4) {
-    wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st3, kt + 3); mma(st0);
-    wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st0, kt + 4); mma(st1);
-    wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st1, kt + 5); mma(st2);
-    wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st2, kt + 6); mma(st3);
+  issue(st3, 3);
+  step(st0, st4, 0);
+  for (int kt = 1; kt < nk; kt += 5) {
+    step(st1, st0, kt);
+    if (kt + 1 >= nk) break;
+    step(st2, st1, kt + 1);
+    if (kt + 2 >= nk) break;
+    step(st3, st2, kt + 2);
+    if (kt + 3 >= nk) break;
+    step(st4, st3, kt + 3);
+    if (kt + 4 >= nk) break;
+    step(st0, st4, kt + 4);
   }
-  wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); issue(st3, kt + 3); mma(st0);
-  wait_vm_lgkm0(16); __builtin_amdgcn_s_barrier(); mma(st1);
-  wait_vm_lgkm0(8); __builtin_amdgcn_s_barrier(); mma(st2);
-  wait_vm_lgkm0(0); __builtin_amdgcn_s_barrier(); mma(st3);
   __syncthreads();  // the epilogues reuse the stage arrays
+  float* rs_tile = reinterpret_cast<float*>(&st4[0][0][0]);
+  if (P.epi == EPI_COSINE) {
+    rs_tile[tid] = rs_mine;
+    __syncthreads();
+  }
   const StagedTile L{reinterpret_cast<float*>(&st0[0][0][0]), reinterpret_cast<float*>(&st1[0][0][0]),
                      reinterpret_cast<float*>(&st2[0][0][0]), reinterpret_cast<float*>(&st3[0][0][0])};
   if (P.epi == EPI_COSINE)
