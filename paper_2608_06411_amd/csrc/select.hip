@@ -736,7 +736,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   uint64_t* mkey = reinterpret_cast<uint64_t*>(lds + L.mkey);  // [2][pcap]
   int* pslot = reinterpret_cast<int*>(lds + L.pslot);
   float* prr = reinterpret_cast<float*>(lds + L.pr);     // 1 / r of each pick (0: no basis vector)
-  float* pgain = reinterpret_cast<float*>(lds + L.pgain);
+  uint32_t* pgain = reinterpret_cast<uint32_t*>(lds + L.pgain);  // p (forced) or the key's high word, as bits
   float* pcol = reinterpret_cast<float*>(lds + L.pcol);
   float* U = reinterpret_cast<float*>(lds + L.U);
   float* Rm = reinterpret_cast<float*>(lds + L.RW);
@@ -1175,29 +1175,45 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       const int iv = in ? midx[lane] : 0;
       bool actv = in;
       const float* u0 = U + min(lane, pcap - 1) * us;  // member `lane`'s row (zero past np)
+      // the parts of the member's key that do not change during the round
+      // (make_key's inputs: (qn qn) r2 is formed in make_key's order)
+      const float qsq = qnv * qnv;
+      const bool qpos = qnv > 0.0f;
+      const uint32_t hip = ordered_bits(pv);
+      const uint32_t klo = 0xffffffffu - static_cast<uint32_t>(iv);
       // One pick; NG = the number of groups of 16 picks made so far, so only
       // those groups of the two U rows are read and multiplied.  Returns
       // false when the round's picks are over.
       auto pick = [&](auto ngc) -> bool {
         constexpr int NG = decltype(ngc)::value;
         if (t >= K) return false;
+        // the lane's own row does not depend on the pick: its reads are
+        // issued first and complete under the argmax
+        float4 xs[4 * NG + 1], y0[4 * NG + 1];
+#pragma unroll
+        for (int q = 0; q < 4 * NG; ++q) y0[q] = *reinterpret_cast<const float4*>(u0 + 4 * q);
         int s;
         uint64_t best = 0;
         if (forced) {  // the pool is the top of p in descending order
           s = np < min(pn, K0 - fq) ? np : -1;
         } else {
-          const uint64_t kl = actv ? make_key(r2v, qnv, pv, iv, a.tau2) : 0ull;
+          // make_key's high word without branches
+          const float s2 = qsq * r2v;
+          const uint32_t hs = 0x80000000u | (s2 <= 3.402823466e38f ? __float_as_uint(s2) : 0u);
+          const bool pos = (r2v > a.tau2) & qpos & (s2 > 0.0f);
+          uint32_t khi = pos ? hs : hip;
+          khi = actv ? khi : 0u;
           // the largest high word nearly always belongs to one member; only
           // a tie needs the low words (keys are distinct, so one member wins)
-          const uint32_t khi = static_cast<uint32_t>(kl >> 32);
           const uint32_t mhi = wave_umax32(khi);
           const uint64_t tied = __ballot(khi == mhi);
           int sl;
           if (__builtin_popcountll(tied) == 1) {
             sl = static_cast<int>(__builtin_ctzll(tied));
             best = (static_cast<uint64_t>(mhi) << 32) |
-                   static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(kl)), sl));
+                   static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(klo), sl));
           } else {
+            const uint64_t kl = actv ? ((static_cast<uint64_t>(khi) << 32) | klo) : 0ull;
             best = wave_max_key(kl);
             sl = static_cast<int>(__builtin_ctzll(__ballot(kl == best)));
           }
@@ -1211,12 +1227,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         if (PIPE && __builtin_amdgcn_readlane(iv, s) == c0 + lane) my_state = 2;
         const float rm = Rm[s * rs + min(lane, pn - 1)];
         const float* usr = U + s * us;
-        float4 xs[4 * NG + 1], y0[4 * NG + 1];
 #pragma unroll
-        for (int q = 0; q < 4 * NG; ++q) {
-          xs[q] = *reinterpret_cast<const float4*>(usr + 4 * q);
-          y0[q] = *reinterpret_cast<const float4*>(u0 + 4 * q);
-        }
+        for (int q = 0; q < 4 * NG; ++q) xs[q] = *reinterpret_cast<const float4*>(usr + 4 * q);
         const float r2s = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, r2v), s));
         const float ns = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, nv), s));
         // no basis vector when the unit residual is at most tau (or the row is zero)
@@ -1226,8 +1238,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         if (lane == 0) {
           pslot[np] = s;
           prr[np] = rinv;
-          pgain[np] = forced ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pv), s))
-                             : key_score(best);
+          pgain[np] = forced ? static_cast<uint32_t>(__builtin_amdgcn_readlane(__builtin_bit_cast(int, pv), s))
+                             : static_cast<uint32_t>(best >> 32);
         }
         // dot over the picks so far (entries past np are zero)
         float d4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -1361,7 +1373,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     if (w == 0)  // the selection order and gains of this round
       for (int k = tid; k < np; k += NT) {
         a.order[(long long)b * K + t0 + k] = midx[pslot[k]];
-        a.gain[(long long)b * K + t0 + k] = pgain[k];
+        a.gain[(long long)b * K + t0 + k] =
+            forced ? __uint_as_float(pgain[k]) : key_score(static_cast<uint64_t>(pgain[k]) << 32);
       }
     if (forced) fq += np;
     if (t >= K) {
