@@ -629,41 +629,47 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
 // queries of Eq. (3)): C = RoPE(A B^T + bias), A [M][K] and B [N][K] bf16.
 // With N this small a 128 x 128 tile leaves most compute units idle, each
 // streaming the whole K with a few slices in flight.  Here a workgroup takes
-// 32 rows and all N columns and its eight waves split K: wave w takes the
-// 64-wide chunks w, w + 8, ...  Lane l reads 64 contiguous bytes of row
-// l & 31 per chunk, A and B alike, straight from global memory into
-// registers, and the chunk's four products consume them in an order shared
-// by both operands (any common order of k gives the same sum).  The eight
-// partial tiles are summed in LDS in a fixed order.
-// Requirements (checked by the host): N <= 128, K, lda and ldb multiples of
-// 8, A and B 16-byte aligned, one batch item.
+// 32 rows and one of two groups of RoPE pairs: with half = N / 2 and
+// PG = ceil(half / 2), group g holds pairs c = g PG .. (g + 1) PG - 1, i.e.
+// columns c and c + half, so every rotation is local and each workgroup
+// reads half of B.  Its eight waves split K: wave w takes the 64-wide chunks
+// w, w + 8, ...  Lane l reads 64 contiguous bytes of row l & 31 per chunk, A
+// and B alike, straight from global memory into registers, and the chunk's
+// four products consume them in an order shared by both operands (any
+// common order of k gives the same sum).  The eight partial tiles are summed
+// in LDS in a fixed order.
+// Requirements (checked by the host): N <= 128 and even, K, lda and ldb
+// multiples of 8, A and B 16-byte aligned, one batch item.
 constexpr int kPR = 32;   // rows per workgroup
 constexpr int kPW = 8;    // waves per workgroup
-constexpr int kPS = 132;  // LDS row stride of the partial tiles (floats)
+constexpr int kPG = 2;    // groups of RoPE pairs per row block
+constexpr int kPS = 68;   // LDS row stride of the partial tiles (floats)
 
 __global__ __launch_bounds__(kPW * 64) void proj_rope_kernel(const GemmBatch args) {
   __shared__ float part[kPW][kPR][kPS];
   const int t0 = args.p[0].tiles_m, pi = blockIdx.x < t0 ? 0 : 1;
   const GemmProblem& P = args.p[pi];
-  const int m0 = (blockIdx.x - (pi ? t0 : 0)) * kPR;
-  const int M = P.M, N = P.N, K = P.K, half = N >> 1;
+  const int local = blockIdx.x - (pi ? t0 : 0), g = local % kPG;
+  const int m0 = (local / kPG) * kPR;
+  const int M = P.M, K = P.K, half = P.N >> 1;
+  const int PG = (half + kPG - 1) / kPG, c0 = g * PG, npg = min(PG, half - c0);
+  if (npg <= 0) return;  // a group without pairs (half = 1)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(P.A);
   const bf16_t* __restrict__ B = static_cast<const bf16_t*>(P.B);
 
   const int r = lane & 31, h = lane >> 5;
   const bf16_t* arow = A + (long long)min(m0 + r, M - 1) * P.lda;
-  const bf16_t* brow[4];
+  const int pr = c0 + min(r, npg - 1);  // the pair of tile column r (32 + r: its partner)
+  const bf16_t* brow[2] = {B + (long long)pr * P.ldb, B + (long long)(pr + half) * P.ldb};
+  f32x16_t acc[2];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) brow[j] = B + (long long)min(32 * j + r, N - 1) * P.ldb;
-  f32x16_t acc[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[j][e] = 0.0f;
   const int nchunk = (K + 63) >> 6;
   for (int kc = wave; kc < nchunk; kc += 2 * kPW) {  // two chunks per pass, every load issued first
-    uint4 av[2][4], bv[2][4][4];
+    uint4 av[2][4], bv[2][2][4];
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2)
 #pragma unroll
@@ -672,7 +678,7 @@ __global__ __launch_bounds__(kPW * 64) void proj_rope_kernel(const GemmBatch arg
         const int off = k < K ? k : 0;  // past K: a valid address, zeroed below
         av[c2][q] = *reinterpret_cast<const uint4*>(arow + off);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) bv[c2][j][q] = *reinterpret_cast<const uint4*>(brow[j] + off);
+        for (int j = 0; j < 2; ++j) bv[c2][j][q] = *reinterpret_cast<const uint4*>(brow[j] + off);
       }
     __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the products
 #pragma unroll
@@ -683,42 +689,42 @@ __global__ __launch_bounds__(kPW * 64) void proj_rope_kernel(const GemmBatch arg
         const uint4 z = {0u, 0u, 0u, 0u};
         const bf16x8_t a = __builtin_bit_cast(bf16x8_t, k < K ? av[c2][q] : z);
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 2; ++j)
           acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, bv[c2][j][q]), acc[j],
                                                            0, 0, 0);
       }
   }
-  // the epilogue's (cos, sin) pairs and biases (item e = row e / half, pair
-  // e % half; at most four per thread), in flight while the partials meet
-  constexpr int EI = kPR * 64 / (kPW * 64);
+  // the epilogue's (cos, sin) pairs and biases (item e = row e / npg, pair
+  // c0 + e % npg; at most two per thread), in flight while the partials meet
+  constexpr int EI = kPR * 32 / (kPW * 64);
   float2 cs[EI];
   float bl[EI], bh[EI];
 #pragma unroll
   for (int u = 0; u < EI; ++u) {
-    const int e = min(tid + kPW * 64 * u, kPR * half - 1), rl = e / half, c = e - rl * half;
+    const int e = min(tid + kPW * 64 * u, kPR * npg - 1), rl = e / npg, c = c0 + e - rl * npg;
     cs[u] = P.rope_cs[(long long)min(m0 + rl, M - 1) * half + c];
     bl[u] = P.rope_bias ? P.rope_bias[c] : 0.0f;
     bh[u] = P.rope_bias ? P.rope_bias[c + half] : 0.0f;
   }
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int e = 0; e < 16; ++e) part[wave][acc_row(e, lane)][32 * j + acc_col(lane)] = acc[j][e];
   __syncthreads();
   float* __restrict__ out = static_cast<float*>(P.C);
 #pragma unroll
   for (int u = 0; u < EI; ++u) {
-    const int e = tid + kPW * 64 * u, rl = e / half, c = e - rl * half;
-    if (e >= kPR * half || m0 + rl >= M) continue;
+    const int e = tid + kPW * 64 * u, rl = e / npg, cl = e - rl * npg;
+    if (e >= kPR * npg || m0 + rl >= M) continue;
     float s0[kPW], s1[kPW];
 #pragma unroll
     for (int w = 0; w < kPW; ++w) {
-      s0[w] = part[w][rl][c];
-      s1[w] = part[w][rl][c + half];
+      s0[w] = part[w][rl][cl];
+      s1[w] = part[w][rl][32 + cl];
     }
     const float a = (((s0[0] + s0[1]) + (s0[2] + s0[3])) + ((s0[4] + s0[5]) + (s0[6] + s0[7]))) + bl[u];
     const float b = (((s1[0] + s1[1]) + (s1[2] + s1[3])) + ((s1[4] + s1[5]) + (s1[6] + s1[7]))) + bh[u];
-    float* o = out + (long long)(m0 + rl) * P.ldc + c;
+    float* o = out + (long long)(m0 + rl) * P.ldc + c0 + cl;
     o[0] = a * cs[u].x - b * cs[u].y;
     o[half] = b * cs[u].x + a * cs[u].y;
   }
@@ -769,7 +775,7 @@ hipError_t launch_proj_rope(map_dtype dt, const GemmBatch& g, const char* name, 
   GemmBatch q = g;
   int total = 0;
   for (int i = 0; i < q.count; ++i) {
-    q.p[i].tiles_m = q.p[i].M > 0 ? (q.p[i].M + kPR - 1) / kPR : 0;
+    q.p[i].tiles_m = q.p[i].M > 0 ? kPG * ((q.p[i].M + kPR - 1) / kPR) : 0;
     total += q.p[i].tiles_m;
   }
   if (q.count == 1) q.p[1].tiles_m = 0;
