@@ -149,6 +149,8 @@ def main():
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run a plain float32 copy kernel over this many MiB (three times), "
                          "the reference dispatch for calibrating HBM byte counters")
+    ap.add_argument("--subset", type=int, default=0,
+                    help="map_prune's candidate subset: -1 never, 0 automatic (default), n > 0 that many tokens")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -174,6 +176,7 @@ def main():
     V, T = to_dev(x["V_store"]), to_dev(x["T_store"])
     pos_v, pos_t = torch.from_numpy(x["pos_v"]).to(dev), torch.from_numpy(x["pos_t"]).to(dev)
     t_off = x["t_off"]
+    mp.set_subset_tokens(args.subset)
     ws = mp.PruneWorkspace(w, V, t_off, cfg.K)
     if args.copy_calibration_mib > 0:
         src = torch.ones(args.copy_calibration_mib << 18, dtype=torch.float32, device=dev)

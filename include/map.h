@@ -171,6 +171,21 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N,
                      float* p_out, int32_t* order_out, float* gain_out,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* map_prune's candidate subset.  A greedy pick of Eq. (4) scores
+ * p_i n_i r_i <= p_i n_i, so map_prune may run the selection on a subset J
+ * of each image's tokens: R0 plus the tokens with the largest bounds
+ * p_i n_i, about K0 + max(2 (K - K0), N / 4) of them (bf16, N <= 8192).  It
+ * forms the cosine similarity only among J, and keeps J's selection when
+ * every greedy pick scores above the largest bound left out.  Otherwise that
+ * image is selected again over all its tokens.  Either way the result is
+ * the selection over all tokens; only the time differs.
+ *   n < 0: never use a subset; n = 0: automatic (the default); n > 0: a
+ *   subset of max(n, K) tokens whenever that is fewer than N.
+ * The setting is process-wide and read by map_prune_workspace and map_prune
+ * alike: change it only between calls, and query the workspace after.
+ * Returns MAP_OK. */
+map_status map_set_subset_tokens(int n);
+
 /* Per-kernel timing for measurement.  While enabled, every kernel the
  * library launches is bracketed by a pair of HIP events recorded on the
  * launch stream.  map_timing_read() waits for those events, accumulates the

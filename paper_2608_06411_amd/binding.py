@@ -22,7 +22,7 @@ MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
 EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
-    "map_prune", "map_timing_enable", "map_timing_read", "map_timing_reset",
+    "map_prune", "map_set_subset_tokens", "map_timing_enable", "map_timing_read", "map_timing_reset",
 )
 
 
@@ -50,6 +50,7 @@ _SIGS = {
     "map_select": (_I, [_I, _I, _P, _P, _P, map_select_params, _P, _P, _P, _P, _SZ, _P]),
     "map_prune": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
                        map_select_params, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "map_set_subset_tokens": (_I, [_I]),
     "map_timing_enable": (_I, [_I]),
     "map_timing_read": (_I, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
                              ctypes.POINTER(ctypes.c_int), _I]),
@@ -259,6 +260,13 @@ def map_prune(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torc
                            _ptr(o["pos_out"]), _ptr(o["p"]), _ptr(o["order"]), _ptr(o["gain"]),
                            _ptr(workspace.buf), workspace.nbytes, _stream(dev)), "map_prune")
     return o
+
+
+def set_subset_tokens(n: int):
+    """map_prune's candidate subset: n < 0 never, 0 automatic, n > 0 that
+    many tokens.  Process-wide; workspaces sized before a change may be too
+    small after it (map_prune then reports a workspace error)."""
+    _check(lib().map_set_subset_tokens(int(n)), "map_set_subset_tokens")
 
 
 def timing_enable(on: bool = True):

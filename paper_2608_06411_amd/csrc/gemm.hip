@@ -142,7 +142,10 @@ __device__ __forceinline__ int acc_col(int lane) { return lane & 31; }
 // The tiles of the problems before args.first_tiles run first, each class
 // XCD-contiguous: the launch puts the layer-1 and fold tiles there, so the
 // second wave of workgroups holds only Gram tiles, whose epilogue is shorter.
-__device__ __forceinline__ void decode_tile(const GemmBatch& args, int& pi, int& bt, int& tm, int& tn) {
+// A problem split over K (ksplit > 1) runs its tiles once per K range kc,
+// the ranges outermost, so that concurrent tiles read the same K columns.
+__device__ __forceinline__ void decode_tile(const GemmBatch& args, int& pi, int& bt, int& tm, int& tn, int& kc,
+                                            int& local) {
   const int b = blockIdx.x, f = args.first_tiles;
   const int tile = b < f ? xcd_remap(b, f) : f + xcd_remap(b - f, args.total_tiles - f);
   pi = 0;
@@ -150,9 +153,11 @@ __device__ __forceinline__ void decode_tile(const GemmBatch& args, int& pi, int&
   for (int q = 1; q < kMaxGemmProblems; ++q)
     if (q < args.count && tile >= args.p[q].tile_begin) pi = q;
   const GemmProblem& P = args.p[pi];
-  const int local = tile - P.tile_begin;
+  local = tile - P.tile_begin;
   bt = local / P.tiles_per_batch;
   int tt = local - bt * P.tiles_per_batch;
+  kc = tt / P.tiles_tri;
+  tt -= kc * P.tiles_tri;
   if (P.triangular) {  // upper triangle, row by row: row tm holds tiles_n - tm tiles
     tm = 0;
     while (tt >= P.tiles_n - tm) { tt -= P.tiles_n - tm; ++tm; }
@@ -296,9 +301,10 @@ __global__ __launch_bounds__(NT) void gemm_kernel(const GemmBatch args) {
   constexpr int VEC = Slice<T>::VEC;
   constexpr int BK = Slice<T>::BK;
 
-  int pi, bt, tm, tn;
-  decode_tile(args, pi, bt, tm, tn);
+  int pi, bt, tm, tn, kc, local;
+  decode_tile(args, pi, bt, tm, tn, kc, local);
   const GemmProblem& P = args.p[pi];
+  if (P.run_if && P.run_if[bt] == 0) return;  // (index maps and K ranges: direct-load kernel only)
   const int M = P.M, N = P.N, K = P.K;
   const T* __restrict__ A = static_cast<const T*>(P.A) + bt * P.strideA;
   const T* __restrict__ B = static_cast<const T*>(P.B) + bt * P.strideB;
@@ -533,16 +539,18 @@ __device__ __forceinline__ void wait_vm_lgkm0(int outstanding) {
 
 __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
   __shared__ uint4 st0[2][BM][8], st1[2][BM][8], st2[2][BM][8], st3[2][BM][8], st4[2][BM][8];  // 5 x 32 KiB
-  int pi, bt, tm, tn;
-  decode_tile(args, pi, bt, tm, tn);
+  int pi, bt, tm, tn, kc, local;
+  decode_tile(args, pi, bt, tm, tn, kc, local);
   const GemmProblem& P = args.p[pi];
+  if (P.run_if && P.run_if[bt] == 0) return;
   const int M = P.M, N = P.N;
-  const bf16_t* __restrict__ A = static_cast<const bf16_t*>(P.A) + bt * P.strideA;
-  const bf16_t* __restrict__ B = static_cast<const bf16_t*>(P.B) + bt * P.strideB;
+  const int kl = P.ksplit > 1 ? P.K / P.ksplit : P.K;  // this workgroup's K range: kc kl .. (kc + 1) kl
+  const bf16_t* __restrict__ A = static_cast<const bf16_t*>(P.A) + bt * P.strideA + (long long)kc * kl;
+  const bf16_t* __restrict__ B = static_cast<const bf16_t*>(P.B) + bt * P.strideB + (long long)kc * kl;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int nk = P.K / 64;
+  const int nk = kl / 64;
   float rs_mine = 0.0f;  // cosine epilogue: reciprocal norm of tile row tid, or of column tid - BM
   if (P.epi == EPI_COSINE) {
     const float* rs = P.rs + (long long)bt * M;
@@ -551,15 +559,19 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
   }
 
   // Per-lane global row pointers of this wave's 4 A rows and 4 B rows
-  // (rows past the matrix read its last row; they are never stored).
+  // (rows past the matrix read its last row; they are never stored), through
+  // the index maps when there are any.
+  const int32_t* mapA = P.mapA ? P.mapA + bt * P.mapStride : nullptr;
+  const int32_t* mapB = P.mapB ? P.mapB + bt * P.mapStride : nullptr;
   const bf16_t* ga[4];
   const bf16_t* gb[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = 32 * wave + 8 * j + (lane >> 3);
     const int v = (lane & 7) ^ swz(r);  // the chunk the swizzle puts at position lane & 7 of row r
-    ga[j] = A + (long long)min(m0 + r, M - 1) * P.lda + 8 * v;
-    gb[j] = B + (long long)min(n0 + r, N - 1) * P.ldb + 8 * v;
+    const int ra = min(m0 + r, M - 1), rb = min(n0 + r, N - 1);
+    ga[j] = A + (long long)(mapA ? mapA[ra] : ra) * P.lda + 8 * v;
+    gb[j] = B + (long long)(mapB ? mapB[rb] : rb) * P.ldb + 8 * v;
   }
   // this wave's first destination row inside a stage: 32 wave rows of 128 bytes
   const uint32_t wrow = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave)) * 32u * 128u;
@@ -608,6 +620,20 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
     step(st4, st3, kt + 3);
     if (kt + 4 >= nk) break;
     step(st0, st4, kt + 4);
+  }
+  if (P.epi == EPI_PARTIAL) {
+    // the raw sums of this K range: float4 q = (2 i + j) 4 + e / 4 of thread
+    // tid at q * 256 + tid (every store of a wave contiguous)
+    float4* dst = static_cast<float4*>(P.C) + (long long)local * (16 * NT);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          dst[((2 * i + j) * 4 + g) * NT + tid] =
+              make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+    return;
   }
   __syncthreads();  // the epilogues reuse the stage arrays
   float* rs_tile = reinterpret_cast<float*>(&st4[0][0][0]);
@@ -730,7 +756,78 @@ __global__ __launch_bounds__(kPW * 64) void proj_rope_kernel(const GemmBatch arg
   }
 }
 
+// The K ranges of a split problem summed in order kc = 0, 1, ...: workgroup
+// (tile t, piece q, batch item) takes float4 q of every thread of the
+// tile's partials, i.e. accumulator block (i, j) = (q / 8, q / 4 % 2), rows
+// 4 (q % 4) .. + 3 of the thread's 32 x 32 block layout, and writes those
+// entries of S and their mirror as the cosine epilogue does.
+__global__ __launch_bounds__(NT) void gram_reduce_kernel(const GemmProblem P, float* out, int ldc,
+                                                         const float* rs_all) {
+  const int bt = blockIdx.y, t = blockIdx.x >> 4, q = blockIdx.x & 15;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int ks = P.ksplit > 1 ? P.ksplit : 1;
+  int tm = 0, tt = t;
+  while (tt >= P.tiles_n - tm) {
+    tt -= P.tiles_n - tm;
+    ++tm;
+  }
+  const int tn = tm + tt;
+  const float4* src = static_cast<const float4*>(P.C) + (long long)bt * P.tiles_per_batch * (16 * NT);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 x[16];
+#pragma unroll
+  for (int kc = 0; kc < 16; ++kc)
+    if (kc < ks) x[kc] = src[((long long)kc * P.tiles_tri + t) * (16 * NT) + q * NT + tid];
+#pragma unroll
+  for (int kc = 0; kc < 16; ++kc)
+    if (kc < ks) {
+      v.x += x[kc].x;
+      v.y += x[kc].y;
+      v.z += x[kc].z;
+      v.w += x[kc].w;
+    }
+  for (int kc = 16; kc < ks; ++kc) {
+    const float4 y = src[((long long)kc * P.tiles_tri + t) * (16 * NT) + q * NT + tid];
+    v.x += y.x;
+    v.y += y.y;
+    v.z += y.z;
+    v.w += y.w;
+  }
+  const int i = q >> 3, j = (q >> 2) & 1, g = q & 3;
+  const int M = P.M, m0 = tm * BM, n0 = tn * BN;
+  const bool diag = tm == tn;
+  const int col = n0 + wn * 64 + j * 32 + acc_col(lane);
+  const int row0 = m0 + wm * 64 + i * 32 + 8 * g + 4 * (lane >> 5);
+  if (col >= M) return;
+  const float* rs = rs_all + (long long)bt * M;
+  float* S = out + (long long)bt * M * ldc;
+  const float sc = rs[col];
+  const float a[4] = {v.x, v.y, v.z, v.w};
+  float w[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int row = row0 + e;
+    w[e] = row < M ? a[e] * (rs[row] * sc) : 0.0f;
+    if (row < M && (!diag || row <= col)) S[(long long)row * ldc + col] = w[e];
+  }
+  float* dst = S + (long long)col * ldc + row0;  // S[col][row0 .. row0 + 3]
+  if (!diag && (ldc & 3) == 0 && row0 + 3 < M) {
+    *reinterpret_cast<float4*>(dst) = make_float4(w[0], w[1], w[2], w[3]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (row0 + e < M && (!diag || row0 + e < col)) dst[e] = w[e];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_gram_reduce(const GemmProblem& partial, float* out, int ldc, const float* rs, hipStream_t s) {
+  if (partial.tiles_tri == 0 || partial.batch == 0) return hipSuccess;
+  return launch_kernel("gram_reduce", gram_reduce_kernel, dim3(partial.tiles_tri * 16, partial.batch), dim3(NT), 0,
+                       s, partial, out, ldc, rs);
+}
 
 void gemm_finalize(GemmBatch& g) {
   int begin = 0;
@@ -738,7 +835,8 @@ void gemm_finalize(GemmBatch& g) {
     GemmProblem& p = g.p[i];
     p.tiles_m = (p.M + BM - 1) / BM;
     p.tiles_n = (p.N + BN - 1) / BN;
-    p.tiles_per_batch = p.triangular ? p.tiles_m * (p.tiles_m + 1) / 2 : p.tiles_m * p.tiles_n;
+    p.tiles_tri = p.triangular ? p.tiles_m * (p.tiles_m + 1) / 2 : p.tiles_m * p.tiles_n;
+    p.tiles_per_batch = p.tiles_tri * (p.ksplit > 1 ? p.ksplit : 1);
     p.tile_begin = begin;
     begin += p.tiles_per_batch * p.batch;
   }
@@ -755,9 +853,12 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
       const GemmProblem& p = g.p[i];
       dma = dma && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
             (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
-            p.strideA % 8 == 0 && p.strideB % 8 == 0;
+            p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
+            (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));
     }
     if (dma) return launch_kernel(name, gemm_dma_kernel, dim3(g.total_tiles), dim3(NT), 0, s, g);
+    for (int i = 0; i < g.count; ++i)  // index maps and K ranges exist in the direct-load kernel only
+      if (g.p[i].epi == EPI_PARTIAL || g.p[i].mapA || g.p[i].mapB) return hipErrorInvalidValue;
     return launch_kernel(name, gemm_kernel<bf16_t>, dim3(g.total_tiles), dim3(NT), 0, s, g);
   }
   return launch_kernel(name, gemm_kernel<float>, dim3(g.total_tiles), dim3(NT), 0, s, g);

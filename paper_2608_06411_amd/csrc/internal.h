@@ -74,6 +74,7 @@ enum EpiMode : int {
   EPI_BIAS = 1,       // C[m][n] = acc + bias[n] (no bias when null), stored as T
   EPI_COSINE = 2,     // S[m][n] = acc * rs[m] * rs[n] (float32), mirrored; A == B
   EPI_ROPE = 3,       // out[m][:] = RoPE(acc[m][:] + rope_bias) (float32) with the row's cos/sin
+  EPI_PARTIAL = 4,    // the raw float32 accumulators of a K range, for gram_reduce (bf16 direct-load kernel)
 };
 
 struct GemmProblem {
@@ -88,9 +89,15 @@ struct GemmProblem {
   const float* rs;         // EPI_COSINE: [batch][M] reciprocal norms
   const float2* rope_cs;   // EPI_ROPE: [M][N/2] (cos, sin) per row and pair
   const float* rope_bias;  // EPI_ROPE: [N] float32 added before the rotation (may be null)
-  int triangular;          // EPI_COSINE: only tiles with tile_n >= tile_m
+  int triangular;          // EPI_COSINE, EPI_PARTIAL: only tiles with tile_n >= tile_m
+  // rows of A and B through index maps ([batch][mapStride]; null: row m is row m)
+  const int32_t* mapA;
+  const int32_t* mapB;
+  long long mapStride;
+  int ksplit;              // EPI_PARTIAL: K ranges per tile (K / ksplit each, a multiple of 256)
+  const int32_t* run_if;   // [batch] batch items whose flag is 0 are skipped (null: none)
   // filled by the host helper
-  int tiles_m, tiles_n, tiles_per_batch, tile_begin;
+  int tiles_m, tiles_n, tiles_tri, tiles_per_batch, tile_begin;
 };
 
 constexpr int kMaxGemmProblems = 6;
@@ -106,6 +113,30 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
 // The projection with the RoPE epilogue (every problem EPI_ROPE, at most two):
 // a K-split kernel for bf16 and N <= 128, else launch_gemm.
 hipError_t launch_proj_rope(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s);
+// The split-K sums of an EPI_PARTIAL problem (finalized, ksplit > 1) in a
+// fixed order, then the cosine epilogue into out (symmetric, ldc, rs as in
+// EPI_COSINE).
+hipError_t launch_gram_reduce(const GemmProblem& partial, float* out, int ldc, const float* rs, hipStream_t s);
+
+// ---------------------------------------------------------------- subset
+// The candidate subset J of map_prune (R0 plus the largest score bounds),
+// compacted in token order, and the largest bound key left out.
+struct SubsetArgs {
+  const float* p;       // [B][N]
+  const float* norms;   // [B][N]
+  const float* ninv;    // [B][N]
+  int32_t* jmap;        // [B][Nc] token of each subset position, ascending
+  float* pJ;            // [B][Nc]
+  float* nJ;            // [B][Nc]
+  float* ninvJ;         // [B][Nc]
+  uint32_t* hout;       // [B] high word of the largest bound key outside J
+  int32_t* uncert;      // [B] cleared here; set by the selection when a pick is not certified
+  unsigned int* clear_bar;  // [B] barrier counters of the full selection behind the subset, cleared here
+  int B, N, Nc, K0;
+  float tau2;
+};
+constexpr int kSubsetMaxN = 8192;
+hipError_t launch_subset(const SubsetArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- prep
 // Row norms of the visual tokens (and their reciprocals) plus the RoPE
@@ -170,6 +201,15 @@ struct SelectArgs {
   void* gV_out;           // [B][K] rows of row_bytes
   int32_t* gpos_out;      // [B][K]
   int row_bytes;
+  // map_prune on a candidate subset: N is the subset's size, token k of the
+  // subset is token jmap[b][k] of the image (Ng tokens in gV and gpos)
+  const int32_t* jmap;    // [B][N] ascending (null: no subset)
+  int32_t* order_map;     // [B][K] the selection order as image tokens (may be null)
+  const uint32_t* hout;   // [B] greedy picks must key above it (null: no check)
+  int32_t* uncert;        // [B] set to 1 when a greedy pick does not
+  const int32_t* run_if;  // [B] images whose flag is 0 are skipped (null: none)
+  int Ng;
+  int fallback;           // the launches are the full selection behind a subset (timing names)
   int B, N, K, K0, G, ch, pcap;
   float tau2;
 };

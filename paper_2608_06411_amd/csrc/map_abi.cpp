@@ -9,9 +9,17 @@
 //                   Gram matrix (one launch, both stream V) -> layer 2 ->
 //                   projections -> logits -> softmax-mean -> top-K0 ->
 //                   selection -> restore order -> gather
+//                   or, on a candidate subset (bf16, N <= 8192):
+//                   prep -> GEMM layer 1 -> projections -> logits ->
+//                   softmax-mean -> subset -> cosine entries among the
+//                   subset (K-split GEMM + ordered sum) -> selection with
+//                   gather on the subset -> for the images whose picks are
+//                   not certified: Gram matrix -> selection with gather
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -123,12 +131,60 @@ struct SelectWs {
   int32_t* r0flag;
 };
 
+// map_prune's candidate subset: its size per image (0: the full path).
+std::atomic<int> g_subset_tokens{0};  // < 0 off, 0 automatic, > 0 that many tokens
+
+int subset_size(map_dtype dt, int N, int D, const map_select_params& sp) {
+  const int o = g_subset_tokens.load();
+  if (o < 0 || dt != MAP_BF16 || D % 256 != 0 || N > kSubsetMaxN) return 0;
+  int nc = o;
+  if (o == 0) {
+    nc = (sp.K0 + std::max(2 * (sp.K - sp.K0), N / 4) + 63) & ~63;
+    if (4 * nc > 3 * N) return 0;  // too close to N to pay
+  }
+  nc = std::max(nc, sp.K);
+  return nc < N ? nc : 0;
+}
+
+int subset_ksplit(int D) { return D % 512 == 0 ? D / 512 : D / 256; }
+
+int subset_tiles(int nc) {
+  const int t = (nc + 127) / 128;
+  return t * (t + 1) / 2;
+}
+
+struct SubsetWs {
+  int32_t* jmap;
+  float* pJ;
+  float* nJ;
+  float* ninvJ;
+  uint32_t* hout;
+  int32_t* uncert;
+  float* SJ;
+  float* partial;
+  int32_t* order_img;
+};
+
+SubsetWs carve_subset(Carver& c, int B, int K, int nc, int D) {
+  SubsetWs s;
+  s.jmap = c.take<int32_t>((size_t)B * nc);
+  s.pJ = c.take<float>((size_t)B * nc);
+  s.nJ = c.take<float>((size_t)B * nc);
+  s.ninvJ = c.take<float>((size_t)B * nc);
+  s.hout = c.take<uint32_t>(B);
+  s.uncert = c.take<int32_t>(B);
+  s.SJ = c.take<float>((size_t)B * nc * nc);
+  s.partial = c.take<float>((size_t)B * subset_tiles(nc) * subset_ksplit(D) * 128 * 128);
+  s.order_img = c.take<int32_t>((size_t)B * K);
+  return s;
+}
+
 SelectWs carve_select(Carver& c, int B, int N, int K) {
   SelectWs s;
   s.C = c.take<float>((size_t)B * N * ((K + 3) & ~3));  // token-major, rows of K rounded up to 4
   s.r2 = c.take<float>((size_t)B * N);
   s.pub = c.take<uint64_t>((size_t)B * 2 * 128 * (kPub + 1));
-  s.bar = c.take<unsigned int>(B);
+  s.bar = c.take<unsigned int>(2 * (size_t)B);  // the second B: the full selection behind a subset
   s.err = c.take<int32_t>(4);
   s.order = c.take<int32_t>((size_t)B * K);
   s.gain = c.take<float>((size_t)B * K);
@@ -266,12 +322,35 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
 // selection's counters and the gather ranks the selection order itself.
 // With `ga` (map_prune), the selection kernel also gathers the kept rows when
 // its order fits in LDS; *gathered says whether it did.
+// With `sub` the selection runs on a candidate subset (or is the full
+// selection behind one, for the images the subset's run flagged).
+struct SubsetSel {
+  const int32_t* jmap;
+  int32_t* order_map;
+  const uint32_t* hout;
+  int32_t* uncert;
+  const int32_t* run_if;
+  int Ng;
+  int fallback;
+};
+
 hipError_t enqueue_select(int B, int N, const float* p, const float* S, const float* norms,
                           const map_select_params& sp, int32_t* idx_out, int32_t* order_out,
                           float* gain_out, const SelectWs& w, hipStream_t st, bool fused = false,
-                          const GatherArgs* ga = nullptr, bool* gathered = nullptr) {
+                          const GatherArgs* ga = nullptr, bool* gathered = nullptr,
+                          const SubsetSel* sub = nullptr) {
   SelectArgs a;
   memset(&a, 0, sizeof(a));
+  a.Ng = N;
+  if (sub) {
+    a.jmap = sub->jmap;
+    a.order_map = sub->order_map;
+    a.hout = sub->hout;
+    a.uncert = sub->uncert;
+    a.run_if = sub->run_if;
+    a.Ng = sub->Ng;
+    a.fallback = sub->fallback;
+  }
   a.p = p;
   a.S = S;
   a.norms = norms;
@@ -368,6 +447,100 @@ LaunchEvents timing_events(const char* name) {
 
 }  // namespace mapk
 
+// map_prune on a candidate subset (see subset.hip), with the full
+// selection behind it for the images whose picks it cannot certify.
+map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, const void* V, const int32_t* pos_v,
+                           const void* T, const int32_t* pos_t, const int32_t* t_off_host,
+                           const map_select_params& sp, int32_t* idx_out, void* V_out, int32_t* pos_out, float* p,
+                           int32_t* order_out, float* gain_out, const ScoreWs& s, const SelectWs& sw, float* S,
+                           float* norms, float* ninv, const SubsetWs& u, int nc, hipStream_t st) {
+  hipError_t e =
+      enqueue_score(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, nullptr, norms, ninv, st, sw.bar, sw.err);
+  if (e != hipSuccess) return MAP_ERR_HIP;
+  SubsetArgs sa;
+  memset(&sa, 0, sizeof(sa));
+  sa.p = p;
+  sa.norms = norms;
+  sa.ninv = ninv;
+  sa.jmap = u.jmap;
+  sa.pJ = u.pJ;
+  sa.nJ = u.nJ;
+  sa.ninvJ = u.ninvJ;
+  sa.hout = u.hout;
+  sa.uncert = u.uncert;
+  sa.B = B;
+  sa.N = N;
+  sa.Nc = nc;
+  sa.K0 = sp.K0;
+  sa.tau2 = sp.tau * sp.tau;
+  sa.clear_bar = sw.bar + B;
+  if ((e = launch_subset(sa, st)) != hipSuccess) return MAP_ERR_HIP;
+
+  // cosine entries among the subset: raw sums per K range, then their
+  // ordered sum with the cosine scaling
+  GemmBatch g;
+  memset(&g, 0, sizeof(g));
+  g.p[0] = gram(V, B, nc, w.D, u.partial, nullptr);
+  g.p[0].strideA = (long long)N * w.D;
+  g.p[0].strideB = (long long)N * w.D;
+  g.p[0].epi = EPI_PARTIAL;
+  g.p[0].mapA = u.jmap;
+  g.p[0].mapB = u.jmap;
+  g.p[0].mapStride = nc;
+  g.p[0].ksplit = subset_ksplit(w.D);
+  g.count = 1;
+  gemm_finalize(g);
+  if ((e = launch_gemm(dt, g, "gemm_subset", st)) != hipSuccess) return MAP_ERR_HIP;
+  if ((e = launch_gram_reduce(g.p[0], u.SJ, nc, u.ninvJ, st)) != hipSuccess) return MAP_ERR_HIP;
+
+  int32_t* order_img = order_out ? order_out : u.order_img;
+  GatherArgs ga;
+  ga.V = V;
+  ga.pos_v = pos_v;
+  ga.order = order_img;
+  ga.err = sw.err;
+  ga.idx_out = idx_out;
+  ga.V_out = V_out;
+  ga.pos_out = pos_out;
+  ga.B = B;
+  ga.N = N;
+  ga.K = sp.K;
+  ga.row_bytes = static_cast<int>(w.D * elem_size(dt));
+  SubsetSel sub;
+  memset(&sub, 0, sizeof(sub));
+  sub.jmap = u.jmap;
+  sub.order_map = order_img;
+  sub.hout = u.hout;
+  sub.uncert = u.uncert;
+  sub.Ng = N;
+  bool gathered = false;
+  e = enqueue_select(B, nc, u.pJ, u.SJ, u.nJ, sp, idx_out, sw.order, gain_out, sw, st, true, &ga, &gathered, &sub);
+  if (e != hipSuccess) return MAP_ERR_HIP;
+  if (!gathered && (e = launch_gather(ga, st)) != hipSuccess) return MAP_ERR_HIP;
+
+  // the images whose picks were not certified: the full Gram matrix and
+  // selection (every workgroup of a certified image returns at once; its
+  // barrier counters are the second set, which the subset kernel cleared)
+  GemmBatch gf;
+  memset(&gf, 0, sizeof(gf));
+  gf.p[0] = gram(V, B, N, w.D, S, ninv);
+  gf.p[0].run_if = u.uncert;
+  gf.count = 1;
+  gemm_finalize(gf);
+  if ((e = launch_gemm(dt, gf, "gemm_gram_full", st)) != hipSuccess) return MAP_ERR_HIP;
+  SubsetSel full;
+  memset(&full, 0, sizeof(full));
+  full.run_if = u.uncert;
+  full.Ng = N;
+  full.fallback = 1;
+  gathered = false;
+  SelectWs sw2 = sw;
+  sw2.bar = sw.bar + B;
+  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_img, gain_out, sw2, st, true, &ga, &gathered, &full);
+  if (e != hipSuccess) return MAP_ERR_HIP;
+  return gathered ? MAP_OK : hip_status(launch_gather(ga, st));
+}
+
 extern "C" {
 
 const char* map_status_string(int status) {
@@ -402,8 +575,22 @@ size_t map_prune_workspace(map_dtype dt, int B, int N, int sum_M, const map_weig
   if (!valid_dtype(dt) || !valid_bn(B, N) || !valid_weights(w) || sum_M < B || K < 1 || K > N ||
       K > MAP_MAX_K)
     return 0;
+  map_select_params sp;
+  sp.K = K;
+  sp.K0 = K / 2;  // the subset's size does not depend on K0 beyond this bound
+  sp.tau = 0.0f;
+  size_t sub = 0;
+  for (int k0 : {0, K}) {  // the largest subset any K0 can ask for
+    sp.K0 = k0;
+    const int nc = subset_size(dt, N, w->D, sp);
+    if (nc > 0) {
+      Carver c(nullptr);
+      carve_subset(c, B, K, nc, w->D);
+      sub = std::max(sub, c.off);
+    }
+  }
   return score_ws_bytes(dt, B, N, sum_M, *w) + select_ws_bytes(B, N, K) +
-         align_up((size_t)B * N * N * sizeof(float)) + 3 * align_up((size_t)B * N * sizeof(float));
+         align_up((size_t)B * N * N * sizeof(float)) + 3 * align_up((size_t)B * N * sizeof(float)) + sub;
 }
 
 map_status map_score(const map_weights* w, map_dtype dt, int B, int N, const void* V,
@@ -480,6 +667,10 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   float* norms = c.take<float>((size_t)B * N);
   float* ninv = c.take<float>((size_t)B * N);
   float* p = p_out ? p_out : c.take<float>((size_t)B * N);
+  const int nc = subset_size(dt, N, w->D, sp);
+  if (nc > 0) return prune_on_subset(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, sp, idx_out, V_out, pos_out,
+                                     p, order_out, gain_out, s, sw, S, norms, ninv, carve_subset(c, B, sp.K, nc, w->D),
+                                     nc, st);
   const GemmProblem g = gram(V, B, N, w->D, S, ninv);
   hipError_t e =
       enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, &g, norms, ninv, st, sw.bar, sw.err);
@@ -500,6 +691,11 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st, true, &ga, &gathered);
   if (e != hipSuccess) return MAP_ERR_HIP;
   return gathered ? MAP_OK : hip_status(launch_gather(ga, st));  // else its own kernel
+}
+
+map_status map_set_subset_tokens(int n) {
+  g_subset_tokens.store(n);
+  return MAP_OK;
 }
 
 map_status map_timing_enable(int enable) {

@@ -280,6 +280,7 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   const int N = a.N, K0 = a.K0, K = a.K, Kp = (K + 3) & ~3;
   const int b = blockIdx.y, w = blockIdx.x;
+  if (a.run_if && a.run_if[b] == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* p = a.p + (long long)b * N;
   const float* nrm = a.norms + (long long)b * N;
@@ -493,6 +494,7 @@ __global__ __launch_bounds__(NT) void r0_kernel(const SelectArgs a) {
       if (tid < K0) {
         a.order[(long long)b * K + tid] = rmine;
         a.gain[(long long)b * K + tid] = (pmine > 0.0f && pmine <= 3.402823466e38f) ? pmine : 0.0f;
+        if (a.order_map) a.order_map[(long long)b * K + tid] = a.jmap[(long long)b * N + rmine];
       }
     }
     if (tid == 0) {
@@ -726,6 +728,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   const int G = a.G, ch = a.ch, pcap = a.pcap, K = a.K, K0 = a.K0, N = a.N;
   const int Kp = (K + 3) & ~3;
   const int b = b_begin + blockIdx.x / G, w = blockIdx.x % G;
+  if (a.run_if && a.run_if[b] == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const Lds L = lds_layout(K, G, ch, pcap, PIPE);
   int* midx = reinterpret_cast<int*>(lds + L.midx);
@@ -841,18 +844,19 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
           r4[3] += (x.w < v) + (y.w < v);
         }
         const int rk = (r4[0] + r4[1]) + (r4[2] + r4[3]);
-        if (rk % G == w) share[rk / G] = v;
+        // (a subset's positions order like its tokens: the ranks hold)
+        if (rk % G == w) share[rk / G] = a.jmap ? a.jmap[(long long)b * N + v] : v;
       }
       __syncthreads();
     }
     for (int sI = tid; sI < nshare; sI += NT) {
       const int k = w + G * sI, v = bad ? -1 : share[sI];
       a.idx_out[(long long)b * K + k] = v;
-      a.gpos_out[(long long)b * K + k] = bad ? -1 : a.gpos[(long long)b * N + v];
+      a.gpos_out[(long long)b * K + k] = bad ? -1 : a.gpos[(long long)b * a.Ng + v];
     }
     // rows, 16 bytes per piece; every load of a thread before its first store
     const int chunks = a.row_bytes >> 4, total = nshare * chunks;
-    const uint4* src = static_cast<const uint4*>(a.gV) + (long long)b * N * chunks;
+    const uint4* src = static_cast<const uint4*>(a.gV) + (long long)b * a.Ng * chunks;
     uint4* dst = static_cast<uint4*>(a.gV_out) + (long long)b * K * chunks;
     constexpr int GU = 4;
     for (int e0 = tid; e0 < total; e0 += GU * NT) {
@@ -1375,6 +1379,9 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         a.order[(long long)b * K + t0 + k] = midx[pslot[k]];
         a.gain[(long long)b * K + t0 + k] =
             forced ? __uint_as_float(pgain[k]) : key_score(static_cast<uint64_t>(pgain[k]) << 32);
+        if (a.order_map) a.order_map[(long long)b * K + t0 + k] = a.jmap[(long long)b * N + midx[pslot[k]]];
+        // on a subset a greedy pick stands only if no token left out could beat it
+        if (a.hout && !forced && pgain[k] <= a.hout[b]) a.uncert[b] = 1;
       }
     if (forced) fq += np;
     if (t >= K) {
@@ -1672,17 +1679,18 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
                                                hipFuncAttributeMaxDynamicSharedMemorySize, rb);
       if (e != hipSuccess) return e;
     }
-    const hipError_t e = launch_kernel("select_r0", r0_kernel, dim3((a.N + 63) / 64, a.B), dim3(NT),
+    const hipError_t e = launch_kernel(a.fallback ? "select_r0_full" : "select_r0", r0_kernel,
+                                       dim3((a.N + 63) / 64, a.B), dim3(NT),
                                        static_cast<size_t>(rb), s, a);
     if (e != hipSuccess) return e;
   }
   for (int b0 = 0; b0 < a.B; b0 += per_launch) {
     const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
     const hipError_t e =
-        chosen_pipe ? launch_kernel("select", select_kernel<true>, dim3(nb * chosen_G), dim3(NT),
-                                    static_cast<size_t>(chosen_bytes), s, a, b0)
-                    : launch_kernel("select", select_kernel<false>, dim3(nb * chosen_G), dim3(NT),
-                                    static_cast<size_t>(chosen_bytes), s, a, b0);
+        chosen_pipe ? launch_kernel(a.fallback ? "select_full" : "select", select_kernel<true>, dim3(nb * chosen_G),
+                                    dim3(NT), static_cast<size_t>(chosen_bytes), s, a, b0)
+                    : launch_kernel(a.fallback ? "select_full" : "select", select_kernel<false>, dim3(nb * chosen_G),
+                                    dim3(NT), static_cast<size_t>(chosen_bytes), s, a, b0);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

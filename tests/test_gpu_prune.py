@@ -4,6 +4,9 @@
 * The selection, replayed on the oracle with the GPU's own p_hat (exactly as
   float64): every pick is the oracle's, except below a 1e-4 decisive gap.
 * The gather: kept rows and positions byte-exact, indices ascending.
+* The candidate subset (bf16): automatic, off, and one so small that the
+  certificate rejects its picks and the images are selected again in full;
+  every mode meets the same bar.
 """
 import numpy as np
 import pytest
@@ -86,3 +89,27 @@ def test_prune_is_deterministic():
     for k in ("p", "idx", "order", "gain", "pos_out"):
         np.testing.assert_array_equal(a[k].numpy(), b[k].numpy())
     np.testing.assert_array_equal(a["V_store_out"], b["V_store_out"])
+
+
+@pytest.mark.parametrize("mode", ["auto", "off", "K", "half"])
+def test_prune_subset_modes(mode):
+    from paper_2608_06411_amd import set_subset_tokens
+    cfg = get_config("sweep", B=2, N=960, M=(16, 64), K=96, K0=48)
+    announce(f"prune subset mode {mode}")
+    x = make_inputs(cfg)
+    set_subset_tokens({"auto": 0, "off": -1, "K": cfg.K, "half": cfg.N // 2}[mode])
+    try:
+        out = _prune(x, cfg.K, cfg.K0, cfg.tau)
+    finally:
+        set_subset_tokens(0)
+    _check(x, out, cfg.K, cfg.K0, cfg.tau, 2e-2)
+
+
+def test_prune_subset_multiframe_image():
+    """D = 3584 (seven K ranges of 512) and a subset too small for the
+    eight-frame image's picks: the full selection behind it decides."""
+    cfg = get_config("multiframe", B=1)
+    announce("prune multiframe B=1")
+    x = make_inputs(cfg)
+    out = _prune(x, cfg.K, cfg.K0, cfg.tau)
+    _check(x, out, cfg.K, cfg.K0, cfg.tau, 2e-2)
