@@ -99,14 +99,26 @@ __device__ void block_max_min32(uint32_t& mx, uint32_t& mn, BlockScratch& s) {
   __syncthreads();
 }
 
+// Inclusive prefix sum over the lanes of a wave64 (row shifts within each
+// row of 16 lanes, then the row broadcasts).
+template <int CTRL, int ROW_MASK, int BANK_MASK, bool BOUND>
+__device__ __forceinline__ int dpp_add(int v) {
+  return v + __builtin_amdgcn_update_dpp(0, v, CTRL, ROW_MASK, BANK_MASK, BOUND);
+}
+__device__ __forceinline__ int wave_inclusive_sum(int v) {
+  v = dpp_add<0x111, 0xf, 0xf, true>(v);   // row_shr:1
+  v = dpp_add<0x112, 0xf, 0xf, true>(v);   // row_shr:2
+  v = dpp_add<0x114, 0xf, 0xf, true>(v);   // row_shr:4
+  v = dpp_add<0x118, 0xf, 0xf, true>(v);   // row_shr:8: each row scanned
+  v = dpp_add<0x142, 0xa, 0xf, false>(v);  // row_bcast:15 into rows 1 and 3
+  v = dpp_add<0x143, 0xc, 0xf, false>(v);  // row_bcast:31 into rows 2 and 3
+  return v;
+}
+
 // Exclusive prefix sum over the workgroup's threads (thread order), and the total.
 __device__ int block_exclusive_sum(int v, int& total, BlockScratch& s) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int x = v;
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  const int x = wave_inclusive_sum(v);
   if (lane == 63) s.part[wave] = x;
   __syncthreads();
   int before = 0;
@@ -119,59 +131,54 @@ __device__ int block_exclusive_sum(int v, int& total, BlockScratch& s) {
   return before + x - v;
 }
 
-// Keys per thread: token i = tid + NT u is kept in register slot u.
+// Most register slots of one thread: token i = tid + NT u sits in slot u.
 constexpr int kKpt = kSubsetMaxN / NT;
 
-// One histogram of the keys (register slots u < nu) that lie in [lo, hi]
-// over 1024 bins of equal width 2^sh; returns the lower edge of the highest
-// bin at which the count from the top reaches `need` -- every key at or above
-// it is taken, at least `need` of them -- when `atleast`, else the lowest
-// edge above which at most `need` keys lie (fewer may).
-__device__ uint64_t hist_edge(const uint64_t (&kr)[kKpt], int nu, int need, bool atleast, uint64_t lo,
-                              uint64_t hi, int* hist, BlockScratch& s) {
+// One histogram of the keys over 1024 bins of equal width: the keys of the
+// valid register slots (u < nu) whose high words lie in [mn, mx], binned by
+// high word ((h - mn) >> sh, sh chosen so that the bins cover the range).
+// Returns the lowest high word of the bin at which the count from the top
+// reaches `need` (every key of that bin and above is taken, at least `need`
+// of them) when `atleast`; else the lowest high word above which at most
+// `need` keys lie (fewer may): the bin that would overflow is left out.
+template <int KPT>
+__device__ uint64_t hist_edge(const uint32_t (&hr)[KPT], uint32_t valid, int need, bool atleast, uint32_t mn,
+                              uint32_t mx, int* hist, BlockScratch& s) {
   const int tid = threadIdx.x, lane = tid & 63;
-  const uint64_t span = hi - lo;
-  const int bits = span ? 64 - __builtin_clzll(span) : 0;
+  const uint32_t span = mx - mn;
+  const int bits = span ? 32 - __builtin_clz(span) : 0;
   const int sh = bits > 10 ? bits - 10 : 0;  // (span >> sh) < 1024
   for (int j = tid; j < kBins; j += NT) hist[j] = 0;
   __syncthreads();
 #pragma unroll
-  for (int u = 0; u < kKpt; ++u) {
-    const uint64_t x = kr[u];
-    if (u < nu && x >= lo && x <= hi) atomicAdd(&hist[static_cast<int>((x - lo) >> sh)], 1);
-  }
+  for (int u = 0; u < KPT; ++u)
+    if ((valid >> u) & 1u) atomicAdd(&hist[(hr[u] - mn) >> sh], 1);
   __syncthreads();
-  if (tid < 64) {  // lane l: bins 16 l .. 16 l + 15
+  if (tid < 64) {  // lane l: bins 16 (63 - l) .. + 15, so the lane prefix sums count from the top
+    const int base = 16 * (63 - lane);
     int c[16], mine = 0;
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
-      c[q] = hist[16 * lane + q];
+      c[q] = hist[base + q];
       mine += c[q];
     }
-    int suf = mine;  // keys in bins 16 lane and above
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_down(suf, o);
-      if (lane + o < 64) suf += y;
-    }
     if (lane == 0) s.sel[1] = atleast ? 0 : -1;  // (not atleast and no bin overflows: every key fits)
-    int cum = suf - mine;  // keys above bin 16 lane + 15
+    int cum = wave_inclusive_sum(mine) - mine;  // keys above bin base + 15
 #pragma unroll
     for (int q = 15; q >= 0; --q) {
-      const int bin = 16 * lane + q;
-      if (atleast ? (cum < need && need <= cum + c[q]) : (cum <= need && cum + c[q] > need)) s.sel[1] = bin;
+      if (atleast ? (cum < need && need <= cum + c[q]) : (cum <= need && cum + c[q] > need)) s.sel[1] = base + q;
       cum += c[q];
     }
   }
   __syncthreads();
-  // atleast: the bin where the count reaches need; else the bin that would
-  // overflow it (the edge is the one above it)
   const int bin = s.sel[1];
   __syncthreads();
-  return atleast ? lo + (static_cast<uint64_t>(bin) << sh) : lo + (static_cast<uint64_t>(bin + 1) << sh);
+  return static_cast<uint64_t>(mn) + (static_cast<uint64_t>(atleast ? bin : bin + 1) << sh);
 }
 
 // LDS: p, the norms and their reciprocals [N] float each, then one
-// membership byte per token.
+// membership byte per token.  KPT >= ceil(N / NT) register slots per thread.
+template <int KPT>
 __global__ __launch_bounds__(NT) void subset_kernel(const SubsetArgs a) {
   extern __shared__ __attribute__((aligned(16))) float pv[];
   __shared__ int hist[kBins];
@@ -183,73 +190,74 @@ __global__ __launch_bounds__(NT) void subset_kernel(const SubsetArgs a) {
   const float* p = a.p + (long long)b * N;
   const float* nrm = a.norms + (long long)b * N;
   const float* ninv = a.ninv + (long long)b * N;
-  const int nu = (N - tid + NT - 1) / NT;  // this thread's tokens: tid + NT u, u < nu
-  // every load issued first, at clamped addresses
-  float pr[kKpt], nr[kKpt], ir[kKpt];
+  // this thread's tokens: tid + NT u for the slots u set in `valid`; every
+  // load issued first, at clamped addresses
+  uint32_t valid = 0u;
+  float pr[KPT], nr[KPT], ir[KPT];
 #pragma unroll
-  for (int u = 0; u < kKpt; ++u) {
-    const int i = min(tid + NT * u, N - 1);
-    pr[u] = p[i];
-    nr[u] = nrm[i];
-    ir[u] = ninv[i];
-  }
-  // R0 (the K0 largest p, ties to the lower index) is inside the tokens
-  // whose p keys reach the histogram bin holding the K0-th largest
-  uint64_t kr[kKpt];
-  uint32_t mn = 0xffffffffu, mx = 0u;  // high words of the keys
-#pragma unroll
-  for (int u = 0; u < kKpt; ++u) {
+  for (int u = 0; u < KPT; ++u) {
     const int i = tid + NT * u;
-    const uint32_t h = sub_ordered_bits(pr[u]);
-    kr[u] = (static_cast<uint64_t>(h) << 14) | static_cast<uint64_t>(16383 - i);
-    if (u < nu) {
+    valid |= i < N ? 1u << u : 0u;
+    pr[u] = p[min(i, N - 1)];
+    nr[u] = nrm[min(i, N - 1)];
+    ir[u] = ninv[min(i, N - 1)];
+  }
+  // R0 (the K0 largest p, ties to the lower index) lies inside the tokens
+  // whose p reaches the histogram bin holding the K0-th largest; keys are
+  // high word << 14 | 16383 - index
+  uint32_t hr[KPT];
+  uint32_t mn = 0xffffffffu, mx = 0u;
+#pragma unroll
+  for (int u = 0; u < KPT; ++u) {
+    const int i = tid + NT * u;
+    hr[u] = sub_ordered_bits(pr[u]);
+    if ((valid >> u) & 1u) {
       pv[i] = pr[u];
       nv[i] = nr[u];
       iv[i] = ir[u];
-      mn = h < mn ? h : mn;
-      mx = h > mx ? h : mx;
+      mn = hr[u] < mn ? hr[u] : mn;
+      mx = hr[u] > mx ? hr[u] : mx;
     }
   }
   block_max_min32(mx, mn, s);
-  const uint64_t t0 = K0 > 0 ? hist_edge(kr, nu, K0, true, static_cast<uint64_t>(mn) << 14,
-                                         (static_cast<uint64_t>(mx) << 14) | 16383u, hist, s)
-                             : ~0ull;
-  // the others by their bound keys (the R0 candidates' keys become 0)
+  // R0's candidates: the p high words at or above the bin edge (all of them
+  // when K0 = 0 is not the case; none when K0 = 0)
+  const uint64_t e0 = K0 > 0 ? hist_edge<KPT>(hr, valid, K0, true, mn, mx, hist, s) : 0u;
+  uint32_t r0m = 0u;  // slots holding R0 candidates
   int nr0 = 0;
+#pragma unroll
+  for (int u = 0; u < KPT; ++u)
+    if (K0 > 0 && ((valid >> u) & 1u) && hr[u] >= e0) {
+      r0m |= 1u << u;
+      ++nr0;
+    }
+  // the others by their bound keys' high words
   mn = 0xffffffffu;
   mx = 0u;
 #pragma unroll
-  for (int u = 0; u < kKpt; ++u) {
-    const int i = tid + NT * u;
-    const bool r0 = kr[u] >= t0;
-    const uint32_t h = bound_hi(pr[u], nr[u], a.tau2);
-    kr[u] = r0 ? 0ull : ((static_cast<uint64_t>(h) << 14) | static_cast<uint64_t>(16383 - i));
-    if (u < nu) {
-      nr0 += r0 ? 1 : 0;
-      if (!r0) {
-        mn = h < mn ? h : mn;
-        mx = h > mx ? h : mx;
-      }
+  for (int u = 0; u < KPT; ++u) {
+    hr[u] = bound_hi(pr[u], nr[u], a.tau2);
+    if (((valid & ~r0m) >> u) & 1u) {
+      mn = hr[u] < mn ? hr[u] : mn;
+      mx = hr[u] > mx ? hr[u] : mx;
     }
   }
   int total_r0 = 0;
   (void)block_exclusive_sum(nr0, total_r0, s);
   block_max_min32(mx, mn, s);
-  // the largest bound keys that still fit beside them (mn > mx: no token left)
+  // the largest bounds that still fit beside them (mn > mx: no token left)
   const int room = Nc - total_r0;
-  const uint64_t t1 = (room > 0 && mn <= mx) ? hist_edge(kr, nu, room, false, static_cast<uint64_t>(mn) << 14,
-                                                          (static_cast<uint64_t>(mx) << 14) | 16383u, hist, s)
-                                             : ~0ull;
-  // J = keys 0 (R0 candidates) and keys >= t1; hout = the largest bound key left out
+  const uint64_t e1 = (room > 0 && mn <= mx) ? hist_edge<KPT>(hr, valid & ~r0m, room, false, mn, mx, hist, s)
+                                             : 0x100000000ull;
+  // J = R0's candidates and the bounds at or above e1 (above every high word: none)
+  const bool none = e1 > mx;
   uint32_t hout = 0u, unused = 0u;
 #pragma unroll
-  for (int u = 0; u < kKpt; ++u) {
-    if (u < nu) {
-      const uint64_t x = kr[u];
-      const bool in = x == 0ull || x >= t1;
+  for (int u = 0; u < KPT; ++u) {
+    if ((valid >> u) & 1u) {
+      const bool in = ((r0m >> u) & 1u) || (!none && hr[u] >= e1);
       member[tid + NT * u] = in ? 1 : 0;
-      const uint32_t h = static_cast<uint32_t>(x >> 14);
-      if (!in) hout = h > hout ? h : hout;
+      if (!in) hout = hr[u] > hout ? hr[u] : hout;
     }
   }
   block_max_min32(hout, unused, s);  // (its barrier also publishes the membership bytes)
@@ -293,14 +301,26 @@ __global__ __launch_bounds__(NT) void subset_kernel(const SubsetArgs a) {
 
 size_t subset_lds_bytes(int N) { return static_cast<size_t>(N) * (3 * sizeof(float) + 1); }
 
-hipError_t launch_subset(const SubsetArgs& a, hipStream_t s) {
+template <int KPT>
+hipError_t launch_subset_kpt(const SubsetArgs& a, hipStream_t s) {
   const size_t bytes = subset_lds_bytes(a.N);
   if (bytes > 48 * 1024) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(subset_kernel),
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(subset_kernel<KPT>),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
     if (e != hipSuccess) return e;
   }
-  return launch_kernel("subset", subset_kernel, dim3(a.B), dim3(NT), bytes, s, a);
+  return launch_kernel("subset", subset_kernel<KPT>, dim3(a.B), dim3(NT), bytes, s, a);
+}
+
+hipError_t launch_subset(const SubsetArgs& a, hipStream_t s) {
+  const int kpt = (a.N + NT - 1) / NT;
+  if (a.N < 1 || kpt > kKpt) return hipErrorInvalidValue;
+  if (kpt <= 4) return launch_subset_kpt<4>(a, s);
+  if (kpt <= 8) return launch_subset_kpt<8>(a, s);
+  if (kpt <= 12) return launch_subset_kpt<12>(a, s);
+  if (kpt <= 16) return launch_subset_kpt<16>(a, s);
+  if (kpt <= 24) return launch_subset_kpt<24>(a, s);
+  return launch_subset_kpt<32>(a, s);
 }
 
 }  // namespace mapk
