@@ -29,18 +29,45 @@ PEAK_HBM = 8000.0         # GB/s
 R0_FACTOR_MAX = 128  # largest K0 the selection places by one factorisation (its own kernel)
 
 
-def algorithmic_work(cfg, sumM, gathered=True):
+def subset_tokens(cfg, setting=0):
+    """Size of map_prune's candidate subset per image (0: the full path); the
+    library's rule, restated (setting as for --subset)."""
+    if setting < 0 or cfg.dtype != "bf16" or cfg.pred.D % 256 or cfg.N > 8192:
+        return 0
+    nc = setting
+    if setting == 0:
+        nc = (cfg.K0 + max(2 * (cfg.K - cfg.K0), cfg.N // 4) + 63) // 64 * 64
+        if 4 * nc > 3 * cfg.N:
+            return 0
+    nc = max(nc, cfg.K)
+    return nc if nc < cfg.N else 0
+
+
+def algorithmic_work(cfg, sumM, gathered=True, nc=0):
     """Per-launch algorithmic work of each kernel: (bound, amount, unit).
-    `gathered`: the selection launch also gathers the kept rows (no gather launch)."""
+    `gathered`: the selection launch also gathers the kept rows (no gather launch).
+    `nc`: tokens per image of the candidate subset the selection runs on (0: all N)."""
     B, N, K, K0 = cfg.B, cfg.N, cfg.K, cfg.K0
     K0f = K0 if 0 < K0 <= R0_FACTOR_MAX else 0  # picks placed by the R0 kernel
     D, H, dp = cfg.pred.D, cfg.pred.D_h, cfg.pred.d_p
     el = 2 if cfg.dtype == "bf16" else 4
     rows = B * N + sumM
+    Ns = nc if nc else N  # tokens the selection works on
+    ks = D // 512 if D % 512 == 0 else D // 256
+    tiles = ((nc + 127) // 128) * ((nc + 127) // 128 + 1) // 2
     return {
         # layer 1 of f_V and f_T, the folded weights W_K W2 and W_Q W2, and the
         # unique half (with the diagonal) of each Gram matrix
         "gemm_layer1_gram": ("mfma", 2.0 * rows * D * H + 2.0 * 2 * dp * H * H + B * N * (N + 1) * D, "flop"),
+        # the same without the Gram matrix (candidate subset)
+        "gemm_layer1": ("mfma", 2.0 * rows * D * H + 2.0 * 2 * dp * H * H, "flop"),
+        # the subset: p, the norms and their reciprocals in; the subset's
+        # tokens, p, norms and reciprocals out
+        "subset": ("hbm", B * (12.0 * N + 16.0 * nc), "byte"),
+        # the unique half (with the diagonal) of the subset's Gram matrix
+        "gemm_subset": ("mfma", 1.0 * B * nc * (nc + 1) * D, "flop"),
+        # the K-range partial sums in, the subset's cosine matrix out
+        "gram_reduce": ("hbm", 4.0 * B * tiles * ks * 128 * 128 + 4.0 * B * nc * nc, "byte"),
         # second layer and projection as one product with the folded weights
         "gemm_proj_rope": ("mfma", 2.0 * rows * H * dp, "flop"),
         # read V, write norms, 1/norms and the cos/sin table; transpose the two
@@ -55,11 +82,11 @@ def algorithmic_work(cfg, sumM, gathered=True):
         "softmax_mean": ("hbm", 4.0 * sumM * N + 8.0 * sumM * ((N + 63) // 64) + 4.0 * B * N, "byte"),
         # R0 (K0 <= 128): p, the norms and the K0 similarity rows of R0 in; the
         # K0 coefficient rows of every token, r^2, order and gain out
-        "select_r0": ("hbm", B * (12.0 * N + 8.0 * K0 * N + 8.0 * K0), "byte"),
+        "select_r0": ("hbm", B * (12.0 * Ns + 8.0 * K0 * Ns + 8.0 * K0), "byte"),
         # the greedy picks of Eq. (4): p, the norms, r^2 and the coefficient rows
         # so far in, the similarity rows of the picks; order, gain and indices
         # out; and, gathered in the same launch, the kept rows and positions
-        "select": ("hbm", B * (12.0 * N + 4.0 * K0f * N + 4.0 * (K - K0f) * N + 12.0 * (K - K0f))
+        "select": ("hbm", B * (12.0 * Ns + 4.0 * K0f * Ns + 4.0 * (K - K0f) * Ns + 12.0 * (K - K0f))
                    + (2.0 * B * K * D * el + 16.0 * B * K if gathered else 0.0), "byte"),
     }
 
@@ -69,6 +96,10 @@ def algorithmic_work(cfg, sumM, gathered=True):
 KERNEL_SOURCES = {
     "prep": ("prep.hip", "internal.h"),
     "gemm_layer1_gram": ("gemm.hip", "internal.h"),
+    "gemm_layer1": ("gemm.hip", "internal.h"),
+    "gemm_subset": ("gemm.hip", "internal.h"),
+    "gram_reduce": ("gemm.hip", "internal.h"),
+    "subset": ("subset.hip", "internal.h"),
     "gemm_proj_rope": ("gemm.hip", "internal.h"),
     "logits": ("score.hip", "internal.h"),
     "softmax_mean": ("score.hip", "internal.h"),
@@ -216,10 +247,14 @@ def main():
     mp.timing_reset()
 
     sumM = int(t_off[-1])
-    work = algorithmic_work(cfg, sumM, gathered="gather" not in per_kernel)
+    nc = subset_tokens(cfg, args.subset) if "subset" in per_kernel else 0
+    work = algorithmic_work(cfg, sumM, gathered="gather" not in per_kernel, nc=nc)
     kern = {k: {"avg_us": 1e3 * v[0] / v[1], "launches_per_step": v[1] / args.steps}
             for k, v in per_kernel.items()}
-    dominant = max(kern, key=lambda k: kern[k]["avg_us"] * kern[k]["launches_per_step"])
+    # (the full-path launches behind a subset do work only for images the
+    # subset cannot certify: they are never the dominant kernel)
+    dominant = max((k for k in kern if not k.endswith("_full")),
+                   key=lambda k: kern[k]["avg_us"] * kern[k]["launches_per_step"])
     roof = roofline(dominant, work, kern, cfg, args.workload)
     gemm = max((k for k in kern if work.get(k, ("",))[0] == "mfma"), key=lambda k: kern[k]["avg_us"])
     roof_mfma = roofline(gemm, work, kern, cfg, args.workload)
@@ -236,7 +271,8 @@ def main():
         "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic (seeded mixture, random-init predictor)",
         "config": {"workload": f"{cfg.name}: B={cfg.B} N={cfg.N} D={cfg.pred.D} M={sumM} K={cfg.K} "
                                f"K0={cfg.K0} tau={cfg.tau} D_h={cfg.pred.D_h} d_p={cfg.pred.d_p} {cfg.dtype}",
-                   "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "single GPU"},
+                   "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "single GPU",
+                   "subset_tokens": nc},
         "wall_s_timed": wall, "kernels": kern, "dominant_kernel": dominant, "roofline": roof,
         "roofline_mfma": roof_mfma,
     }

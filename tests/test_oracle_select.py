@@ -223,3 +223,33 @@ def test_invalid_arguments():
         greedy_select(p, V, K=11, K0=0)
     with pytest.raises(ValueError):
         greedy_select(p, V, K=3, K0=4)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_subset_selection_is_exact_when_certified(seed):
+    """A greedy pick's score p n r never exceeds its bound p n.  So the
+    selection run on a subset J (R0 plus the largest bounds) makes the full
+    selection's picks whenever each greedy gain on J exceeds every bound
+    left out -- the certificate map_prune's candidate subset relies on.
+    Brute force: the full and the subset selection of small images, for
+    subsets from barely past K to all tokens."""
+    rng = np.random.default_rng(100 + seed)
+    N, D, K, K0, tau = 160, 24, 20, 6, 1e-2
+    V = rng.normal(size=(N, D)) * rng.uniform(0.5, 2.0, size=(N, 1))
+    p = rng.dirichlet(np.full(N, 2.0))
+    full = greedy_select(p, V, K, K0, tau)
+    bound = p * np.linalg.norm(V, axis=1)
+    r0 = set(top_k0(p, K0).tolist())
+    by_bound = [i for i in np.lexsort((np.arange(N), -bound)) if i not in r0]
+    certified = rejected = 0
+    for t in range(K - K0, N - K0 + 1, 7):
+        J = np.sort(np.array(sorted(r0) + by_bound[:t]))
+        sub = greedy_select(p[J], V[J], K, K0, tau)
+        left_out = np.setdiff1d(np.arange(N), J)
+        hout = bound[left_out].max() if left_out.size else -np.inf
+        if np.all(sub.gain[K0:] > hout):
+            certified += 1
+            np.testing.assert_array_equal(J[sub.order], full.order)
+        else:
+            rejected += 1
+    assert certified >= 2 and rejected >= 1
