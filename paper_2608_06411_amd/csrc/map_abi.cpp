@@ -513,14 +513,13 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   sub.hout = u.hout;
   sub.uncert = u.uncert;
   sub.Ng = N;
-  bool gathered = false;
-  e = enqueue_select(B, nc, u.pJ, u.SJ, u.nJ, sp, idx_out, sw.order, gain_out, sw, st, true, &ga, &gathered, &sub);
+  e = enqueue_select(B, nc, u.pJ, u.SJ, u.nJ, sp, idx_out, sw.order, gain_out, sw, st, true, nullptr, nullptr, &sub);
   if (e != hipSuccess) return MAP_ERR_HIP;
-  if (!gathered && (e = launch_gather(ga, st)) != hipSuccess) return MAP_ERR_HIP;
 
   // the images whose picks were not certified: the full Gram matrix and
-  // selection (every workgroup of a certified image returns at once; its
-  // barrier counters are the second set, which the subset kernel cleared)
+  // selection (its barrier counters are the second set, which the subset
+  // kernel cleared); the workgroups of a certified image only gather its
+  // kept rows, from the order the subset's selection wrote as image tokens
   GemmBatch gf;
   memset(&gf, 0, sizeof(gf));
   gf.p[0] = gram(V, B, N, w.D, S, ninv);
@@ -533,7 +532,7 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   full.run_if = u.uncert;
   full.Ng = N;
   full.fallback = 1;
-  gathered = false;
+  bool gathered = false;
   SelectWs sw2 = sw;
   sw2.bar = sw.bar + B;
   e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_img, gain_out, sw2, st, true, &ga, &gathered, &full);

@@ -728,7 +728,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   const int G = a.G, ch = a.ch, pcap = a.pcap, K = a.K, K0 = a.K0, N = a.N;
   const int Kp = (K + 3) & ~3;
   const int b = b_begin + blockIdx.x / G, w = blockIdx.x % G;
-  if (a.run_if && a.run_if[b] == 0) return;
+  const bool skip = a.run_if && a.run_if[b] == 0;  // (uniform over the image's workgroups)
+  if (skip && !a.gV) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const Lds L = lds_layout(K, G, ch, pcap, PIPE);
   int* midx = reinterpret_cast<int*>(lds + L.midx);
@@ -876,6 +877,13 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
     }
   };
+
+  // A skipped image (its selection was made on a candidate subset) only
+  // gathers: its whole order is in the order array, as image tokens.
+  if (skip) {
+    gather_share(false, K);
+    return;
+  }
 
   // R0 placed by r0_kernel (when it fits and did not give up): take over the
   // own tokens' state and coefficient rows; otherwise the first rounds place it
