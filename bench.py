@@ -100,6 +100,9 @@ KERNEL_SOURCES = {
     "gemm_subset": ("gemm.hip", "internal.h"),
     "gram_reduce": ("gemm.hip", "internal.h"),
     "subset": ("subset.hip", "internal.h"),
+    "gemm_gram_full": ("gemm.hip", "internal.h"),
+    "select_r0_full": ("select.hip", "internal.h"),
+    "select_full": ("select.hip", "internal.h"),
     "gemm_proj_rope": ("gemm.hip", "internal.h"),
     "logits": ("score.hip", "internal.h"),
     "softmax_mean": ("score.hip", "internal.h"),
