@@ -87,7 +87,11 @@ def algorithmic_work(cfg, sumM, gathered=True, nc=0):
         # so far in, the similarity rows of the picks; order, gain and indices
         # out; and, gathered in the same launch, the kept rows and positions
         "select": ("hbm", B * (12.0 * Ns + 4.0 * K0f * Ns + 4.0 * (K - K0f) * Ns + 12.0 * (K - K0f))
-                   + (2.0 * B * K * D * el + 16.0 * B * K if gathered else 0.0), "byte"),
+                   + (2.0 * B * K * D * el + 16.0 * B * K if gathered and not nc else 0.0), "byte"),
+        # behind a subset: the full path's launches work only for images the
+        # subset cannot certify; the selection launch gathers the kept rows of
+        # the others
+        "select_full": ("hbm", 2.0 * B * K * D * el + 16.0 * B * K if gathered else 0.0, "byte"),
     }
 
 
