@@ -105,6 +105,23 @@ def test_prune_subset_modes(mode):
     _check(x, out, cfg.K, cfg.K0, cfg.tau, 2e-2)
 
 
+@pytest.mark.parametrize("K,K0,n", [(96, 0, 0), (64, 64, 0), (64, 64, 64), (100, 37, 101)])
+def test_prune_subset_edges(K, K0, n):
+    """The subset with no R0 (K0 = 0), with R0 alone (K0 = K: plain top-K),
+    with R0 filling the whole subset (R0's candidates may overflow it: the
+    full selection decides), and with an odd K0 and subset size."""
+    from paper_2608_06411_amd import set_subset_tokens
+    cfg = get_config("sweep", B=2, N=1000, M=(16, 64), K=K, K0=K0)
+    announce(f"prune subset edges K={K} K0={K0} n={n}")
+    x = make_inputs(cfg)
+    set_subset_tokens(n)
+    try:
+        out = _prune(x, K, K0, cfg.tau)
+    finally:
+        set_subset_tokens(0)
+    _check(x, out, K, K0, cfg.tau, 2e-2)
+
+
 def test_prune_subset_multiframe_image():
     """D = 3584 (seven K ranges of 512) and a subset too small for the
     eight-frame image's picks: the full selection behind it decides."""
