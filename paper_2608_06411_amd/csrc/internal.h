@@ -132,6 +132,7 @@ struct SubsetArgs {
   uint32_t* hout;       // [B] high word of the largest bound key outside J
   int32_t* uncert;      // [B] cleared here; set by the selection when a pick is not certified
   unsigned int* clear_bar;  // [B] barrier counters of the full selection behind the subset, cleared here
+  int32_t* clear_r0flag;    // [B] its R0 flags, cleared here (it places R0 in its own rounds)
   int B, N, Nc, K0;
   float tau2;
 };
@@ -210,6 +211,7 @@ struct SelectArgs {
   const int32_t* run_if;  // [B] images whose flag is 0 are skipped (null: none)
   int Ng;
   int fallback;           // the launches are the full selection behind a subset (timing names)
+  int no_r0_kernel;       // R0 is placed by the selection's own rounds (r0flag must read 0)
   int B, N, K, K0, G, ch, pcap;
   float tau2;
 };

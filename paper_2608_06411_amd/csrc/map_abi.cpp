@@ -188,7 +188,7 @@ SelectWs carve_select(Carver& c, int B, int N, int K) {
   s.err = c.take<int32_t>(4);
   s.order = c.take<int32_t>((size_t)B * K);
   s.gain = c.take<float>((size_t)B * K);
-  s.r0flag = c.take<int32_t>(B);
+  s.r0flag = c.take<int32_t>(2 * (size_t)B);  // the second B: the full selection behind a subset
   return s;
 }
 
@@ -332,6 +332,7 @@ struct SubsetSel {
   const int32_t* run_if;
   int Ng;
   int fallback;
+  int no_r0_kernel;
 };
 
 hipError_t enqueue_select(int B, int N, const float* p, const float* S, const float* norms,
@@ -350,6 +351,7 @@ hipError_t enqueue_select(int B, int N, const float* p, const float* S, const fl
     a.run_if = sub->run_if;
     a.Ng = sub->Ng;
     a.fallback = sub->fallback;
+    a.no_r0_kernel = sub->no_r0_kernel;
   }
   a.p = p;
   a.S = S;
@@ -474,6 +476,7 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   sa.K0 = sp.K0;
   sa.tau2 = sp.tau * sp.tau;
   sa.clear_bar = sw.bar + B;
+  sa.clear_r0flag = sw.r0flag + B;
   if ((e = launch_subset(sa, st)) != hipSuccess) return MAP_ERR_HIP;
 
   // cosine entries among the subset: raw sums per K range, then their
@@ -532,9 +535,11 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   full.run_if = u.uncert;
   full.Ng = N;
   full.fallback = 1;
+  full.no_r0_kernel = 1;  // (R0 in its own rounds: slower, and only for a flagged image)
   bool gathered = false;
   SelectWs sw2 = sw;
   sw2.bar = sw.bar + B;
+  sw2.r0flag = sw.r0flag + B;
   e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_img, gain_out, sw2, st, true, &ga, &gathered, &full);
   if (e != hipSuccess) return MAP_ERR_HIP;
   return gathered ? MAP_OK : hip_status(launch_gather(ga, st));

@@ -1680,15 +1680,14 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
   }
   const int per_launch = static_cast<int>(((long long)per_cu * cus) / chosen_G);
   if (per_launch < 1) return hipErrorInvalidConfiguration;
-  if (r0_by_factor(a.K0)) {
+  if (r0_by_factor(a.K0) && !a.no_r0_kernel) {
     const int rb = r0_layout(a.K0).bytes;
     if (rb > 65536) {
       const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(r0_kernel),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, rb);
       if (e != hipSuccess) return e;
     }
-    const hipError_t e = launch_kernel(a.fallback ? "select_r0_full" : "select_r0", r0_kernel,
-                                       dim3((a.N + 63) / 64, a.B), dim3(NT),
+    const hipError_t e = launch_kernel("select_r0", r0_kernel, dim3((a.N + 63) / 64, a.B), dim3(NT),
                                        static_cast<size_t>(rb), s, a);
     if (e != hipSuccess) return e;
   }

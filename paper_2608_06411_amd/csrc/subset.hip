@@ -294,6 +294,7 @@ __global__ __launch_bounds__(NT) void subset_kernel(const SubsetArgs a) {
     // of nearly equal p): J is cut short, and the image is selected in full
     a.uncert[b] = total > Nc ? 1 : 0;
     a.clear_bar[b] = 0u;
+    a.clear_r0flag[b] = 0;
   }
 }
 
