@@ -537,8 +537,61 @@ __device__ __forceinline__ void wait_vm_lgkm0(int outstanding) {
   else __builtin_amdgcn_s_waitcnt(0x0070);
 }
 
+// Row norms for the workgroups past the tiles: rows of one block spread over
+// its waves, two rows per wave at a time.  Each row is summed as prep sums
+// it: lane l squares 16-byte chunks l, l + 64, ... in that order, in groups
+// of eight, then the wave adds its lanes by a butterfly.
+__device__ __forceinline__ void norm_rows(const GemmBatch& args, int blk) {
+  const int rows = args.norm_rows, D = args.norm_D, nb = args.norm_blocks;
+  const int per = (rows + nb - 1) / nb, r0 = blk * per, r1 = min(rows, r0 + per);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int VEC = 8, U = 8;
+  const int nchunk = D / VEC;
+  for (int r = r0 + 2 * wave; r < r1; r += 2 * (NT / 64)) {
+    const bf16_t* row0 = static_cast<const bf16_t*>(args.norm_V) + (long long)r * D;
+    const bf16_t* row1 = static_cast<const bf16_t*>(args.norm_V) + (long long)min(r + 1, r1 - 1) * D;
+    float acc[2] = {0.0f, 0.0f};
+    for (int c0 = lane; c0 < nchunk; c0 += 64 * U) {
+      uint4 uv[2][U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        uv[0][u] = *reinterpret_cast<const uint4*>(row0 + min(c0 + 64 * u, nchunk - 1) * VEC);
+        uv[1][u] = *reinterpret_cast<const uint4*>(row1 + min(c0 + 64 * u, nchunk - 1) * VEC);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (c0 + 64 * u < nchunk) {
+            // the chunk's eight values in order (low half of each word first)
+            const uint32_t wv[4] = {uv[h][u].x, uv[h][u].y, uv[h][u].z, uv[h][u].w};
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) {
+              const uint32_t bits = (k & 1) ? (wv[k >> 1] & 0xffff0000u) : (wv[k >> 1] << 16);
+              const float x = __uint_as_float(bits);
+              acc[h] = fmaf(x, x, acc[h]);
+            }
+          }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) acc[h] += __shfl_xor(acc[h], off);
+      if (lane == 0 && r + h < r1) {
+        const float n = sqrtf(acc[h]);
+        args.norms[r + h] = n;
+        args.ninv[r + h] = n > 0.0f ? 1.0f / n : 0.0f;
+      }
+    }
+  }
+}
+
 __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
   __shared__ uint4 st0[2][BM][8], st1[2][BM][8], st2[2][BM][8], st3[2][BM][8], st4[2][BM][8];  // 5 x 32 KiB
+  if (static_cast<int>(blockIdx.x) >= args.total_tiles) {
+    norm_rows(args, blockIdx.x - args.total_tiles);
+    return;
+  }
   int pi, bt, tm, tn, kc, local;
   decode_tile(args, pi, bt, tm, tn, kc, local);
   const GemmProblem& P = args.p[pi];
@@ -845,6 +898,19 @@ void gemm_finalize(GemmBatch& g) {
   g.first_tiles = g.count > 1 && g.p[g.count - 1].epi == EPI_COSINE ? g.p[g.count - 1].tile_begin : 0;
 }
 
+bool gemm_direct_loads(map_dtype dt, const GemmBatch& g) {
+  if (dt != MAP_BF16) return false;
+  bool dma = true;  // every problem meets the direct-load requirements
+  for (int i = 0; i < g.count; ++i) {
+    const GemmProblem& p = g.p[i];
+    dma = dma && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+          (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
+          p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
+          (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));
+  }
+  return dma;
+}
+
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s) {
   if (g.total_tiles == 0) return hipSuccess;
   if (dt == MAP_BF16) {
@@ -856,7 +922,8 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
             p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
             (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));
     }
-    if (dma) return launch_kernel(name, gemm_dma_kernel, dim3(g.total_tiles), dim3(NT), 0, s, g);
+    if (dma) return launch_kernel(name, gemm_dma_kernel, dim3(g.total_tiles + g.norm_blocks), dim3(NT), 0, s, g);
+    if (g.norm_blocks) return hipErrorInvalidValue;
     for (int i = 0; i < g.count; ++i)  // index maps and K ranges exist in the direct-load kernel only
       if (g.p[i].epi == EPI_PARTIAL || g.p[i].mapA || g.p[i].mapB) return hipErrorInvalidValue;
     return launch_kernel(name, gemm_kernel<bf16_t>, dim3(g.total_tiles), dim3(NT), 0, s, g);

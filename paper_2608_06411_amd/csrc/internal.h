@@ -106,9 +106,19 @@ struct GemmBatch {
   int count;
   int total_tiles;
   int first_tiles;  // tiles dispatched before the rest (0: one class)
+  // bf16 direct-load launches only: norm_blocks more workgroups, dispatched
+  // after every tile (on compute units the tiles leave idle), write the row
+  // norms of norm_V [norm_rows][norm_D] and their reciprocals, summed in
+  // prep's order (bitwise the same values)
+  int norm_blocks;
+  const void* norm_V;
+  int norm_rows, norm_D;
+  float* norms;
+  float* ninv;
 };
 
 void gemm_finalize(GemmBatch& g);  // computes the tile counts
+bool gemm_direct_loads(map_dtype dt, const GemmBatch& g);  // launch_gemm would use the direct-load kernel
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s);
 // The projection with the RoPE epilogue (every problem EPI_ROPE, at most two):
 // a K-split kernel for bf16 and N <= 128, else launch_gemm.

@@ -243,7 +243,8 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
                          const int32_t* pos_v, const void* T, const int32_t* pos_t,
                          const int32_t* t_off, float* p_out, const ScoreWs& s,
                          const GemmProblem* extra_l1, float* norms, float* ninv, hipStream_t st,
-                         unsigned int* clear_bar = nullptr, int32_t* clear_err = nullptr) {
+                         unsigned int* clear_bar = nullptr, int32_t* clear_err = nullptr,
+                         bool norms_in_layer1 = false) {
   const int sumM = t_off[B], rowsV = B * N;
   PrepArgs pa;
   memset(&pa, 0, sizeof(pa));
@@ -274,9 +275,6 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   pa.fout[1] = s.bc_t;
   pa.frows = w.d_p;
   pa.fcols = w.D_h;
-  hipError_t e = launch_prep(dt, pa, norms != nullptr, true, true, st);
-  if (e != hipSuccess) return e;
-
   GemmBatch g1;
   memset(&g1, 0, sizeof(g1));
   g1.p[0] = linear(V, rowsV, w.w1_v, w.b1_v, s.h1_v, w.D_h, w.D, EPI_BIAS_GELU);
@@ -287,6 +285,26 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   // the Gram matrix last: its tiles are dispatched after every tile above
   if (extra_l1) g1.p[g1.count++] = *extra_l1;
   gemm_finalize(g1);
+  // The row norms: by prep, or (norms_in_layer1) by workgroups of the
+  // layer-1 launch on the compute units its last wave of tiles leaves idle,
+  // when there are at least 16 of them and at most 128 rows each.
+  if (norms_in_layer1 && gemm_direct_loads(dt, g1) && (reinterpret_cast<uintptr_t>(V) & 15) == 0) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0) {
+      const int idle = (cus - g1.total_tiles % cus) % cus;
+      if (idle >= 16 && (long long)idle * 128 >= rowsV) {
+        g1.norm_blocks = idle;
+        g1.norm_V = V;
+        g1.norm_rows = rowsV;
+        g1.norm_D = w.D;
+        g1.norms = norms;
+        g1.ninv = ninv;
+      }
+    }
+  }
+  hipError_t e = launch_prep(dt, pa, norms != nullptr && g1.norm_blocks == 0, true, true, st);
+  if (e != hipSuccess) return e;
   if ((e = launch_gemm(dt, g1, extra_l1 ? "gemm_layer1_gram" : "gemm_layer1", st)) != hipSuccess) return e;
 
   GemmBatch g3;
@@ -457,7 +475,7 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
                            int32_t* order_out, float* gain_out, const ScoreWs& s, const SelectWs& sw, float* S,
                            float* norms, float* ninv, const SubsetWs& u, int nc, hipStream_t st) {
   hipError_t e =
-      enqueue_score(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, nullptr, norms, ninv, st, sw.bar, sw.err);
+      enqueue_score(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, nullptr, norms, ninv, st, sw.bar, sw.err, true);
   if (e != hipSuccess) return MAP_ERR_HIP;
   SubsetArgs sa;
   memset(&sa, 0, sizeof(sa));
