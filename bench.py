@@ -72,7 +72,8 @@ def algorithmic_work(cfg, sumM, gathered=True, nc=0):
         "gemm_proj_rope": ("mfma", 2.0 * rows * H * dp, "flop"),
         # read V, write norms, 1/norms and the cos/sin table; transpose the two
         # second-layer weights and fold the biases
-        "prep": ("hbm", B * N * D * el + 8.0 * B * N + 8.0 * rows * dp / 2 + 2 * 2.0 * H * H * el
+        # (on the subset path the layer-1 launch forms the norms: no V here)
+        "prep": ("hbm", (0.0 if nc else B * N * D * el + 8.0 * B * N) + 8.0 * rows * dp / 2 + 2 * 2.0 * H * H * el
                  + 2 * (dp * H + H) * el + 8.0 * dp, "byte"),
         # read the selection order and the kept rows, write the rows, indices and positions
         "gather": ("hbm", 2.0 * B * K * D * el + 16.0 * B * K, "byte"),
