@@ -106,7 +106,6 @@ KERNEL_SOURCES = {
     "gram_reduce": ("gemm.hip", "internal.h"),
     "subset": ("subset.hip", "internal.h"),
     "gemm_gram_full": ("gemm.hip", "internal.h"),
-    "select_r0_full": ("select.hip", "internal.h"),
     "select_full": ("select.hip", "internal.h"),
     "gemm_proj_rope": ("gemm.hip", "internal.h"),
     "logits": ("score.hip", "internal.h"),
