@@ -8,19 +8,19 @@
 // float32 product r^2 (p n)^2 with r^2 <= 1 rounds to at most (p n)^2),
 // else bits(p).
 //
-// For each image this kernel takes J = R0 (the K0 largest p, which the
-// selection places first) plus the tokens with the largest bound keys, at
-// most Nc tokens in ascending token order, padded to Nc with tokens of
-// weight zero, and records hout, the largest bound key of a token left out.  A selection run on J then makes exactly
+// For each image this kernel takes J = R0's candidates (a superset of the K0
+// largest p, which the selection places first) plus the tokens with the
+// largest bound keys, at most Nc tokens in ascending token order, padded to
+// Nc with tokens of weight zero, and records hout, the largest bound key's
+// high word of a token left out.  A selection run on J then makes exactly
 // the picks of the selection over all tokens if every greedy pick's key
 // (its high word) exceeds hout: no token outside J could have beaten it.
 // The selection checks that itself and flags the image otherwise, and the
 // image is then selected again over all its tokens.
 //
-// One workgroup per image; each thread keeps its tokens' keys in registers
-// as 46-bit integers (key high word << 14 | 16383 - index, which orders
-// like the key for N <= 16384).  One 1024-bin histogram of each kind of key
-// places the thresholds at bin edges: J holds whole bins.
+// One workgroup per image; each thread keeps its tokens' key high words in
+// registers.  One 1024-bin histogram of each kind of key places the
+// thresholds at bin edges: J holds whole bins (ties included).
 #include "internal.h"
 
 namespace mapk {
@@ -47,7 +47,6 @@ struct BlockScratch {
   uint32_t red[2][NT / 64];
   int part[NT / 64];
   int sel[2];
-  uint64_t key;
 };
 
 // wave64 maximum / minimum on the DPP network (row shifts, then row
@@ -203,8 +202,8 @@ __global__ __launch_bounds__(NT) void subset_kernel(const SubsetArgs a) {
     ir[u] = ninv[min(i, N - 1)];
   }
   // R0 (the K0 largest p, ties to the lower index) lies inside the tokens
-  // whose p reaches the histogram bin holding the K0-th largest; keys are
-  // high word << 14 | 16383 - index
+  // whose p reaches the histogram bin holding the K0-th largest (ranked by
+  // the keys' high words, bits(p): ties in p all fall in one bin)
   uint32_t hr[KPT];
   uint32_t mn = 0xffffffffu, mx = 0u;
 #pragma unroll
