@@ -171,6 +171,23 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N,
                      float* p_out, int32_t* order_out, float* gain_out,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* map_assemble -- the language model's layer-0 input after pruning (section
+ * "Inference-Time Token Pruning": the kept tokens, in their original order
+ * and with their positional indices, are combined with the question
+ * tokens).  Image b's block starts at row b*K + t_off[b]: its K kept rows
+ * (as map_prune wrote them), then its M_b question rows; the positions
+ * likewise.  A pure copy: rows byte-exact, dt their element type.
+ * V_out   [B][K][D], pos_out [B][K]   (device; map_prune's outputs)
+ * T       [sum M][D], pos_t [sum M]   (device; map_prune's inputs)
+ * t_off_host [B+1]                    (host, as for map_prune)
+ * X_out   [B*K + sum M][D], pos_x_out [B*K + sum M]  (device, caller-owned)
+ * V_out, T and X_out 16-byte aligned.  Asynchronous on `stream`.
+ * MAP_ERR_INVALID_ARG: a null or misaligned pointer, an unknown dtype,
+ * D % 8 != 0, B or K out of range, bad offsets. */
+map_status map_assemble(map_dtype dt, int B, int K, int D, const void* V_out, const int32_t* pos_out,
+                        const void* T, const int32_t* pos_t, const int32_t* t_off_host,
+                        void* X_out, int32_t* pos_x_out, void* stream);
+
 /* map_prune's candidate subset.  A greedy pick of Eq. (4) scores
  * p_i n_i r_i <= p_i n_i, so map_prune may run the selection on a subset J
  * of each image's tokens: R0 plus the tokens with the largest bounds

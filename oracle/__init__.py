@@ -22,9 +22,10 @@ float64 from the exact stored input values.
 from .predictor import gelu_erf, mlp, predicted_attention, predicted_attention_batch, rope
 from .select import (SelectResult, greedy_select, replay_check, restore_order, top_k0)
 from .similarity import cosine_entries, cosine_similarity, row_norms
-from .pipeline import prune
+from .pipeline import assemble, prune
 
 __all__ = [
+    "assemble",
     "gelu_erf", "mlp", "rope", "predicted_attention", "predicted_attention_batch",
     "row_norms", "cosine_similarity", "cosine_entries", "top_k0", "greedy_select",
     "restore_order", "replay_check", "SelectResult", "prune",

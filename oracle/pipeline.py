@@ -36,3 +36,18 @@ def prune(V, T, t_off, pos_v, pos_t, w: dict, K: int, K0: int, tau: float = 1e-2
     V_out = np.take_along_axis(V, idx[:, :, None], axis=1)
     pos_out = np.take_along_axis(np.asarray(pos_v), idx, axis=1)
     return PruneResult(p, idx, order, V_out, pos_out)
+
+
+def assemble(V_out, pos_out, T, pos_t, t_off):
+    """The language model's layer-0 input after pruning (section
+    "Inference-Time Token Pruning": the kept tokens, in their original order
+    with their positional indices, are combined with the question tokens):
+    per image its K kept rows, then its question rows, packed in image order."""
+    V_out, pos_out = np.asarray(V_out), np.asarray(pos_out)
+    T, pos_t = np.asarray(T), np.asarray(pos_t)
+    rows, pos = [], []
+    for b in range(V_out.shape[0]):
+        lo, hi = int(t_off[b]), int(t_off[b + 1])
+        rows += [V_out[b], T[lo:hi]]
+        pos += [pos_out[b], pos_t[lo:hi]]
+    return np.concatenate(rows, axis=0), np.concatenate(pos)

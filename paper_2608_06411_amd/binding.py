@@ -22,7 +22,8 @@ MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
 EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
-    "map_prune", "map_set_subset_tokens", "map_timing_enable", "map_timing_read", "map_timing_reset",
+    "map_prune", "map_assemble", "map_set_subset_tokens", "map_timing_enable", "map_timing_read",
+    "map_timing_reset",
 )
 
 
@@ -50,6 +51,7 @@ _SIGS = {
     "map_select": (_I, [_I, _I, _P, _P, _P, map_select_params, _P, _P, _P, _P, _SZ, _P]),
     "map_prune": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
                        map_select_params, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "map_assemble": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
     "map_set_subset_tokens": (_I, [_I]),
     "map_timing_enable": (_I, [_I]),
     "map_timing_read": (_I, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
@@ -260,6 +262,20 @@ def map_prune(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torc
                            _ptr(o["pos_out"]), _ptr(o["p"]), _ptr(o["order"]), _ptr(o["gain"]),
                            _ptr(workspace.buf), workspace.nbytes, _stream(dev)), "map_prune")
     return o
+
+
+def map_assemble(V_out: torch.Tensor, pos_out: torch.Tensor, T: torch.Tensor, pos_t: torch.Tensor,
+                 t_off: Sequence[int]):
+    """The layer-0 input after pruning: per image its K kept rows, then its
+    question rows, packed; returns (X [B K + sum M][D], positions)."""
+    B, K, D = V_out.shape
+    dev = V_out.device
+    offs, sumM = _offsets(t_off)
+    X = torch.empty(B * K + sumM, D, dtype=V_out.dtype, device=dev)
+    pos = torch.empty(B * K + sumM, dtype=torch.int32, device=dev)
+    _check(lib().map_assemble(_dtype_code(V_out), B, K, D, _ptr(V_out), _ptr(pos_out), _ptr(T), _ptr(pos_t), offs,
+                              _ptr(X), _ptr(pos), _stream(dev)), "map_assemble")
+    return X, pos
 
 
 def set_subset_tokens(n: int):

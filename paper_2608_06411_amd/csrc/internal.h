@@ -243,4 +243,18 @@ struct GatherArgs {
 };
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 
+// The language model's layer-0 input: per image its K kept rows, then its
+// question rows, packed (image b from row b K + t_off[b]).
+struct AssembleArgs {
+  const void* V_out;      // [B][K] rows of row_bytes
+  const int32_t* pos_out; // [B][K]
+  const void* T;          // [sum M] rows of row_bytes
+  const int32_t* pos_t;   // [sum M]
+  void* X;                // [B K + sum M] rows of row_bytes
+  int32_t* pos_x;         // [B K + sum M]
+  int B, K, row_bytes, max_rows;
+  int t_off[MAP_MAX_BATCH + 1];
+};
+hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s);
+
 }  // namespace mapk

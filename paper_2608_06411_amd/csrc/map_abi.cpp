@@ -715,6 +715,30 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   return gathered ? MAP_OK : hip_status(launch_gather(ga, st));  // else its own kernel
 }
 
+map_status map_assemble(map_dtype dt, int B, int K, int D, const void* V_out, const int32_t* pos_out,
+                        const void* T, const int32_t* pos_t, const int32_t* t_off_host, void* X_out,
+                        int32_t* pos_x_out, void* stream) {
+  if (!valid_dtype(dt) || B < 1 || B > MAP_MAX_BATCH || K < 1 || K > MAP_MAX_K || D <= 0 || D % 8 || !V_out ||
+      !pos_out || !T || !pos_t || !X_out || !pos_x_out || !valid_offsets(t_off_host, B) ||
+      ((reinterpret_cast<uintptr_t>(V_out) | reinterpret_cast<uintptr_t>(T) | reinterpret_cast<uintptr_t>(X_out)) &
+       15) != 0)
+    return MAP_ERR_INVALID_ARG;
+  AssembleArgs a;
+  memset(&a, 0, sizeof(a));
+  a.V_out = V_out;
+  a.pos_out = pos_out;
+  a.T = T;
+  a.pos_t = pos_t;
+  a.X = X_out;
+  a.pos_x = pos_x_out;
+  a.B = B;
+  a.K = K;
+  a.row_bytes = static_cast<int>(D * elem_size(dt));
+  for (int b = 0; b <= B; ++b) a.t_off[b] = t_off_host[b];
+  for (int b = 0; b < B; ++b) a.max_rows = std::max(a.max_rows, K + t_off_host[b + 1] - t_off_host[b]);
+  return hip_status(launch_assemble(a, static_cast<hipStream_t>(stream)));
+}
+
 map_status map_set_subset_tokens(int n) {
   g_subset_tokens.store(n);
   return MAP_OK;
