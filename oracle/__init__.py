@@ -11,7 +11,11 @@ Attention in MLLMs for Visual Token Pruning"):
                     Eq. (4) and the restoration of the original order
                     (section "Inference-Time Token Pruning"), plus a replay
                     checker for another implementation's selection order;
-* ``pipeline``   -- the three chained, with the gather of the kept tokens.
+* ``pipeline``   -- the three chained, with the gather of the kept tokens,
+                    and the language model's layer-0 input after pruning;
+* ``teacher``    -- teacher selection for predictor training: Eq. (1),
+                    Eq. (2) and QCTS-n (section "Question Contrastive
+                    Teacher Selection").
 
 Only the test suite, the smoke entry point and the benchmark's CPU-baseline
 leg may import this package.  The HIP product path never calls it, and it
@@ -23,8 +27,10 @@ from .predictor import gelu_erf, mlp, predicted_attention, predicted_attention_b
 from .select import (SelectResult, greedy_select, replay_check, restore_order, top_k0)
 from .similarity import cosine_entries, cosine_similarity, row_norms
 from .pipeline import assemble, prune
+from .teacher import TeacherResult, js_divergence, layer_distributions, teacher_selection
 
 __all__ = [
+    "TeacherResult", "js_divergence", "layer_distributions", "teacher_selection",
     "assemble",
     "gelu_erf", "mlp", "rope", "predicted_attention", "predicted_attention_batch",
     "row_norms", "cosine_similarity", "cosine_entries", "top_k0", "greedy_select",

@@ -133,3 +133,32 @@ def peaked_scores(B: int, N: int, alpha: float = 0.1, seed: int = 7) -> np.ndarr
     p = np.maximum(p, 1e-12)
     p /= p.sum(axis=1, keepdims=True)
     return p.astype(np.float32)
+
+
+_TAG_A = 15
+
+
+def make_attention(L: int, H: int, M: int, N: int, *, dtype: str = "bf16", seed: int = 21, question: int = 0,
+                   reference: bool = False, share: float = 0.5, focus_peak: float = 2.5, noise: float = 0.7):
+    """Synthetic text-to-vision attention A [L][H][M][N] of one sample.
+
+    Each row is a softmax over the N visual tokens scaled by ``share`` (the
+    rest of the row's mass sits on the other tokens of the sequence).  Its
+    logits are a per-layer image field g_l[n] ~ N(0, 1) shared by every
+    question on the image, plus, for the input question (``reference`` False),
+    beta_l * f[n] with a question field f ~ N(0, 1) keyed by ``question`` and
+    a weight beta_l that peaks at ``focus_peak`` in the middle layers, plus
+    per-(head, token) noise N(0, noise^2).  Returns (float32 values, stored
+    array), stored as float32 or bf16 bit patterns.
+    """
+    g = _rng(seed, _TAG_A, 0).standard_normal((L, 1, 1, N)).astype(np.float32)
+    z = g + noise * _rng(seed, _TAG_A, 1, question, int(reference)).standard_normal((L, H, M, N), dtype=np.float32)
+    if not reference:
+        f = _rng(seed, _TAG_A, 2, question).standard_normal(N).astype(np.float32)
+        x = (np.arange(L, dtype=np.float32) + 0.5) / L
+        beta = focus_peak * np.exp(-((x - 0.45) / 0.2) ** 2) * (1.0 + 0.3 * _rng(seed, _TAG_A, 3, question).random(L))
+        z += beta.astype(np.float32)[:, None, None, None] * f[None, None, None, :]
+    z -= z.max(axis=3, keepdims=True)
+    np.exp(z, out=z)
+    z *= np.float32(share) / z.sum(axis=3, keepdims=True)
+    return _store(z, dtype)
