@@ -171,6 +171,37 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N,
                      float* p_out, int32_t* order_out, float* gain_out,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* map_teacher -- teacher selection for training the predictor (section
+ * "Question Contrastive Teacher Selection", Eq. (1)-(2); QCTS-n of the
+ * teacher-selection ablation).  For each sample b and layer l:
+ *   p[b][l][n]     = sum_{h,m} A[l][h][m][n] / sum_{h,m,n'} A[l][h][m][n']
+ *                    (Eq. (1)'s head/question mean, l1-normalised; uniform
+ *                    1/N for a layer whose attention sums to zero)
+ *   p_ref[b][l][n] = the same for the reference question's attention
+ *   js[b][l]       = D_JS(p, p_ref), natural logarithm, 0 log 0 = 0
+ *   layers[b][k]   = the layer with the (k+1)-th largest js (ties to the
+ *                    lower layer); layers[b][0] is Eq. (2)'s l*
+ *   teacher[b][n]  = mean over k < n_top of p[b][layers[b][k]][n]
+ * A      sample b's [L][H][M_b][N] text-to-vision attention (question token
+ *        rows), samples back to back; M_b = m_off[b+1] - m_off[b]; dtype dt,
+ *        values finite and >= 0; device, 16-byte aligned
+ * A_ref  [B][L][H][M_ref][N] the reference question's attention, as A
+ * m_off_host [B+1]  host, m_off[0] = 0, 1 <= M_b <= 8192
+ * p_out, p_ref_out [B][L][N] float32; js_out [B][L] float64;
+ * layers_out [B][n_top] int32; teacher_out [B][N] float32 (device, caller-owned)
+ * ws     at least map_teacher_workspace(B, L, N) bytes of device memory
+ * Limits: 1 <= B <= MAP_MAX_BATCH, 1 <= L <= 256, 1 <= H <= 1024,
+ *   1 <= N <= MAP_MAX_N with N * sizeof(element) a multiple of 16,
+ *   1 <= M_ref <= 8192, 1 <= n_top <= L.
+ * MAP_ERR_INVALID_ARG for anything outside them (checked before any work is
+ * enqueued); MAP_ERR_WORKSPACE for a short workspace.  Asynchronous on
+ * `stream`, bitwise deterministic. */
+size_t map_teacher_workspace(int B, int L, int N);
+map_status map_teacher(map_dtype dt, int B, int L, int H, int N, const void* A, const int32_t* m_off_host,
+                       const void* A_ref, int M_ref, int n_top, float* p_out, float* p_ref_out,
+                       double* js_out, int32_t* layers_out, float* teacher_out, void* ws, size_t ws_bytes,
+                       void* stream);
+
 /* map_assemble -- the language model's layer-0 input after pruning (section
  * "Inference-Time Token Pruning": the kept tokens, in their original order
  * and with their positional indices, are combined with the question

@@ -7,11 +7,12 @@ kept tokens -- as hand-written HIP kernels for gfx950 behind a C ABI
 (include/map.h).  This package is the Python binding of that library.
 """
 from .binding import (EXPORTS, MAP_BF16, MAP_F32, MapError, PredictorWeights, PruneWorkspace,
-                      lib, map_assemble, map_prune, map_score, map_select, map_similarity, set_subset_tokens,
+                      lib, map_assemble, map_prune, map_score, map_select, map_similarity, map_teacher,
+                      set_subset_tokens,
                       timing_enable, timing_read, timing_reset)
 
 __all__ = [
     "EXPORTS", "MAP_BF16", "MAP_F32", "MapError", "PredictorWeights", "PruneWorkspace", "lib",
-    "map_assemble", "map_prune", "map_score", "map_select", "map_similarity", "set_subset_tokens", "timing_enable",
+    "map_assemble", "map_prune", "map_score", "map_select", "map_similarity", "map_teacher", "set_subset_tokens", "timing_enable",
     "timing_read", "timing_reset",
 ]

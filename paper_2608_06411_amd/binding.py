@@ -22,7 +22,7 @@ MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
 EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
-    "map_prune", "map_assemble", "map_set_subset_tokens", "map_timing_enable", "map_timing_read",
+    "map_prune", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens", "map_timing_enable", "map_timing_read",
     "map_timing_reset",
 )
 
@@ -52,6 +52,8 @@ _SIGS = {
     "map_prune": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
                        map_select_params, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "map_assemble": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "map_teacher_workspace": (_SZ, [_I, _I, _I]),
+    "map_teacher": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "map_set_subset_tokens": (_I, [_I]),
     "map_timing_enable": (_I, [_I]),
     "map_timing_read": (_I, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
@@ -276,6 +278,36 @@ def map_assemble(V_out: torch.Tensor, pos_out: torch.Tensor, T: torch.Tensor, po
     _check(lib().map_assemble(_dtype_code(V_out), B, K, D, _ptr(V_out), _ptr(pos_out), _ptr(T), _ptr(pos_t), offs,
                               _ptr(X), _ptr(pos), _stream(dev)), "map_assemble")
     return X, pos
+
+
+def map_teacher(A: torch.Tensor, A_ref: torch.Tensor, m_off: Sequence[int], L: int, H: int, N: int, M_ref: int,
+                n_top: int = 1, out: Optional[dict] = None) -> dict:
+    """Teacher selection (Eq. (1)-(2), QCTS-n).  A holds sample b's
+    [L][H][M_b][N] attention back to back (M_b from m_off), A_ref is
+    [B][L][H][M_ref][N]; both contiguous, same dtype.  Returns p, p_ref
+    [B, L, N], js [B, L] (float64), layers [B, n_top] and teacher [B, N];
+    ``out`` (a previous result) is written in place when given."""
+    dev = A.device
+    offs, sumM = _offsets(m_off)
+    B = len(offs) - 1
+    dt = _dtype_code(A)
+    if A.numel() != L * H * sumM * N or A_ref.numel() != B * L * H * M_ref * N:
+        raise ValueError("A or A_ref does not hold the sizes given")
+    if A_ref.dtype != A.dtype or not A.is_contiguous() or not A_ref.is_contiguous() or A_ref.device != dev:
+        raise ValueError("A and A_ref must be contiguous, of one dtype, on one device")
+    if out is None:
+        out = dict(p=torch.empty(B, L, N, dtype=torch.float32, device=dev),
+                   p_ref=torch.empty(B, L, N, dtype=torch.float32, device=dev),
+                   js=torch.empty(B, L, dtype=torch.float64, device=dev),
+                   layers=torch.empty(B, n_top, dtype=torch.int32, device=dev),
+                   teacher=torch.empty(B, N, dtype=torch.float32, device=dev))
+        nbytes = lib().map_teacher_workspace(B, L, N)
+        out["_ws"] = _workspace(nbytes, dev)
+    ws = out["_ws"]
+    _check(lib().map_teacher(dt, B, L, H, N, _ptr(A), offs, _ptr(A_ref), M_ref, n_top, _ptr(out["p"]),
+                             _ptr(out["p_ref"]), _ptr(out["js"]), _ptr(out["layers"]), _ptr(out["teacher"]),
+                             _ptr(ws), 0 if ws is None else ws.numel(), _stream(dev)), "map_teacher")
+    return out
 
 
 def set_subset_tokens(n: int):

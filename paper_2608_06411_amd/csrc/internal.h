@@ -257,4 +257,21 @@ struct AssembleArgs {
 };
 hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s);
 
+// ---------------------------------------------------------------- teacher selection
+constexpr int kTeacherMaxLayers = 256;
+constexpr int kTeacherMaxSlices = 16;
+struct TeacherArgs {
+  const void* A;      // per sample [L][H][M_b][N], samples back to back
+  const void* A_ref;  // [B][L][H][M_ref][N]
+  float* part;        // [2][B][L][S][N] partial column sums
+  float* p;           // [B][L][N]
+  float* p_ref;       // [B][L][N]
+  double* js;         // [B][L]
+  int32_t* layers;    // [B][n_top]
+  float* teacher;     // [B][N]
+  int B, L, H, N, M_ref, S, n_top;
+  int m_off[MAP_MAX_BATCH + 1];
+};
+hipError_t launch_teacher(map_dtype dt, const TeacherArgs& a, hipStream_t s);
+
 }  // namespace mapk

@@ -739,6 +739,49 @@ map_status map_assemble(map_dtype dt, int B, int K, int D, const void* V_out, co
   return hip_status(launch_assemble(a, static_cast<hipStream_t>(stream)));
 }
 
+static int teacher_slices(int B, int L, int N) {
+  // about 4096 workgroups (16 per compute unit) for the column sums
+  const long long wgs = 2LL * B * L * ((N + 511) / 512);
+  return static_cast<int>(std::min<long long>(kTeacherMaxSlices, std::max<long long>(1, (4096 + wgs - 1) / wgs)));
+}
+
+size_t map_teacher_workspace(int B, int L, int N) {
+  if (B < 1 || B > MAP_MAX_BATCH || L < 1 || L > kTeacherMaxLayers || N < 1 || N > MAP_MAX_N) return 0;
+  return 2ull * B * L * teacher_slices(B, L, N) * N * sizeof(float);
+}
+
+map_status map_teacher(map_dtype dt, int B, int L, int H, int N, const void* A, const int32_t* m_off_host,
+                       const void* A_ref, int M_ref, int n_top, float* p_out, float* p_ref_out, double* js_out,
+                       int32_t* layers_out, float* teacher_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!valid_dtype(dt) || B < 1 || B > MAP_MAX_BATCH || L < 1 || L > kTeacherMaxLayers || H < 1 || H > 1024 ||
+      N < 1 || N > MAP_MAX_N || (N * elem_size(dt)) % 16 != 0 || M_ref < 1 || M_ref > kMaxQuestion || n_top < 1 ||
+      n_top > L || !A || !A_ref || !p_out || !p_ref_out || !js_out || !layers_out || !teacher_out ||
+      !valid_offsets(m_off_host, B) ||
+      ((reinterpret_cast<uintptr_t>(A) | reinterpret_cast<uintptr_t>(A_ref)) & 15) != 0)
+    return MAP_ERR_INVALID_ARG;
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) & 15) || ws_bytes < map_teacher_workspace(B, L, N))
+    return MAP_ERR_WORKSPACE;
+  TeacherArgs a;
+  memset(&a, 0, sizeof(a));
+  a.A = A;
+  a.A_ref = A_ref;
+  a.part = static_cast<float*>(ws);
+  a.p = p_out;
+  a.p_ref = p_ref_out;
+  a.js = js_out;
+  a.layers = layers_out;
+  a.teacher = teacher_out;
+  a.B = B;
+  a.L = L;
+  a.H = H;
+  a.N = N;
+  a.M_ref = M_ref;
+  a.S = teacher_slices(B, L, N);
+  a.n_top = n_top;
+  for (int b = 0; b <= B; ++b) a.m_off[b] = m_off_host[b];
+  return hip_status(launch_teacher(dt, a, static_cast<hipStream_t>(stream)));
+}
+
 map_status map_set_subset_tokens(int n) {
   g_subset_tokens.store(n);
   return MAP_OK;
