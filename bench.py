@@ -113,6 +113,10 @@ KERNEL_SOURCES = {
     "select_r0": ("select.hip", "internal.h"),
     "select": ("select.hip", "internal.h"),
     "gather": ("gather.hip", "internal.h"),
+    "attn_colsum": ("teacher.hip", "internal.h"),
+    "layer_sum": ("teacher.hip", "internal.h"),
+    "layer_js": ("teacher.hip", "internal.h"),
+    "teacher": ("teacher.hip", "internal.h"),
 }
 
 
@@ -154,6 +158,71 @@ def roofline(kernel, work, kern, cfg, workload):
     return roof
 
 
+TEACHER_SHAPE = dict(L=32, H=32, M=64, M_ref=8, N=2880, n_top=1)  # LLaVA-NeXT-7B (Vicuna-7B: 32 layers x 32 heads)
+
+
+def teacher_slices(B, L, N):
+    """The library's slice count for the column sums, restated."""
+    wgs = 2 * B * L * ((N + 511) // 512)
+    return min(16, max(1, -(-4096 // wgs)))
+
+
+def teacher_bench(args, mp, torch, dev):
+    """Teacher selection (Eq. (1)-(2)) for one training sample of the
+    LLaVA-NeXT shape, bf16 attention resident in HBM: samples/s, per-kernel
+    times and the HBM roofline of the column-sum launch (algorithmic bytes:
+    every attention element read once, plus the float32 partial rows)."""
+    from workloads import make_attention
+    sh = TEACHER_SHAPE
+    L, H, M, M_ref, N = sh["L"], sh["H"], sh["M"], sh["M_ref"], sh["N"]
+    A_f, A_s = make_attention(L, H, M, N, dtype="bf16", seed=40)
+    R_f, R_s = make_attention(L, H, M_ref, N, dtype="bf16", seed=40, reference=True)
+    A = torch.from_numpy(A_s.reshape(-1).view(np.int16)).to(dev).view(torch.bfloat16)
+    R = torch.from_numpy(R_s.reshape(-1).view(np.int16)).to(dev).view(torch.bfloat16)
+    m_off = [0, M]
+    out = mp.map_teacher(A, R, m_off, L, H, N, M_ref, sh["n_top"])
+    for _ in range(args.warmup):
+        mp.map_teacher(A, R, m_off, L, H, N, M_ref, sh["n_top"], out=out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        mp.map_teacher(A, R, m_off, L, H, N, M_ref, sh["n_top"], out=out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    mp.timing_reset()
+    mp.timing_enable(True)
+    for _ in range(args.steps):
+        mp.map_teacher(A, R, m_off, L, H, N, M_ref, sh["n_top"], out=out)
+    torch.cuda.synchronize()
+    per = mp.timing_read()
+    mp.timing_enable(False)
+    mp.timing_reset()
+    kern = {k: {"avg_us": 1e3 * v[0] / v[1], "launches_per_step": v[1] / args.steps} for k, v in per.items()}
+    S = teacher_slices(1, L, N)
+    colsum_bytes = 2 * L * H * (M + M_ref) * N + 2 * L * S * N * 4
+    avg_s = kern["attn_colsum"]["avg_us"] * 1e-6
+    roof = {"bound": "hbm", "achieved": colsum_bytes / avg_s / 1e9, "peak": PEAK_HBM, "unit": "GB/s",
+            "frac": colsum_bytes / avg_s / 1e9 / PEAK_HBM, "traffic": measured_traffic(args.workload, "attn_colsum"),
+            "kernel": "attn_colsum", "avg_us": kern["attn_colsum"]["avg_us"],
+            "algorithmic_per_launch": colsum_bytes, "algorithmic_unit": "bytes"}
+    res = {"metric": "teacher-selected samples/s", "value": 1000.0 / ms, "unit": "samples/s", "ms_per_step": ms,
+           "workload": f"teacher selection, LLaVA-NeXT-7B shape: L={L} H={H} N={N} M={M} M_ref={M_ref} "
+                       f"n_top={sh['n_top']} bf16 attention (synthetic), one sample per step",
+           "kernels": kern, "roofline": roof, "layers": out["layers"][0].tolist()}
+    if not args.no_cpu_baseline:
+        import oracle
+        t0 = time.perf_counter()
+        ref = oracle.teacher_selection(A_f, R_f, sh["n_top"])
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": 1.0 / dt, "unit": "samples/s", "cores": 1, "kind": "oracle",
+                               "sample": "one sample of the same workload (fp64 numpy reductions, one thread)"}
+        res["oracle_layers"] = ref.layers.tolist()
+    return res
+
+
 def cpu_baseline(x, cfg, min_seconds=10.0, max_runs=8):
     """The oracle as it stands, timed on this host: the workload's first image,
     run again until at least `min_seconds` of CPU work (at most `max_runs`)."""
@@ -184,6 +253,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llava_next")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-teacher", action="store_true", help="skip the teacher-selection measurement")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run a plain float32 copy kernel over this many MiB (three times), "
                          "the reference dispatch for calibrating HBM byte counters")
@@ -285,6 +355,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"], _ = cpu_baseline(x, cfg)
+    if not args.no_teacher:
+        line["teacher_selection"] = teacher_bench(args, mp, torch, dev)
     print(json.dumps(line), flush=True)
 
 

@@ -263,13 +263,15 @@ constexpr int kTeacherMaxSlices = 16;
 struct TeacherArgs {
   const void* A;      // per sample [L][H][M_b][N], samples back to back
   const void* A_ref;  // [B][L][H][M_ref][N]
-  float* part;        // [2][B][L][S][N] partial column sums
+  float* part;        // [2][B][L][S][N] partial column sums; slice 0 then holds the column sums
+  double* tot;        // [2][B][L][NB] float64 totals of 256-column chunks
+  double* js_part;    // [B][L][NB] each chunk's share of the divergence
   float* p;           // [B][L][N]
   float* p_ref;       // [B][L][N]
   double* js;         // [B][L]
   int32_t* layers;    // [B][n_top]
   float* teacher;     // [B][N]
-  int B, L, H, N, M_ref, S, n_top;
+  int B, L, H, N, M_ref, S, NB, n_top;  // NB = ceil(N / 256)
   int m_off[MAP_MAX_BATCH + 1];
 };
 hipError_t launch_teacher(map_dtype dt, const TeacherArgs& a, hipStream_t s);

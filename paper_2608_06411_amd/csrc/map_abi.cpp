@@ -747,7 +747,8 @@ static int teacher_slices(int B, int L, int N) {
 
 size_t map_teacher_workspace(int B, int L, int N) {
   if (B < 1 || B > MAP_MAX_BATCH || L < 1 || L > kTeacherMaxLayers || N < 1 || N > MAP_MAX_N) return 0;
-  return 2ull * B * L * teacher_slices(B, L, N) * N * sizeof(float);
+  const size_t nb = (N + 255) / 256, part = 2ull * B * L * teacher_slices(B, L, N) * N * sizeof(float);
+  return (part + 255) / 256 * 256 + 3ull * B * L * nb * sizeof(double);
 }
 
 map_status map_teacher(map_dtype dt, int B, int L, int H, int N, const void* A, const int32_t* m_off_host,
@@ -765,7 +766,12 @@ map_status map_teacher(map_dtype dt, int B, int L, int H, int N, const void* A, 
   memset(&a, 0, sizeof(a));
   a.A = A;
   a.A_ref = A_ref;
+  a.S = teacher_slices(B, L, N);
+  a.NB = (N + 255) / 256;
   a.part = static_cast<float*>(ws);
+  a.tot = reinterpret_cast<double*>(static_cast<char*>(ws) +
+                                    (2ull * B * L * a.S * N * sizeof(float) + 255) / 256 * 256);
+  a.js_part = a.tot + 2ull * B * L * a.NB;
   a.p = p_out;
   a.p_ref = p_ref_out;
   a.js = js_out;
@@ -776,7 +782,6 @@ map_status map_teacher(map_dtype dt, int B, int L, int H, int N, const void* A, 
   a.H = H;
   a.N = N;
   a.M_ref = M_ref;
-  a.S = teacher_slices(B, L, N);
   a.n_top = n_top;
   for (int b = 0; b <= B; ++b) a.m_off[b] = m_off_host[b];
   return hip_status(launch_teacher(dt, a, static_cast<hipStream_t>(stream)));

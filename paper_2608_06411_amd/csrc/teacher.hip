@@ -1,17 +1,20 @@
 // Teacher selection for predictor training (section "Question Contrastive
 // Teacher Selection", Eq. (1)-(2), and QCTS-n of the teacher ablation).
 //
-// Three launches per call:
+// Four launches per call:
 //  * attn_colsum: the HBM-bound part.  Sample b's attention for layer l is a
 //    slab of H*M rows (heads, then question tokens) of N visual tokens.  A
 //    workgroup sums a slice of those rows for 64*VEC columns (16-byte loads,
 //    four waves on interleaved rows) and writes one float32 partial row.
 //    Input and reference question share the launch (grid z).
-//  * layer_js: per (layer, sample) the partial rows summed in slice order,
-//    their totals (Eq. (1)'s 1/(H M) cancels in the l1 normalisation), p^l
-//    and p^l_ref, and D_JS(p^l, p^l_ref) in float64 with the natural log.
-//  * teacher: per sample the layers ranked by divergence (ties to the lower
-//    layer), and the mean of p^l over the n_top highest (Eq. (2) for n = 1).
+//  * layer_sum: per column the partial rows summed in slice order, and per
+//    256-column chunk their float64 total.
+//  * layer_js: per chunk, p^l and p^l_ref (the column sums over the layer's
+//    total: Eq. (1)'s 1/(H M) cancels in the l1 normalisation) and the
+//    chunk's share of D_JS(p^l, p^l_ref), float64, natural log.
+//  * teacher: per sample the divergence of each layer (chunk shares summed
+//    in order), the layers ranked by it (ties to the lower layer), and the
+//    mean of p^l over the n_top highest (Eq. (2) for n = 1).
 // Every sum runs in a fixed order: the results are bitwise deterministic.
 #include "internal.h"
 
@@ -92,67 +95,80 @@ __device__ double block_sum(double v, double* red) {
   return r;
 }
 
-__global__ __launch_bounds__(256) void layer_js_kernel(const TeacherArgs a) {
+// Per column n of layer l: the slice partials summed in slice order, written
+// back over slice 0; per 256-column chunk the float64 sum of those sums.
+__global__ __launch_bounds__(256) void layer_sum_kernel(const TeacherArgs a) {
   __shared__ double red[256];
-  const int l = blockIdx.x, b = blockIdx.y, N = a.N, S = a.S;
-  const float* q = a.part + (((long long)b * a.L + l) * S) * N;
-  const float* r = a.part + (((long long)(a.B + b) * a.L + l) * S) * N;
-  double tq = 0.0, tr = 0.0;
-  for (int n = threadIdx.x; n < N; n += 256) {
-    float aq = 0.0f, ar = 0.0f;
-    for (int s = 0; s < S; ++s) {
-      aq += q[(long long)s * N + n];
-      ar += r[(long long)s * N + n];
-    }
-    tq += aq;
-    tr += ar;
+  const int z = blockIdx.z, l = blockIdx.y, n = blockIdx.x * 256 + threadIdx.x, N = a.N, S = a.S;
+  float* col = a.part + (((long long)z * a.L + l) * S) * N;
+  float v = 0.0f;
+  if (n < N) {
+    for (int s = 0; s < S; ++s) v += col[(long long)s * N + n];
   }
-  tq = block_sum(tq, red);
-  tr = block_sum(tr, red);
-  float* p_out = a.p + ((long long)b * a.L + l) * N;
-  float* pr_out = a.p_ref + ((long long)b * a.L + l) * N;
-  double js = 0.0;
-  for (int n = threadIdx.x; n < N; n += 256) {
-    float aq = 0.0f, ar = 0.0f;
-    for (int s = 0; s < S; ++s) {
-      aq += q[(long long)s * N + n];
-      ar += r[(long long)s * N + n];
-    }
-    const double pd = tq > 0.0 ? aq / tq : 1.0 / N, qd = tr > 0.0 ? ar / tr : 1.0 / N;
-    p_out[n] = static_cast<float>(pd);
-    pr_out[n] = static_cast<float>(qd);
-    const double m = 0.5 * (pd + qd);
-    js += 0.5 * ((pd > 0.0 ? pd * log(pd / m) : 0.0) + (qd > 0.0 ? qd * log(qd / m) : 0.0));
-  }
-  js = block_sum(js, red);
-  if (threadIdx.x == 0) a.js[(long long)b * a.L + l] = js;
+  const double t = block_sum(v, red);
+  if (n < N) col[n] = v;  // every slice of this column has been read by this thread
+  if (threadIdx.x == 0) a.tot[((long long)z * a.L + l) * a.NB + blockIdx.x] = t;
 }
 
+// Per 256-column chunk of layer l: p and p_ref from the column sums and the
+// layer totals (chunk totals summed in chunk order), and the chunk's share of
+// D_JS in float64 with the natural log.
+__global__ __launch_bounds__(256) void layer_js_kernel(const TeacherArgs a) {
+  __shared__ double red[256];
+  const int b = blockIdx.z, l = blockIdx.y, n = blockIdx.x * 256 + threadIdx.x, N = a.N, NB = a.NB;
+  const double* tq_part = a.tot + ((long long)b * a.L + l) * NB;
+  const double* tr_part = a.tot + ((long long)(a.B + b) * a.L + l) * NB;
+  double tq = 0.0, tr = 0.0;
+  for (int k = 0; k < NB; ++k) {
+    tq += tq_part[k];
+    tr += tr_part[k];
+  }
+  double term = 0.0;
+  if (n < N) {
+    const float aq = a.part[(((long long)b * a.L + l) * a.S) * N + n];
+    const float ar = a.part[(((long long)(a.B + b) * a.L + l) * a.S) * N + n];
+    const double pd = tq > 0.0 ? aq / tq : 1.0 / N, qd = tr > 0.0 ? ar / tr : 1.0 / N;
+    a.p[((long long)b * a.L + l) * N + n] = static_cast<float>(pd);
+    a.p_ref[((long long)b * a.L + l) * N + n] = static_cast<float>(qd);
+    const double m = 0.5 * (pd + qd);
+    term = 0.5 * ((pd > 0.0 ? pd * log(pd / m) : 0.0) + (qd > 0.0 ? qd * log(qd / m) : 0.0));
+  }
+  const double js = block_sum(term, red);
+  if (threadIdx.x == 0) a.js_part[((long long)b * a.L + l) * NB + blockIdx.x] = js;
+}
+
+// Workgroup (chunk c, sample b): the divergence of every layer (chunk
+// shares summed in chunk order) and their ranking, repeated by each chunk's
+// workgroup (L <= 256 values); chunk 0 writes js and the ranked layers; each
+// writes the teacher's 256 columns of its chunk.
 __global__ __launch_bounds__(256) void teacher_kernel(const TeacherArgs a) {
   __shared__ int top[kTeacherMaxLayers];
-  const int b = blockIdx.x, L = a.L, tid = threadIdx.x;
+  __shared__ double jsl[kTeacherMaxLayers];
+  const int b = blockIdx.y, L = a.L, tid = threadIdx.x, first = blockIdx.x == 0;
   top[tid] = 0;
-  __syncthreads();
-  const double* js = a.js + (long long)b * L;
   if (tid < L) {
-    // a divergence is >= 0; a NaN ranks below every number
-    const double mine = js[tid] >= 0.0 ? js[tid] : -1.0;
+    const double* part = a.js_part + ((long long)b * L + tid) * a.NB;
+    double js = 0.0;
+    for (int k = 0; k < a.NB; ++k) js += part[k];
+    if (first) a.js[(long long)b * L + tid] = js;
+    jsl[tid] = js >= 0.0 ? js : -1.0;  // a divergence is >= 0; a NaN ranks below every number
+  }
+  __syncthreads();
+  if (tid < L) {
+    const double mine = jsl[tid];
     int rank = 0;
-    for (int k = 0; k < L; ++k) {
-      const double o = js[k] >= 0.0 ? js[k] : -1.0;
-      rank += (o > mine) || (o == mine && k < tid);
-    }
+    for (int k = 0; k < L; ++k) rank += (jsl[k] > mine) || (jsl[k] == mine && k < tid);
     if (rank < a.n_top) {
       top[rank] = tid;
-      a.layers[(long long)b * a.n_top + rank] = tid;
+      if (first) a.layers[(long long)b * a.n_top + rank] = tid;
     }
   }
   __syncthreads();
-  const double inv = 1.0 / a.n_top;
-  for (int n = tid; n < a.N; n += 256) {
+  const int n = blockIdx.x * 256 + tid;
+  if (n < a.N) {
     double s = 0.0;
     for (int k = 0; k < a.n_top; ++k) s += a.p[((long long)b * L + top[k]) * a.N + n];
-    a.teacher[(long long)b * a.N + n] = static_cast<float>(s * inv);
+    a.teacher[(long long)b * a.N + n] = static_cast<float>(s / a.n_top);
   }
 }
 
@@ -164,9 +180,11 @@ hipError_t launch_teacher(map_dtype dt, const TeacherArgs& a, hipStream_t s) {
   hipError_t e = dt == MAP_BF16 ? launch_kernel("attn_colsum", attn_colsum_kernel<true>, g, dim3(256), 0, s, a)
                                 : launch_kernel("attn_colsum", attn_colsum_kernel<false>, g, dim3(256), 0, s, a);
   if (e != hipSuccess) return e;
-  e = launch_kernel("layer_js", layer_js_kernel, dim3(a.L, a.B), dim3(256), 0, s, a);
+  e = launch_kernel("layer_sum", layer_sum_kernel, dim3(a.NB, a.L, 2 * a.B), dim3(256), 0, s, a);
   if (e != hipSuccess) return e;
-  return launch_kernel("teacher", teacher_kernel, dim3(a.B), dim3(256), 0, s, a);
+  e = launch_kernel("layer_js", layer_js_kernel, dim3(a.NB, a.L, a.B), dim3(256), 0, s, a);
+  if (e != hipSuccess) return e;
+  return launch_kernel("teacher", teacher_kernel, dim3(a.NB, a.B), dim3(256), 0, s, a);
 }
 
 }  // namespace mapk
