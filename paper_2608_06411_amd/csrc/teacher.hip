@@ -4,8 +4,9 @@
 // Four launches per call:
 //  * attn_colsum: the HBM-bound part.  Sample b's attention for layer l is a
 //    slab of H*M rows (heads, then question tokens) of N visual tokens.  A
-//    workgroup sums a slice of those rows for 64*VEC columns (16-byte loads,
-//    four waves on interleaved rows) and writes one float32 partial row.
+//    workgroup sums a slice of those rows for 64*VEC columns (16-byte
+//    non-temporal loads, eight rows in flight per thread, four waves on
+//    interleaved rows) and writes one float32 partial row.
 //    Input and reference question share the launch (grid z).
 //  * layer_sum: per column the partial rows summed in slice order, and per
 //    256-column chunk their float64 total.
@@ -21,6 +22,14 @@
 namespace mapk {
 
 namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load that bypasses the caches' retention (data read once)
+__device__ __forceinline__ uint4 load_once(const uint4* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 template <bool BF16>
 __device__ __forceinline__ void accumulate(float* acc, const uint4 v) {
@@ -54,16 +63,16 @@ __global__ __launch_bounds__(256) void attn_colsum_kernel(const TeacherArgs a) {
   for (int e = 0; e < VEC; ++e) acc[e] = 0.0f;
   if (col < N) {
     const uint4* src = static_cast<const uint4*>(t ? a.A_ref : a.A) + slab * stride + col / VEC;
+    // the attention is read once: non-temporal loads, eight rows in flight
     int r = r_lo + w;
-    for (; r + 12 < r_hi; r += 16) {
-      const uint4 v0 = src[(long long)r * stride], v1 = src[(long long)(r + 4) * stride];
-      const uint4 v2 = src[(long long)(r + 8) * stride], v3 = src[(long long)(r + 12) * stride];
-      accumulate<BF16>(acc, v0);
-      accumulate<BF16>(acc, v1);
-      accumulate<BF16>(acc, v2);
-      accumulate<BF16>(acc, v3);
+    for (; r + 28 < r_hi; r += 32) {
+      uint4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = load_once(src + (long long)(r + 4 * u) * stride);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) accumulate<BF16>(acc, v[u]);
     }
-    for (; r < r_hi; r += 4) accumulate<BF16>(acc, src[(long long)r * stride]);
+    for (; r < r_hi; r += 4) accumulate<BF16>(acc, load_once(src + (long long)r * stride));
   }
   __shared__ float red[3][VEC * 64];
   if (w > 0) {
