@@ -117,6 +117,7 @@ KERNEL_SOURCES = {
     "layer_sum": ("teacher.hip", "internal.h"),
     "layer_js": ("teacher.hip", "internal.h"),
     "teacher": ("teacher.hip", "internal.h"),
+    "assemble": ("gather.hip", "internal.h"),
 }
 
 
@@ -221,6 +222,31 @@ def teacher_bench(args, mp, torch, dev):
                                "sample": "one sample of the same workload (fp64 numpy reductions, one thread)"}
         res["oracle_layers"] = ref.layers.tolist()
     return res
+
+
+def assembly_bench(args, mp, torch, dev, out, T, pos_t, t_off, cfg):
+    """map_assemble after the timed map_prune steps: the layer-0 input of the
+    language model (kept rows, then question rows) for the same image.  HBM
+    roofline on its algorithmic bytes: every row read once and written once,
+    plus 4 B of position each way per row."""
+    X, pos = mp.map_assemble(out["V_out"], out["pos_out"], T, pos_t, t_off)
+    mp.timing_reset()
+    mp.timing_enable(True)
+    for _ in range(args.steps):
+        mp.map_assemble(out["V_out"], out["pos_out"], T, pos_t, t_off)
+    torch.cuda.synchronize()
+    per = mp.timing_read()
+    mp.timing_enable(False)
+    mp.timing_reset()
+    avg_us = 1e3 * per["assemble"][0] / per["assemble"][1]
+    rows = X.shape[0]
+    nbytes = 2 * rows * (X.shape[1] * X.element_size() + 4)
+    return {"workload": f"layer-0 input of {cfg.name}: {cfg.B} x ({cfg.K} kept + question) rows x {X.shape[1]} "
+                        f"{cfg.dtype}", "rows": rows, "avg_us": avg_us,
+            "roofline": {"bound": "hbm", "achieved": nbytes / (avg_us * 1e-6) / 1e9, "peak": PEAK_HBM, "unit": "GB/s",
+                         "frac": nbytes / (avg_us * 1e-6) / 1e9 / PEAK_HBM,
+                         "traffic": measured_traffic(args.workload, "assemble"), "kernel": "assemble",
+                         "algorithmic_per_launch": nbytes, "algorithmic_unit": "bytes"}}
 
 
 def cpu_baseline(x, cfg, min_seconds=10.0, max_runs=8):
@@ -355,6 +381,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"], _ = cpu_baseline(x, cfg)
+    line["assembly"] = assembly_bench(args, mp, torch, dev, out, T, pos_t, t_off, cfg)
     if not args.no_teacher:
         line["teacher_selection"] = teacher_bench(args, mp, torch, dev)
     print(json.dumps(line), flush=True)

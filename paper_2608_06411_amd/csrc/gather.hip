@@ -58,31 +58,26 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
   }
 }
 
-// Workgroup (x, image b) copies rows x * 8 .. + 7 of the image's K + M_b
-// rows, 16 bytes per thread per step, and their positions.
+// Workgroup (x, image b) copies row x of the image's K + M_b rows (one
+// workgroup per row: the copy is short, so the grid spreads it over the
+// chip), 16 bytes per thread per step, and its position.
 __global__ __launch_bounds__(256) void assemble_kernel(const AssembleArgs a) {
   const int b = blockIdx.y, K = a.K, M = a.t_off[b + 1] - a.t_off[b];
-  const int rows = K + M, r0 = blockIdx.x * 8;
-  if (r0 >= rows) return;
+  const int l = blockIdx.x;
+  if (l >= K + M) return;
   const int chunks = a.row_bytes >> 4, out0 = b * K + a.t_off[b];
-  const int nr = min(8, rows - r0), total = nr * chunks;
-  for (int e = threadIdx.x; e < total; e += 256) {
-    const int l = r0 + e / chunks, c = e - (e / chunks) * chunks;
-    const uint4* src = l < K ? static_cast<const uint4*>(a.V_out) + ((long long)b * K + l) * chunks
-                             : static_cast<const uint4*>(a.T) + ((long long)a.t_off[b] + l - K) * chunks;
-    static_cast<uint4*>(a.X)[(long long)(out0 + l) * chunks + c] = src[c];
-  }
-  if (threadIdx.x < nr) {
-    const int l = r0 + threadIdx.x;
-    a.pos_x[out0 + l] = l < K ? a.pos_out[(long long)b * K + l] : a.pos_t[a.t_off[b] + l - K];
-  }
+  const uint4* src = l < K ? static_cast<const uint4*>(a.V_out) + ((long long)b * K + l) * chunks
+                           : static_cast<const uint4*>(a.T) + ((long long)a.t_off[b] + l - K) * chunks;
+  uint4* dst = static_cast<uint4*>(a.X) + (long long)(out0 + l) * chunks;
+  for (int c = threadIdx.x; c < chunks; c += 256) dst[c] = src[c];
+  if (threadIdx.x == 0) a.pos_x[out0 + l] = l < K ? a.pos_out[(long long)b * K + l] : a.pos_t[a.t_off[b] + l - K];
 }
 
 }  // namespace
 
 hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s) {
   if (a.B == 0 || a.max_rows == 0) return hipSuccess;
-  return launch_kernel("assemble", assemble_kernel, dim3((a.max_rows + 7) / 8, a.B), dim3(256), 0, s, a);
+  return launch_kernel("assemble", assemble_kernel, dim3(a.max_rows, a.B), dim3(256), 0, s, a);
 }
 
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
