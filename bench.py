@@ -4,9 +4,13 @@ Workload: the LLaVA-NeXT-7B shape -- one image of 2880 visual tokens x 4096
 (bf16), a 64-token question, keep 160 (K0 = 80) -- from the seeded synthetic
 generator (random-init predictor weights).  A step is one map_prune call:
 predictor scoring, cosine similarity, selection and gather, inputs resident
-in HBM.  Prints one JSON line.
+in HBM.  Prints one JSON line.  Two objects in it measure the other entry
+points: `assembly` (map_assemble, the layer-0 input built from the same
+image's kept rows) and `teacher_selection` (map_teacher, Eq. (1)-(2), on
+synthetic attention of LLaVA-NeXT-7B's shape: 32 layers x 32 heads x 2880
+tokens, with its own oracle CPU baseline).
 
-    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-teacher]
 """
 import argparse
 import hashlib
