@@ -15,7 +15,11 @@ Attention in MLLMs for Visual Token Pruning"):
                     and the language model's layer-0 input after pruning;
 * ``teacher``    -- teacher selection for predictor training: Eq. (1),
                     Eq. (2) and QCTS-n (section "Question Contrastive
-                    Teacher Selection").
+                    Teacher Selection");
+* ``train``      -- one predictor training step: the KL divergence from the
+                    teacher distribution to p_hat and its gradient with
+                    respect to every predictor parameter (section
+                    "Cross-Modal Attention Distillation").
 
 Only the test suite, the smoke entry point and the benchmark's CPU-baseline
 leg may import this package.  The HIP product path never calls it, and it
@@ -28,8 +32,10 @@ from .select import (SelectResult, greedy_select, replay_check, restore_order, t
 from .similarity import cosine_entries, cosine_similarity, row_norms
 from .pipeline import assemble, prune
 from .teacher import TeacherResult, js_divergence, layer_distributions, teacher_selection
+from .train import TrainStepResult, gelu_erf_grad, kl_divergence, train_step
 
 __all__ = [
+    "TrainStepResult", "gelu_erf_grad", "kl_divergence", "train_step",
     "TeacherResult", "js_divergence", "layer_distributions", "teacher_selection",
     "assemble",
     "gelu_erf", "mlp", "rope", "predicted_attention", "predicted_attention_batch",
