@@ -43,7 +43,8 @@
  *   device-wide barriers).  The library sizes each launch to fit the device;
  *   if other work kept them off the device past a bounded wait (seconds),
  *   the selection stops and every idx_out entry of the call is -1 (map_prune
- *   then writes pos_out = -1 and zero rows).  The kernels never hang.
+ *   then writes pos_out = -1 and zero rows), and the workspace's status word
+ *   reads 1 (map_selection_status).  The kernels never hang.
  * Limits.  1 <= B <= MAP_MAX_BATCH, 1 <= N <= MAP_MAX_N,
  *   1 <= K <= min(N, MAP_MAX_K), 0 <= K0 <= K, D % 8 == 0, D_h % 8 == 0,
  *   d_p a multiple of 4 and <= 128, 1 <= question length <= 8192.
@@ -91,9 +92,11 @@ typedef struct {
  * (K0 == K gives plain top-K by p_hat; K0 == 0 starts the greedy rule from
  * an empty basis).  tau: rank-deficiency threshold; a token whose residual
  * against the current basis is at most tau times its own norm adds no basis
- * vector and scores 0 in Eq. (4).  Ties go to the higher p_hat, then to the
- * lower index; when every remaining candidate scores 0 the candidate with the
- * highest p_hat is taken. */
+ * vector and scores 0 in Eq. (4).  Ties: the top-K0 set prefers the higher
+ * p_hat, then the lower index; a greedy step takes the highest score, and
+ * between equal scores the lower index.  When every remaining candidate
+ * scores 0 the candidate with the highest p_hat (then the lower index) is
+ * taken. */
 typedef struct {
   int32_t K;
   int32_t K0;
@@ -137,7 +140,8 @@ map_status map_score(const map_weights* w, map_dtype dt, int B, int N,
  *   norms[b][i] = ||v_i||,  S[b][i][j] = <v_i, v_j> / (norms_i norms_j)
  * (a zero row has norm 0 and a zero row and column in S).  The residual of
  * Eq. (4) is evaluated from S and the norms.
- * V [B][N][D] dtype dt;  S_out [B][N][N] float32;  norms_out [B][N] float32. */
+ * V [B][N][D] dtype dt;  S_out [B][N][N] float32, or NULL for the norms
+ * alone;  norms_out [B][N] float32 (required). */
 map_status map_similarity(map_dtype dt, int B, int N, int D, const void* V,
                           float* S_out, float* norms_out,
                           void* ws, size_t ws_bytes, void* stream);
@@ -234,12 +238,33 @@ map_status map_assemble(map_dtype dt, int B, int K, int D, const void* V_out, co
  * Returns MAP_OK. */
 map_status map_set_subset_tokens(int n);
 
+/* map_selection_status -- the selection status word of the last map_select
+ * or map_prune call that used workspace `ws` (the word sits in the first
+ * 256 bytes of those workspaces).  Enqueues a copy of it into the device
+ * int32 *status_out on `stream`; read it once the stream has passed the
+ * copy.  Values:
+ *   0  the selection completed;
+ *   1  a device-wide barrier wait of the selection expired: that call's
+ *      idx_out entries are -1 (map_prune: pos_out -1 and zero rows).
+ * MAP_ERR_INVALID_ARG for a null or misaligned pointer; MAP_ERR_HIP if the
+ * copy cannot be enqueued. */
+map_status map_selection_status(const void* ws, int32_t* status_out, void* stream);
+
+/* At most n images per persistent selection launch (n <= 0: as many as
+ * can be resident at once, the default).  Larger batches then run as
+ * several launches, as they do by themselves when the device cannot hold
+ * every image's workgroups; the result does not change.  Meant for testing
+ * that multi-launch path at small sizes.  Process-wide; change it only
+ * between calls.  Returns MAP_OK. */
+map_status map_set_select_images_per_launch(int n);
+
 /* Per-kernel timing for measurement.  While enabled, every kernel the
  * library launches is bracketed by a pair of HIP events recorded on the
  * launch stream.  map_timing_read() waits for those events, accumulates the
  * elapsed time per kernel name and fills up to `cap` entries (names point to
  * static strings); it returns the number of kernel names seen.
- * map_timing_reset() drops everything recorded so far. */
+ * map_timing_reset() drops everything recorded so far and destroys the
+ * library's events (after a reset the library holds no HIP object). */
 map_status map_timing_enable(int enable);
 int map_timing_read(const char** names, double* total_ms, int* launches, int cap);
 void map_timing_reset(void);

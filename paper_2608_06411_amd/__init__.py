@@ -8,11 +8,12 @@ kept tokens -- as hand-written HIP kernels for gfx950 behind a C ABI
 """
 from .binding import (EXPORTS, MAP_BF16, MAP_F32, MapError, PredictorWeights, PruneWorkspace,
                       lib, map_assemble, map_prune, map_score, map_select, map_similarity, map_teacher,
-                      set_subset_tokens,
+                      selection_status, set_select_images_per_launch, set_subset_tokens,
                       timing_enable, timing_read, timing_reset)
 
 __all__ = [
     "EXPORTS", "MAP_BF16", "MAP_F32", "MapError", "PredictorWeights", "PruneWorkspace", "lib",
-    "map_assemble", "map_prune", "map_score", "map_select", "map_similarity", "map_teacher", "set_subset_tokens", "timing_enable",
+    "map_assemble", "map_prune", "map_score", "map_select", "map_similarity", "map_teacher", "selection_status",
+    "set_select_images_per_launch", "set_subset_tokens", "timing_enable",
     "timing_read", "timing_reset",
 ]

@@ -4,6 +4,11 @@ Every function takes and returns torch tensors that live on a ROCm device;
 all arithmetic happens in the library's HIP kernels, enqueued on the current
 torch stream.  There is no CPU fallback: if libmap.so is missing or a call
 fails, an exception is raised.
+
+Every tensor argument (inputs, reused outputs, workspaces) is checked against
+the sizes the call implies -- shape, dtype, contiguity, device -- before the
+library is called, and a mismatch raises ValueError or TypeError with nothing
+enqueued: the kernels trust the shapes they are given.
 """
 import ctypes
 import os
@@ -22,7 +27,8 @@ MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
 EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
-    "map_prune", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens", "map_timing_enable", "map_timing_read",
+    "map_prune", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
+    "map_selection_status", "map_set_select_images_per_launch", "map_timing_enable", "map_timing_read",
     "map_timing_reset",
 )
 
@@ -55,6 +61,8 @@ _SIGS = {
     "map_teacher_workspace": (_SZ, [_I, _I, _I]),
     "map_teacher": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "map_set_subset_tokens": (_I, [_I]),
+    "map_selection_status": (_I, [_P, _P, _P]),
+    "map_set_select_images_per_launch": (_I, [_I]),
     "map_timing_enable": (_I, [_I]),
     "map_timing_read": (_I, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
                              ctypes.POINTER(ctypes.c_int), _I]),
@@ -109,11 +117,40 @@ def _dtype_code(t: torch.Tensor) -> int:
 
 
 def _need(t: torch.Tensor, name: str, shape, dtype, device):
+    """Raise unless t is a contiguous `dtype` tensor of `shape` on `device`
+    (device None: only checked to be a GPU device, by _on_gpu)."""
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
-    if t.device != device or t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
-        raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)} on {device}, got "
-                         f"{t.dtype} {tuple(t.shape)} on {t.device}")
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)}, got "
+                         f"{t.dtype} {tuple(t.shape)}{'' if t.is_contiguous() else ' (not contiguous)'}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name}: expected a tensor on {device}, got one on {t.device}")
+
+
+def _on_gpu(t: torch.Tensor, name: str):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a ROCm device, got {t.device}")
+    return t.device
+
+
+def _dims(t: torch.Tensor, name: str, ndim: int):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dim() != ndim:
+        raise ValueError(f"{name}: expected {ndim} dimensions, got shape {tuple(t.shape)}")
+    return tuple(t.shape)
+
+
+def _need_ws(ws: Optional[torch.Tensor], nbytes: int, device, name="workspace"):
+    if nbytes == 0:
+        return
+    if ws is None or not isinstance(ws, torch.Tensor) or ws.dtype != torch.uint8 or not ws.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous uint8 buffer")
+    if ws.numel() < nbytes or ws.device != device or ws.data_ptr() % 256:
+        raise ValueError(f"{name}: needs {nbytes} bytes, 256-byte aligned, on {device}")
 
 
 def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
@@ -155,6 +192,17 @@ class PredictorWeights:
     def dtype(self):
         return self.w1_v.dtype
 
+    def check(self, D: int, dtype, device):
+        """Raise unless every weight has the shape the predictor implies for
+        feature width D (torch.nn.Linear layout), the call's dtype and device."""
+        _dims(self.w1_v, "w1_v", 2)
+        _dims(self.w_k, "w_k", 2)
+        Dh, dp = self.D_h, self.d_p
+        shapes = {"w1_v": (Dh, D), "b1_v": (Dh,), "w2_v": (Dh, Dh), "b2_v": (Dh,), "w_k": (dp, Dh),
+                  "w1_t": (Dh, D), "b1_t": (Dh,), "w2_t": (Dh, Dh), "b2_t": (Dh,), "w_q": (dp, Dh)}
+        for n, shape in shapes.items():
+            _need(getattr(self, n), f"weight {n}", shape, dtype, device)
+
     def struct(self) -> map_weights:
         s = map_weights()
         for n in ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q"):
@@ -166,22 +214,38 @@ class PredictorWeights:
         return s
 
 
-def _offsets(t_off) -> (ctypes.Array, int):
+def _offsets(t_off, B: Optional[int] = None) -> (ctypes.Array, int):
     vals = [int(x) for x in (t_off.tolist() if hasattr(t_off, "tolist") else t_off)]
+    if B is not None and len(vals) != B + 1:
+        raise ValueError(f"offsets need B + 1 = {B + 1} entries, got {len(vals)}")
+    if len(vals) < 2 or vals[0] != 0 or any(b <= a for a, b in zip(vals, vals[1:])):
+        raise ValueError("offsets must start at 0 and increase strictly")
     arr = (ctypes.c_int32 * len(vals))(*vals)
     return arr, vals[-1]
+
+
+def _check_features(w: PredictorWeights, V, pos_v, T, pos_t, t_off):
+    """The inputs of map_score / map_prune: returns (B, N, D, sumM, offsets, device)."""
+    B, N, D = _dims(V, "V", 3)
+    _dtype_code(V)
+    offs, sumM = _offsets(t_off, B)
+    _need(V, "V", (B, N, D), V.dtype, None)
+    dev = V.device  # (checked to be a GPU device before the library is called)
+    _need(pos_v, "pos_v", (B, N), torch.int32, dev)
+    _need(T, "T", (sumM, D), V.dtype, dev)
+    _need(pos_t, "pos_t", (sumM,), torch.int32, dev)
+    w.check(D, V.dtype, dev)
+    return B, N, D, sumM, offs, dev
 
 
 def map_score(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torch.Tensor,
               pos_t: torch.Tensor, t_off: Sequence[int], p_out: Optional[torch.Tensor] = None):
     """Predicted attention p_hat [B, N] (Eq. (3))."""
-    B, N, D = V.shape
-    dev = V.device
-    offs, sumM = _offsets(t_off)
-    if len(offs) != B + 1:
-        raise ValueError("t_off needs B + 1 entries")
+    B, N, D, sumM, offs, dev = _check_features(w, V, pos_v, T, pos_t, t_off)
     if p_out is None:
         p_out = torch.empty(B, N, dtype=torch.float32, device=dev)
+    _need(p_out, "p_out", (B, N), torch.float32, dev)
+    _on_gpu(V, "V")
     ws_struct = w.struct()
     dt = _dtype_code(V)
     nbytes = lib().map_score_workspace(dt, B, N, sumM, ctypes.byref(ws_struct))
@@ -195,15 +259,23 @@ def map_score(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torc
 
 
 def map_similarity(V: torch.Tensor, S_out: Optional[torch.Tensor] = None,
-                   norms_out: Optional[torch.Tensor] = None):
-    """Cosine similarity S [B, N, N] and row norms [B, N] of the visual tokens."""
-    B, N, D = V.shape
+                   norms_out: Optional[torch.Tensor] = None, norms_only: bool = False):
+    """Cosine similarity S [B, N, N] and row norms [B, N] of the visual tokens.
+    With norms_only the library forms the norms alone and S is None."""
+    B, N, D = _dims(V, "V", 3)
+    dt = _dtype_code(V)
+    _need(V, "V", (B, N, D), V.dtype, None)
     dev = V.device
-    if S_out is None:
+    if S_out is None and not norms_only:
         S_out = torch.empty(B, N, N, dtype=torch.float32, device=dev)
     if norms_out is None:
         norms_out = torch.empty(B, N, dtype=torch.float32, device=dev)
-    dt = _dtype_code(V)
+    if norms_only:
+        S_out = None
+    else:
+        _need(S_out, "S_out", (B, N, N), torch.float32, dev)
+    _need(norms_out, "norms_out", (B, N), torch.float32, dev)
+    _on_gpu(V, "V")
     nbytes = lib().map_similarity_workspace(dt, B, N, D)
     ws = _workspace(nbytes, dev)
     _check(lib().map_similarity(dt, B, N, D, _ptr(V), _ptr(S_out), _ptr(norms_out), _ptr(ws),
@@ -214,12 +286,21 @@ def map_similarity(V: torch.Tensor, S_out: Optional[torch.Tensor] = None,
 def map_select(p: torch.Tensor, S: torch.Tensor, norms: torch.Tensor, K: int, K0: int,
                tau: float = 1e-2, idx_out=None, order_out=None, gain_out=None):
     """Diversity-aware selection (Eq. (4)): returns (idx ascending, order, gain), each [B, K]."""
-    B, N = p.shape
+    B, N = _dims(p, "p", 2)
+    _need(p, "p", (B, N), torch.float32, None)
     dev = p.device
+    _need(S, "S", (B, N, N), torch.float32, dev)
+    _need(norms, "norms", (B, N), torch.float32, dev)
     idx_out = torch.empty(B, K, dtype=torch.int32, device=dev) if idx_out is None else idx_out
     order_out = torch.empty(B, K, dtype=torch.int32, device=dev) if order_out is None else order_out
     gain_out = torch.empty(B, K, dtype=torch.float32, device=dev) if gain_out is None else gain_out
+    _need(idx_out, "idx_out", (B, K), torch.int32, dev)
+    _need(order_out, "order_out", (B, K), torch.int32, dev)
+    _need(gain_out, "gain_out", (B, K), torch.float32, dev)
+    _on_gpu(p, "p")
     nbytes = lib().map_select_workspace(B, N, K)
+    if nbytes == 0:
+        raise MapError(MAP_ERR_INVALID_ARG, "map_select_workspace")
     ws = _workspace(nbytes, dev)
     sp = map_select_params(K, K0, tau)
     _check(lib().map_select(B, N, _ptr(p), _ptr(S), _ptr(norms), sp, _ptr(idx_out), _ptr(order_out),
@@ -231,12 +312,19 @@ class PruneWorkspace:
     """Reusable workspace for repeated map_prune calls of one shape."""
 
     def __init__(self, w: PredictorWeights, V: torch.Tensor, t_off, K: int):
-        B, N, _ = V.shape
-        offs, sumM = _offsets(t_off)
+        B, N, D = _dims(V, "V", 3)
+        offs, sumM = _offsets(t_off, B)
+        dev = _on_gpu(V, "V")
         self.nbytes = lib().map_prune_workspace(_dtype_code(V), B, N, sumM, ctypes.byref(w.struct()), K)
         if self.nbytes == 0:
             raise MapError(MAP_ERR_INVALID_ARG, "map_prune_workspace")
-        self.buf = _workspace(self.nbytes, V.device)
+        self.buf = _workspace(self.nbytes, dev)
+        self.device = dev
+
+    def status(self) -> int:
+        """The selection status word of the last call on this workspace
+        (0: completed; 1: a barrier wait expired).  Synchronises the stream."""
+        return selection_status(self.buf)
 
 
 def map_prune(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torch.Tensor,
@@ -245,9 +333,7 @@ def map_prune(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torc
     """Fused score + similarity + selection + gather.  Returns a dict with
     idx, V_out, pos_out, p, order and gain (the given `out` tensors are
     filled in place)."""
-    B, N, D = V.shape
-    dev = V.device
-    offs, sumM = _offsets(t_off)
+    B, N, D, sumM, offs, dev = _check_features(w, V, pos_v, T, pos_t, t_off)
     o = dict(out or {})
     o.setdefault("idx", torch.empty(B, K, dtype=torch.int32, device=dev))
     o.setdefault("V_out", torch.empty(B, K, D, dtype=V.dtype, device=dev))
@@ -255,8 +341,17 @@ def map_prune(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torc
     o.setdefault("p", torch.empty(B, N, dtype=torch.float32, device=dev))
     o.setdefault("order", torch.empty(B, K, dtype=torch.int32, device=dev))
     o.setdefault("gain", torch.empty(B, K, dtype=torch.float32, device=dev))
+    for name, shape, dtype in (("idx", (B, K), torch.int32), ("V_out", (B, K, D), V.dtype),
+                               ("pos_out", (B, K), torch.int32), ("p", (B, N), torch.float32),
+                               ("order", (B, K), torch.int32), ("gain", (B, K), torch.float32)):
+        _need(o[name], f"out[{name!r}]", shape, dtype, dev)
+    _on_gpu(V, "V")
     if workspace is None:
         workspace = PruneWorkspace(w, V, t_off, K)
+    need = lib().map_prune_workspace(_dtype_code(V), B, N, sumM, ctypes.byref(w.struct()), K)
+    if need == 0:
+        raise MapError(MAP_ERR_INVALID_ARG, "map_prune_workspace")
+    _need_ws(workspace.buf, need, dev)
     ws_struct = w.struct()
     sp = map_select_params(K, K0, tau)
     _check(lib().map_prune(ctypes.byref(ws_struct), _dtype_code(V), B, N, _ptr(V), _ptr(pos_v),
@@ -270,9 +365,15 @@ def map_assemble(V_out: torch.Tensor, pos_out: torch.Tensor, T: torch.Tensor, po
                  t_off: Sequence[int]):
     """The layer-0 input after pruning: per image its K kept rows, then its
     question rows, packed; returns (X [B K + sum M][D], positions)."""
-    B, K, D = V_out.shape
+    B, K, D = _dims(V_out, "V_out", 3)
+    _dtype_code(V_out)
+    offs, sumM = _offsets(t_off, B)
+    _need(V_out, "V_out", (B, K, D), V_out.dtype, None)
     dev = V_out.device
-    offs, sumM = _offsets(t_off)
+    _need(pos_out, "pos_out", (B, K), torch.int32, dev)
+    _need(T, "T", (sumM, D), V_out.dtype, dev)
+    _need(pos_t, "pos_t", (sumM,), torch.int32, dev)
+    _on_gpu(V_out, "V_out")
     X = torch.empty(B * K + sumM, D, dtype=V_out.dtype, device=dev)
     pos = torch.empty(B * K + sumM, dtype=torch.int32, device=dev)
     _check(lib().map_assemble(_dtype_code(V_out), B, K, D, _ptr(V_out), _ptr(pos_out), _ptr(T), _ptr(pos_t), offs,
@@ -287,14 +388,19 @@ def map_teacher(A: torch.Tensor, A_ref: torch.Tensor, m_off: Sequence[int], L: i
     [B][L][H][M_ref][N]; both contiguous, same dtype.  Returns p, p_ref
     [B, L, N], js [B, L] (float64), layers [B, n_top] and teacher [B, N];
     ``out`` (a previous result) is written in place when given."""
-    dev = A.device
     offs, sumM = _offsets(m_off)
     B = len(offs) - 1
     dt = _dtype_code(A)
     if A.numel() != L * H * sumM * N or A_ref.numel() != B * L * H * M_ref * N:
         raise ValueError("A or A_ref does not hold the sizes given")
-    if A_ref.dtype != A.dtype or not A.is_contiguous() or not A_ref.is_contiguous() or A_ref.device != dev:
-        raise ValueError("A and A_ref must be contiguous, of one dtype, on one device")
+    if A_ref.dtype != A.dtype or not A.is_contiguous() or not A_ref.is_contiguous():
+        raise ValueError("A and A_ref must be contiguous and of one dtype")
+    dev = A.device
+    if A_ref.device != dev:
+        raise ValueError("A and A_ref must be on one device")
+    if not 1 <= n_top <= L:
+        raise ValueError(f"n_top must lie in [1, L = {L}]")
+    _on_gpu(A, "A")
     if out is None:
         out = dict(p=torch.empty(B, L, N, dtype=torch.float32, device=dev),
                    p_ref=torch.empty(B, L, N, dtype=torch.float32, device=dev),
@@ -303,7 +409,12 @@ def map_teacher(A: torch.Tensor, A_ref: torch.Tensor, m_off: Sequence[int], L: i
                    teacher=torch.empty(B, N, dtype=torch.float32, device=dev))
         nbytes = lib().map_teacher_workspace(B, L, N)
         out["_ws"] = _workspace(nbytes, dev)
-    ws = out["_ws"]
+    for name, shape, dtype in (("p", (B, L, N), torch.float32), ("p_ref", (B, L, N), torch.float32),
+                               ("js", (B, L), torch.float64), ("layers", (B, n_top), torch.int32),
+                               ("teacher", (B, N), torch.float32)):
+        _need(out[name], f"out[{name!r}]", shape, dtype, dev)
+    ws = out.get("_ws")
+    _need_ws(ws, lib().map_teacher_workspace(B, L, N), dev, "out['_ws']")
     _check(lib().map_teacher(dt, B, L, H, N, _ptr(A), offs, _ptr(A_ref), M_ref, n_top, _ptr(out["p"]),
                              _ptr(out["p_ref"]), _ptr(out["js"]), _ptr(out["layers"]), _ptr(out["teacher"]),
                              _ptr(ws), 0 if ws is None else ws.numel(), _stream(dev)), "map_teacher")
@@ -315,6 +426,22 @@ def set_subset_tokens(n: int):
     many tokens.  Process-wide; workspaces sized before a change may be too
     small after it (map_prune then reports a workspace error)."""
     _check(lib().map_set_subset_tokens(int(n)), "map_set_subset_tokens")
+
+
+def selection_status(ws: torch.Tensor) -> int:
+    """The status word map_select / map_prune left at the start of workspace
+    `ws` (0: completed; 1: a selection barrier wait expired and the call's
+    indices are -1).  Copies it on the current stream and synchronises."""
+    dev = _on_gpu(ws, "ws")
+    word = torch.empty(1, dtype=torch.int32, device=dev)
+    _check(lib().map_selection_status(_ptr(ws), _ptr(word), _stream(dev)), "map_selection_status")
+    return int(word.item())
+
+
+def set_select_images_per_launch(n: int):
+    """At most n images per persistent selection launch (n <= 0: as many as
+    fit, the default).  Process-wide; for testing the multi-launch path."""
+    _check(lib().map_set_select_images_per_launch(int(n)), "map_set_select_images_per_launch")
 
 
 def timing_enable(on: bool = True):

@@ -226,6 +226,9 @@ struct SelectArgs {
   float tau2;
 };
 constexpr int kPub = 8;  // keys each workgroup publishes per round
+// At most this many images per selection launch (0: as many as can be
+// resident at once); map_set_select_images_per_launch sets it.
+void set_select_images_per_launch(int n);
 hipError_t launch_select_clear(const SelectArgs& a, hipStream_t s);
 hipError_t launch_select(SelectArgs& a, hipStream_t s);
 hipError_t launch_restore(const SelectArgs& a, hipStream_t s);

@@ -120,6 +120,10 @@ ScoreWs carve_score(Carver& c, map_dtype dt, int B, int N, int sumM, const map_w
   return s;
 }
 
+// The first 256 bytes of map_select's and map_prune's workspaces hold the
+// selection status word (map_selection_status copies it out).
+constexpr size_t kStatusBytes = 256;
+
 struct SelectWs {
   float* C;
   float* r2;
@@ -185,12 +189,14 @@ SelectWs carve_select(Carver& c, int B, int N, int K) {
   s.r2 = c.take<float>((size_t)B * N);
   s.pub = c.take<uint64_t>((size_t)B * 2 * 128 * (kPub + 1));
   s.bar = c.take<unsigned int>(2 * (size_t)B);  // the second B: the full selection behind a subset
-  s.err = c.take<int32_t>(4);
+  s.err = nullptr;  // the status word at the workspace's start (see carve_status)
   s.order = c.take<int32_t>((size_t)B * K);
   s.gain = c.take<float>((size_t)B * K);
   s.r0flag = c.take<int32_t>(2 * (size_t)B);  // the second B: the full selection behind a subset
   return s;
 }
+
+int32_t* carve_status(Carver& c) { return static_cast<int32_t*>(c.take_bytes(kStatusBytes)); }
 
 void fill_inv_freq(PrepArgs& pa, const map_weights& w) {
   const int half = w.d_p / 2;
@@ -412,6 +418,7 @@ size_t score_ws_bytes(map_dtype dt, int B, int N, int sumM, const map_weights& w
 
 size_t select_ws_bytes(int B, int N, int K) {
   Carver c(nullptr);
+  carve_status(c);
   carve_select(c, B, N, K);
   return c.off;
 }
@@ -633,8 +640,7 @@ map_status map_score(const map_weights* w, map_dtype dt, int B, int N, const voi
 
 map_status map_similarity(map_dtype dt, int B, int N, int D, const void* V, float* S_out,
                           float* norms_out, void* ws, size_t ws_bytes, void* stream) {
-  if (!valid_dtype(dt) || !valid_bn(B, N) || D <= 0 || D % 8 || !V || !S_out || !norms_out)
-    return MAP_ERR_INVALID_ARG;
+  if (!valid_dtype(dt) || !valid_bn(B, N) || D <= 0 || D % 8 || !V || !norms_out) return MAP_ERR_INVALID_ARG;
   const map_status ws_ok = check_ws(ws, ws_bytes, map_similarity_workspace(dt, B, N, D));
   if (ws_ok != MAP_OK) return ws_ok;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -649,6 +655,7 @@ map_status map_similarity(map_dtype dt, int B, int N, int D, const void* V, floa
   pa.ninv = ninv;
   hipError_t e = launch_prep(dt, pa, true, false, false, st);
   if (e != hipSuccess) return MAP_ERR_HIP;
+  if (!S_out) return MAP_OK;  // norms only
   GemmBatch g;
   memset(&g, 0, sizeof(g));
   g.p[0] = gram(V, B, N, D, S_out, ninv);
@@ -665,7 +672,9 @@ map_status map_select(int B, int N, const float* p, const float* S, const float*
   const map_status ws_ok = check_ws(ws, ws_bytes, select_ws_bytes(B, N, sp.K));
   if (ws_ok != MAP_OK) return ws_ok;
   Carver c(ws);
-  const SelectWs w = carve_select(c, B, N, sp.K);
+  int32_t* status = carve_status(c);
+  SelectWs w = carve_select(c, B, N, sp.K);
+  w.err = status;
   return hip_status(enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, w,
                                    static_cast<hipStream_t>(stream)));
 }
@@ -683,8 +692,10 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   if (ws_ok != MAP_OK) return ws_ok;
   hipStream_t st = static_cast<hipStream_t>(stream);
   Carver c(ws);
+  int32_t* status = carve_status(c);
   const ScoreWs s = carve_score(c, dt, B, N, sumM, *w);
-  const SelectWs sw = carve_select(c, B, N, sp.K);
+  SelectWs sw = carve_select(c, B, N, sp.K);
+  sw.err = status;
   float* S = c.take<float>((size_t)B * N * N);
   float* norms = c.take<float>((size_t)B * N);
   float* ninv = c.take<float>((size_t)B * N);
@@ -792,6 +803,17 @@ map_status map_set_subset_tokens(int n) {
   return MAP_OK;
 }
 
+map_status map_set_select_images_per_launch(int n) {
+  set_select_images_per_launch(n);
+  return MAP_OK;
+}
+
+map_status map_selection_status(const void* ws, int32_t* status_out, void* stream) {
+  if (!ws || !status_out || (reinterpret_cast<uintptr_t>(ws) & (kAlign - 1))) return MAP_ERR_INVALID_ARG;
+  return hip_status(hipMemcpyAsync(status_out, ws, sizeof(int32_t), hipMemcpyDeviceToDevice,
+                                   static_cast<hipStream_t>(stream)));
+}
+
 map_status map_timing_enable(int enable) {
   TimingState& t = timing();
   std::lock_guard<std::mutex> g(t.mu);
@@ -831,12 +853,16 @@ int map_timing_read(const char** names, double* total_ms, int* launches, int cap
 void map_timing_reset(void) {
   TimingState& t = timing();
   std::lock_guard<std::mutex> g(t.mu);
+  // every event is destroyed here, so that after a reset the library holds
+  // no HIP object (nothing is left for the runtime's teardown at exit)
   for (const TimingRecord& r : t.pending) {
     (void)hipEventSynchronize(r.stop);
-    t.spare.push_back(r.start);
-    t.spare.push_back(r.stop);
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
   }
+  for (hipEvent_t e : t.spare) (void)hipEventDestroy(e);
   t.pending.clear();
+  t.spare.clear();
   t.names.clear();
   t.total_ms.clear();
   t.launches.clear();

@@ -35,6 +35,8 @@
 //
 // Keys order candidates as the rule does: positive scores first (by score),
 // then zero scores by p, ties to the lower index; selected tokens key 0.
+#include <atomic>
+
 #include "internal.h"
 
 namespace mapk {
@@ -1602,6 +1604,8 @@ __global__ __launch_bounds__(NT) void restore_kernel(const SelectArgs a) {
   }
 }
 
+std::atomic<int> g_images_per_launch{0};
+
 struct DeviceInfo {
   int cus = 0;
 };
@@ -1619,6 +1623,8 @@ DeviceInfo& device_info() {
 }
 
 }  // namespace
+
+void set_select_images_per_launch(int n) { g_images_per_launch.store(n > 0 ? n : 0); }
 
 hipError_t launch_select_clear(const SelectArgs& a, hipStream_t s) {
   return launch_kernel("select_clear", select_clear_kernel, dim3(1), dim3(64), 0, s, a);
@@ -1678,8 +1684,10 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
     const int rw = 4 * chosen_pcap * (L.rs > L.ws ? L.rs : L.ws);
     if (4 * ((K + 7) & ~7) > rw || (a.row_bytes & 15) != 0) a.gV = nullptr;
   }
-  const int per_launch = static_cast<int>(((long long)per_cu * cus) / chosen_G);
+  int per_launch = static_cast<int>(((long long)per_cu * cus) / chosen_G);
   if (per_launch < 1) return hipErrorInvalidConfiguration;
+  const int cap = g_images_per_launch.load();
+  if (cap > 0 && cap < per_launch) per_launch = cap;
   if (r0_by_factor(a.K0) && !a.no_r0_kernel) {
     const int rb = r0_layout(a.K0).bytes;
     if (rb > 65536) {

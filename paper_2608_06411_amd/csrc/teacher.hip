@@ -160,7 +160,10 @@ __global__ __launch_bounds__(256) void teacher_kernel(const TeacherArgs a) {
     double js = 0.0;
     for (int k = 0; k < a.NB; ++k) js += part[k];
     if (first) a.js[(long long)b * L + tid] = js;
-    jsl[tid] = js >= 0.0 ? js : -1.0;  // a divergence is >= 0; a NaN ranks below every number
+    // A divergence is >= 0: a negative sum is rounding of terms below log's
+    // precision (p close to p_ref) and ranks as 0, tying with exact zeros
+    // (lower layer first); a NaN ranks below every number.
+    jsl[tid] = js != js ? -1.0 : (js > 0.0 ? js : 0.0);
   }
   __syncthreads();
   if (tid < L) {

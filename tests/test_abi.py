@@ -112,8 +112,18 @@ def test_score_and_prune_argument_checks(L):
 
 def test_similarity_argument_checks(L):
     assert L.map_similarity(bd.MAP_F32, 1, 10, 12, P(1), P(1), P(1), None, 0, None) == bd.MAP_ERR_INVALID_ARG
-    assert L.map_similarity(bd.MAP_F32, 1, 10, 16, P(1), None, P(1), None, 0, None) == bd.MAP_ERR_INVALID_ARG
+    assert L.map_similarity(bd.MAP_F32, 1, 10, 16, P(1), P(1), None, None, 0, None) == bd.MAP_ERR_INVALID_ARG
     assert L.map_similarity(bd.MAP_F32, 1, 10, 16, P(1), P(1), P(1), None, 0, None) == bd.MAP_ERR_WORKSPACE
+    # a norms-only call (S_out NULL) is valid: it still needs its workspace
+    assert L.map_similarity(bd.MAP_F32, 1, 10, 16, P(1), None, P(1), None, 0, None) == bd.MAP_ERR_WORKSPACE
+
+
+def test_selection_status_argument_checks(L):
+    assert L.map_selection_status(None, P(0x1000), None) == bd.MAP_ERR_INVALID_ARG
+    assert L.map_selection_status(P(0x1000), None, None) == bd.MAP_ERR_INVALID_ARG
+    assert L.map_selection_status(P(0x1010), P(0x1000), None) == bd.MAP_ERR_INVALID_ARG
+    assert L.map_set_select_images_per_launch(3) == bd.MAP_OK
+    assert L.map_set_select_images_per_launch(0) == bd.MAP_OK
 
 
 def test_timing_registry_without_launches(L):
@@ -121,3 +131,95 @@ def test_timing_registry_without_launches(L):
     mp.timing_enable(True)
     assert mp.timing_read() == {}
     mp.timing_enable(False)
+
+
+# ------------------------------------------------ binding argument checks
+# The binding checks every tensor against the sizes the call implies before
+# the library is called; these run on CPU tensors, and each expects a
+# ValueError or TypeError with nothing enqueued.  Tensors that pass every
+# size check still stop at the device check (they are not on a GPU).
+torch = pytest.importorskip("torch")
+
+
+def _cpu_case(B=2, N=12, D=16, Dh=8, dp=4, dtype=None, Ms=(3, 5)):
+    dtype = dtype or torch.bfloat16
+    sumM = sum(Ms)
+    w = mp.PredictorWeights(
+        w1_v=torch.zeros(Dh, D, dtype=dtype), b1_v=torch.zeros(Dh, dtype=dtype),
+        w2_v=torch.zeros(Dh, Dh, dtype=dtype), b2_v=torch.zeros(Dh, dtype=dtype),
+        w_k=torch.zeros(dp, Dh, dtype=dtype),
+        w1_t=torch.zeros(Dh, D, dtype=dtype), b1_t=torch.zeros(Dh, dtype=dtype),
+        w2_t=torch.zeros(Dh, Dh, dtype=dtype), b2_t=torch.zeros(Dh, dtype=dtype),
+        w_q=torch.zeros(dp, Dh, dtype=dtype))
+    return dict(w=w, V=torch.zeros(B, N, D, dtype=dtype), pos_v=torch.zeros(B, N, dtype=torch.int32),
+                T=torch.zeros(sumM, D, dtype=dtype), pos_t=torch.zeros(sumM, dtype=torch.int32),
+                t_off=[0, Ms[0], sumM])
+
+
+def _prune_cpu(c, **kw):
+    c = dict(c, **kw)
+    return mp.map_prune(c["w"], c["V"], c["pos_v"], c["T"], c["pos_t"], c["t_off"], 4, 2, out=c.get("out"))
+
+
+@pytest.mark.parametrize("bad,match", [
+    (dict(pos_v=torch.zeros(2, 12, dtype=torch.int64)), "pos_v"),
+    (dict(pos_v=torch.zeros(2, 11, dtype=torch.int32)), "pos_v"),
+    (dict(T=torch.zeros(7, 16, dtype=torch.bfloat16)), "T"),
+    (dict(T=torch.zeros(8, 16, dtype=torch.float32)), "T"),
+    (dict(pos_t=torch.zeros(9, dtype=torch.int32)), "pos_t"),
+    (dict(t_off=[0, 3]), "offsets"),
+    (dict(t_off=[0, 5, 5]), "offsets"),
+    (dict(V=torch.zeros(2, 12, 16, dtype=torch.float16)), "dtype"),
+    (dict(V=torch.zeros(2, 16, 12, dtype=torch.bfloat16).transpose(1, 2)), "contiguous"),
+    (dict(out={"idx": torch.zeros(2, 3, dtype=torch.int32)}), "idx"),
+    (dict(out={"V_out": torch.zeros(2, 4, 16, dtype=torch.float32)}), "V_out"),
+    (dict(out={"p": torch.zeros(2, 13)}), "'p'"),
+    (dict(), "ROCm device"),
+])
+def test_binding_rejects_bad_prune_arguments(bad, match):
+    with pytest.raises((ValueError, TypeError), match=match):
+        _prune_cpu(_cpu_case(), **bad)
+
+
+def test_binding_rejects_bad_weights():
+    c = _cpu_case()
+    c["w"].w_k = torch.zeros(4, 9, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="w_k"):
+        _prune_cpu(c)
+    c = _cpu_case()
+    c["w"].b1_t = torch.zeros(8, dtype=torch.float32)
+    with pytest.raises(ValueError, match="b1_t"):
+        mp.map_score(c["w"], c["V"], c["pos_v"], c["T"], c["pos_t"], c["t_off"])
+
+
+def test_binding_rejects_bad_select_similarity_assemble_arguments():
+    p = torch.zeros(2, 10)
+    with pytest.raises(ValueError, match="S"):
+        mp.map_select(p, torch.zeros(2, 10, 9), torch.zeros(2, 10), 4, 2)
+    with pytest.raises(ValueError, match="norms"):
+        mp.map_select(p, torch.zeros(2, 10, 10), torch.zeros(2, 10, dtype=torch.float64), 4, 2)
+    with pytest.raises(ValueError, match="order_out"):
+        mp.map_select(p, torch.zeros(2, 10, 10), torch.zeros(2, 10), 4, 2,
+                      order_out=torch.zeros(2, 4, dtype=torch.int64))
+    with pytest.raises(ValueError, match="S_out"):
+        mp.map_similarity(torch.zeros(1, 8, 16), S_out=torch.zeros(1, 8, 7))
+    with pytest.raises(ValueError, match="ROCm device"):
+        mp.map_similarity(torch.zeros(1, 8, 16), norms_only=True)
+    V_out = torch.zeros(2, 4, 16, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="T"):
+        mp.map_assemble(V_out, torch.zeros(2, 4, dtype=torch.int32), torch.zeros(6, 16, dtype=torch.bfloat16),
+                        torch.zeros(8, dtype=torch.int32), [0, 3, 8])
+    with pytest.raises(ValueError, match="pos_out"):
+        mp.map_assemble(V_out, torch.zeros(2, 4, dtype=torch.int64), torch.zeros(8, 16, dtype=torch.bfloat16),
+                        torch.zeros(8, dtype=torch.int32), [0, 3, 8])
+
+
+def test_binding_rejects_bad_teacher_arguments():
+    A = torch.zeros(2 * 2 * 3 * 16, dtype=torch.bfloat16)
+    R = torch.zeros(2 * 2 * 1 * 16, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="n_top"):
+        mp.map_teacher(A, R, [0, 3], 2, 2, 16, 1, 3)
+    with pytest.raises(ValueError, match="sizes"):
+        mp.map_teacher(A, R, [0, 3], 2, 2, 15, 1, 1)
+    with pytest.raises(ValueError, match="ROCm device"):
+        mp.map_teacher(A, R, [0, 3], 2, 2, 16, 1, 1)

@@ -42,6 +42,10 @@ CASES = {
     # the logits and the projection's K split, an odd number of RoPE pairs
     "odd_width_bf16": ("sweep", {"B": 2, "N": 131, "M": (2, 17),
                                  "pred": PredictorShape(D=256, D_h=200, d_p=36)}, 2e-2),
+    # a peaked predictor (weights N(0, 0.03^2)): p_hat spans a factor of ~40,
+    # where a 10 % logit-scale error moves p_hat by more than the bf16 bar
+    "peaked_bf16": ("tiny", {"dtype": "bf16", "pred": PredictorShape(weight_std=0.03)}, 2e-2),
+    "peaked_f32": ("tiny", {"pred": PredictorShape(weight_std=0.03)}, 1e-5),
 }
 
 

@@ -30,7 +30,7 @@ def _slices(B, L, N):
     return min(16, max(1, -(-4096 // wgs)))
 
 
-def _case(dtype, L, H, Ms, M_ref, N, zero_layer=None):
+def _case(dtype, L, H, Ms, M_ref, N, zero_layer=None, same_layers=()):
     A_f, A_s, R_f, R_s = [], [], [], []
     for b, M in enumerate(Ms):
         af, a_s = make_attention(L, H, M, N, dtype=dtype, seed=40 + b, question=b)
@@ -38,6 +38,8 @@ def _case(dtype, L, H, Ms, M_ref, N, zero_layer=None):
         if zero_layer is not None:
             for x in (af, a_s, rf, r_s):
                 x[zero_layer] = 0
+        for l in same_layers:  # the reference question attends exactly like the question
+            rf[l], r_s[l] = af[l], a_s[l]
         A_f.append(af), A_s.append(a_s), R_f.append(rf), R_s.append(r_s)
     return A_f, A_s, R_f, R_s
 
@@ -49,10 +51,10 @@ def _dev(stores, dtype, dev):
     return torch.from_numpy(np.ascontiguousarray(flat, dtype=np.float32)).to(dev)
 
 
-def _run_and_check(dtype, L, H, Ms, M_ref, N, n_top, zero_layer=None):
+def _run_and_check(dtype, L, H, Ms, M_ref, N, n_top, zero_layer=None, same_layers=()):
     from paper_2608_06411_amd import map_teacher
     announce(f"teacher {dtype} L={L} H={H} M={Ms} M_ref={M_ref} N={N} n_top={n_top}")
-    A_f, A_s, R_f, R_s = _case(dtype, L, H, Ms, M_ref, N, zero_layer)
+    A_f, A_s, R_f, R_s = _case(dtype, L, H, Ms, M_ref, N, zero_layer, same_layers)
     dev = device()
     m_off = np.concatenate([[0], np.cumsum(Ms)]).astype(np.int32)
     out = map_teacher(_dev(A_s, dtype, dev), _dev(R_s, dtype, dev), m_off, L, H, N, M_ref, n_top)
@@ -96,6 +98,15 @@ def test_teacher_zero_layer_is_uniform():
     assert got["js"][0][2] == 0.0
 
 
+def test_teacher_identical_layers_tie_at_zero():
+    """Two layers whose question and reference attention are identical have
+    D_JS = 0 exactly on both sides; they rank last, the lower layer first
+    (Eq. (2) with ties to the lower layer), after every positive divergence."""
+    got = _run_and_check("bf16", 8, 2, (4,), 4, 256, 8, same_layers=(2, 5))
+    assert got["js"][0][2] == 0.0 and got["js"][0][5] == 0.0
+    assert got["layers"][0][-2:].tolist() == [2, 5]
+
+
 def test_teacher_is_deterministic():
     from paper_2608_06411_amd import map_teacher
     announce("teacher determinism")
@@ -124,5 +135,5 @@ def test_teacher_rejects_bad_arguments():
         map_teacher(A, R, [0, 3], 2, 2, 12, 1, 1)
     A = torch.zeros(2 * 2 * 3 * 16, dtype=torch.bfloat16, device=dev)
     R = torch.zeros(2 * 2 * 1 * 16, dtype=torch.bfloat16, device=dev)
-    with pytest.raises(MapError):
+    with pytest.raises((MapError, ValueError)):  # the binding refuses it before the library does
         map_teacher(A, R, [0, 3], 2, 2, 16, 1, 3)      # n_top > L

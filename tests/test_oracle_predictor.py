@@ -169,3 +169,29 @@ def test_mlp_is_tokenwise():
     for i in range(7):
         np.testing.assert_allclose(full[i], mlp(X[i:i + 1], w["w1_v"], w["b1_v"], w["w2_v"],
                                                 w["b2_v"])[0], rtol=1e-14)
+
+
+def test_peaked_workload_makes_the_bf16_bar_discriminate():
+    """On the default workload (weights N(0, 0.02^2)) p_hat is nearly flat,
+    and a 10 % error in the logit scale moves it by less than the 2e-2 bf16
+    bar; with weights N(0, 0.03^2) the same error moves it by more, and so
+    does dropping the bias of f_V's second layer: the GPU score tests run
+    that workload so that such mistakes cannot pass."""
+    from workloads import PredictorShape, get_config, make_inputs
+    names = ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")
+
+    def rel_moves(std):
+        cfg = get_config("tiny", N=576, pred=PredictorShape(weight_std=std))
+        x = make_inputs(cfg)
+        w = {n: x[n + "_f32"].astype(np.float64) for n in names}
+        args = (x["V_f32"][0], x["T_f32"], x["pos_v"][0], x["pos_t"])
+        p = predicted_attention(*args, w)
+        scaled = dict(w, w_q=1.1 * w["w_q"])        # logits times 1.1
+        no_bias = dict(w, b2_v=0.0 * w["b2_v"])     # f_V's second bias dropped
+        return (np.max(np.abs(predicted_attention(*args, scaled) / p - 1)),
+                np.max(np.abs(predicted_attention(*args, no_bias) / p - 1)), p.max() / p.min())
+
+    flat_scale, _, flat_span = rel_moves(0.02)
+    assert flat_scale < 2e-2 and flat_span < 1.5
+    peaked_scale, peaked_bias, peaked_span = rel_moves(0.03)
+    assert peaked_scale > 2e-2 and peaked_bias > 2e-2 and peaked_span > 10
