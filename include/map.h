@@ -68,7 +68,9 @@ typedef enum {
   MAP_ERR_INVALID_ARG = 1,  /* a size, pointer or parameter is out of range */
   MAP_ERR_UNSUPPORTED = 2,  /* valid request the library does not implement */
   MAP_ERR_WORKSPACE = 3,    /* ws is NULL, misaligned or smaller than needed */
-  MAP_ERR_HIP = 4           /* the HIP runtime reported an error            */
+  MAP_ERR_HIP = 4,          /* the HIP runtime reported an error            */
+  MAP_ERR_TOO_LARGE = 5     /* the call needs more scratch than the static
+                               buffer of map_prune_noalloc holds            */
 } map_status;
 
 typedef enum { MAP_F32 = 0, MAP_BF16 = 1 } map_dtype;
@@ -174,6 +176,29 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N,
                      map_select_params sp, int32_t* idx_out, void* V_out, int32_t* pos_out,
                      float* p_out, int32_t* order_out, float* gain_out,
                      void* ws, size_t ws_bytes, void* stream);
+
+/* map_prune_noalloc -- map_prune for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  The same kernels, arguments and outputs as map_prune,
+ * without ws / ws_bytes: the workspace is a static device buffer of
+ * MAP_PRUNE_NOALLOC_MAX_BYTES that the library holds on every device it
+ * runs on until the process ends.  The call allocates nothing and calls no
+ * allocating routine.
+ * Limit: map_prune_workspace(dt, B, N, sum_M, w, K) must not exceed
+ * MAP_PRUNE_NOALLOC_MAX_BYTES (96 MiB: one image of 2880 tokens x 4096 up
+ * to K = 640, or 4 images of 1024 tokens), else MAP_ERR_TOO_LARGE and
+ * nothing is enqueued.  Other argument errors as for map_prune.
+ * Sharing: every call on one device uses that device's one buffer, which
+ * keeps the last call's contents (map_prune initialises what it reads);
+ * calls that overlap in time on one device -- on several streams or from
+ * several threads -- race on it, and the caller must order them (one
+ * stream, or events between streams). */
+#define MAP_PRUNE_NOALLOC_MAX_BYTES ((size_t)96 << 20)
+map_status map_prune_noalloc(const map_weights* w, map_dtype dt, int B, int N,
+                             const void* V, const int32_t* pos_v,
+                             const void* T, const int32_t* pos_t, const int32_t* t_off_host,
+                             map_select_params sp, int32_t* idx_out, void* V_out, int32_t* pos_out,
+                             float* p_out, int32_t* order_out, float* gain_out, void* stream);
 
 /* map_teacher -- teacher selection for training the predictor (section
  * "Question Contrastive Teacher Selection", Eq. (1)-(2); QCTS-n of the

@@ -19,7 +19,8 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmap.so")
 
-MAP_OK, MAP_ERR_INVALID_ARG, MAP_ERR_UNSUPPORTED, MAP_ERR_WORKSPACE, MAP_ERR_HIP = range(5)
+MAP_OK, MAP_ERR_INVALID_ARG, MAP_ERR_UNSUPPORTED, MAP_ERR_WORKSPACE, MAP_ERR_HIP, MAP_ERR_TOO_LARGE = range(6)
+MAP_PRUNE_NOALLOC_MAX_BYTES = 96 << 20
 MAP_F32, MAP_BF16 = 0, 1
 MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
 
@@ -27,7 +28,7 @@ MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
 EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
-    "map_prune", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
+    "map_prune", "map_prune_noalloc", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
     "map_selection_status", "map_set_select_images_per_launch", "map_timing_enable", "map_timing_read",
     "map_timing_reset",
 )
@@ -57,6 +58,8 @@ _SIGS = {
     "map_select": (_I, [_I, _I, _P, _P, _P, map_select_params, _P, _P, _P, _P, _SZ, _P]),
     "map_prune": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
                        map_select_params, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "map_prune_noalloc": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
+                               map_select_params, _P, _P, _P, _P, _P, _P, _P]),
     "map_assemble": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
     "map_teacher_workspace": (_SZ, [_I, _I, _I]),
     "map_teacher": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),

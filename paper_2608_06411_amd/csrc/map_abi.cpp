@@ -579,6 +579,7 @@ const char* map_status_string(int status) {
     case MAP_ERR_UNSUPPORTED: return "unsupported";
     case MAP_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case MAP_ERR_HIP: return "HIP runtime error";
+    case MAP_ERR_TOO_LARGE: return "the call needs more scratch than map_prune_noalloc's static buffer holds";
     default: return "unknown status";
   }
 }
@@ -724,6 +725,52 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st, true, &ga, &gathered);
   if (e != hipSuccess) return MAP_ERR_HIP;
   return gathered ? MAP_OK : hip_status(launch_gather(ga, st));  // else its own kernel
+}
+
+}  // extern "C"
+
+// map_prune_noalloc's workspace: a static device array, one per device the
+// library runs on, held until the process ends.  Host code never uses the
+// array's name as an address (on the host it is only a stand-in for the
+// symbol): its device address is looked up once per device, with that
+// device current, and only that address is passed on.
+static __device__ __align__(256) unsigned char scratch[MAP_PRUNE_NOALLOC_MAX_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// The current device's address of `scratch` (null if it cannot be had).
+void* scratch_address() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+    g_scratch_addr[dev] = p;
+  }
+  return g_scratch_addr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+map_status map_prune_noalloc(const map_weights* w, map_dtype dt, int B, int N, const void* V,
+                             const int32_t* pos_v, const void* T, const int32_t* pos_t,
+                             const int32_t* t_off_host, map_select_params sp, int32_t* idx_out, void* V_out,
+                             int32_t* pos_out, float* p_out, int32_t* order_out, float* gain_out, void* stream) {
+  if (!valid_bn(B, N) || !valid_offsets(t_off_host, B)) return MAP_ERR_INVALID_ARG;
+  const size_t need = map_prune_workspace(dt, B, N, t_off_host[B], w, sp.K);
+  if (need > MAP_PRUNE_NOALLOC_MAX_BYTES) return MAP_ERR_TOO_LARGE;
+  void* ws = nullptr;
+  if (need > 0 && !(ws = scratch_address())) return MAP_ERR_HIP;
+  // (need == 0: invalid sizes, which map_prune reports before touching ws)
+  return map_prune(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, sp, idx_out, V_out, pos_out, p_out, order_out,
+                   gain_out, ws, need > 0 ? MAP_PRUNE_NOALLOC_MAX_BYTES : 0, stream);
 }
 
 map_status map_assemble(map_dtype dt, int B, int K, int D, const void* V_out, const int32_t* pos_out,
