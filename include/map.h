@@ -248,6 +248,39 @@ map_status map_assemble(map_dtype dt, int B, int K, int D, const void* V_out, co
                         const void* T, const int32_t* pos_t, const int32_t* t_off_host,
                         void* X_out, int32_t* pos_x_out, void* stream);
 
+/* Gradients of the predictor parameters, float32 device buffers of the
+ * shapes of the matching map_weights fields (w1_* [D_h][D], b1_* [D_h],
+ * w2_* [D_h][D_h], b2_* [D_h], w_k and w_q [d_p][D_h]). */
+typedef struct {
+  float *w1_v, *b1_v, *w2_v, *b2_v, *w_k;
+  float *w1_t, *b1_t, *w2_t, *b2_t, *w_q;
+} map_grads;
+
+/* map_train_step -- one training step of the predictor (section
+ * "Cross-Modal Attention Distillation": the predictor is trained offline by
+ * minimising the KL divergence from the teacher layer's distribution
+ * p^{l*} of Eq. (1)-(2), e.g. map_teacher's teacher_out, to the predicted
+ * p_hat of Eq. (3)):
+ *   loss_out[b] = D_KL(p_teacher[b] || p_hat[b]) = sum_n p* log(p* / p_hat)
+ *                 (natural log, 0 log 0 = 0), float32 per image;
+ *   grads       = the gradient of (1/B) sum_b loss[b] with respect to every
+ *                 predictor parameter (written, not accumulated).
+ * The forward pass is map_score's (same arguments, same rounding points);
+ * p_out [B][N] receives p_hat when not NULL.  p_teacher [B][N] float32
+ * (device) must hold distributions over the N visual tokens.
+ * Arithmetic: the call's dtype for stored activations and the operands of
+ * the matrix-core products (hidden states, GELU'(a), the gradients of the
+ * projections' inputs and of layer 1's pre-activation), float32
+ * accumulation, float32 gradients.  Requires d_p % 8 == 0.
+ * ws: map_train_workspace(dt, B, N, sum_M, w) bytes, 256-byte aligned.
+ * MAP_ERR_INVALID_ARG / MAP_ERR_WORKSPACE / MAP_ERR_HIP as for map_score. */
+size_t map_train_workspace(map_dtype dt, int B, int N, int sum_M, const map_weights* w);
+map_status map_train_step(const map_weights* w, map_dtype dt, int B, int N,
+                          const void* V, const int32_t* pos_v,
+                          const void* T, const int32_t* pos_t, const int32_t* t_off_host,
+                          const float* p_teacher, float* loss_out, float* p_out,
+                          const map_grads* grads, void* ws, size_t ws_bytes, void* stream);
+
 /* map_prune's candidate subset.  A greedy pick of Eq. (4) scores
  * p_i n_i r_i <= p_i n_i, so map_prune may run the selection on a subset J
  * of each image's tokens: R0 plus the tokens with the largest bounds

@@ -29,6 +29,7 @@ EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
     "map_prune", "map_prune_noalloc", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
+    "map_train_workspace", "map_train_step",
     "map_selection_status", "map_set_select_images_per_launch", "map_timing_enable", "map_timing_read",
     "map_timing_reset",
 )
@@ -39,6 +40,11 @@ class map_weights(ctypes.Structure):
                 ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")] + \
                [("D", ctypes.c_int32), ("D_h", ctypes.c_int32), ("d_p", ctypes.c_int32),
                 ("rope_theta", ctypes.c_float)]
+
+
+class map_grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")]
 
 
 class map_select_params(ctypes.Structure):
@@ -63,6 +69,9 @@ _SIGS = {
     "map_assemble": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
     "map_teacher_workspace": (_SZ, [_I, _I, _I]),
     "map_teacher": (_I, [_I, _I, _I, _I, _I, _P, _P, _P, _I, _I, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "map_train_workspace": (_SZ, [_I, _I, _I, _I, ctypes.POINTER(map_weights)]),
+    "map_train_step": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P,
+                            ctypes.POINTER(map_grads), _P, _SZ, _P]),
     "map_set_subset_tokens": (_I, [_I]),
     "map_selection_status": (_I, [_P, _P, _P]),
     "map_set_select_images_per_launch": (_I, [_I]),
@@ -429,6 +438,56 @@ def set_subset_tokens(n: int):
     many tokens.  Process-wide; workspaces sized before a change may be too
     small after it (map_prune then reports a workspace error)."""
     _check(lib().map_set_subset_tokens(int(n)), "map_set_subset_tokens")
+
+
+GRAD_NAMES = ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")
+
+
+class TrainWorkspace:
+    """Reusable workspace for repeated map_train_step calls of one shape."""
+
+    def __init__(self, w: PredictorWeights, V: torch.Tensor, t_off):
+        B, N, D = _dims(V, "V", 3)
+        offs, sumM = _offsets(t_off, B)
+        dev = _on_gpu(V, "V")
+        self.nbytes = lib().map_train_workspace(_dtype_code(V), B, N, sumM, ctypes.byref(w.struct()))
+        if self.nbytes == 0:
+            raise MapError(MAP_ERR_INVALID_ARG, "map_train_workspace")
+        self.buf = _workspace(self.nbytes, dev)
+
+
+def map_train_step(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torch.Tensor,
+                   pos_t: torch.Tensor, t_off: Sequence[int], p_teacher: torch.Tensor,
+                   grads: Optional[dict] = None, p_out: Optional[torch.Tensor] = None,
+                   workspace: Optional[TrainWorkspace] = None):
+    """One predictor training step: the KL divergence from the teacher rows
+    p_teacher [B, N] to p_hat (float32 per image) and the float32 gradients of
+    the batch mean with respect to every predictor parameter (a dict keyed
+    like PredictorWeights' fields, written in place when given).
+    Returns (loss [B], p_hat [B, N], grads)."""
+    B, N, D, sumM, offs, dev = _check_features(w, V, pos_v, T, pos_t, t_off)
+    _need(p_teacher, "p_teacher", (B, N), torch.float32, dev)
+    if grads is None:
+        grads = {n: torch.empty(tuple(getattr(w, n).shape), dtype=torch.float32, device=dev) for n in GRAD_NAMES}
+    for n in GRAD_NAMES:
+        _need(grads[n], f"grads[{n!r}]", tuple(getattr(w, n).shape), torch.float32, dev)
+    if p_out is None:
+        p_out = torch.empty(B, N, dtype=torch.float32, device=dev)
+    _need(p_out, "p_out", (B, N), torch.float32, dev)
+    loss = torch.empty(B, dtype=torch.float32, device=dev)
+    _on_gpu(V, "V")
+    if workspace is None:
+        workspace = TrainWorkspace(w, V, t_off)
+    need = lib().map_train_workspace(_dtype_code(V), B, N, sumM, ctypes.byref(w.struct()))
+    if need == 0:
+        raise MapError(MAP_ERR_INVALID_ARG, "map_train_workspace")
+    _need_ws(workspace.buf, need, dev)
+    gs = map_grads(*[grads[n].data_ptr() for n in GRAD_NAMES])
+    ws_struct = w.struct()
+    _check(lib().map_train_step(ctypes.byref(ws_struct), _dtype_code(V), B, N, _ptr(V), _ptr(pos_v), _ptr(T),
+                                _ptr(pos_t), offs, _ptr(p_teacher), _ptr(loss), _ptr(p_out), ctypes.byref(gs),
+                                _ptr(workspace.buf), workspace.nbytes, _stream(dev)), "map_train_step")
+    return loss, p_out, grads
 
 
 def selection_status(ws: torch.Tensor) -> int:

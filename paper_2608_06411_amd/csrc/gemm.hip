@@ -67,6 +67,11 @@ __device__ __forceinline__ float gelu_erf(float x) {
   return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f));
 }
 
+// d/dx [x Phi(x)] = Phi(x) + x phi(x), with Phi from the same erf.
+__device__ __forceinline__ float gelu_erf_grad(float x) {
+  return fmaf(x * 0.39894228040143268f, __expf(-0.5f * x * x), 0.5f * (1.0f + erf_as(x * 0.70710678118654752f)));
+}
+
 template <typename T>
 __device__ __forceinline__ void mma_slice(const uint4 (*As)[8], const uint4 (*Bs)[8], int wm, int wn,
                                           int lane, f32x16_t (&acc)[2][2]);
@@ -176,7 +181,33 @@ __device__ __forceinline__ void epilogue(const GemmProblem& P, int bt, int tm, i
                                          float* tile_lo, float* tile_hi, int tid, int lane, int wm, int wn) {
   const int M = P.M, N = P.N;
   const int m0 = tm * BM, n0 = tn * BN;
-  if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS) {
+  if (P.epi == EPI_F32 || P.epi == EPI_GELU2 || P.epi == EPI_MUL) {
+    const int e = P.epi;
+    const T* __restrict__ bias = static_cast<const T*>(P.bias);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wn * 64 + j * 32 + acc_col(lane);
+      if (col >= N) continue;
+      const float bv = (e == EPI_GELU2 && bias) ? to_f32<T>(bias[col]) : 0.0f;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * 64 + i * 32 + acc_row(r, lane);
+          if (row >= M) continue;
+          const long long at = bt * P.strideC + (long long)row * P.ldc + col;
+          const float v = acc[i][j][r] + bv;
+          if (e == EPI_F32) {
+            static_cast<float*>(P.C)[at] = v;
+          } else if (e == EPI_GELU2) {
+            static_cast<T*>(P.C)[at] = from_f32<T>(gelu_erf(v));
+            static_cast<T*>(P.aux)[at] = from_f32<T>(gelu_erf_grad(v));
+          } else {
+            static_cast<T*>(P.C)[at] = from_f32<T>(v * to_f32<T>(static_cast<const T*>(P.aux)[at]));
+          }
+        }
+    }
+  } else if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS) {
     T* __restrict__ C = static_cast<T*>(P.C) + bt * P.strideC;
     const T* __restrict__ bias = static_cast<const T*>(P.bias);
     const bool gelu = P.epi == EPI_BIAS_GELU;
@@ -903,7 +934,7 @@ bool gemm_direct_loads(map_dtype dt, const GemmBatch& g) {
   bool dma = true;  // every problem meets the direct-load requirements
   for (int i = 0; i < g.count; ++i) {
     const GemmProblem& p = g.p[i];
-    dma = dma && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+    dma = dma && p.epi <= EPI_PARTIAL && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
           (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
           p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
           (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));
@@ -917,7 +948,7 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
     bool dma = true;  // every problem meets the direct-load requirements
     for (int i = 0; i < g.count; ++i) {
       const GemmProblem& p = g.p[i];
-      dma = dma && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+      dma = dma && p.epi <= EPI_PARTIAL && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
             (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
             p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
             (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));

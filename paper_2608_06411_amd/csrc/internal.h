@@ -75,6 +75,10 @@ enum EpiMode : int {
   EPI_COSINE = 2,     // S[m][n] = acc * rs[m] * rs[n] (float32), mirrored; A == B
   EPI_ROPE = 3,       // out[m][:] = RoPE(acc[m][:] + rope_bias) (float32) with the row's cos/sin
   EPI_PARTIAL = 4,    // the raw float32 accumulators of a K range, for gram_reduce (bf16 direct-load kernel)
+  // the training step's products (register-staged kernel only):
+  EPI_F32 = 5,        // C[m][n] = acc, stored as float32
+  EPI_GELU2 = 6,      // v = acc + bias[n]: C[m][n] = GELU(v) and aux[m][n] = GELU'(v), both stored as T
+  EPI_MUL = 7,        // C[m][n] = acc * aux[m][n] (aux of type T, leading dimension ldc), stored as T
 };
 
 struct GemmProblem {
@@ -96,6 +100,7 @@ struct GemmProblem {
   long long mapStride;
   int ksplit;              // EPI_PARTIAL: K ranges per tile (K / ksplit each, a multiple of 256)
   const int32_t* run_if;   // [batch] batch items whose flag is 0 are skipped (null: none)
+  void* aux;               // EPI_GELU2: second output; EPI_MUL: the factor (both [M][ldc] of type T)
   // filled by the host helper
   int tiles_m, tiles_n, tiles_tri, tiles_per_batch, tile_begin;
 };
@@ -259,6 +264,71 @@ struct AssembleArgs {
   int t_off[MAP_MAX_BATCH + 1];
 };
 hipError_t launch_assemble(const AssembleArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- training step
+// The gradient of the batch-mean KL divergence from the teacher to p_hat,
+// from the logits back to the projections' inputs (before RoPE).
+struct TrainArgs {
+  const float* logits;     // [sum_M][N] (scaled by 1/sqrt(d_p))
+  const float2* partial;   // [sum_M][nblk] per-block (max, sum of exp) of the logits
+  const float* p_hat;      // [B][N]
+  const float* p_star;     // [B][N] teacher distributions
+  float* loss;             // [B] each image's divergence
+  float* G;                // [sum_M][N] dL/dlogits / sqrt(d_p)
+  const float* q;          // [sum_M][d_p] queries after RoPE
+  const float* k;          // [B N][d_p] keys after RoPE
+  const float2* cs_v;      // [B N][d_p / 2] RoPE (cos, sin)
+  const float2* cs_t;      // [sum_M][d_p / 2]
+  float* dq_part;          // [nch][sum_M][d_p] token-chunk partials of dL/dq
+  void* dk_rows;           // [B N][d_p] dL/dz of the keys, element type of the call
+  void* dk_cols;           // [d_p][ldv] the same, tokens contiguous (zero padded)
+  void* dq_rows;           // [sum_M][d_p]
+  void* dq_cols;           // [d_p][ldt]
+  int B, N, d_p, nblk, nch, ldv, ldt;
+  float inv_B, scale;      // 1 / B, 1 / sqrt(d_p)
+  int t_off[MAP_MAX_BATCH + 1];
+};
+hipError_t launch_train_grads(map_dtype dt, const TrainArgs& a, hipStream_t s);
+
+// dst[c][r] = src[r][c] (r < rows, c < cols), zero for rows <= r < ldd.
+struct TransposeJob {
+  const void* src;
+  void* dst;
+  int rows, cols, lds, ldd;
+  int tile_begin;  // filled by transpose_finalize
+};
+constexpr int kMaxTransposeJobs = 8;
+struct TransposeBatch {
+  TransposeJob job[kMaxTransposeJobs];
+  int count, total_tiles;
+};
+void transpose_finalize(TransposeBatch& t);
+hipError_t launch_transpose(map_dtype dt, const TransposeBatch& t, const char* name, hipStream_t s);
+
+// out[r] = sum_{c < cols} src[r][c] (element type of the call), float32.
+struct RowsumJob {
+  const void* src;
+  float* out;
+  int rows, cols, ld;
+  int row_begin;  // filled by launch_rowsum
+};
+struct RowsumBatch {
+  RowsumJob job[4];
+  int count;
+};
+hipError_t launch_rowsum(map_dtype dt, RowsumBatch& t, hipStream_t s);
+
+// Per branch s (0 visual, 1 text): db2[s] = W[s]^T csum[s] and the rank-one
+// term dW[s] += csum[s] b2[s]^T of the projection's gradient.
+struct FinishArgs {
+  const void* W[2];    // [d_p][D_h] W_K, W_Q
+  const void* b2[2];   // [D_h]
+  const float* csum[2];  // [d_p] sum over tokens of dL/dz
+  float* db2[2];       // [D_h]
+  float* dW[2];        // [d_p][D_h]
+  int D_h, d_p;
+};
+hipError_t launch_finish(map_dtype dt, const FinishArgs& f, hipStream_t s);
 
 // ---------------------------------------------------------------- teacher selection
 constexpr int kTeacherMaxLayers = 256;

@@ -250,7 +250,7 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
                          const int32_t* t_off, float* p_out, const ScoreWs& s,
                          const GemmProblem* extra_l1, float* norms, float* ninv, hipStream_t st,
                          unsigned int* clear_bar = nullptr, int32_t* clear_err = nullptr,
-                         bool norms_in_layer1 = false) {
+                         bool norms_in_layer1 = false, void* gprime_v = nullptr, void* gprime_t = nullptr) {
   const int sumM = t_off[B], rowsV = B * N;
   PrepArgs pa;
   memset(&pa, 0, sizeof(pa));
@@ -285,6 +285,11 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   memset(&g1, 0, sizeof(g1));
   g1.p[0] = linear(V, rowsV, w.w1_v, w.b1_v, s.h1_v, w.D_h, w.D, EPI_BIAS_GELU);
   g1.p[1] = linear(T, sumM, w.w1_t, w.b1_t, s.h1_t, w.D_h, w.D, EPI_BIAS_GELU);
+  if (gprime_v && gprime_t) {  // the training step also keeps GELU'(a) of layer 1
+    g1.p[0].epi = g1.p[1].epi = EPI_GELU2;
+    g1.p[0].aux = gprime_v;
+    g1.p[1].aux = gprime_t;
+  }
   g1.count = 2;
   g1.p[g1.count++] = linear(w.w_k, w.d_p, s.w2t_v, nullptr, s.wc_v, w.D_h, w.D_h, EPI_BIAS);  // W_K W2
   g1.p[g1.count++] = linear(w.w_q, w.d_p, s.w2t_t, nullptr, s.wc_t, w.D_h, w.D_h, EPI_BIAS);  // W_Q W2
@@ -421,6 +426,197 @@ size_t select_ws_bytes(int B, int N, int K) {
   carve_status(c);
   carve_select(c, B, N, K);
   return c.off;
+}
+
+// ------------------------------------------------------------ training step
+struct TrainWs {
+  int32_t* status;
+  ScoreWs s;
+  void *gp_v, *gp_t;              // GELU'(a) of layer 1: [B N][D_h], [sum_M][D_h]
+  float* G;                       // [sum_M][N]
+  float* dq_part;                 // [nch][sum_M][d_p]
+  void *dk_rows, *dk_cols, *dq_rows, *dq_cols;
+  void *VT, *TT, *HvT, *HtT;      // [D][ldv], [D][ldt], [D_h][ldv], [D_h][ldt]
+  void *WKT, *WQT, *WcvT, *WctT;  // [D_h][d_p]
+  void *Xv, *Xt, *XvT, *XtT;      // [d_p][D_h], [D_h][d_p]
+  void *dAv, *dAt, *dAvT, *dAtT;  // [B N][D_h], [sum_M][D_h], [D_h][ldv], [D_h][ldt]
+  float *csum_v, *csum_t;         // [d_p]
+  float* p;                       // [B][N]
+  int ldv, ldt, nch;
+};
+
+int pad8(int n) { return (n + 7) & ~7; }
+
+TrainWs carve_train(Carver& c, map_dtype dt, int B, int N, int sumM, const map_weights& w) {
+  TrainWs t;
+  const size_t es = elem_size(dt), BN = (size_t)B * N, Dh = w.D_h, dp = w.d_p;
+  t.ldv = pad8(B * N);
+  t.ldt = pad8(sumM);
+  t.nch = (N + 255) / 256;
+  t.status = carve_status(c);
+  t.s = carve_score(c, dt, B, N, sumM, w);
+  t.gp_v = c.take_bytes(BN * Dh * es);
+  t.gp_t = c.take_bytes((size_t)sumM * Dh * es);
+  t.G = c.take<float>((size_t)sumM * N);
+  t.dq_part = c.take<float>((size_t)t.nch * sumM * dp);
+  t.dk_rows = c.take_bytes(BN * dp * es);
+  t.dk_cols = c.take_bytes(dp * t.ldv * es);
+  t.dq_rows = c.take_bytes((size_t)sumM * dp * es);
+  t.dq_cols = c.take_bytes(dp * t.ldt * es);
+  t.VT = c.take_bytes((size_t)w.D * t.ldv * es);
+  t.TT = c.take_bytes((size_t)w.D * t.ldt * es);
+  t.HvT = c.take_bytes(Dh * t.ldv * es);
+  t.HtT = c.take_bytes(Dh * t.ldt * es);
+  t.WKT = c.take_bytes(Dh * dp * es);
+  t.WQT = c.take_bytes(Dh * dp * es);
+  t.WcvT = c.take_bytes(Dh * dp * es);
+  t.WctT = c.take_bytes(Dh * dp * es);
+  t.Xv = c.take_bytes(dp * Dh * es);
+  t.Xt = c.take_bytes(dp * Dh * es);
+  t.XvT = c.take_bytes(Dh * dp * es);
+  t.XtT = c.take_bytes(Dh * dp * es);
+  t.dAv = c.take_bytes(BN * Dh * es);
+  t.dAt = c.take_bytes((size_t)sumM * Dh * es);
+  t.dAvT = c.take_bytes(Dh * t.ldv * es);
+  t.dAtT = c.take_bytes(Dh * t.ldt * es);
+  t.csum_v = c.take<float>(dp);
+  t.csum_t = c.take<float>(dp);
+  t.p = c.take<float>(BN);
+  return t;
+}
+
+size_t train_ws_bytes(map_dtype dt, int B, int N, int sumM, const map_weights& w) {
+  Carver c(nullptr);
+  carve_train(c, dt, B, N, sumM, w);
+  return c.off;
+}
+
+bool valid_grads(const map_grads* g) {
+  if (!g) return false;
+  const float* ptrs[] = {g->w1_v, g->b1_v, g->w2_v, g->b2_v, g->w_k, g->w1_t, g->b1_t, g->w2_t, g->b2_t, g->w_q};
+  for (const float* p : ptrs)
+    if (!p) return false;
+  return true;
+}
+
+TransposeJob tjob(const void* src, void* dst, int rows, int cols, int ldd) {
+  TransposeJob j;
+  memset(&j, 0, sizeof(j));
+  j.src = src;
+  j.dst = dst;
+  j.rows = rows;
+  j.cols = cols;
+  j.lds = cols;
+  j.ldd = ldd;
+  return j;
+}
+
+hipError_t enqueue_train(const map_weights& w, map_dtype dt, int B, int N, const void* V, const int32_t* pos_v,
+                         const void* T, const int32_t* pos_t, const int32_t* t_off, const float* p_teacher,
+                         float* loss_out, float* p, const map_grads& g, const TrainWs& t, hipStream_t st) {
+  const int sumM = t_off[B], BN = B * N, Dh = w.D_h, dp = w.d_p;
+  hipError_t e = enqueue_score(w, dt, B, N, V, pos_v, T, pos_t, t_off, p, t.s, nullptr, nullptr, nullptr, st,
+                               nullptr, nullptr, false, t.gp_v, t.gp_t);
+  if (e != hipSuccess) return e;
+  // dL/dlogits, then dL/dz of the keys and queries (before RoPE), in both layouts
+  TrainArgs a;
+  memset(&a, 0, sizeof(a));
+  a.logits = t.s.logits;
+  a.partial = t.s.partial;
+  a.p_hat = p;
+  a.p_star = p_teacher;
+  a.loss = loss_out;
+  a.G = t.G;
+  a.q = t.s.q;
+  a.k = t.s.k;
+  a.cs_v = t.s.cs_v;
+  a.cs_t = t.s.cs_t;
+  a.dq_part = t.dq_part;
+  a.dk_rows = t.dk_rows;
+  a.dk_cols = t.dk_cols;
+  a.dq_rows = t.dq_rows;
+  a.dq_cols = t.dq_cols;
+  a.B = B;
+  a.N = N;
+  a.d_p = dp;
+  a.nblk = (N + 63) / 64;
+  a.nch = t.nch;
+  a.ldv = t.ldv;
+  a.ldt = t.ldt;
+  a.inv_B = 1.0f / static_cast<float>(B);
+  a.scale = 1.0f / sqrtf(static_cast<float>(dp));
+  for (int b = 0; b <= B; ++b) a.t_off[b] = t_off[b];
+  if ((e = launch_train_grads(dt, a, st)) != hipSuccess) return e;
+  // the operands of the reductions over tokens, tokens contiguous
+  TransposeBatch ta;
+  memset(&ta, 0, sizeof(ta));
+  ta.job[ta.count++] = tjob(V, t.VT, BN, w.D, t.ldv);
+  ta.job[ta.count++] = tjob(T, t.TT, sumM, w.D, t.ldt);
+  ta.job[ta.count++] = tjob(t.s.h1_v, t.HvT, BN, Dh, t.ldv);
+  ta.job[ta.count++] = tjob(t.s.h1_t, t.HtT, sumM, Dh, t.ldt);
+  ta.job[ta.count++] = tjob(w.w_k, t.WKT, dp, Dh, dp);
+  ta.job[ta.count++] = tjob(w.w_q, t.WQT, dp, Dh, dp);
+  ta.job[ta.count++] = tjob(t.s.wc_v, t.WcvT, dp, Dh, dp);
+  ta.job[ta.count++] = tjob(t.s.wc_t, t.WctT, dp, Dh, dp);
+  transpose_finalize(ta);
+  if ((e = launch_transpose(dt, ta, "transpose_in", st)) != hipSuccess) return e;
+  // X = dz^T h (per branch) and dL/da = (dz (W W2)) * GELU'(a)
+  GemmBatch g1;
+  memset(&g1, 0, sizeof(g1));
+  g1.p[0] = linear(t.dk_cols, dp, t.HvT, nullptr, t.Xv, Dh, t.ldv, EPI_BIAS);
+  g1.p[1] = linear(t.dq_cols, dp, t.HtT, nullptr, t.Xt, Dh, t.ldt, EPI_BIAS);
+  g1.p[2] = linear(t.dk_rows, BN, t.WcvT, nullptr, t.dAv, Dh, dp, EPI_MUL);
+  g1.p[2].aux = t.gp_v;
+  g1.p[3] = linear(t.dq_rows, sumM, t.WctT, nullptr, t.dAt, Dh, dp, EPI_MUL);
+  g1.p[3].aux = t.gp_t;
+  g1.count = 4;
+  gemm_finalize(g1);
+  if ((e = launch_gemm(dt, g1, "gemm_train_x_da", st)) != hipSuccess) return e;
+  TransposeBatch tb;
+  memset(&tb, 0, sizeof(tb));
+  tb.job[tb.count++] = tjob(t.dAv, t.dAvT, BN, Dh, t.ldv);
+  tb.job[tb.count++] = tjob(t.dAt, t.dAtT, sumM, Dh, t.ldt);
+  tb.job[tb.count++] = tjob(t.Xv, t.XvT, dp, Dh, dp);
+  tb.job[tb.count++] = tjob(t.Xt, t.XtT, dp, Dh, dp);
+  transpose_finalize(tb);
+  if ((e = launch_transpose(dt, tb, "transpose_da", st)) != hipSuccess) return e;
+  // the weight gradients (float32):
+  //   dW1 = dA^T X_in,  dW_K = X W2^T (+ the rank-one term below),  dW2 = W_K^T X
+  GemmBatch g2;
+  memset(&g2, 0, sizeof(g2));
+  g2.p[0] = linear(t.dAvT, Dh, t.VT, nullptr, g.w1_v, w.D, t.ldv, EPI_F32);
+  g2.p[1] = linear(t.dAtT, Dh, t.TT, nullptr, g.w1_t, w.D, t.ldt, EPI_F32);
+  g2.p[2] = linear(t.Xv, dp, w.w2_v, nullptr, g.w_k, Dh, Dh, EPI_F32);
+  g2.p[3] = linear(t.Xt, dp, w.w2_t, nullptr, g.w_q, Dh, Dh, EPI_F32);
+  g2.p[4] = linear(t.WKT, Dh, t.XvT, nullptr, g.w2_v, Dh, dp, EPI_F32);
+  g2.p[5] = linear(t.WQT, Dh, t.XtT, nullptr, g.w2_t, Dh, dp, EPI_F32);
+  g2.count = 6;
+  gemm_finalize(g2);
+  if ((e = launch_gemm(dt, g2, "gemm_train_dw", st)) != hipSuccess) return e;
+  // bias gradients and the sums of dz over tokens
+  RowsumBatch rs;
+  memset(&rs, 0, sizeof(rs));
+  rs.job[0] = RowsumJob{t.dAvT, g.b1_v, Dh, t.ldv, t.ldv, 0};
+  rs.job[1] = RowsumJob{t.dAtT, g.b1_t, Dh, t.ldt, t.ldt, 0};
+  rs.job[2] = RowsumJob{t.dk_cols, t.csum_v, dp, t.ldv, t.ldv, 0};
+  rs.job[3] = RowsumJob{t.dq_cols, t.csum_t, dp, t.ldt, t.ldt, 0};
+  rs.count = 4;
+  if ((e = launch_rowsum(dt, rs, st)) != hipSuccess) return e;
+  FinishArgs f;
+  memset(&f, 0, sizeof(f));
+  f.W[0] = w.w_k;
+  f.W[1] = w.w_q;
+  f.b2[0] = w.b2_v;
+  f.b2[1] = w.b2_t;
+  f.csum[0] = t.csum_v;
+  f.csum[1] = t.csum_t;
+  f.db2[0] = g.b2_v;
+  f.db2[1] = g.b2_t;
+  f.dW[0] = g.w_k;
+  f.dW[1] = g.w_q;
+  f.D_h = Dh;
+  f.d_p = dp;
+  return launch_finish(dt, f, st);
 }
 
 // ------------------------------------------------------------ timing
@@ -843,6 +1039,27 @@ map_status map_teacher(map_dtype dt, int B, int L, int H, int N, const void* A, 
   a.n_top = n_top;
   for (int b = 0; b <= B; ++b) a.m_off[b] = m_off_host[b];
   return hip_status(launch_teacher(dt, a, static_cast<hipStream_t>(stream)));
+}
+
+size_t map_train_workspace(map_dtype dt, int B, int N, int sum_M, const map_weights* w) {
+  if (!valid_dtype(dt) || !valid_bn(B, N) || !valid_weights(w) || w->d_p % 8 || sum_M < B) return 0;
+  return train_ws_bytes(dt, B, N, sum_M, *w);
+}
+
+map_status map_train_step(const map_weights* w, map_dtype dt, int B, int N, const void* V, const int32_t* pos_v,
+                          const void* T, const int32_t* pos_t, const int32_t* t_off_host, const float* p_teacher,
+                          float* loss_out, float* p_out, const map_grads* grads, void* ws, size_t ws_bytes,
+                          void* stream) {
+  if (!valid_dtype(dt) || !valid_bn(B, N) || !valid_weights(w) || w->d_p % 8 || !V || !pos_v || !T || !pos_t ||
+      !p_teacher || !loss_out || !valid_grads(grads) || !valid_offsets(t_off_host, B))
+    return MAP_ERR_INVALID_ARG;
+  const int sumM = t_off_host[B];
+  const map_status ws_ok = check_ws(ws, ws_bytes, train_ws_bytes(dt, B, N, sumM, *w));
+  if (ws_ok != MAP_OK) return ws_ok;
+  Carver c(ws);
+  const TrainWs t = carve_train(c, dt, B, N, sumM, *w);
+  return hip_status(enqueue_train(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p_teacher, loss_out,
+                                  p_out ? p_out : t.p, *grads, t, static_cast<hipStream_t>(stream)));
 }
 
 map_status map_set_subset_tokens(int n) {
