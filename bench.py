@@ -4,13 +4,26 @@ Workload: the LLaVA-NeXT-7B shape -- one image of 2880 visual tokens x 4096
 (bf16), a 64-token question, keep 160 (K0 = 80) -- from the seeded synthetic
 generator (random-init predictor weights).  A step is one map_prune call:
 predictor scoring, cosine similarity, selection and gather, inputs resident
-in HBM.  Prints one JSON line.  Two objects in it measure the other entry
-points: `assembly` (map_assemble, the layer-0 input built from the same
-image's kept rows) and `teacher_selection` (map_teacher, Eq. (1)-(2), on
-synthetic attention of LLaVA-NeXT-7B's shape: 32 layers x 32 heads x 2880
-tokens, with its own oracle CPU baseline).
+in HBM.  Prints one JSON line: the headline (exactly K timed steps, plus
+the median / p10 / p90 of individually timed steps), its kernels and
+rooflines, and objects for the rest:
+* `assembly`: map_assemble, the layer-0 input built from the same image's
+  kept rows;
+* `training_step`: map_train_step, the predictor's KL step on the same
+  image against a Dirichlet(1) teacher;
+* `decoder_layer_context`: one random-init 7B-shaped decoder layer built
+  from PyTorch-ROCm ops (not this library) over the unpruned 2944-token and
+  the pruned 224-token sequence, and the pruning time as a fraction of the
+  first;
+* `teacher_selection`: map_teacher, Eq. (1)-(2), on synthetic attention of
+  LLaVA-NeXT-7B's shape (32 layers x 32 heads x 2880 tokens), with its own
+  oracle CPU baseline;
+* `configs`: the other workloads (the small fp32 image, the 16-image sweep
+  at each K, the 8-image multi-frame batch), each with its rooflines;
+* `cpu_baseline`: the oracle on this host, all BLAS threads and one.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-teacher]
+                    [--no-configs] [--no-context] [--no-train]
 """
 import argparse
 import hashlib
@@ -253,27 +266,287 @@ def assembly_bench(args, mp, torch, dev, out, T, pos_t, t_off, cfg):
                          "algorithmic_per_launch": nbytes, "algorithmic_unit": "bytes"}}
 
 
-def cpu_baseline(x, cfg, min_seconds=10.0, max_runs=8):
-    """The oracle as it stands, timed on this host: the workload's first image,
-    run again until at least `min_seconds` of CPU work (at most `max_runs`)."""
-    import oracle
-    from threadpoolctl import threadpool_info
+def _oracle_weights(x):
     names = ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")
-    w = {n: x[n + "_f32"] for n in names}
+    return {n: x[n + "_f32"] for n in names}
+
+
+def _oracle_prune_one(x, cfg):
+    import oracle
     lo, hi = int(x["t_off"][0]), int(x["t_off"][1])
+    return oracle.prune(x["V_f32"][:1], x["T_f32"][lo:hi], np.array([0, hi - lo]), x["pos_v"][:1],
+                        x["pos_t"][lo:hi], _oracle_weights(x), cfg.K, cfg.K0, cfg.tau, cfg.pred.rope_theta)
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(x, cfg, tiny_x=None, tiny_cfg=None, min_seconds=10.0, max_runs=8):
+    """The oracle as it stands, timed on this host: the workload's first image,
+    run again until at least `min_seconds` of CPU work (at most `max_runs`),
+    with every BLAS thread; then once on one thread; and the small fp32
+    workload's image both ways.  `value` is the all-thread rate."""
+    from threadpoolctl import threadpool_info, threadpool_limits
     runs, t0 = 0, time.perf_counter()
     while True:
-        r = oracle.prune(x["V_f32"][:1], x["T_f32"][lo:hi], np.array([0, hi - lo]), x["pos_v"][:1],
-                         x["pos_t"][lo:hi], w, cfg.K, cfg.K0, cfg.tau, cfg.pred.rope_theta)
+        _oracle_prune_one(x, cfg)
         runs += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds or runs >= max_runs:
             break
     threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    with threadpool_limits(limits=1, user_api="blas"):
+        t1 = time.perf_counter()
+        _oracle_prune_one(x, cfg)
+        single = time.perf_counter() - t1
+    per_config = {cfg.name: {"all_threads_s_per_image": dt / runs, "single_thread_s_per_image": single}}
+    if tiny_x is not None:
+        t2 = time.perf_counter()
+        _oracle_prune_one(tiny_x, tiny_cfg)
+        a = time.perf_counter() - t2
+        with threadpool_limits(limits=1, user_api="blas"):
+            t3 = time.perf_counter()
+            _oracle_prune_one(tiny_x, tiny_cfg)
+            b = time.perf_counter() - t3
+        per_config[tiny_cfg.name] = {"all_threads_s_per_image": a, "single_thread_s_per_image": b}
     return {"value": runs / dt, "unit": "images/s", "cores": int(threads or 1), "kind": "oracle",
-            "sample": f"{runs} run(s) of one image of the workload (N={cfg.N}, D={cfg.pred.D}, M={hi - lo}, "
-                      f"K={cfg.K}, K0={cfg.K0}): float64 predictor, literal Eq. (4) greedy, gather; "
-                      f"{dt:.2f} s on {os.cpu_count()} visible CPUs"}, r
+            "sample": f"{runs} run(s) of one image of the workload (N={cfg.N}, D={cfg.pred.D}, "
+                      f"M={int(x['t_off'][1])}, K={cfg.K}, K0={cfg.K0}): float64 predictor, literal Eq. (4) "
+                      f"greedy, gather; {dt:.2f} s with {threads} BLAS threads on {os.cpu_count()} visible CPUs",
+            "single_thread": {"value": 1.0 / single, "unit": "images/s", "cores": 1,
+                              "sample": "one run of the same image on one BLAS thread"},
+            "cpu_model": _cpu_model(), "per_config": per_config}
+
+
+def _to_dev(torch, dev, a, dtype):
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+WEIGHT_NAMES = ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")
+
+
+def _upload(mp, torch, dev, x, cfg):
+    w = mp.PredictorWeights(**{n: _to_dev(torch, dev, x[n + "_store"], cfg.dtype) for n in WEIGHT_NAMES},
+                            rope_theta=cfg.pred.rope_theta)
+    return dict(w=w, V=_to_dev(torch, dev, x["V_store"], cfg.dtype), T=_to_dev(torch, dev, x["T_store"], cfg.dtype),
+                pos_v=torch.from_numpy(x["pos_v"]).to(dev), pos_t=torch.from_numpy(x["pos_t"]).to(dev))
+
+
+def _kernel_table(mp, torch, run, steps):
+    """Per-kernel average durations over `steps` calls of run(), measured with
+    HIP events on the launch stream by the library's timing registry."""
+    mp.timing_reset()
+    mp.timing_enable(True)
+    for _ in range(steps):
+        run()
+    torch.cuda.synchronize()
+    per = mp.timing_read()
+    mp.timing_enable(False)
+    mp.timing_reset()
+    return {k: {"avg_us": 1e3 * v[0] / v[1], "launches_per_step": v[1] / steps} for k, v in per.items()}
+
+
+def _time_steps(torch, dev, run, steps, warmup, per_step=0):
+    """ms per call over exactly `steps` timed calls (events bracketing the
+    region, synchronised on both sides), and optionally the median, p10 and
+    p90 of `per_step` individually timed calls."""
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    res = {"ms_per_step": e0.elapsed_time(e1) / steps, "wall_s_timed": wall}
+    if per_step:
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(per_step)]
+        for a, b in ev:
+            a.record(stream)
+            run()
+            b.record(stream)
+        torch.cuda.synchronize()
+        us = np.array([1e3 * a.elapsed_time(b) for a, b in ev])
+        res["step_us"] = {"median": float(np.median(us)), "p10": float(np.percentile(us, 10)),
+                          "p90": float(np.percentile(us, 90)), "samples": per_step}
+    return res
+
+
+def measure_prune(mp, torch, dev, cfg, x, d, steps, warmup, subset=0, per_step=0, workload_key=None):
+    """One workload's map_prune: throughput, per-kernel times and rooflines.
+    Returns (result dict, output tensors)."""
+    t_off = x["t_off"]
+    mp.set_subset_tokens(subset)
+    ws = mp.PruneWorkspace(d["w"], d["V"], t_off, cfg.K)
+    out = mp.map_prune(d["w"], d["V"], d["pos_v"], d["T"], d["pos_t"], t_off, cfg.K, cfg.K0, cfg.tau, workspace=ws)
+
+    def step():
+        mp.map_prune(d["w"], d["V"], d["pos_v"], d["T"], d["pos_t"], t_off, cfg.K, cfg.K0, cfg.tau, out=out,
+                     workspace=ws)
+
+    tm = _time_steps(torch, dev, step, steps, warmup, per_step)
+    kern = _kernel_table(mp, torch, step, steps)
+    sumM = int(t_off[-1])
+    nc = subset_tokens(cfg, subset) if "subset" in kern else 0
+    work = algorithmic_work(cfg, sumM, gathered="gather" not in kern, nc=nc)
+    # (the full-path launches behind a subset do work only for images the
+    # subset cannot certify: they are never the dominant kernel)
+    dominant = max((k for k in kern if not k.endswith("_full")),
+                   key=lambda k: kern[k]["avg_us"] * kern[k]["launches_per_step"])
+    key = workload_key or cfg.name
+    roof = roofline(dominant, work, kern, cfg, key)
+    gemm = max((k for k in kern if work.get(k, ("",))[0] == "mfma"), key=lambda k: kern[k]["avg_us"])
+    roof_mfma = roofline(gemm, work, kern, cfg, key)
+    if dominant == "select":
+        # a chain of dependent picks: per-pick latency, not bandwidth, sets its time
+        greedy = cfg.K - (cfg.K0 if 0 < cfg.K0 <= R0_FACTOR_MAX else 0)
+        roof["note"] = (f"latency-bound: {greedy} sequential greedy picks per image, "
+                        f"{kern[dominant]['avg_us'] / max(greedy, 1):.2f} us per pick (all images at once)")
+    hbm = {}
+    for k in kern:
+        if work.get(k, ("",))[0] == "hbm" and k not in ("select", "select_r0", "subset"):
+            r = roofline(k, work, kern, cfg, key)
+            hbm[k] = {"achieved": r["achieved"], "frac": r["frac"], "avg_us": r["avg_us"],
+                      "algorithmic_per_launch": r["algorithmic_per_launch"]}
+    ms = tm["ms_per_step"]
+    res = {"value": cfg.B * 1000.0 / ms, "unit": "images/s", "us_per_image": 1000.0 * ms / cfg.B,
+           "dtype": cfg.dtype,
+           "workload": f"{cfg.name}: B={cfg.B} N={cfg.N} D={cfg.pred.D} M={sumM} K={cfg.K} K0={cfg.K0} "
+                       f"tau={cfg.tau} D_h={cfg.pred.D_h} d_p={cfg.pred.d_p} {cfg.dtype}",
+           "subset_tokens": nc, **tm, "kernels": kern, "dominant_kernel": dominant, "roofline": roof,
+           "roofline_mfma": roof_mfma, "hbm_stages": hbm}
+    mp.set_subset_tokens(0)
+    return res, out
+
+
+def train_flops(cfg, sumM):
+    """Algorithmic flops of one training step's matrix products: the forward
+    (layer 1, the folded weights, the projection) and the backward (X = dz^T h
+    and dL/da per branch, dW1, dW_K, dW2)."""
+    D, H, dp = cfg.pred.D, cfg.pred.D_h, cfg.pred.d_p
+    rows = cfg.B * cfg.N + sumM
+    fwd = 2.0 * rows * D * H + 4.0 * dp * H * H + 2.0 * rows * H * dp
+    bwd = 4.0 * dp * H * rows + 2.0 * H * D * rows + 8.0 * dp * H * H
+    return {"gemm_layer1": 2.0 * rows * D * H + 4.0 * dp * H * H, "gemm_proj_rope": 2.0 * rows * H * dp,
+            "gemm_train_x_da": 4.0 * dp * H * rows, "gemm_train_dw": 2.0 * H * D * rows + 8.0 * dp * H * H,
+            "total": fwd + bwd}
+
+
+def train_bench(mp, torch, dev, cfg, x, d, steps, warmup):
+    """One predictor training step (KL from a teacher to p_hat, forward and
+    backward) on the workload: steps/s, per-kernel times, and the matrix-core
+    roofline of the whole step and of its largest product."""
+    rng = np.random.default_rng(5)
+    p_star = torch.from_numpy(rng.dirichlet(np.ones(cfg.N), size=cfg.B).astype(np.float32)).to(dev)
+    ws = mp.TrainWorkspace(d["w"], d["V"], x["t_off"])
+    loss, p, g = mp.map_train_step(d["w"], d["V"], d["pos_v"], d["T"], d["pos_t"], x["t_off"], p_star, workspace=ws)
+
+    def step():
+        mp.map_train_step(d["w"], d["V"], d["pos_v"], d["T"], d["pos_t"], x["t_off"], p_star, grads=g, p_out=p,
+                          workspace=ws)
+
+    tm = _time_steps(torch, dev, step, steps, warmup)
+    kern = _kernel_table(mp, torch, step, steps)
+    fl = train_flops(cfg, int(x["t_off"][-1]))
+    ms = tm["ms_per_step"]
+    peak = PEAK_MFMA_BF16 if cfg.dtype == "bf16" else PEAK_MFMA_F32
+    big = max((k for k in kern if k in fl), key=lambda k: kern[k]["avg_us"])
+    ach = fl[big] / (kern[big]["avg_us"] * 1e-6) / 1e12
+    return {"metric": "predictor training steps/s", "value": 1000.0 / ms, "unit": "steps/s", **tm,
+            "workload": f"training step on {cfg.name}: B={cfg.B} N={cfg.N} D={cfg.pred.D} "
+                        f"M={int(x['t_off'][-1])} D_h={cfg.pred.D_h} d_p={cfg.pred.d_p} {cfg.dtype}, "
+                        f"Dirichlet(1) teacher",
+            "loss": float(loss.mean().item()), "kernels": kern,
+            "roofline_step": {"bound": "mfma", "achieved": fl["total"] / (ms * 1e-3) / 1e12, "peak": peak,
+                              "unit": "TFLOP/s", "frac": fl["total"] / (ms * 1e-3) / 1e12 / peak,
+                              "algorithmic_per_step": fl["total"], "algorithmic_unit": "flop"},
+            "roofline_mfma": {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
+                              "traffic": None, "kernel": big, "avg_us": kern[big]["avg_us"],
+                              "algorithmic_per_launch": fl[big], "algorithmic_unit": "flop"}}
+
+
+def decoder_layer_context(torch, dev, prune_us, steps=20, warmup=5):
+    """One random-init 7B-shaped decoder layer (d 4096, 32 heads x 128, SwiGLU
+    11008, RMSNorm, RoPE, causal attention; bf16) built from PyTorch-ROCm
+    ops, outside the library, timed over the unpruned (2944) and pruned
+    (224) sequences of the LLaVA-NeXT workload: the context for the pruning
+    stage's own time."""
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    d, H, hd, ff = 4096, 32, 128, 11008
+    g = torch.Generator(device=dev).manual_seed(0)
+
+    def W(o, i):
+        return (0.02 * torch.randn(o, i, generator=g, device=dev)).to(torch.bfloat16)
+
+    Wqkv, Wo, Wg, Wu, Wd = W(3 * d, d), W(d, d), W(ff, d), W(ff, d), W(d, ff)
+    n1 = torch.ones(d, device=dev, dtype=torch.bfloat16)
+    n2 = torch.ones(d, device=dev, dtype=torch.bfloat16)
+
+    def rms(x, wt):
+        xf = x.float()
+        return (xf * torch.rsqrt(xf.pow(2).mean(-1, keepdim=True) + 1e-6)).to(torch.bfloat16) * wt
+
+    def rope_tab(S):
+        inv = 1.0 / (10000.0 ** (torch.arange(0, hd, 2, device=dev, dtype=torch.float32) / hd))
+        ang = torch.arange(S, device=dev, dtype=torch.float32)[:, None] * inv[None, :]
+        return torch.cat([ang.cos()] * 2, 1).to(torch.bfloat16), torch.cat([ang.sin()] * 2, 1).to(torch.bfloat16)
+
+    def rot(x, c, s):
+        x1, x2 = x[..., :hd // 2], x[..., hd // 2:]
+        return x * c + torch.cat([-x2, x1], -1) * s
+
+    def layer(x, c, s, backend):
+        S = x.shape[0]
+        qkv = F.linear(rms(x, n1), Wqkv).view(S, 3, H, hd).permute(1, 2, 0, 3).contiguous()  # [3, H, S, hd]
+        q, k, v = rot(qkv[0], c, s)[None], rot(qkv[1], c, s)[None], qkv[2][None].contiguous()
+        with sdpa_kernel([backend]):
+            a = F.scaled_dot_product_attention(q.contiguous(), k.contiguous(), v, is_causal=True)
+        x = x + F.linear(a[0].transpose(0, 1).reshape(S, d), Wo)
+        h = rms(x, n2)
+        return x + F.linear(F.silu(F.linear(h, Wg)) * F.linear(h, Wu), Wd)
+
+    res = {"layer": "random-init 7B-shaped decoder layer: d=4096, 32 heads x 128, SwiGLU 11008, RMSNorm, RoPE, "
+                    "causal attention, bf16, batch 1 (PyTorch-ROCm ops, not this library)"}
+    backend = None
+    for b in (SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION):
+        try:
+            c, s = rope_tab(64)
+            layer(torch.zeros(64, d, device=dev, dtype=torch.bfloat16), c, s, b)
+            torch.cuda.synchronize()
+            backend = b
+            break
+        except RuntimeError:
+            continue
+    if backend is None:
+        res["error"] = "no fused SDPA backend available (the bf16 math path is not used here)"
+        return res
+    res["sdpa_backend"] = str(backend).split(".")[-1]
+    for S in (2944, 224):
+        x = (0.5 * torch.randn(S, d, generator=g, device=dev)).to(torch.bfloat16)
+        c, s = rope_tab(S)
+        tm = _time_steps(torch, dev, lambda: layer(x, c, s, backend), steps, warmup)
+        us = 1e3 * tm["ms_per_step"]
+        flops = 2.0 * S * d * (3 * d + d + 3 * ff) + 2.0 * S * S * d  # causal attention: half of 4 S^2 d
+        res[f"prefill_us_S{S}"] = us
+        res[f"achieved_tflops_S{S}"] = flops / (us * 1e-6) / 1e12
+    res["prune_us_per_image"] = prune_us
+    res["prune_over_layer_prefill_2944"] = prune_us / res["prefill_us_S2944"]
+    res["layer_prefill_2944_over_224"] = res["prefill_us_S2944"] / res["prefill_us_S224"]
+    return res
 
 
 def main():
@@ -284,6 +557,11 @@ def main():
     ap.add_argument("--workload", default="llava_next")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-teacher", action="store_true", help="skip the teacher-selection measurement")
+    ap.add_argument("--no-configs", action="store_true", help="skip the other workloads' lines")
+    ap.add_argument("--no-context", action="store_true", help="skip the decoder-layer context timing")
+    ap.add_argument("--no-train", action="store_true", help="skip the training-step measurement")
+    ap.add_argument("--percentile-steps", type=int, default=200,
+                    help="individually timed steps for the median / p10 / p90 (0: none)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run a plain float32 copy kernel over this many MiB (three times), "
                          "the reference dispatch for calibrating HBM byte counters")
@@ -299,23 +577,12 @@ def main():
     import torch
     import paper_2608_06411_amd as mp
     from workloads import get_config, make_inputs
+    from workloads.configs import SWEEP_K
 
     cfg = get_config(args.workload)
     x = make_inputs(cfg)
     dev = torch.device("cuda:0")
-
-    def to_dev(a):
-        if cfg.dtype == "bf16":
-            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
-        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-
-    names = ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")
-    w = mp.PredictorWeights(**{n: to_dev(x[n + "_store"]) for n in names}, rope_theta=cfg.pred.rope_theta)
-    V, T = to_dev(x["V_store"]), to_dev(x["T_store"])
-    pos_v, pos_t = torch.from_numpy(x["pos_v"]).to(dev), torch.from_numpy(x["pos_t"]).to(dev)
-    t_off = x["t_off"]
-    mp.set_subset_tokens(args.subset)
-    ws = mp.PruneWorkspace(w, V, t_off, cfg.K)
+    d = _upload(mp, torch, dev, x, cfg)
     if args.copy_calibration_mib > 0:
         src = torch.ones(args.copy_calibration_mib << 18, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
@@ -323,72 +590,57 @@ def main():
             torch.mul(src, 1.0, out=dst)  # reads and writes copy_calibration_mib MiB each
         torch.cuda.synchronize()
         del src, dst
-    out = mp.map_prune(w, V, pos_v, T, pos_t, t_off, cfg.K, cfg.K0, cfg.tau, workspace=ws)
 
-    def step():
-        mp.map_prune(w, V, pos_v, T, pos_t, t_off, cfg.K, cfg.K0, cfg.tau, out=out, workspace=ws)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream(dev)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    w0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    ms = e0.elapsed_time(e1) / args.steps
-
-    # Per-kernel durations, measured with HIP events on the launch stream
-    # (the library brackets each of its launches while timing is enabled).
-    mp.timing_reset()
-    mp.timing_enable(True)
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    per_kernel = mp.timing_read()
-    mp.timing_enable(False)
-    mp.timing_reset()
-
-    sumM = int(t_off[-1])
-    nc = subset_tokens(cfg, args.subset) if "subset" in per_kernel else 0
-    work = algorithmic_work(cfg, sumM, gathered="gather" not in per_kernel, nc=nc)
-    kern = {k: {"avg_us": 1e3 * v[0] / v[1], "launches_per_step": v[1] / args.steps}
-            for k, v in per_kernel.items()}
-    # (the full-path launches behind a subset do work only for images the
-    # subset cannot certify: they are never the dominant kernel)
-    dominant = max((k for k in kern if not k.endswith("_full")),
-                   key=lambda k: kern[k]["avg_us"] * kern[k]["launches_per_step"])
-    roof = roofline(dominant, work, kern, cfg, args.workload)
-    gemm = max((k for k in kern if work.get(k, ("",))[0] == "mfma"), key=lambda k: kern[k]["avg_us"])
-    roof_mfma = roofline(gemm, work, kern, cfg, args.workload)
-    if dominant == "select":
-        # a chain of dependent picks: per-pick latency, not bandwidth, sets its time
-        greedy = cfg.K - (cfg.K0 if 0 < cfg.K0 <= R0_FACTOR_MAX else 0)
-        roof["note"] = (f"latency-bound: {greedy} sequential greedy picks, "
-                        f"{kern[dominant]['avg_us'] / max(greedy, 1):.2f} us per pick")
-
+    head, out = measure_prune(mp, torch, dev, cfg, x, d, args.steps, args.warmup, subset=args.subset,
+                              per_step=args.percentile_steps, workload_key=args.workload)
+    sumM = int(x["t_off"][-1])
     line = {
-        "metric": METRIC, "value": cfg.B * 1000.0 / ms, "unit": "images/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
-        "us_per_image": 1000.0 * ms / cfg.B, "higher_is_better": True, "scaling": "weak",
+        "metric": METRIC, "value": head["value"], "unit": "images/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "us_per_image": head["us_per_image"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic (seeded mixture, random-init predictor)",
-        "config": {"workload": f"{cfg.name}: B={cfg.B} N={cfg.N} D={cfg.pred.D} M={sumM} K={cfg.K} "
-                               f"K0={cfg.K0} tau={cfg.tau} D_h={cfg.pred.D_h} d_p={cfg.pred.d_p} {cfg.dtype}",
-                   "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "single GPU",
-                   "subset_tokens": nc},
-        "wall_s_timed": wall, "kernels": kern, "dominant_kernel": dominant, "roofline": roof,
-        "roofline_mfma": roof_mfma,
+        "config": {"workload": head["workload"], "global_batch": cfg.B, "seq_len": cfg.N,
+                   "parallelism": "single GPU", "subset_tokens": head["subset_tokens"]},
+        "wall_s_timed": head["wall_s_timed"], "step_us": head.get("step_us"), "kernels": head["kernels"],
+        "dominant_kernel": head["dominant_kernel"], "roofline": head["roofline"],
+        "roofline_mfma": head["roofline_mfma"], "hbm_stages": head["hbm_stages"],
     }
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"], _ = cpu_baseline(x, cfg)
-    line["assembly"] = assembly_bench(args, mp, torch, dev, out, T, pos_t, t_off, cfg)
+    line["assembly"] = assembly_bench(args, mp, torch, dev, out, d["T"], d["pos_t"], x["t_off"], cfg)
+    if not args.no_train:
+        line["training_step"] = train_bench(mp, torch, dev, cfg, x, d, min(args.steps, 20), min(args.warmup, 5))
+    if not args.no_context:
+        line["decoder_layer_context"] = decoder_layer_context(torch, dev, head["us_per_image"])
     if not args.no_teacher:
         line["teacher_selection"] = teacher_bench(args, mp, torch, dev)
+    tiny_cfg, tiny_x = get_config("tiny"), None
+    if not args.no_configs:
+        # the other workloads: a few steps each (their inputs are generated here, so
+        # each costs seconds of host time), one object per workload and K
+        cfgs = [("tiny", tiny_cfg)] + [(f"sweep_K{k}", get_config("sweep", K=k, K0=k // 2)) for k in SWEEP_K] + \
+               [("multiframe", get_config("multiframe"))]
+        line["configs"] = {}
+        sweep_x = None
+        for key, c in cfgs:
+            if key.startswith("sweep"):
+                sweep_x = sweep_x if sweep_x is not None else make_inputs(c)
+                cx = dict(sweep_x, cfg=c)
+            else:
+                cx = make_inputs(c)
+            if key == "tiny":
+                tiny_x = cx
+            cd = _upload(mp, torch, dev, cx, c)
+            r, _ = measure_prune(mp, torch, dev, c, cx, cd, steps=10, warmup=3)
+            line["configs"][key] = r
+            del cd
+            torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        if tiny_x is None:
+            tiny_x = make_inputs(tiny_cfg)
+        line["cpu_baseline"] = cpu_baseline(x, cfg, tiny_x, tiny_cfg)
     print(json.dumps(line), flush=True)
+    # the library holds no HIP object after a timing reset: nothing is left
+    # for the runtime's teardown at exit
+    mp.timing_reset()
 
 
 if __name__ == "__main__":
