@@ -177,6 +177,26 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N,
                      float* p_out, int32_t* order_out, float* gain_out,
                      void* ws, size_t ws_bytes, void* stream);
 
+/* map_prune_assemble -- map_prune writing the language model's layer-0
+ * input directly (section "Inference-Time Token Pruning": the pruned visual
+ * tokens, in their original order with their positional indices, are
+ * combined with the question tokens before the first layer), so that no
+ * separate copy of the kept rows is needed.  Same computation and arguments
+ * as map_prune, except that the kept rows and positions go to
+ *   X_out     [B*K + sum_M][D] (dtype dt): image b's K kept rows from row
+ *             b*K + t_off[b], then its M_b question rows (copied from T)
+ *   pos_x_out [B*K + sum_M]    their positional indices (pos_v of the kept
+ *             tokens, then pos_t)
+ * -- the layout map_assemble produces.  idx_out [B][K] as for map_prune.
+ * X_out and T 16-byte aligned, D * sizeof(element) a multiple of 16.
+ * Workspace: map_prune_workspace. */
+map_status map_prune_assemble(const map_weights* w, map_dtype dt, int B, int N,
+                              const void* V, const int32_t* pos_v,
+                              const void* T, const int32_t* pos_t, const int32_t* t_off_host,
+                              map_select_params sp, int32_t* idx_out, void* X_out, int32_t* pos_x_out,
+                              float* p_out, int32_t* order_out, float* gain_out,
+                              void* ws, size_t ws_bytes, void* stream);
+
 /* map_prune_noalloc -- map_prune for callers that cannot allocate device
  * memory: code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc.  The same kernels, arguments and outputs as map_prune,

@@ -28,7 +28,7 @@ MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
 EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
-    "map_prune", "map_prune_noalloc", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
+    "map_prune", "map_prune_assemble", "map_prune_noalloc", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
     "map_train_workspace", "map_train_step",
     "map_selection_status", "map_set_select_images_per_launch", "map_timing_enable", "map_timing_read",
     "map_timing_reset",
@@ -64,6 +64,8 @@ _SIGS = {
     "map_select": (_I, [_I, _I, _P, _P, _P, map_select_params, _P, _P, _P, _P, _SZ, _P]),
     "map_prune": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
                        map_select_params, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "map_prune_assemble": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
+                                map_select_params, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "map_prune_noalloc": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P,
                                map_select_params, _P, _P, _P, _P, _P, _P, _P]),
     "map_assemble": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
@@ -370,6 +372,39 @@ def map_prune(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torc
                            _ptr(T), _ptr(pos_t), offs, sp, _ptr(o["idx"]), _ptr(o["V_out"]),
                            _ptr(o["pos_out"]), _ptr(o["p"]), _ptr(o["order"]), _ptr(o["gain"]),
                            _ptr(workspace.buf), workspace.nbytes, _stream(dev)), "map_prune")
+    return o
+
+
+def map_prune_assemble(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T: torch.Tensor,
+                       pos_t: torch.Tensor, t_off: Sequence[int], K: int, K0: int, tau: float = 1e-2,
+                       out: Optional[dict] = None, workspace: Optional[PruneWorkspace] = None):
+    """map_prune that writes the language model's layer-0 input directly:
+    returns a dict with X [B K + sum M, D] (each image's kept rows in original
+    order, then its question rows), pos_x, idx, p, order and gain."""
+    B, N, D, sumM, offs, dev = _check_features(w, V, pos_v, T, pos_t, t_off)
+    o = dict(out or {})
+    o.setdefault("idx", torch.empty(B, K, dtype=torch.int32, device=dev))
+    o.setdefault("X", torch.empty(B * K + sumM, D, dtype=V.dtype, device=dev))
+    o.setdefault("pos_x", torch.empty(B * K + sumM, dtype=torch.int32, device=dev))
+    o.setdefault("p", torch.empty(B, N, dtype=torch.float32, device=dev))
+    o.setdefault("order", torch.empty(B, K, dtype=torch.int32, device=dev))
+    o.setdefault("gain", torch.empty(B, K, dtype=torch.float32, device=dev))
+    for name, shape, dtype in (("idx", (B, K), torch.int32), ("X", (B * K + sumM, D), V.dtype),
+                               ("pos_x", (B * K + sumM,), torch.int32), ("p", (B, N), torch.float32),
+                               ("order", (B, K), torch.int32), ("gain", (B, K), torch.float32)):
+        _need(o[name], f"out[{name!r}]", shape, dtype, dev)
+    _on_gpu(V, "V")
+    if workspace is None:
+        workspace = PruneWorkspace(w, V, t_off, K)
+    need = lib().map_prune_workspace(_dtype_code(V), B, N, sumM, ctypes.byref(w.struct()), K)
+    if need == 0:
+        raise MapError(MAP_ERR_INVALID_ARG, "map_prune_workspace")
+    _need_ws(workspace.buf, need, dev)
+    ws_struct = w.struct()
+    _check(lib().map_prune_assemble(ctypes.byref(ws_struct), _dtype_code(V), B, N, _ptr(V), _ptr(pos_v), _ptr(T),
+                                    _ptr(pos_t), offs, map_select_params(K, K0, tau), _ptr(o["idx"]), _ptr(o["X"]),
+                                    _ptr(o["pos_x"]), _ptr(o["p"]), _ptr(o["order"]), _ptr(o["gain"]),
+                                    _ptr(workspace.buf), workspace.nbytes, _stream(dev)), "map_prune_assemble")
     return o
 
 

@@ -39,12 +39,22 @@ __global__ __launch_bounds__(256) void gather_kernel(const GatherArgs a) {
   __syncthreads();
   const int i = found;
   const bool ok = !aborted && i >= 0 && i < a.N;
+  const long long orow = (long long)b * K + a.out_off[b];  // the image's first output row
   if (threadIdx.x == 0) {
     a.idx_out[(long long)b * K + k] = ok ? i : -1;
-    a.pos_out[(long long)b * K + k] = ok ? a.pos_v[(long long)b * a.N + i] : -1;
+    a.pos_out[orow + k] = ok ? a.pos_v[(long long)b * a.N + i] : -1;
+  }
+  if (a.qT) {  // layer-0 assembly: question rows k, k + K, ... of the image after its kept rows
+    const int m0 = a.q_off[b], M = a.q_off[b + 1] - m0;
+    const uint4* qs = static_cast<const uint4*>(a.qT) + (long long)m0 * chunks;
+    uint4* qd = static_cast<uint4*>(a.V_out) + (orow + K) * chunks;
+    for (int m = k; m < M; m += K) {
+      for (int c = threadIdx.x; c < chunks; c += 256) qd[(long long)m * chunks + c] = qs[(long long)m * chunks + c];
+      if (threadIdx.x == 0) a.pos_out[orow + K + m] = a.qpos[m0 + m];
+    }
   }
   const uint4* src = static_cast<const uint4*>(a.V) + ((long long)b * a.N + (ok ? i : 0)) * chunks;
-  uint4* dst = static_cast<uint4*>(a.V_out) + ((long long)b * a.K + k) * chunks;
+  uint4* dst = static_cast<uint4*>(a.V_out) + (orow + k) * chunks;
   constexpr int U = 4;  // 16-byte pieces per thread per batch (rows up to 16 KiB in one batch)
   for (int c0 = threadIdx.x; c0 < chunks; c0 += U * 256) {
     uint4 v[U];

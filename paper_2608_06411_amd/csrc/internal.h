@@ -214,9 +214,16 @@ struct SelectArgs {
   // (gV null: none; launch_select clears it when the order does not fit in LDS)
   const void* gV;         // [B][N] rows of row_bytes (the visual tokens)
   const int32_t* gpos;    // [B][N] positions
-  void* gV_out;           // [B][K] rows of row_bytes
-  int32_t* gpos_out;      // [B][K]
+  void* gV_out;           // rows of row_bytes: image b's kept row k at row b K + out_off[b] + k
+  int32_t* gpos_out;      // positions, indexed like gV_out's rows
   int row_bytes;
+  // layer-0 assembly (qT non-null): image b's question rows follow its kept
+  // rows, from row b K + out_off[b] + K on (out_off = q_off: the language
+  // model's input, packed)
+  const void* qT;         // [sum M] question rows of row_bytes
+  const int32_t* qpos;    // [sum M]
+  int out_off[MAP_MAX_BATCH];
+  int q_off[MAP_MAX_BATCH + 1];
   // map_prune on a candidate subset: N is the subset's size, token k of the
   // subset is token jmap[b][k] of the image (Ng tokens in gV and gpos)
   const int32_t* jmap;    // [B][N] ascending (null: no subset)
@@ -245,9 +252,14 @@ struct GatherArgs {
   const int32_t* order;    // [B][K] selection order (distinct indices)
   const int32_t* err;      // selection error flag (set: every index is -1)
   int32_t* idx_out;        // [B][K] kept indices, ascending (written here)
-  void* V_out;             // [B][K][D]
-  int32_t* pos_out;        // [B][K]
+  void* V_out;             // image b's kept row k at row b K + out_off[b] + k
+  int32_t* pos_out;        // indexed like V_out's rows
   int B, N, K, row_bytes;
+  // layer-0 assembly (qT non-null), as in SelectArgs
+  const void* qT;
+  const int32_t* qpos;
+  int out_off[MAP_MAX_BATCH];
+  int q_off[MAP_MAX_BATCH + 1];
 };
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 

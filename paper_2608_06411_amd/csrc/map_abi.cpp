@@ -405,6 +405,10 @@ hipError_t enqueue_select(int B, int N, const float* p, const float* S, const fl
     a.gV_out = ga->V_out;
     a.gpos_out = ga->pos_out;
     a.row_bytes = ga->row_bytes;
+    a.qT = ga->qT;
+    a.qpos = ga->qpos;
+    memcpy(a.out_off, ga->out_off, sizeof(a.out_off));
+    memcpy(a.q_off, ga->q_off, sizeof(a.q_off));
   }
   hipError_t e = fused ? hipSuccess : launch_select_clear(a, st);
   if (e != hipSuccess) return e;
@@ -670,13 +674,48 @@ LaunchEvents timing_events(const char* name) {
 
 }  // namespace mapk
 
+// The language model's layer-0 input as map_prune's destination (section
+// "Inference-Time Token Pruning"): each image's kept rows, then its
+// question rows, packed (image b from row b K + t_off[b]).
+struct Layer0 {
+  const void* T;
+  const int32_t* pos_t;
+  const int32_t* t_off;  // host
+};
+
+GatherArgs gather_args(const void* V, const int32_t* pos_v, const int32_t* order, const int32_t* err,
+                       int32_t* idx_out, void* V_out, int32_t* pos_out, int B, int N, int K, int row_bytes,
+                       const Layer0* l0) {
+  GatherArgs ga;
+  memset(&ga, 0, sizeof(ga));
+  ga.V = V;
+  ga.pos_v = pos_v;
+  ga.order = order;
+  ga.err = err;
+  ga.idx_out = idx_out;
+  ga.V_out = V_out;
+  ga.pos_out = pos_out;
+  ga.B = B;
+  ga.N = N;
+  ga.K = K;
+  ga.row_bytes = row_bytes;
+  if (l0) {
+    ga.qT = l0->T;
+    ga.qpos = l0->pos_t;
+    for (int b = 0; b < B; ++b) ga.out_off[b] = l0->t_off[b];
+    for (int b = 0; b <= B; ++b) ga.q_off[b] = l0->t_off[b];
+  }
+  return ga;
+}
+
 // map_prune on a candidate subset (see subset.hip), with the full
 // selection behind it for the images whose picks it cannot certify.
 map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, const void* V, const int32_t* pos_v,
                            const void* T, const int32_t* pos_t, const int32_t* t_off_host,
                            const map_select_params& sp, int32_t* idx_out, void* V_out, int32_t* pos_out, float* p,
                            int32_t* order_out, float* gain_out, const ScoreWs& s, const SelectWs& sw, float* S,
-                           float* norms, float* ninv, const SubsetWs& u, int nc, hipStream_t st) {
+                           float* norms, float* ninv, const SubsetWs& u, int nc, hipStream_t st,
+                           const Layer0* l0) {
   hipError_t e =
       enqueue_score(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, nullptr, norms, ninv, st, sw.bar, sw.err, true);
   if (e != hipSuccess) return MAP_ERR_HIP;
@@ -718,18 +757,8 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   if ((e = launch_gram_reduce(g.p[0], u.SJ, nc, u.ninvJ, st)) != hipSuccess) return MAP_ERR_HIP;
 
   int32_t* order_img = order_out ? order_out : u.order_img;
-  GatherArgs ga;
-  ga.V = V;
-  ga.pos_v = pos_v;
-  ga.order = order_img;
-  ga.err = sw.err;
-  ga.idx_out = idx_out;
-  ga.V_out = V_out;
-  ga.pos_out = pos_out;
-  ga.B = B;
-  ga.N = N;
-  ga.K = sp.K;
-  ga.row_bytes = static_cast<int>(w.D * elem_size(dt));
+  const GatherArgs ga = gather_args(V, pos_v, order_img, sw.err, idx_out, V_out, pos_out, B, N, sp.K,
+                                    static_cast<int>(w.D * elem_size(dt)), l0);
   SubsetSel sub;
   memset(&sub, 0, sizeof(sub));
   sub.jmap = u.jmap;
@@ -876,11 +905,12 @@ map_status map_select(int B, int N, const float* p, const float* S, const float*
                                    static_cast<hipStream_t>(stream)));
 }
 
-map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const void* V,
-                     const int32_t* pos_v, const void* T, const int32_t* pos_t,
-                     const int32_t* t_off_host, map_select_params sp, int32_t* idx_out, void* V_out,
-                     int32_t* pos_out, float* p_out, int32_t* order_out, float* gain_out, void* ws,
-                     size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+static map_status prune_impl(const map_weights* w, map_dtype dt, int B, int N, const void* V, const int32_t* pos_v,
+                             const void* T, const int32_t* pos_t, const int32_t* t_off_host, map_select_params sp,
+                             int32_t* idx_out, void* V_out, int32_t* pos_out, float* p_out, int32_t* order_out,
+                             float* gain_out, void* ws, size_t ws_bytes, void* stream, bool layer0) {
   if (!valid_dtype(dt) || !valid_bn(B, N) || !valid_weights(w) || !V || !pos_v || !T || !pos_t ||
       !idx_out || !V_out || !pos_out || !valid_offsets(t_off_host, B) || !valid_select(sp, N))
     return MAP_ERR_INVALID_ARG;
@@ -898,29 +928,44 @@ map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const voi
   float* ninv = c.take<float>((size_t)B * N);
   float* p = p_out ? p_out : c.take<float>((size_t)B * N);
   const int nc = subset_size(dt, N, w->D, sp);
+  Layer0 l0{T, pos_t, t_off_host};
+  const Layer0* l0p = layer0 ? &l0 : nullptr;
   if (nc > 0) return prune_on_subset(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, sp, idx_out, V_out, pos_out,
                                      p, order_out, gain_out, s, sw, S, norms, ninv, carve_subset(c, B, sp.K, nc, w->D),
-                                     nc, st);
+                                     nc, st, l0p);
   const GemmProblem g = gram(V, B, N, w->D, S, ninv);
   hipError_t e =
       enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, &g, norms, ninv, st, sw.bar, sw.err);
   if (e != hipSuccess) return MAP_ERR_HIP;
-  GatherArgs ga;
-  ga.V = V;
-  ga.pos_v = pos_v;
-  ga.order = order_out ? order_out : sw.order;
-  ga.err = sw.err;
-  ga.idx_out = idx_out;
-  ga.V_out = V_out;
-  ga.pos_out = pos_out;
-  ga.B = B;
-  ga.N = N;
-  ga.K = sp.K;
-  ga.row_bytes = static_cast<int>(w->D * elem_size(dt));
+  const GatherArgs ga = gather_args(V, pos_v, order_out ? order_out : sw.order, sw.err, idx_out, V_out, pos_out, B,
+                                    N, sp.K, static_cast<int>(w->D * elem_size(dt)), l0p);
   bool gathered = false;
   e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_out, gain_out, sw, st, true, &ga, &gathered);
   if (e != hipSuccess) return MAP_ERR_HIP;
   return gathered ? MAP_OK : hip_status(launch_gather(ga, st));  // else its own kernel
+}
+
+extern "C" {
+
+map_status map_prune(const map_weights* w, map_dtype dt, int B, int N, const void* V, const int32_t* pos_v,
+                     const void* T, const int32_t* pos_t, const int32_t* t_off_host, map_select_params sp,
+                     int32_t* idx_out, void* V_out, int32_t* pos_out, float* p_out, int32_t* order_out,
+                     float* gain_out, void* ws, size_t ws_bytes, void* stream) {
+  return prune_impl(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, sp, idx_out, V_out, pos_out, p_out, order_out,
+                    gain_out, ws, ws_bytes, stream, false);
+}
+
+map_status map_prune_assemble(const map_weights* w, map_dtype dt, int B, int N, const void* V,
+                              const int32_t* pos_v, const void* T, const int32_t* pos_t,
+                              const int32_t* t_off_host, map_select_params sp, int32_t* idx_out, void* X_out,
+                              int32_t* pos_x_out, float* p_out, int32_t* order_out, float* gain_out, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (dt == MAP_BF16 || dt == MAP_F32) {  // the question rows are copied 16 bytes at a time
+    if (w && ((w->D * elem_size(dt)) & 15)) return MAP_ERR_INVALID_ARG;
+    if (((reinterpret_cast<uintptr_t>(T) | reinterpret_cast<uintptr_t>(X_out)) & 15) != 0) return MAP_ERR_INVALID_ARG;
+  }
+  return prune_impl(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, sp, idx_out, X_out, pos_x_out, p_out, order_out,
+                    gain_out, ws, ws_bytes, stream, true);
 }
 
 }  // extern "C"

@@ -852,15 +852,26 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
       __syncthreads();
     }
+    const long long orow = (long long)b * K + a.out_off[b];  // the image's first output row
     for (int sI = tid; sI < nshare; sI += NT) {
       const int k = w + G * sI, v = bad ? -1 : share[sI];
       a.idx_out[(long long)b * K + k] = v;
-      a.gpos_out[(long long)b * K + k] = bad ? -1 : a.gpos[(long long)b * a.Ng + v];
+      a.gpos_out[orow + k] = bad ? -1 : a.gpos[(long long)b * a.Ng + v];
     }
     // rows, 16 bytes per piece; every load of a thread before its first store
     const int chunks = a.row_bytes >> 4, total = nshare * chunks;
     const uint4* src = static_cast<const uint4*>(a.gV) + (long long)b * a.Ng * chunks;
-    uint4* dst = static_cast<uint4*>(a.gV_out) + (long long)b * K * chunks;
+    uint4* dst = static_cast<uint4*>(a.gV_out) + orow * chunks;
+    if (a.qT) {  // layer-0 assembly: question rows w, w + G, ... of the image after its kept rows
+      const int m0 = a.q_off[b], M = a.q_off[b + 1] - m0, nq = w < M ? (M - w + G - 1) / G : 0;
+      const uint4* qs = static_cast<const uint4*>(a.qT) + (long long)m0 * chunks;
+      uint4* qd = dst + (long long)K * chunks;
+      for (int e = tid; e < nq * chunks; e += NT) {
+        const int j = e / chunks, c = e - j * chunks, m = w + G * j;
+        qd[(long long)m * chunks + c] = qs[(long long)m * chunks + c];
+      }
+      for (int j = tid; j < nq; j += NT) a.gpos_out[orow + K + w + G * j] = a.qpos[m0 + w + G * j];
+    }
     constexpr int GU = 4;
     for (int e0 = tid; e0 < total; e0 += GU * NT) {
       uint4 v[GU];
