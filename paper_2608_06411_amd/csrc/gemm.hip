@@ -181,31 +181,46 @@ __device__ __forceinline__ void epilogue(const GemmProblem& P, int bt, int tm, i
                                          float* tile_lo, float* tile_hi, int tid, int lane, int wm, int wn) {
   const int M = P.M, N = P.N;
   const int m0 = tm * BM, n0 = tn * BN;
-  if (P.epi == EPI_F32 || P.epi == EPI_GELU2 || P.epi == EPI_MUL) {
+  if (epi_direct(P.epi)) {
     const int e = P.epi;
     const T* __restrict__ bias = static_cast<const T*>(P.bias);
+    const long long base = bt * P.strideC;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int col = n0 + wn * 64 + j * 32 + acc_col(lane);
       if (col >= N) continue;
       const float bv = (e == EPI_GELU2 && bias) ? to_f32<T>(bias[col]) : 0.0f;
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < 2; ++i) {
+        // the factor or residual of all 16 entries first (clamped rows), so
+        // that no load waits behind this lane's stores
+        float f[16];
+        if (e == EPI_MUL || e == EPI_RESID) {
+          const T* __restrict__ aux = static_cast<const T*>(P.aux) + base;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = min(m0 + wm * 64 + i * 32 + acc_row(r, lane), M - 1);
+            f[r] = to_f32<T>(aux[(long long)row * P.ldc + col]);
+          }
+        }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int row = m0 + wm * 64 + i * 32 + acc_row(r, lane);
           if (row >= M) continue;
-          const long long at = bt * P.strideC + (long long)row * P.ldc + col;
+          const long long at = base + (long long)row * P.ldc + col;
           const float v = acc[i][j][r] + bv;
           if (e == EPI_F32) {
             static_cast<float*>(P.C)[at] = v;
           } else if (e == EPI_GELU2) {
             static_cast<T*>(P.C)[at] = from_f32<T>(gelu_erf(v));
             static_cast<T*>(P.aux)[at] = from_f32<T>(gelu_erf_grad(v));
+          } else if (e == EPI_MUL) {
+            static_cast<T*>(P.C)[at] = from_f32<T>(v * f[r]);
           } else {
-            static_cast<T*>(P.C)[at] = from_f32<T>(v * to_f32<T>(static_cast<const T*>(P.aux)[at]));
+            static_cast<T*>(P.C)[at] = from_f32<T>(v + f[r]);
           }
         }
+      }
     }
   } else if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS) {
     T* __restrict__ C = static_cast<T*>(P.C) + bt * P.strideC;
@@ -934,7 +949,7 @@ bool gemm_direct_loads(map_dtype dt, const GemmBatch& g) {
   bool dma = true;  // every problem meets the direct-load requirements
   for (int i = 0; i < g.count; ++i) {
     const GemmProblem& p = g.p[i];
-    dma = dma && p.epi <= EPI_PARTIAL && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+    dma = dma && (p.epi <= EPI_PARTIAL || epi_direct(p.epi)) && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
           (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
           p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
           (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));
@@ -948,7 +963,7 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
     bool dma = true;  // every problem meets the direct-load requirements
     for (int i = 0; i < g.count; ++i) {
       const GemmProblem& p = g.p[i];
-      dma = dma && p.epi <= EPI_PARTIAL && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+      dma = dma && (p.epi <= EPI_PARTIAL || epi_direct(p.epi)) && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
             (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
             p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
             (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));

@@ -75,11 +75,14 @@ enum EpiMode : int {
   EPI_COSINE = 2,     // S[m][n] = acc * rs[m] * rs[n] (float32), mirrored; A == B
   EPI_ROPE = 3,       // out[m][:] = RoPE(acc[m][:] + rope_bias) (float32) with the row's cos/sin
   EPI_PARTIAL = 4,    // the raw float32 accumulators of a K range, for gram_reduce (bf16 direct-load kernel)
-  // the training step's products (register-staged kernel only):
+  // the training step's and the decoder layer's products:
   EPI_F32 = 5,        // C[m][n] = acc, stored as float32
   EPI_GELU2 = 6,      // v = acc + bias[n]: C[m][n] = GELU(v) and aux[m][n] = GELU'(v), both stored as T
   EPI_MUL = 7,        // C[m][n] = acc * aux[m][n] (aux of type T, leading dimension ldc), stored as T
+  EPI_RESID = 8,      // C[m][n] = acc + aux[m][n] (a residual connection), stored as T
 };
+// Epilogues written lane by lane in registers (no staging): every kernel runs them.
+__host__ __device__ inline bool epi_direct(int e) { return e >= EPI_F32 && e <= EPI_RESID; }
 
 struct GemmProblem {
   const void* A;
@@ -100,7 +103,8 @@ struct GemmProblem {
   long long mapStride;
   int ksplit;              // EPI_PARTIAL: K ranges per tile (K / ksplit each, a multiple of 256)
   const int32_t* run_if;   // [batch] batch items whose flag is 0 are skipped (null: none)
-  void* aux;               // EPI_GELU2: second output; EPI_MUL: the factor (both [M][ldc] of type T)
+  void* aux;               // EPI_GELU2: second output; EPI_MUL, EPI_RESID: the factor or the residual
+                           // (each [M][ldc] of type T)
   // filled by the host helper
   int tiles_m, tiles_n, tiles_tri, tiles_per_batch, tile_begin;
 };
@@ -292,15 +296,25 @@ struct TrainArgs {
   const float2* cs_v;      // [B N][d_p / 2] RoPE (cos, sin)
   const float2* cs_t;      // [sum_M][d_p / 2]
   float* dq_part;          // [nch][sum_M][d_p] token-chunk partials of dL/dq
-  void* dk_rows;           // [B N][d_p] dL/dz of the keys, element type of the call
+  void* dk_rows;           // [B N][kdp] dL/dz of the keys, element type of the call (zero past d_p)
   void* dk_cols;           // [d_p][ldv] the same, tokens contiguous (zero padded)
-  void* dq_rows;           // [sum_M][d_p]
+  void* dq_rows;           // [sum_M][kdp]
   void* dq_cols;           // [d_p][ldt]
-  int B, N, d_p, nblk, nch, ldv, ldt;
+  int B, N, d_p, nblk, nch, ldv, ldt, kdp;
   float inv_B, scale;      // 1 / B, 1 / sqrt(d_p)
   int t_off[MAP_MAX_BATCH + 1];
 };
 hipError_t launch_train_grads(map_dtype dt, const TrainArgs& a, hipStream_t s);
+
+// X = dz^T h per branch from token-chunk partials (see train.hip).
+struct XReduceArgs {
+  const float* part[2];  // [nc][d_p][D_h]
+  void* X[2];            // [d_p][D_h]
+  void* XT[2];           // [D_h][kdp]
+  int nc[2];
+  int d_p, D_h, kdp;
+};
+hipError_t launch_x_reduce(map_dtype dt, const XReduceArgs& r, hipStream_t s);
 
 // dst[c][r] = src[r][c] (r < rows, c < cols), zero for rows <= r < ldd.
 struct TransposeJob {

@@ -441,44 +441,51 @@ struct TrainWs {
   float* dq_part;                 // [nch][sum_M][d_p]
   void *dk_rows, *dk_cols, *dq_rows, *dq_cols;
   void *VT, *TT, *HvT, *HtT;      // [D][ldv], [D][ldt], [D_h][ldv], [D_h][ldt]
-  void *WKT, *WQT, *WcvT, *WctT;  // [D_h][d_p]
-  void *Xv, *Xt, *XvT, *XtT;      // [d_p][D_h], [D_h][d_p]
+  void *WKT, *WQT, *WcvT, *WctT;  // [D_h][kdp]
+  void *Xv, *Xt, *XvT, *XtT;      // [d_p][D_h], [D_h][kdp]
+  float *Xpv, *Xpt;               // [ldv / 256][d_p][D_h], [ldt / 256][d_p][D_h] token-chunk partials of X
   void *dAv, *dAt, *dAvT, *dAtT;  // [B N][D_h], [sum_M][D_h], [D_h][ldv], [D_h][ldt]
   float *csum_v, *csum_t;         // [d_p]
   float* p;                       // [B][N]
-  int ldv, ldt, nch;
+  int ldv, ldt, nch, kdp;  // kdp: d_p padded with zeros to 256, the products over d_p on the direct-load GEMM
 };
 
-int pad8(int n) { return (n + 7) & ~7; }
+// Token counts of the token-contiguous operands, padded with zeros to a
+// multiple of 256: the reductions over tokens then run on the direct-load GEMM.
+int pad256(int n) { return (n + 255) & ~255; }
 
 TrainWs carve_train(Carver& c, map_dtype dt, int B, int N, int sumM, const map_weights& w) {
   TrainWs t;
   const size_t es = elem_size(dt), BN = (size_t)B * N, Dh = w.D_h, dp = w.d_p;
-  t.ldv = pad8(B * N);
-  t.ldt = pad8(sumM);
-  t.nch = (N + 255) / 256;
+  t.ldv = pad256(B * N);
+  t.ldt = pad256(sumM);
+  t.nch = (N + 63) / 64;
+  t.kdp = pad256(w.d_p);
+  const size_t kdp = t.kdp;
   t.status = carve_status(c);
   t.s = carve_score(c, dt, B, N, sumM, w);
   t.gp_v = c.take_bytes(BN * Dh * es);
   t.gp_t = c.take_bytes((size_t)sumM * Dh * es);
   t.G = c.take<float>((size_t)sumM * N);
   t.dq_part = c.take<float>((size_t)t.nch * sumM * dp);
-  t.dk_rows = c.take_bytes(BN * dp * es);
+  t.dk_rows = c.take_bytes(BN * kdp * es);
   t.dk_cols = c.take_bytes(dp * t.ldv * es);
-  t.dq_rows = c.take_bytes((size_t)sumM * dp * es);
+  t.dq_rows = c.take_bytes((size_t)sumM * kdp * es);
   t.dq_cols = c.take_bytes(dp * t.ldt * es);
   t.VT = c.take_bytes((size_t)w.D * t.ldv * es);
   t.TT = c.take_bytes((size_t)w.D * t.ldt * es);
   t.HvT = c.take_bytes(Dh * t.ldv * es);
   t.HtT = c.take_bytes(Dh * t.ldt * es);
-  t.WKT = c.take_bytes(Dh * dp * es);
-  t.WQT = c.take_bytes(Dh * dp * es);
-  t.WcvT = c.take_bytes(Dh * dp * es);
-  t.WctT = c.take_bytes(Dh * dp * es);
+  t.WKT = c.take_bytes(Dh * kdp * es);
+  t.WQT = c.take_bytes(Dh * kdp * es);
+  t.WcvT = c.take_bytes(Dh * kdp * es);
+  t.WctT = c.take_bytes(Dh * kdp * es);
   t.Xv = c.take_bytes(dp * Dh * es);
   t.Xt = c.take_bytes(dp * Dh * es);
-  t.XvT = c.take_bytes(Dh * dp * es);
-  t.XtT = c.take_bytes(Dh * dp * es);
+  t.XvT = c.take_bytes(Dh * kdp * es);
+  t.XtT = c.take_bytes(Dh * kdp * es);
+  t.Xpv = c.take<float>((size_t)(t.ldv / 256) * dp * Dh);
+  t.Xpt = c.take<float>((size_t)(t.ldt / 256) * dp * Dh);
   t.dAv = c.take_bytes(BN * Dh * es);
   t.dAt = c.take_bytes((size_t)sumM * Dh * es);
   t.dAvT = c.take_bytes(Dh * t.ldv * es);
@@ -547,6 +554,7 @@ hipError_t enqueue_train(const map_weights& w, map_dtype dt, int B, int N, const
   a.nch = t.nch;
   a.ldv = t.ldv;
   a.ldt = t.ldt;
+  a.kdp = t.kdp;
   a.inv_B = 1.0f / static_cast<float>(B);
   a.scale = 1.0f / sqrtf(static_cast<float>(dp));
   for (int b = 0; b <= B; ++b) a.t_off[b] = t_off[b];
@@ -558,30 +566,53 @@ hipError_t enqueue_train(const map_weights& w, map_dtype dt, int B, int N, const
   ta.job[ta.count++] = tjob(T, t.TT, sumM, w.D, t.ldt);
   ta.job[ta.count++] = tjob(t.s.h1_v, t.HvT, BN, Dh, t.ldv);
   ta.job[ta.count++] = tjob(t.s.h1_t, t.HtT, sumM, Dh, t.ldt);
-  ta.job[ta.count++] = tjob(w.w_k, t.WKT, dp, Dh, dp);
-  ta.job[ta.count++] = tjob(w.w_q, t.WQT, dp, Dh, dp);
-  ta.job[ta.count++] = tjob(t.s.wc_v, t.WcvT, dp, Dh, dp);
-  ta.job[ta.count++] = tjob(t.s.wc_t, t.WctT, dp, Dh, dp);
+  ta.job[ta.count++] = tjob(w.w_k, t.WKT, dp, Dh, t.kdp);
+  ta.job[ta.count++] = tjob(w.w_q, t.WQT, dp, Dh, t.kdp);
+  ta.job[ta.count++] = tjob(t.s.wc_v, t.WcvT, dp, Dh, t.kdp);
+  ta.job[ta.count++] = tjob(t.s.wc_t, t.WctT, dp, Dh, t.kdp);
   transpose_finalize(ta);
   if ((e = launch_transpose(dt, ta, "transpose_in", st)) != hipSuccess) return e;
-  // X = dz^T h (per branch) and dL/da = (dz (W W2)) * GELU'(a)
+  // X = dz^T h per branch: a reduction over tokens, in chunks of 256 tokens
+  // (batch items of one launch, float32 partials), then their ordered sum
   GemmBatch g1;
   memset(&g1, 0, sizeof(g1));
-  g1.p[0] = linear(t.dk_cols, dp, t.HvT, nullptr, t.Xv, Dh, t.ldv, EPI_BIAS);
-  g1.p[1] = linear(t.dq_cols, dp, t.HtT, nullptr, t.Xt, Dh, t.ldt, EPI_BIAS);
-  g1.p[2] = linear(t.dk_rows, BN, t.WcvT, nullptr, t.dAv, Dh, dp, EPI_MUL);
-  g1.p[2].aux = t.gp_v;
-  g1.p[3] = linear(t.dq_rows, sumM, t.WctT, nullptr, t.dAt, Dh, dp, EPI_MUL);
-  g1.p[3].aux = t.gp_t;
-  g1.count = 4;
+  const void* xa[2] = {t.dk_cols, t.dq_cols};
+  const void* xb[2] = {t.HvT, t.HtT};
+  float* xp[2] = {t.Xpv, t.Xpt};
+  const int xld[2] = {t.ldv, t.ldt};
+  for (int br = 0; br < 2; ++br) {
+    GemmProblem& q = g1.p[g1.count++];
+    q = linear(xa[br], dp, xb[br], nullptr, xp[br], Dh, 256, EPI_F32);
+    q.lda = q.ldb = xld[br];
+    q.batch = xld[br] / 256;
+    q.strideA = q.strideB = 256;
+    q.strideC = (long long)dp * Dh;
+  }
+  // and in the same launch dL/da = (dz (W W2)) * GELU'(a), over d_p padded to kdp
+  g1.p[g1.count] = linear(t.dk_rows, BN, t.WcvT, nullptr, t.dAv, Dh, t.kdp, EPI_MUL);
+  g1.p[g1.count++].aux = t.gp_v;
+  g1.p[g1.count] = linear(t.dq_rows, sumM, t.WctT, nullptr, t.dAt, Dh, t.kdp, EPI_MUL);
+  g1.p[g1.count++].aux = t.gp_t;
   gemm_finalize(g1);
   if ((e = launch_gemm(dt, g1, "gemm_train_x_da", st)) != hipSuccess) return e;
+  XReduceArgs xr;
+  memset(&xr, 0, sizeof(xr));
+  xr.part[0] = t.Xpv;
+  xr.part[1] = t.Xpt;
+  xr.X[0] = t.Xv;
+  xr.X[1] = t.Xt;
+  xr.XT[0] = t.XvT;
+  xr.XT[1] = t.XtT;
+  xr.nc[0] = t.ldv / 256;
+  xr.nc[1] = t.ldt / 256;
+  xr.d_p = dp;
+  xr.D_h = Dh;
+  xr.kdp = t.kdp;
+  if ((e = launch_x_reduce(dt, xr, st)) != hipSuccess) return e;
   TransposeBatch tb;
   memset(&tb, 0, sizeof(tb));
   tb.job[tb.count++] = tjob(t.dAv, t.dAvT, BN, Dh, t.ldv);
   tb.job[tb.count++] = tjob(t.dAt, t.dAtT, sumM, Dh, t.ldt);
-  tb.job[tb.count++] = tjob(t.Xv, t.XvT, dp, Dh, dp);
-  tb.job[tb.count++] = tjob(t.Xt, t.XtT, dp, Dh, dp);
   transpose_finalize(tb);
   if ((e = launch_transpose(dt, tb, "transpose_da", st)) != hipSuccess) return e;
   // the weight gradients (float32):
@@ -592,10 +623,11 @@ hipError_t enqueue_train(const map_weights& w, map_dtype dt, int B, int N, const
   g2.p[1] = linear(t.dAtT, Dh, t.TT, nullptr, g.w1_t, w.D, t.ldt, EPI_F32);
   g2.p[2] = linear(t.Xv, dp, w.w2_v, nullptr, g.w_k, Dh, Dh, EPI_F32);
   g2.p[3] = linear(t.Xt, dp, w.w2_t, nullptr, g.w_q, Dh, Dh, EPI_F32);
-  g2.p[4] = linear(t.WKT, Dh, t.XvT, nullptr, g.w2_v, Dh, dp, EPI_F32);
-  g2.p[5] = linear(t.WQT, Dh, t.XtT, nullptr, g.w2_t, Dh, dp, EPI_F32);
+  g2.p[4] = linear(t.WKT, Dh, t.XvT, nullptr, g.w2_v, Dh, t.kdp, EPI_F32);
+  g2.p[5] = linear(t.WQT, Dh, t.XtT, nullptr, g.w2_t, Dh, t.kdp, EPI_F32);
   g2.count = 6;
   gemm_finalize(g2);
+  g2.first_tiles = g2.p[1].tile_begin;  // dW1_v's long tiles first, spread over every XCD
   if ((e = launch_gemm(dt, g2, "gemm_train_dw", st)) != hipSuccess) return e;
   // bias gradients and the sums of dz over tokens
   RowsumBatch rs;

@@ -97,14 +97,40 @@ __global__ __launch_bounds__(NT) void kl_grad_kernel(const TrainArgs a) {
   const float* lrow = a.logits + (long long)m * N;
   const float* ps = a.p_star + (long long)b * N;
   const float* ph = a.p_hat + (long long)b * N;
-  float s = 0.0f;
-  for (int n = tid; n < N; n += NT) {
-    const float P = __expf(lrow[n] - mx) * inv_sum;
-    s += P * kl_dp(ps[n], ph[n]);
-  }
-  s = block_sum_f(s, redf) * a.inv_B;
   const float c = a.scale / static_cast<float>(M);
   float* grow = a.G + (long long)m * N;
+  // the row in chunks of 16 values per thread held in registers between the
+  // row sum and the write (rows up to 4096 tokens in one chunk)
+  constexpr int RV = 16;
+  for (int n0 = 0; n0 < N; n0 += RV * NT) {
+    float P[RV], g[RV];
+#pragma unroll
+    for (int u = 0; u < RV; ++u) {
+      const int n = min(n0 + u * NT + tid, N - 1);
+      P[u] = lrow[n];
+      g[u] = kl_dp(ps[n], ph[n]);
+    }
+    float s = 0.0f;
+#pragma unroll
+    for (int u = 0; u < RV; ++u) {
+      const bool ok = n0 + u * NT + tid < N;
+      P[u] = ok ? __expf(P[u] - mx) * inv_sum : 0.0f;
+      s += P[u] * g[u];
+    }
+    if (n0 == 0 && n0 + RV * NT >= N) {  // the whole row is in registers: one pass
+      s = block_sum_f(s, redf) * a.inv_B;
+#pragma unroll
+      for (int u = 0; u < RV; ++u) {
+        const int n = n0 + u * NT + tid;
+        if (n < N) grow[n] = c * P[u] * (g[u] * a.inv_B - s);
+      }
+      return;
+    }
+    break;  // longer rows: the two-pass form below
+  }
+  float s = 0.0f;
+  for (int n = tid; n < N; n += NT) s += __expf(lrow[n] - mx) * inv_sum * kl_dp(ps[n], ph[n]);
+  s = block_sum_f(s, redf) * a.inv_B;
   for (int n = tid; n < N; n += NT) {
     const float P = __expf(lrow[n] - mx) * inv_sum;
     grow[n] = c * P * (kl_dp(ps[n], ph[n]) * a.inv_B - s);
@@ -116,51 +142,60 @@ __device__ __forceinline__ void store_T(void* base, long long i, float v) {
   static_cast<T*>(base)[i] = from_f32<T>(v);
 }
 
-// Workgroup (64 visual tokens, image b): dk_n = sum_m G_mn q_m over the
-// image's question rows, 32 rows at a time through LDS; then RoPE's
-// transpose, pair by pair, and the result in both layouts: rows
-// [B N][d_p] and columns [d_p][ldv].
+// Workgroup (16 visual tokens, image b): dk_n = sum_m G_mn q_m over the
+// image's question rows, 64 rows at a time through LDS (queries as float4,
+// d_p % 8 == 0); then RoPE's transpose, pair by pair, and the result in
+// both layouts: rows [B N][d_p] and columns [d_p][ldv].
 template <typename T>
 __global__ __launch_bounds__(NT) void attn_grad_k_kernel(const TrainArgs a) {
-  __shared__ float Qs[32][128];
-  __shared__ float Gs[32][64];
-  __shared__ float tile[64][129];
-  const int tid = threadIdx.x, b = blockIdx.y, n0 = blockIdx.x * 64, N = a.N, dp = a.d_p;
+  constexpr int TK = 16;
+  __shared__ float4 Qs[64][32];
+  __shared__ float Gs[64][TK + 1];
+  __shared__ float tile[TK][129];
+  const int tid = threadIdx.x, b = blockIdx.y, n0 = blockIdx.x * TK, N = a.N, dp = a.d_p, dp4 = dp >> 2;
   const int mb = a.t_off[b], M = a.t_off[b + 1] - mb;
-  const int nl = tid >> 2, d0 = (tid & 3) * 32;
-  float acc[32];
+  const int nl = tid >> 4, d4 = (tid & 15) * 2;  // two float4 of dims per thread
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int m0 = 0; m0 < M; m0 += 64) {
+    float4 qv[8];
+    float gv[4];
 #pragma unroll
-  for (int k = 0; k < 32; ++k) acc[k] = 0.0f;
-  for (int m0 = 0; m0 < M; m0 += 32) {
-    for (int i = tid; i < 32 * 128; i += NT) {
-      const int r = i >> 7, d = i & 127;
-      Qs[r][d] = (m0 + r < M && d < dp) ? a.q[(long long)(mb + m0 + r) * dp + d] : 0.0f;
+    for (int u = 0; u < 8; ++u) {  // every load of the chunk issued before the first LDS store
+      const int i = tid + u * NT, r = i >> 5, q = i & 31;
+      qv[u] = (m0 + r < M && q < dp4) ? reinterpret_cast<const float4*>(a.q + (long long)(mb + m0 + r) * dp)[q]
+                                      : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    for (int i = tid; i < 32 * 64; i += NT) {
-      const int r = i >> 6, n = i & 63;
-      Gs[r][n] = (m0 + r < M && n0 + n < N) ? a.G[(long long)(mb + m0 + r) * N + n0 + n] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = tid + u * NT, r = i / TK, n = i - r * TK;
+      gv[u] = (m0 + r < M && n0 + n < N) ? a.G[(long long)(mb + m0 + r) * N + n0 + n] : 0.0f;
     }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) Qs[(tid + u * NT) >> 5][(tid + u * NT) & 31] = qv[u];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) Gs[(tid + u * NT) / TK][(tid + u * NT) % TK] = gv[u];
     __syncthreads();
-#pragma unroll 4
-    for (int r = 0; r < 32; ++r) {
+#pragma unroll 8
+    for (int r = 0; r < 64; ++r) {
       const float g = Gs[r][nl];
-#pragma unroll
-      for (int k = 0; k < 32; k += 4) {
-        const float4 q = *reinterpret_cast<const float4*>(&Qs[r][d0 + k]);
-        acc[k] = fmaf(g, q.x, acc[k]);
-        acc[k + 1] = fmaf(g, q.y, acc[k + 1]);
-        acc[k + 2] = fmaf(g, q.z, acc[k + 2]);
-        acc[k + 3] = fmaf(g, q.w, acc[k + 3]);
-      }
+      const float4 q0 = Qs[r][d4], q1 = Qs[r][d4 + 1];
+      acc[0] = fmaf(g, q0.x, acc[0]);
+      acc[1] = fmaf(g, q0.y, acc[1]);
+      acc[2] = fmaf(g, q0.z, acc[2]);
+      acc[3] = fmaf(g, q0.w, acc[3]);
+      acc[4] = fmaf(g, q1.x, acc[4]);
+      acc[5] = fmaf(g, q1.y, acc[5]);
+      acc[6] = fmaf(g, q1.z, acc[6]);
+      acc[7] = fmaf(g, q1.w, acc[7]);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int k = 0; k < 32; ++k) tile[nl][d0 + k] = acc[k];
+  for (int k = 0; k < 8; ++k) tile[nl][4 * d4 + k] = acc[k];
   __syncthreads();
   // RoPE's transpose: (x, y) -> (c x + s y, -s x + c y) for pair (i, i + half)
   const int half = dp >> 1;
-  for (int e = tid; e < 64 * half; e += NT) {
+  for (int e = tid; e < TK * half; e += NT) {
     const int nn = e / half, i = e - nn * half, n = n0 + nn;
     if (n >= N) continue;
     const float2 cs = a.cs_v[((long long)b * N + n) * half + i];
@@ -170,66 +205,60 @@ __global__ __launch_bounds__(NT) void attn_grad_k_kernel(const TrainArgs a) {
   }
   __syncthreads();
   const long long row0 = (long long)b * N + n0;
-  for (int e = tid; e < 64 * dp; e += NT) {
-    const int nn = e / dp, d = e - nn * dp;
-    if (n0 + nn < N) store_T<T>(a.dk_rows, (row0 + nn) * dp + d, tile[nn][d]);
+  for (int e = tid; e < TK * a.kdp; e += NT) {  // rows padded with zeros to kdp columns
+    const int nn = e / a.kdp, d = e - nn * a.kdp;
+    if (n0 + nn < N) store_T<T>(a.dk_rows, (row0 + nn) * a.kdp + d, d < dp ? tile[nn][d] : 0.0f);
   }
-  for (int e = tid; e < 64 * dp; e += NT) {
-    const int d = e >> 6, nn = e & 63;
+  for (int e = tid; e < TK * dp; e += NT) {
+    const int d = e / TK, nn = e - d * TK;
     if (n0 + nn < N) store_T<T>(a.dk_cols, (long long)d * a.ldv + row0 + nn, tile[nn][d]);
   }
-  if (blockIdx.x == 0 && b == 0) {  // the padding columns of the transposed layout
-    const int pad = a.ldv - a.B * N;
-    for (int e = tid; e < pad * dp; e += NT)
+  {  // the padding columns of the transposed layout, spread over every workgroup
+    const int pad = a.ldv - a.B * N, wg = blockIdx.y * gridDim.x + blockIdx.x, nwg = gridDim.x * gridDim.y;
+    for (int e = wg * NT + tid; e < pad * dp; e += nwg * NT)
       store_T<T>(a.dk_cols, (long long)(e / pad) * a.ldv + a.B * N + e % pad, 0.0f);
   }
 }
 
-// Workgroup (256-token chunk c, 16 question rows, image b): the chunk's part
-// of dq_m = sum_n G_mn k_n, 64 tokens at a time through LDS, written to
-// dq_part[c][m][:].
+// Workgroup (64-token chunk c, 16 question rows, image b): the chunk's part
+// of dq_m = sum_n G_mn k_n through LDS (keys as float4, d_p % 8 == 0),
+// written to dq_part[c][m][:].
 __global__ __launch_bounds__(NT) void attn_grad_q_kernel(const TrainArgs a) {
-  __shared__ float Ks[64][128];
-  __shared__ float Gs[16][64];
-  const int tid = threadIdx.x, c = blockIdx.x, b = blockIdx.z, N = a.N, dp = a.d_p;
+  __shared__ float4 Ks[64][32];
+  __shared__ float Gs[16][65];
+  const int tid = threadIdx.x, c = blockIdx.x, b = blockIdx.z, N = a.N, dp = a.d_p, dp4 = dp >> 2;
   const int mb = a.t_off[b], M = a.t_off[b + 1] - mb, m0 = blockIdx.y * 16;
   if (m0 >= M) return;
-  const int ml = tid >> 4, d0 = (tid & 15) * 8;
-  float acc[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
-  const int nbeg = c * 256, nend = min(N, nbeg + 256);
-  for (int s0 = nbeg; s0 < nend; s0 += 64) {
-    for (int i = tid; i < 64 * 128; i += NT) {
-      const int r = i >> 7, d = i & 127;
-      Ks[r][d] = (s0 + r < nend && d < dp) ? a.k[((long long)b * N + s0 + r) * dp + d] : 0.0f;
-    }
-    for (int i = tid; i < 16 * 64; i += NT) {
-      const int r = i >> 6, n = i & 63;
-      Gs[r][n] = (m0 + r < M && s0 + n < nend) ? a.G[(long long)(mb + m0 + r) * N + s0 + n] : 0.0f;
-    }
-    __syncthreads();
-#pragma unroll 4
-    for (int n = 0; n < 64; ++n) {
-      const float g = Gs[ml][n];
-      const float4 k0 = *reinterpret_cast<const float4*>(&Ks[n][d0]);
-      const float4 k1 = *reinterpret_cast<const float4*>(&Ks[n][d0 + 4]);
-      acc[0] = fmaf(g, k0.x, acc[0]);
-      acc[1] = fmaf(g, k0.y, acc[1]);
-      acc[2] = fmaf(g, k0.z, acc[2]);
-      acc[3] = fmaf(g, k0.w, acc[3]);
-      acc[4] = fmaf(g, k1.x, acc[4]);
-      acc[5] = fmaf(g, k1.y, acc[5]);
-      acc[6] = fmaf(g, k1.z, acc[6]);
-      acc[7] = fmaf(g, k1.w, acc[7]);
-    }
-    __syncthreads();
+  const int ml = tid >> 4, d4 = (tid & 15) * 2;  // two float4 of dims per thread
+  const int s0 = c * 64, ns = min(64, N - s0);
+  for (int i = tid; i < 64 * 32; i += NT) {
+    const int r = i >> 5, q = i & 31;
+    Ks[r][q] = (r < ns && q < dp4) ? reinterpret_cast<const float4*>(a.k + ((long long)b * N + s0 + r) * dp)[q]
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  if (m0 + ml < M && d0 < dp) {
-    float* out = a.dq_part + ((long long)c * a.t_off[a.B] + mb + m0 + ml) * dp + d0;
-#pragma unroll
-    for (int k = 0; k < 8; ++k)
-      if (d0 + k < dp) out[k] = acc[k];
+  for (int i = tid; i < 16 * 64; i += NT) {
+    const int r = i >> 6, n = i & 63;
+    Gs[r][n] = (m0 + r < M && n < ns) ? a.G[(long long)(mb + m0 + r) * N + s0 + n] : 0.0f;
+  }
+  __syncthreads();
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int n = 0; n < 64; ++n) {
+    const float g = Gs[ml][n];
+    const float4 k0 = Ks[n][d4], k1 = Ks[n][d4 + 1];
+    acc[0] = fmaf(g, k0.x, acc[0]);
+    acc[1] = fmaf(g, k0.y, acc[1]);
+    acc[2] = fmaf(g, k0.z, acc[2]);
+    acc[3] = fmaf(g, k0.w, acc[3]);
+    acc[4] = fmaf(g, k1.x, acc[4]);
+    acc[5] = fmaf(g, k1.y, acc[5]);
+    acc[6] = fmaf(g, k1.z, acc[6]);
+    acc[7] = fmaf(g, k1.w, acc[7]);
+  }
+  if (m0 + ml < M && 4 * d4 < dp) {
+    float4* out = reinterpret_cast<float4*>(a.dq_part + ((long long)c * a.t_off[a.B] + mb + m0 + ml) * dp) + d4;
+    out[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    out[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
   }
 }
 
@@ -237,36 +266,85 @@ __global__ __launch_bounds__(NT) void attn_grad_q_kernel(const TrainArgs a) {
 // order, RoPE's transpose, both layouts (rows [sum_M][d_p], columns
 // [d_p][ldt]); workgroup 0 also zeroes the padding columns.
 template <typename T>
-__global__ __launch_bounds__(128) void dq_finish_kernel(const TrainArgs a) {
+__global__ __launch_bounds__(1024) void dq_finish_kernel(const TrainArgs a) {
   __shared__ float v[128];
-  const int m = blockIdx.x, tid = threadIdx.x, dp = a.d_p, sumM = a.t_off[a.B];
-  if (tid < dp) {
+  __shared__ float grp[8][128];
+  const int m = blockIdx.x, dp = a.d_p, sumM = a.t_off[a.B];
+  const int tid = threadIdx.x & 127, g = threadIdx.x >> 7;  // dimension, chunk group
+  if (tid < dp) {  // group g sums chunks g, g + 8, ... (loads issued 8 at a time)
+    const float* src = a.dq_part + (long long)m * dp + tid;
+    const long long cs = (long long)sumM * dp;
     float s = 0.0f;
-    for (int c = 0; c < a.nch; ++c) s += a.dq_part[((long long)c * sumM + m) * dp + tid];
-    v[tid] = s;
+    for (int c0 = g; c0 < a.nch; c0 += 64) {
+      float x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = c0 + 8 * u < a.nch ? src[(c0 + 8 * u) * cs] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += x[u];
+    }
+    grp[g][tid] = s;
   }
   __syncthreads();
+  if (g == 0 && tid < dp)  // the eight groups in a fixed order
+    v[tid] = ((grp[0][tid] + grp[1][tid]) + (grp[2][tid] + grp[3][tid])) +
+             ((grp[4][tid] + grp[5][tid]) + (grp[6][tid] + grp[7][tid]));
+  __syncthreads();
+  {  // the padding columns of the transposed layout, spread over every workgroup
+    const int pad = a.ldt - sumM;
+    for (int e = m * 1024 + threadIdx.x; e < pad * dp; e += sumM * 1024)
+      store_T<T>(a.dq_cols, (long long)(e / pad) * a.ldt + sumM + e % pad, 0.0f);
+  }
+  if (g != 0) return;
   const int half = dp >> 1;
   if (tid < half) {
     const float2 cs = a.cs_t[(long long)m * half + tid];
     const float x = v[tid], y = v[tid + half];
     const float zx = cs.x * x + cs.y * y, zy = cs.x * y - cs.y * x;
-    store_T<T>(a.dq_rows, (long long)m * dp + tid, zx);
-    store_T<T>(a.dq_rows, (long long)m * dp + tid + half, zy);
+    store_T<T>(a.dq_rows, (long long)m * a.kdp + tid, zx);
+    store_T<T>(a.dq_rows, (long long)m * a.kdp + tid + half, zy);
     store_T<T>(a.dq_cols, (long long)tid * a.ldt + m, zx);
     store_T<T>(a.dq_cols, (long long)(tid + half) * a.ldt + m, zy);
   }
-  if (m == 0) {
-    const int pad = a.ldt - sumM;
-    for (int e = tid; e < pad * dp; e += 128) store_T<T>(a.dq_cols, (long long)(e / pad) * a.ldt + sumM + e % pad, 0.0f);
+  for (int d = dp + tid; d < a.kdp; d += 128) store_T<T>(a.dq_rows, (long long)m * a.kdp + d, 0.0f);
+}
+
+// X = dz^T h from its token-chunk partials (float32 [nc][d_p][D_h]), summed
+// in chunk order: X [d_p][D_h] and its transpose [D_h][kdp] (zero past d_p),
+// both in the call's element type; blockIdx.y is the branch.
+template <typename T>
+__global__ __launch_bounds__(NT) void x_reduce_kernel(const XReduceArgs r) {
+  const int s = blockIdx.y, per = r.d_p * r.D_h;
+  const int e = blockIdx.x * NT + threadIdx.x;
+  if (e < per) {
+    const float* src = r.part[s] + e;
+    float v = 0.0f;
+    for (int c0 = 0; c0 < r.nc[s]; c0 += 8) {
+      float x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = c0 + u < r.nc[s] ? src[(long long)(c0 + u) * per] : 0.0f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v += x[u];
+    }
+    const int p = e / r.D_h, j = e - p * r.D_h;
+    store_T<T>(r.X[s], e, v);
+    store_T<T>(r.XT[s], (long long)j * r.kdp + p, v);
   }
+  // the transposed rows' padding
+  const int pad = r.kdp - r.d_p;
+  for (int q = e; q < r.D_h * pad; q += gridDim.x * NT) store_T<T>(r.XT[s], (long long)(q / pad) * r.kdp + r.d_p + q % pad, 0.0f);
 }
 
 // dst[c][r] = src[r][c] for r < rows, and 0 for rows <= r < ldd: 64 x 64
-// tiles through LDS, reads along the source rows and writes along the
-// destination rows.
+// tiles through LDS, 16-byte pieces along the source rows on the way in and
+// along the destination rows on the way out (cols, lds and ldd multiples of
+// the piece's element count VE, checked by the host).
 template <typename E>
 __global__ __launch_bounds__(NT) void transpose_kernel(const TransposeBatch t) {
+  constexpr int VE = 16 / sizeof(E);
+  union Piece {
+    uint4 u;
+    E e[VE];
+  };
   __shared__ E tile[64][65];
   int j = 0, blk = blockIdx.x;
   while (j + 1 < t.count && blk >= t.job[j + 1].tile_begin) ++j;
@@ -276,21 +354,37 @@ __global__ __launch_bounds__(NT) void transpose_kernel(const TransposeBatch t) {
   const int r0 = (blk % tr) * 64, c0 = (blk / tr) * 64;
   const E* src = static_cast<const E*>(J.src);
   E* dst = static_cast<E*>(J.dst);
-  for (int i = threadIdx.x; i < 64 * 64; i += NT) {
-    const int r = i >> 6, c = i & 63;
-    tile[r][c] = (r0 + r < J.rows && c0 + c < J.cols) ? src[(long long)(r0 + r) * J.lds + c0 + c] : E(0);
+  constexpr int PR = 64 / VE;  // pieces per tile row
+  for (int i = threadIdx.x; i < 64 * PR; i += NT) {
+    const int r = i / PR, q = i - r * PR;
+    Piece v;
+    v.u = make_uint4(0u, 0u, 0u, 0u);
+    if (r0 + r < J.rows && c0 + VE * q < J.cols)
+      v.u = *reinterpret_cast<const uint4*>(src + (long long)(r0 + r) * J.lds + c0 + VE * q);
+#pragma unroll
+    for (int e = 0; e < VE; ++e) tile[r][VE * q + e] = v.e[e];
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < 64 * 64; i += NT) {
-    const int c = i >> 6, r = i & 63;
-    if (c0 + c < J.cols && r0 + r < J.ldd) dst[(long long)(c0 + c) * J.ldd + r0 + r] = tile[r][c];
+  for (int i = threadIdx.x; i < 64 * PR; i += NT) {
+    const int c = i / PR, q = i - c * PR;
+    if (c0 + c >= J.cols || r0 + VE * q >= J.ldd) continue;
+    Piece v;
+#pragma unroll
+    for (int e = 0; e < VE; ++e) v.e[e] = tile[VE * q + e][c];
+    *reinterpret_cast<uint4*>(dst + (long long)(c0 + c) * J.ldd + r0 + VE * q) = v.u;
   }
 }
 
-// out[r] = sum_c src[r][c] in float32: one wave per row, lanes strided,
-// then a butterfly (a fixed order).
+// out[r] = sum_c src[r][c] in float32: one wave per row, 16-byte pieces
+// strided over the lanes, then a butterfly (a fixed order); cols and ld are
+// multiples of the piece's element count.
 template <typename T>
 __global__ __launch_bounds__(NT) void rowsum_kernel(const RowsumBatch t) {
+  constexpr int VE = 16 / sizeof(T);
+  union Piece {
+    uint4 u;
+    T e[VE];
+  };
   int j = 0;
   const int wave_id = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   while (j + 1 < t.count && wave_id >= t.job[j + 1].row_begin) ++j;
@@ -299,27 +393,39 @@ __global__ __launch_bounds__(NT) void rowsum_kernel(const RowsumBatch t) {
   if (r >= J.rows) return;
   const T* src = static_cast<const T*>(J.src) + (long long)r * J.ld;
   float s = 0.0f;
-  for (int c = lane; c < J.cols; c += 64) s += to_f32<T>(src[c]);
+  for (int c = lane * VE; c < J.cols; c += 64 * VE) {
+    Piece v;
+    v.u = *reinterpret_cast<const uint4*>(src + c);
+#pragma unroll
+    for (int e = 0; e < VE; ++e) s += to_f32<T>(v.e[e]);
+  }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
   if (lane == 0) J.out[r] = s;
 }
 
-// Per branch (blockIdx.y: visual, text) and column j of D_h:
-//   db2[j] = sum_p W[p][j] csum[p]   and   dW[p][j] += csum[p] b2[j]
+// Both branches (s = 0 visual, 1 text).  Workgroups [0, nA): one element of
+// dW each, dW[s][p][j] += csum[s][p] b2[s][j]; the rest: one j each,
+// db2[s][j] = sum_p W[s][p][j] csum[s][p].
 template <typename T>
 __global__ __launch_bounds__(NT) void finish_kernel(const FinishArgs f) {
-  const int j = blockIdx.x * NT + threadIdx.x, s = blockIdx.y;
-  if (j >= f.D_h) return;
-  const T* W = static_cast<const T*>(f.W[s]);
-  const float b2 = to_f32<T>(static_cast<const T*>(f.b2[s])[j]);
-  float acc = 0.0f;
-  for (int p = 0; p < f.d_p; ++p) {
-    const float cs = f.csum[s][p];
-    acc = fmaf(to_f32<T>(W[(long long)p * f.D_h + j]), cs, acc);
-    f.dW[s][(long long)p * f.D_h + j] += cs * b2;
+  const int Dh = f.D_h, dp = f.d_p, per = dp * Dh;
+  const int nA = (2 * per + NT - 1) / NT;
+  if (static_cast<int>(blockIdx.x) < nA) {
+    const int e = blockIdx.x * NT + threadIdx.x;
+    if (e >= 2 * per) return;
+    const int s = e / per, rem = e - s * per, p = rem / Dh, jj = rem - p * Dh;
+    f.dW[s][rem] += f.csum[s][p] * to_f32<T>(static_cast<const T*>(f.b2[s])[jj]);
+    return;
   }
-  f.db2[s][j] = acc;
+  const int e = (blockIdx.x - nA) * NT + threadIdx.x;
+  if (e >= 2 * Dh) return;
+  const int s = e / Dh, jj = e - s * Dh;
+  const T* W = static_cast<const T*>(f.W[s]);
+  float acc = 0.0f;
+#pragma unroll 8
+  for (int p = 0; p < dp; ++p) acc = fmaf(to_f32<T>(W[(long long)p * Dh + jj]), f.csum[s][p], acc);
+  f.db2[s][jj] = acc;
 }
 
 }  // namespace
@@ -330,15 +436,15 @@ hipError_t launch_train_grads(map_dtype dt, const TrainArgs& a, hipStream_t s) {
   for (int b = 0; b < a.B; ++b) maxM = a.t_off[b + 1] - a.t_off[b] > maxM ? a.t_off[b + 1] - a.t_off[b] : maxM;
   hipError_t e = launch_kernel("kl_grad", kl_grad_kernel, dim3(sumM + a.B), dim3(NT), 0, s, a);
   if (e != hipSuccess) return e;
-  e = dt == MAP_BF16 ? launch_kernel("attn_grad_k", attn_grad_k_kernel<bf16_t>, dim3((a.N + 63) / 64, a.B),
+  e = dt == MAP_BF16 ? launch_kernel("attn_grad_k", attn_grad_k_kernel<bf16_t>, dim3((a.N + 15) / 16, a.B),
                                      dim3(NT), 0, s, a)
-                     : launch_kernel("attn_grad_k", attn_grad_k_kernel<float>, dim3((a.N + 63) / 64, a.B),
+                     : launch_kernel("attn_grad_k", attn_grad_k_kernel<float>, dim3((a.N + 15) / 16, a.B),
                                      dim3(NT), 0, s, a);
   if (e != hipSuccess) return e;
   e = launch_kernel("attn_grad_q", attn_grad_q_kernel, dim3(a.nch, (maxM + 15) / 16, a.B), dim3(NT), 0, s, a);
   if (e != hipSuccess) return e;
-  return dt == MAP_BF16 ? launch_kernel("dq_finish", dq_finish_kernel<bf16_t>, dim3(sumM), dim3(128), 0, s, a)
-                        : launch_kernel("dq_finish", dq_finish_kernel<float>, dim3(sumM), dim3(128), 0, s, a);
+  return dt == MAP_BF16 ? launch_kernel("dq_finish", dq_finish_kernel<bf16_t>, dim3(sumM), dim3(1024), 0, s, a)
+                        : launch_kernel("dq_finish", dq_finish_kernel<float>, dim3(sumM), dim3(1024), 0, s, a);
 }
 
 void transpose_finalize(TransposeBatch& t) {
@@ -352,6 +458,9 @@ void transpose_finalize(TransposeBatch& t) {
 
 hipError_t launch_transpose(map_dtype dt, const TransposeBatch& t, const char* name, hipStream_t s) {
   if (t.total_tiles == 0) return hipSuccess;
+  const int ve = dt == MAP_BF16 ? 8 : 4;  // elements per 16-byte piece
+  for (int j = 0; j < t.count; ++j)
+    if (t.job[j].cols % ve || t.job[j].lds % ve || t.job[j].ldd % ve) return hipErrorInvalidValue;
   return dt == MAP_BF16 ? launch_kernel(name, transpose_kernel<uint16_t>, dim3(t.total_tiles), dim3(NT), 0, s, t)
                         : launch_kernel(name, transpose_kernel<float>, dim3(t.total_tiles), dim3(NT), 0, s, t);
 }
@@ -362,13 +471,22 @@ hipError_t launch_rowsum(map_dtype dt, RowsumBatch& t, hipStream_t s) {
     t.job[j].row_begin = begin;
     begin += t.job[j].rows;
   }
+  const int ve = dt == MAP_BF16 ? 8 : 4;  // elements per 16-byte piece
+  for (int j = 0; j < t.count; ++j)
+    if (t.job[j].cols % ve || t.job[j].ld % ve) return hipErrorInvalidValue;
   const dim3 grid((begin + 3) / 4);
   return dt == MAP_BF16 ? launch_kernel("rowsum", rowsum_kernel<bf16_t>, grid, dim3(NT), 0, s, t)
                         : launch_kernel("rowsum", rowsum_kernel<float>, grid, dim3(NT), 0, s, t);
 }
 
+hipError_t launch_x_reduce(map_dtype dt, const XReduceArgs& r, hipStream_t s) {
+  const dim3 grid((r.d_p * r.D_h + NT - 1) / NT, 2);
+  return dt == MAP_BF16 ? launch_kernel("x_reduce", x_reduce_kernel<bf16_t>, grid, dim3(NT), 0, s, r)
+                        : launch_kernel("x_reduce", x_reduce_kernel<float>, grid, dim3(NT), 0, s, r);
+}
+
 hipError_t launch_finish(map_dtype dt, const FinishArgs& f, hipStream_t s) {
-  const dim3 grid((f.D_h + NT - 1) / NT, 2);
+  const dim3 grid((2 * f.d_p * f.D_h + NT - 1) / NT + (2 * f.D_h + NT - 1) / NT);
   return dt == MAP_BF16 ? launch_kernel("finish", finish_kernel<bf16_t>, grid, dim3(NT), 0, s, f)
                         : launch_kernel("finish", finish_kernel<float>, grid, dim3(NT), 0, s, f);
 }
