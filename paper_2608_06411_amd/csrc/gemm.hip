@@ -474,6 +474,100 @@ __device__ __forceinline__ void epi_bias_staged(const GemmProblem& P, int bt, in
   }
 }
 
+// The training step's and the decoder layer's epilogues, staged like the
+// bias epilogue so that every global access moves 16 bytes along a row:
+// EPI_F32 (float32 out), EPI_GELU2 (GELU and GELU' of acc + bias), EPI_MUL
+// and EPI_RESID (acc times, or plus, the bf16 aux entry), bf16 out.
+__device__ __forceinline__ uint4 pack_bf16x8(const float (&f)[8]) {
+  uint4 o;
+  o.x = f32_to_bf16(f[0]) | (static_cast<uint32_t>(f32_to_bf16(f[1])) << 16);
+  o.y = f32_to_bf16(f[2]) | (static_cast<uint32_t>(f32_to_bf16(f[3])) << 16);
+  o.z = f32_to_bf16(f[4]) | (static_cast<uint32_t>(f32_to_bf16(f[5])) << 16);
+  o.w = f32_to_bf16(f[6]) | (static_cast<uint32_t>(f32_to_bf16(f[7])) << 16);
+  return o;
+}
+
+__device__ __forceinline__ void epi_direct_staged(const GemmProblem& P, int bt, int m0, int n0,
+                                                  f32x16_t (&acc)[2][2], const StagedTile& L, int tid,
+                                                  int lane, int wm, int wn) {
+  const int M = P.M, N = P.N, e = P.epi;
+  const bf16_t* __restrict__ bias = static_cast<const bf16_t*>(P.bias);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int cl = wn * 64 + j * 32 + acc_col(lane);
+    const float bv = (e == EPI_GELU2 && bias && n0 + cl < N) ? bf16_to_f32(bias[n0 + cl]) : 0.0f;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) L.row(wm * 64 + i * 32 + acc_row(r, lane))[cl] = acc[i][j][r] + bv;
+  }
+  __syncthreads();
+  const long long base = bt * P.strideC;
+  const bool vec = (P.ldc & 7) == 0 && (reinterpret_cast<uintptr_t>(P.C) & 15) == 0 &&
+                   (!P.aux || (reinterpret_cast<uintptr_t>(P.aux) & 15) == 0) && (base & 7) == 0;
+#pragma unroll 2
+  for (int it = tid; it < BM * (BN / 8); it += NT) {  // 8 columns per item
+    const int r = it >> 4, c8 = (it & 15) * 8;
+    const int row = m0 + r, col = n0 + c8;
+    if (row >= M || col >= N) continue;
+    const float4 x = *reinterpret_cast<const float4*>(L.row(r) + c8);
+    const float4 y = *reinterpret_cast<const float4*>(L.row(r) + c8 + 4);
+    float f[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+    const long long at = base + (long long)row * P.ldc + col;
+    const int n = min(8, N - col);
+    if (e == EPI_F32) {
+      float* dst = static_cast<float*>(P.C) + at;
+      if (vec && n == 8) {
+        reinterpret_cast<float4*>(dst)[0] = x;
+        reinterpret_cast<float4*>(dst)[1] = y;
+      } else {
+        for (int k = 0; k < n; ++k) dst[k] = f[k];
+      }
+      continue;
+    }
+    bf16_t* dst = static_cast<bf16_t*>(P.C) + at;
+    if (e == EPI_GELU2) {
+      float g[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        g[k] = gelu_erf_grad(f[k]);
+        f[k] = gelu_erf(f[k]);
+      }
+      bf16_t* dst2 = static_cast<bf16_t*>(P.aux) + at;
+      if (vec && n == 8) {
+        *reinterpret_cast<uint4*>(dst) = pack_bf16x8(f);
+        *reinterpret_cast<uint4*>(dst2) = pack_bf16x8(g);
+      } else {
+        for (int k = 0; k < n; ++k) {
+          dst[k] = f32_to_bf16(f[k]);
+          dst2[k] = f32_to_bf16(g[k]);
+        }
+      }
+      continue;
+    }
+    const bf16_t* src = static_cast<const bf16_t*>(P.aux) + at;  // EPI_MUL, EPI_RESID
+    float a8[8];
+    if (vec && n == 8) {
+      const uint4 u = *reinterpret_cast<const uint4*>(src);
+      const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        a8[2 * k] = __uint_as_float(w4[k] << 16);
+        a8[2 * k + 1] = __uint_as_float(w4[k] & 0xffff0000u);
+      }
+    } else {
+      for (int k = 0; k < 8; ++k) a8[k] = k < n ? bf16_to_f32(src[k]) : 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) f[k] = e == EPI_MUL ? f[k] * a8[k] : f[k] + a8[k];
+    if (vec && n == 8) {
+      *reinterpret_cast<uint4*>(dst) = pack_bf16x8(f);
+    } else {
+      for (int k = 0; k < n; ++k) dst[k] = f32_to_bf16(f[k]);
+    }
+  }
+}
+
 // Cosine: S[row][col] = acc * rs[row] * rs[col] (float32), written to both
 // (row, col) and (col, row) from the same float, so S is bitwise symmetric.
 // A diagonal tile takes the entries below its diagonal from the transposed
@@ -746,6 +840,8 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
     epi_cosine_staged(P, bt, tm, tn, acc, L, rs_tile, rs_tile + BM, tid, lane, wm, wn);
   else if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS)
     epi_bias_staged(P, bt, m0, n0, acc, L, tid, lane, wm, wn);
+  else if (epi_direct(P.epi))
+    epi_direct_staged(P, bt, m0, n0, acc, L, tid, lane, wm, wn);
   else
     epilogue<bf16_t>(P, bt, tm, tn, acc, L.q0, L.q1, tid, lane, wm, wn);
 }
