@@ -16,6 +16,10 @@ Attention in MLLMs for Visual Token Pruning"):
 * ``teacher``    -- teacher selection for predictor training: Eq. (1),
                     Eq. (2) and QCTS-n (section "Question Contrastive
                     Teacher Selection");
+* ``decoder``    -- the language model's first layer (LLaMA decoder layer:
+                    RMSNorm, RoPE attention with a causal mask, SwiGLU)
+                    over the pruned input, the consumer of the pruning stage
+                    (section "Inference-Time Token Pruning");
 * ``train``      -- one predictor training step: the KL divergence from the
                     teacher distribution to p_hat and its gradient with
                     respect to every predictor parameter (section
@@ -33,8 +37,10 @@ from .similarity import cosine_entries, cosine_similarity, row_norms
 from .pipeline import assemble, prune
 from .teacher import TeacherResult, js_divergence, layer_distributions, teacher_selection
 from .train import TrainStepResult, gelu_erf_grad, kl_divergence, train_step
+from .decoder import decoder_layer
 
 __all__ = [
+    "decoder_layer",
     "TrainStepResult", "gelu_erf_grad", "kl_divergence", "train_step",
     "TeacherResult", "js_divergence", "layer_distributions", "teacher_selection",
     "assemble",
