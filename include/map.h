@@ -301,6 +301,41 @@ map_status map_train_step(const map_weights* w, map_dtype dt, int B, int N,
                           const float* p_teacher, float* loss_out, float* p_out,
                           const map_grads* grads, void* ws, size_t ws_bytes, void* stream);
 
+/* The language model's decoder layer that consumes the pruned input
+ * (section "Inference-Time Token Pruning": after pruning the model processes
+ * only the kept visual tokens and the question tokens; LLaVA's language
+ * models use LLaMA's layer).  Device pointers, bf16, torch.nn.Linear layout:
+ *   attn_norm, ffn_norm [d]      RMSNorm weights
+ *   w_qkv     [3 d][d]           W_q, W_k, W_v stacked by rows
+ *   w_o       [d][d]
+ *   w_gate_up [2 ff][d]          the SwiGLU gate's rows, then the up rows
+ *   w_down    [d][ff]
+ * head_dim must be 128 and d = n_heads * head_dim, with d and ff multiples of
+ * 256 and d <= 8192. */
+typedef struct {
+  const void *attn_norm, *w_qkv, *w_o, *ffn_norm, *w_gate_up, *w_down;
+  int32_t d, n_heads, head_dim, ff;
+  float rope_theta, eps;
+} map_decoder_weights;
+
+/* map_decoder_layer -- one decoder layer's prefill over B packed sequences:
+ *   h = RMSNorm(X) attn_norm;  q, k, v = h W_qkv^T;  RoPE on q and k per
+ *   head at each row's pos (pairs (i, i + 64), theta^(-2i/128));
+ *   o = softmax(q k^T / sqrt(128) + causal mask) v per sequence and head;
+ *   X1 = X + o W_o^T;  Y = X1 + (SiLU(g) * u) W_down^T with
+ *   [g | u] = RMSNorm(X1) ffn_norm W_gate_up^T.
+ * X, Y [R][d] bf16 (16-byte aligned), R = seq_off_host[B]; sequence b is rows
+ * seq_off[b] .. seq_off[b+1]-1 (host array, strictly increasing from 0), and
+ * a row attends to the rows before it in its sequence; pos [R] int32.  The
+ * layout map_prune_assemble writes is such an input (seq_off[b] =
+ * b K + t_off[b]).  Stored intermediates are bf16, arithmetic float32.
+ * ws: map_decoder_workspace(R, w) bytes.  MAP_ERR_UNSUPPORTED for a dtype
+ * other than MAP_BF16; MAP_ERR_INVALID_ARG for shapes outside the limits. */
+size_t map_decoder_workspace(int R, const map_decoder_weights* w);
+map_status map_decoder_layer(const map_decoder_weights* w, map_dtype dt, int B, const void* X,
+                             const int32_t* pos, const int32_t* seq_off_host, void* Y,
+                             void* ws, size_t ws_bytes, void* stream);
+
 /* map_prune's candidate subset.  A greedy pick of Eq. (4) scores
  * p_i n_i r_i <= p_i n_i, so map_prune may run the selection on a subset J
  * of each image's tokens: R0 plus the tokens with the largest bounds

@@ -29,7 +29,7 @@ EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
     "map_prune", "map_prune_assemble", "map_prune_noalloc", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
-    "map_train_workspace", "map_train_step",
+    "map_train_workspace", "map_train_step", "map_decoder_workspace", "map_decoder_layer",
     "map_selection_status", "map_set_select_images_per_launch", "map_timing_enable", "map_timing_read",
     "map_timing_reset",
 )
@@ -45,6 +45,12 @@ class map_weights(ctypes.Structure):
 class map_grads(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("w1_v", "b1_v", "w2_v", "b2_v", "w_k", "w1_t", "b1_t", "w2_t", "b2_t", "w_q")]
+
+
+class map_decoder_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down")] + \
+               [("d", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("ff", ctypes.c_int32), ("rope_theta", ctypes.c_float), ("eps", ctypes.c_float)]
 
 
 class map_select_params(ctypes.Structure):
@@ -74,6 +80,8 @@ _SIGS = {
     "map_train_workspace": (_SZ, [_I, _I, _I, _I, ctypes.POINTER(map_weights)]),
     "map_train_step": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P,
                             ctypes.POINTER(map_grads), _P, _SZ, _P]),
+    "map_decoder_workspace": (_SZ, [_I, ctypes.POINTER(map_decoder_weights)]),
+    "map_decoder_layer": (_I, [ctypes.POINTER(map_decoder_weights), _I, _I, _P, _P, _P, _P, _P, _SZ, _P]),
     "map_set_subset_tokens": (_I, [_I]),
     "map_selection_status": (_I, [_P, _P, _P]),
     "map_set_select_images_per_launch": (_I, [_I]),
@@ -523,6 +531,72 @@ def map_train_step(w: PredictorWeights, V: torch.Tensor, pos_v: torch.Tensor, T:
                                 _ptr(pos_t), offs, _ptr(p_teacher), _ptr(loss), _ptr(p_out), ctypes.byref(gs),
                                 _ptr(workspace.buf), workspace.nbytes, _stream(dev)), "map_train_step")
     return loss, p_out, grads
+
+
+@dataclass
+class DecoderWeights:
+    """One LLaMA-style decoder layer on the device (bf16, torch.nn.Linear
+    layout): w_qkv stacks W_q, W_k, W_v by rows, w_gate_up the gate's rows
+    then the up rows."""
+    attn_norm: torch.Tensor
+    w_qkv: torch.Tensor
+    w_o: torch.Tensor
+    ffn_norm: torch.Tensor
+    w_gate_up: torch.Tensor
+    w_down: torch.Tensor
+    n_heads: int
+    rope_theta: float = 10000.0
+    eps: float = 1e-6
+
+    def struct(self, device) -> map_decoder_weights:
+        d = self.w_o.shape[0]
+        ff = self.w_down.shape[1]
+        shapes = {"attn_norm": (d,), "w_qkv": (3 * d, d), "w_o": (d, d), "ffn_norm": (d,),
+                  "w_gate_up": (2 * ff, d), "w_down": (d, ff)}
+        s = map_decoder_weights()
+        for n, shape in shapes.items():
+            _need(getattr(self, n), f"decoder weight {n}", shape, torch.bfloat16, device)
+            setattr(s, n, getattr(self, n).data_ptr())
+        s.d, s.n_heads, s.ff = d, self.n_heads, ff
+        s.head_dim = d // self.n_heads
+        s.rope_theta, s.eps = float(self.rope_theta), float(self.eps)
+        return s
+
+
+def map_decoder_layer(w: DecoderWeights, X: torch.Tensor, pos: torch.Tensor, seq_off: Sequence[int],
+                      out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    """One decoder layer's prefill over packed sequences X [R, d] (sequence b
+    is rows seq_off[b] .. seq_off[b+1]-1, causal within it; pos [R] the rows'
+    positional indices).  Returns Y [R, d]."""
+    R, d = _dims(X, "X", 2)
+    offs, total = _offsets(seq_off)
+    B = len(offs) - 1
+    if total != R:
+        raise ValueError(f"seq_off ends at {total}, X has {R} rows")
+    _need(X, "X", (R, d), torch.bfloat16, None)
+    dev = X.device
+    _need(pos, "pos", (R,), torch.int32, dev)
+    if out is None:
+        out = torch.empty_like(X)
+    _need(out, "out", (R, d), torch.bfloat16, dev)
+    ws_struct = w.struct(dev)
+    _on_gpu(X, "X")
+    nbytes = lib().map_decoder_workspace(R, ctypes.byref(ws_struct))
+    if nbytes == 0:
+        raise MapError(MAP_ERR_INVALID_ARG, "map_decoder_workspace")
+    ws = workspace if workspace is not None else _workspace(nbytes, dev)
+    _need_ws(ws, nbytes, dev)
+    _check(lib().map_decoder_layer(ctypes.byref(ws_struct), MAP_BF16, B, _ptr(X), _ptr(pos), offs, _ptr(out), _ptr(ws),
+                                   ws.numel(), _stream(dev)), "map_decoder_layer")
+    return out
+
+
+def decoder_workspace(w: DecoderWeights, R: int, device) -> torch.Tensor:
+    """A reusable workspace for map_decoder_layer over R rows."""
+    nbytes = lib().map_decoder_workspace(R, ctypes.byref(w.struct(device)))
+    if nbytes == 0:
+        raise MapError(MAP_ERR_INVALID_ARG, "map_decoder_workspace")
+    return _workspace(nbytes, device)
 
 
 def selection_status(ws: torch.Tensor) -> int:

@@ -737,13 +737,15 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
   const GemmProblem& P = args.p[pi];
   if (P.run_if && P.run_if[bt] == 0) return;
   const int M = P.M, N = P.N;
-  const int kl = P.ksplit > 1 ? P.K / P.ksplit : P.K;  // this workgroup's K range: kc kl .. (kc + 1) kl
+  // this workgroup's K range: kc kl .. min(K, (kc + 1) kl), kl = kchunk (the
+  // last range shorter) or K / ksplit
+  const int kl = P.ksplit > 1 ? (P.kchunk > 0 ? P.kchunk : P.K / P.ksplit) : P.K;
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(P.A) + bt * P.strideA + (long long)kc * kl;
   const bf16_t* __restrict__ B = static_cast<const bf16_t*>(P.B) + bt * P.strideB + (long long)kc * kl;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int nk = kl / 64;
+  const int nk = min(kl, P.K - kc * kl) / 64;
   float rs_mine = 0.0f;  // cosine epilogue: reciprocal norm of tile row tid, or of column tid - BM
   if (P.epi == EPI_COSINE) {
     const float* rs = P.rs + (long long)bt * M;
@@ -1018,6 +1020,54 @@ __global__ __launch_bounds__(NT) void gram_reduce_kernel(const GemmProblem P, fl
 
 }  // namespace
 
+// (tile t, piece q) of a plain (not triangular) problem split over K: the
+// K ranges' float4 q of every thread summed in range order, plus the bf16
+// residual at the same entries, stored as bf16 (the decoder layer's output
+// projections).
+__global__ __launch_bounds__(NT) void splitk_resid_kernel(const GemmProblem P, const bf16_t* __restrict__ res,
+                                                          bf16_t* __restrict__ out, int ldc) {
+  const int t = blockIdx.x >> 4, q = blockIdx.x & 15;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int ks = P.ksplit > 1 ? P.ksplit : 1;
+  const int tm = t / P.tiles_n, tn = t - tm * P.tiles_n;
+  const float4* src = static_cast<const float4*>(P.C);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int kc0 = 0; kc0 < ks; kc0 += 8) {
+    float4 x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (kc0 + u < ks) x[u] = src[((long long)(kc0 + u) * P.tiles_tri + t) * (16 * NT) + q * NT + tid];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (kc0 + u < ks) {
+        v.x += x[u].x;
+        v.y += x[u].y;
+        v.z += x[u].z;
+        v.w += x[u].w;
+      }
+  }
+  const int i = q >> 3, j = (q >> 2) & 1, g = q & 3;
+  const int col = tn * BN + wn * 64 + j * 32 + acc_col(lane);
+  const int row0 = tm * BM + wm * 64 + i * 32 + 8 * g + 4 * (lane >> 5);
+  if (col >= P.N) return;
+  const float f[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int row = row0 + e;
+    if (row < P.M) {
+      const long long at = (long long)row * ldc + col;
+      out[at] = f32_to_bf16(f[e] + bf16_to_f32(res[at]));
+    }
+  }
+}
+
+hipError_t launch_splitk_resid(const GemmProblem& P, const void* res, void* out, int ldc, hipStream_t s) {
+  if (P.tiles_tri == 0) return hipSuccess;
+  return launch_kernel("splitk_resid", splitk_resid_kernel, dim3(P.tiles_tri * 16), dim3(NT), 0, s, P,
+                       static_cast<const bf16_t*>(res), static_cast<bf16_t*>(out), ldc);
+}
+
 hipError_t launch_gram_reduce(const GemmProblem& partial, float* out, int ldc, const float* rs, hipStream_t s) {
   if (partial.tiles_tri == 0 || partial.batch == 0) return hipSuccess;
   return launch_kernel("gram_reduce", gram_reduce_kernel, dim3(partial.tiles_tri * 16, partial.batch), dim3(NT), 0,
@@ -1040,6 +1090,14 @@ void gemm_finalize(GemmBatch& g) {
   g.first_tiles = g.count > 1 && g.p[g.count - 1].epi == EPI_COSINE ? g.p[g.count - 1].tile_begin : 0;
 }
 
+// K ranges of a split problem: equal ranges (K / ksplit) or kchunk-long ones
+// with a shorter last range, each a positive multiple of 256.
+static bool k_ranges_ok(const GemmProblem& p) {
+  if (p.ksplit <= 1) return true;
+  if (p.kchunk > 0) return p.kchunk % 256 == 0 && (long long)(p.ksplit - 1) * p.kchunk < p.K;
+  return p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0;
+}
+
 bool gemm_direct_loads(map_dtype dt, const GemmBatch& g) {
   if (dt != MAP_BF16) return false;
   bool dma = true;  // every problem meets the direct-load requirements
@@ -1048,7 +1106,7 @@ bool gemm_direct_loads(map_dtype dt, const GemmBatch& g) {
     dma = dma && (p.epi <= EPI_PARTIAL || epi_direct(p.epi)) && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
           (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
           p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
-          (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));
+          k_ranges_ok(p);
   }
   return dma;
 }
@@ -1062,7 +1120,7 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
       dma = dma && (p.epi <= EPI_PARTIAL || epi_direct(p.epi)) && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
             (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
             p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
-            (p.ksplit <= 1 || (p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0));
+            k_ranges_ok(p);
     }
     if (dma) return launch_kernel(name, gemm_dma_kernel, dim3(g.total_tiles + g.norm_blocks), dim3(NT), 0, s, g);
     if (g.norm_blocks) return hipErrorInvalidValue;

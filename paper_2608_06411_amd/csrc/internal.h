@@ -102,6 +102,7 @@ struct GemmProblem {
   const int32_t* mapB;
   long long mapStride;
   int ksplit;              // EPI_PARTIAL: K ranges per tile (K / ksplit each, a multiple of 256)
+  int kchunk;              // EPI_PARTIAL, if > 0: ranges of kchunk (a multiple of 256), the last shorter
   const int32_t* run_if;   // [batch] batch items whose flag is 0 are skipped (null: none)
   void* aux;               // EPI_GELU2: second output; EPI_MUL, EPI_RESID: the factor or the residual
                            // (each [M][ldc] of type T)
@@ -355,6 +356,33 @@ struct FinishArgs {
   int D_h, d_p;
 };
 hipError_t launch_finish(map_dtype dt, const FinishArgs& f, hipStream_t s);
+
+// ---------------------------------------------------------------- decoder layer
+// The language model's layer over the pruned input (LLaMA decoder layer,
+// bf16): the kernels around the matrix-core products.
+struct DecoderArgs {
+  const void* X;          // [R][d] layer input (the residual of the attention block)
+  const int32_t* pos;     // [R] positional index of each row
+  const void* attn_norm;  // [d]
+  const void* ffn_norm;   // [d]
+  void* h;                // [R][d] RMSNorm output (attention block, then MLP block)
+  void* qkv;              // [R][3 d] q, k (rotated in place), v
+  void* o;                // [R][d] attention output
+  void* x1;               // [R][d] after the attention block
+  void* gu;               // [R][2 ff] gate, then up
+  void* act;              // [R][ff] SiLU(gate) * up
+  int R, d, n_heads, head_dim, ff, B, max_len;
+  float eps;
+  double inv_freq[64];    // theta^(-2i/head_dim), float64
+  int seq_off[MAP_MAX_BATCH + 1];
+};
+hipError_t launch_rmsnorm(const DecoderArgs& a, const void* x, const void* g, void* out, hipStream_t s);
+hipError_t launch_rope_qkv(const DecoderArgs& a, hipStream_t s);
+hipError_t launch_attention(const DecoderArgs& a, hipStream_t s);
+hipError_t launch_silu_mul(const DecoderArgs& a, hipStream_t s);
+// out = (sum of the K-range partials of P, EPI_PARTIAL, not triangular, batch
+// 1) + res, both [M][ldc] bf16
+hipError_t launch_splitk_resid(const GemmProblem& P, const void* res, void* out, int ldc, hipStream_t s);
 
 // ---------------------------------------------------------------- teacher selection
 constexpr int kTeacherMaxLayers = 256;

@@ -655,6 +655,131 @@ hipError_t enqueue_train(const map_weights& w, map_dtype dt, int B, int N, const
   return launch_finish(dt, f, st);
 }
 
+// ------------------------------------------------------------ decoder layer
+bool valid_decoder(const map_decoder_weights* w) {
+  return w && w->attn_norm && w->w_qkv && w->w_o && w->ffn_norm && w->w_gate_up && w->w_down && w->head_dim == 128 &&
+         w->n_heads >= 1 && w->d == w->n_heads * w->head_dim && w->d % 256 == 0 && w->d <= 8192 && w->ff > 0 &&
+         w->ff % 256 == 0 && isfinite(w->rope_theta) && w->rope_theta > 0.0f && isfinite(w->eps) && w->eps >= 0.0f;
+}
+
+constexpr int kMaxDecoderRows = 1 << 16;
+
+// K ranges for a product of M rows and N columns over K: enough workgroups
+// to cover the device once (split only when the tiles alone leave most of it
+// idle), each range a multiple of 256.
+void split_k(GemmProblem& p, int cus) {
+  const int tiles = ((p.M + 127) / 128) * ((p.N + 127) / 128);
+  int ks = tiles >= cus / 2 ? 1 : std::min(p.K / 256, std::max(1, cus / tiles));
+  if (ks <= 1) return;
+  const int chunk = ((p.K / 256 + ks - 1) / ks) * 256;
+  ks = (p.K + chunk - 1) / chunk;
+  if (ks <= 1) return;
+  p.ksplit = ks;
+  p.kchunk = chunk;
+  p.epi = EPI_PARTIAL;
+}
+
+struct DecoderWs {
+  void *h, *qkv, *o, *x1, *gu, *act;
+  float* partial;
+};
+
+size_t partial_floats(int R, int N, int K, int cus) {
+  GemmProblem p;
+  memset(&p, 0, sizeof(p));
+  p.M = R;
+  p.N = N;
+  p.K = K;
+  split_k(p, cus);
+  return p.ksplit > 1 ? (size_t)((R + 127) / 128) * ((N + 127) / 128) * p.ksplit * 128 * 128 : 0;
+}
+
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                              hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
+DecoderWs carve_decoder(Carver& c, int R, const map_decoder_weights& w, int cus) {
+  DecoderWs t;
+  const size_t r = R, d = w.d, ff = w.ff;
+  t.h = c.take_bytes(r * d * 2);
+  t.qkv = c.take_bytes(r * 3 * d * 2);
+  t.o = c.take_bytes(r * d * 2);
+  t.x1 = c.take_bytes(r * d * 2);
+  t.gu = c.take_bytes(r * 2 * ff * 2);
+  t.act = c.take_bytes(r * ff * 2);
+  t.partial = c.take<float>(std::max(partial_floats(R, w.d, w.d, cus), partial_floats(R, w.d, w.ff, cus)));
+  return t;
+}
+
+// y = acc + residual: split over K into float32 partials and their ordered
+// sum (when the tiles alone would leave the device mostly idle), else the
+// residual epilogue.
+hipError_t resid_product(const void* A, int M, const void* W, int N, int K, const void* res, void* out, float* part,
+                         int cus, const char* name, hipStream_t st) {
+  GemmBatch g;
+  memset(&g, 0, sizeof(g));
+  g.p[0] = linear(A, M, W, nullptr, out, N, K, EPI_RESID);
+  g.p[0].aux = const_cast<void*>(res);
+  split_k(g.p[0], cus);
+  if (g.p[0].epi == EPI_PARTIAL) g.p[0].C = part;
+  g.count = 1;
+  gemm_finalize(g);
+  hipError_t e = launch_gemm(MAP_BF16, g, name, st);
+  if (e != hipSuccess || g.p[0].epi != EPI_PARTIAL) return e;
+  return launch_splitk_resid(g.p[0], res, out, N, st);
+}
+
+hipError_t enqueue_decoder(const map_decoder_weights& w, int B, const void* X, const int32_t* pos,
+                           const int32_t* seq_off, void* Y, const DecoderWs& t, int cus, hipStream_t st) {
+  DecoderArgs a;
+  memset(&a, 0, sizeof(a));
+  const int R = seq_off[B];
+  a.X = X;
+  a.pos = pos;
+  a.attn_norm = w.attn_norm;
+  a.ffn_norm = w.ffn_norm;
+  a.h = t.h;
+  a.qkv = t.qkv;
+  a.o = t.o;
+  a.x1 = t.x1;
+  a.gu = t.gu;
+  a.act = t.act;
+  a.R = R;
+  a.d = w.d;
+  a.n_heads = w.n_heads;
+  a.head_dim = w.head_dim;
+  a.ff = w.ff;
+  a.B = B;
+  a.eps = w.eps;
+  for (int i = 0; i < 64; ++i) a.inv_freq[i] = pow(static_cast<double>(w.rope_theta), -2.0 * i / w.head_dim);
+  for (int b = 0; b <= B; ++b) a.seq_off[b] = seq_off[b];
+  for (int b = 0; b < B; ++b) a.max_len = std::max(a.max_len, seq_off[b + 1] - seq_off[b]);
+  hipError_t e = launch_rmsnorm(a, X, w.attn_norm, t.h, st);
+  if (e != hipSuccess) return e;
+  GemmBatch g;
+  memset(&g, 0, sizeof(g));
+  g.p[0] = linear(t.h, R, w.w_qkv, nullptr, t.qkv, 3 * w.d, w.d, EPI_BIAS);
+  g.count = 1;
+  gemm_finalize(g);
+  if ((e = launch_gemm(MAP_BF16, g, "gemm_qkv", st)) != hipSuccess) return e;
+  if ((e = launch_rope_qkv(a, st)) != hipSuccess) return e;
+  if ((e = launch_attention(a, st)) != hipSuccess) return e;
+  if ((e = resid_product(t.o, R, w.w_o, w.d, w.d, X, t.x1, t.partial, cus, "gemm_o", st)) != hipSuccess) return e;
+  if ((e = launch_rmsnorm(a, t.x1, w.ffn_norm, t.h, st)) != hipSuccess) return e;
+  GemmBatch g2;
+  memset(&g2, 0, sizeof(g2));
+  g2.p[0] = linear(t.h, R, w.w_gate_up, nullptr, t.gu, 2 * w.ff, w.d, EPI_BIAS);
+  g2.count = 1;
+  gemm_finalize(g2);
+  if ((e = launch_gemm(MAP_BF16, g2, "gemm_gate_up", st)) != hipSuccess) return e;
+  if ((e = launch_silu_mul(a, st)) != hipSuccess) return e;
+  return resid_product(t.act, R, w.w_down, w.d, w.ff, t.x1, Y, t.partial, cus, "gemm_down", st);
+}
+
 // ------------------------------------------------------------ timing
 struct TimingRecord {
   const char* name;
@@ -1137,6 +1262,28 @@ map_status map_train_step(const map_weights* w, map_dtype dt, int B, int N, cons
   const TrainWs t = carve_train(c, dt, B, N, sumM, *w);
   return hip_status(enqueue_train(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p_teacher, loss_out,
                                   p_out ? p_out : t.p, *grads, t, static_cast<hipStream_t>(stream)));
+}
+
+size_t map_decoder_workspace(int R, const map_decoder_weights* w) {
+  if (R < 1 || R > kMaxDecoderRows || !valid_decoder(w)) return 0;
+  Carver c(nullptr);
+  carve_decoder(c, R, *w, device_cus());
+  return c.off;
+}
+
+map_status map_decoder_layer(const map_decoder_weights* w, map_dtype dt, int B, const void* X, const int32_t* pos,
+                             const int32_t* seq_off_host, void* Y, void* ws, size_t ws_bytes, void* stream) {
+  if (!valid_dtype(dt) || !valid_decoder(w) || B < 1 || B > MAP_MAX_BATCH || !X || !pos || !Y ||
+      !valid_offsets(seq_off_host, B) || seq_off_host[B] > kMaxDecoderRows ||
+      ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 15) != 0)
+    return MAP_ERR_INVALID_ARG;
+  if (dt != MAP_BF16) return MAP_ERR_UNSUPPORTED;
+  const int R = seq_off_host[B], cus = device_cus();
+  const map_status ws_ok = check_ws(ws, ws_bytes, map_decoder_workspace(R, w));
+  if (ws_ok != MAP_OK) return ws_ok;
+  Carver c(ws);
+  const DecoderWs t = carve_decoder(c, R, *w, cus);
+  return hip_status(enqueue_decoder(*w, B, X, pos, seq_off_host, Y, t, cus, static_cast<hipStream_t>(stream)));
 }
 
 map_status map_set_subset_tokens(int n) {
