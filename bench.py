@@ -535,6 +535,12 @@ def decoder_layer_context(torch, dev, prune_us, steps=20, warmup=5):
         res["error"] = "no fused SDPA backend available (the bf16 math path is not used here)"
         return res
     res["sdpa_backend"] = str(backend).split(".")[-1]
+    # the same layer in this library's kernels (map_decoder_layer), same weights
+    import paper_2608_06411_amd as mp
+    wl = mp.DecoderWeights(attn_norm=n1, w_qkv=Wqkv, w_o=Wo, ffn_norm=n2, w_gate_up=torch.cat([Wg, Wu]).contiguous(),
+                           w_down=Wd, n_heads=H)
+    weight_bytes = 2.0 * (4 * d * d + 3 * d * ff + 2 * d)
+    ours = {}
     for S in (2944, 224):
         x = (0.5 * torch.randn(S, d, generator=g, device=dev)).to(torch.bfloat16)
         c, s = rope_tab(S)
@@ -543,9 +549,31 @@ def decoder_layer_context(torch, dev, prune_us, steps=20, warmup=5):
         flops = 2.0 * S * d * (3 * d + d + 3 * ff) + 2.0 * S * S * d  # causal attention: half of 4 S^2 d
         res[f"prefill_us_S{S}"] = us
         res[f"achieved_tflops_S{S}"] = flops / (us * 1e-6) / 1e12
+        pos = torch.arange(S, device=dev, dtype=torch.int32)
+        ws = mp.decoder_workspace(wl, S, dev)
+        y = torch.empty_like(x)
+        mine = _time_steps(torch, dev, lambda: mp.map_decoder_layer(wl, x, pos, [0, S], out=y, workspace=ws),
+                           steps, warmup)
+        ref = layer(x, c, s, backend).float()
+        upd = (y.float() - x.float()) - (ref - x.float())
+        kern = _kernel_table(mp, torch, lambda: mp.map_decoder_layer(wl, x, pos, [0, S], out=y, workspace=ws), steps)
+        mus = 1e3 * mine["ms_per_step"]
+        ours[f"S{S}"] = {"us": mus, "achieved_tflops": flops / (mus * 1e-6) / 1e12,
+                         "hbm_weight_stream_frac": weight_bytes / (mus * 1e-6) / 1e9 / PEAK_HBM,
+                         "speedup_vs_pytorch": us / mus,
+                         "update_rel_diff_vs_pytorch": float(upd.norm() / (ref - x.float()).norm()),
+                         "kernels": kern}
+    res["map_decoder_layer"] = ours
     res["prune_us_per_image"] = prune_us
     res["prune_over_layer_prefill_2944"] = prune_us / res["prefill_us_S2944"]
     res["layer_prefill_2944_over_224"] = res["prefill_us_S2944"] / res["prefill_us_S224"]
+    # a 32-layer model's prefill, unpruned in PyTorch against pruning plus the
+    # pruned prefill in this library's layer (context: the paper's prefill
+    # figures also cover the vision encoder, which is not here)
+    res["prefill_32_layers_unpruned_pytorch_ms"] = 32 * res["prefill_us_S2944"] / 1e3
+    res["prune_plus_prefill_32_layers_pruned_ms"] = (prune_us + 32 * ours["S224"]["us"]) / 1e3
+    res["prefill_speedup_32_layers"] = res["prefill_32_layers_unpruned_pytorch_ms"] / \
+        res["prune_plus_prefill_32_layers_pruned_ms"]
     return res
 
 
