@@ -13,8 +13,9 @@
 //   rmsnorm     one workgroup per row, 16-byte pieces, float32 sum of squares
 //   rope_qkv    rotates q and k in place, angles pos * theta^(-2i/d_h) in float64
 //   attention   one workgroup per (64 query rows, head, sequence): the key
-//               blocks up to the diagonal through LDS with an online softmax;
-//               the causal mask follows the rows' order in their sequence
+//               blocks up to the diagonal through LDS on the bf16 matrix
+//               cores with an online softmax; the causal mask follows the
+//               rows' order in their sequence
 //   silu_mul    SiLU(gate) * up, 8 entries per thread
 #include "internal.h"
 
@@ -90,129 +91,181 @@ __global__ __launch_bounds__(NT) void rope_qkv_kernel(const DecoderArgs a) {
   }
 }
 
-// Workgroup (query block qb of 64 rows, head h, sequence b).  Thread
-// (ti, tj) = (tid / 16, tid % 16) owns score rows 4 ti .. 4 ti + 3, columns
-// 4 tj .. + 3, and output rows 4 ti .. + 3, dims 8 tj .. + 7; the 16 threads
-// of a row group are 16 consecutive lanes.  LDS (dynamic): q and k
-// transposed [128][68], v [64][132], p transposed [64][68], float32.
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+
+// Row and column of accumulator register r of lane `lane` in a 32 x 32
+// matrix-core block.
+__device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+
+// LDS strides of the attention tiles (bf16 entries; float32 for the scores).
+constexpr int LQ = DH + 8;   // q and k rows: [64][LQ]
+constexpr int LV = 64 + 8;   // v transposed (dims x keys) and p (queries x keys)
+constexpr int LS = 64 + 4;   // scores [64][LS] float32
+constexpr int kAttnLds = 2 * (2 * 64 * LQ + DH * LV + 64 * LV) + 4 * (64 * LS + 3 * 64);  // q, k, v^T, p; s, stats
+
+// Workgroup (query block qb of 64 rows, head h, sequence b), flash-style on
+// the bf16 matrix cores (32 x 32 x 16, float32 accumulation).  For each key
+// block up to the diagonal: wave w forms the 32 x 32 score tile (rows
+// 32 (w / 2), keys 32 (w % 2)) and stores it, scaled and masked, to LDS;
+// four threads per row then take the row's maximum and sum over the block
+// (two quad exchanges) and write p (bf16) and the running statistics; wave
+// w rescales its output tiles (rows 32 (w / 2), dims 64 (w % 2) + 0 and
+// + 32) and adds p v.
 __global__ __launch_bounds__(NT) void attention_kernel(const DecoderArgs a) {
-  extern __shared__ float lds[];
-  float(*QT)[68] = reinterpret_cast<float(*)[68]>(lds);
-  float(*KT)[68] = reinterpret_cast<float(*)[68]>(lds + 128 * 68);
-  float(*Vs)[132] = reinterpret_cast<float(*)[132]>(lds + 2 * 128 * 68);
-  float(*PT)[68] = reinterpret_cast<float(*)[68]>(lds + 2 * 128 * 68 + 64 * 132);
+  extern __shared__ uint4 lds4[];
+  bf16_t* Qs = reinterpret_cast<bf16_t*>(lds4);
+  bf16_t* Ks = Qs + 64 * LQ;
+  bf16_t* VT = Ks + 64 * LQ;
+  bf16_t* Ps = VT + DH * LV;
+  float* Ss = reinterpret_cast<float*>(Ps + 64 * LV);  // [64][LS]
+  float* mrow = Ss + 64 * LS;                           // [64] running maximum
+  float* lrow = mrow + 64;                              // [64] running sum
+  float* alph = lrow + 64;                              // [64] this block's rescaling
   const int qb = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
   const int s0 = a.seq_off[b], S = a.seq_off[b + 1] - s0, q0 = qb * 64;
   if (q0 >= S) return;
-  const int tid = threadIdx.x, ti = tid >> 4, tj = tid & 15;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wi = wave >> 1, wj = wave & 1;
+  const int lr = lane & 31, lh = lane >> 5;
   const long long ld = 3LL * a.d;
   const bf16_t* qkv = static_cast<const bf16_t*>(a.qkv);
-  // the query block, transposed into LDS
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
+  for (int u = 0; u < 4; ++u) {  // the query block, row-major
     const int e = tid + u * NT, r = e >> 4, c = (e & 15) * 8;
-    Bf8 v;
-    v.u = q0 + r < S ? *reinterpret_cast<const uint4*>(qkv + (s0 + q0 + r) * ld + h * DH + c)
-                     : make_uint4(0u, 0u, 0u, 0u);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) QT[c + k][r] = bf16_to_f32(v.e[k]);
+    *reinterpret_cast<uint4*>(Qs + r * LQ + c) =
+        q0 + r < S ? *reinterpret_cast<const uint4*>(qkv + (s0 + q0 + r) * ld + h * DH + c) : make_uint4(0u, 0u, 0u, 0u);
+  }
+  if (tid < 64) {
+    mrow[tid] = -INFINITY;
+    lrow[tid] = 0.0f;
   }
   const float scale = 1.0f / sqrtf(static_cast<float>(DH));
-  float m[4], l[4], O[4][8];
+  f32x16_t o[2];
 #pragma unroll
-  for (int x = 0; x < 4; ++x) {
-    m[x] = -INFINITY;
-    l[x] = 0.0f;
+  for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-    for (int c = 0; c < 8; ++c) O[x][c] = 0.0f;
-  }
+    for (int r = 0; r < 16; ++r) o[jj][r] = 0.0f;
+  const int srow = tid >> 2, sq = tid & 3;  // the row phase: row, quarter of its 64 keys
   for (int kb = 0; kb <= qb; ++kb) {
     const int k0 = kb * 64;
     __syncthreads();  // the previous block's k, v and p are no longer read
+    // keys row-major (16 rows x 16 pieces per pass); values transposed, a
+    // lane per pair of key rows so that each LDS store is one 32-bit word
+    uint4 kv[4], va[2], vb[2];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int e = tid + u * NT, r = e >> 4, c = (e & 15) * 8;
-      const bool ok = k0 + r < S;
-      Bf8 kv, vv;
-      kv.u = ok ? *reinterpret_cast<const uint4*>(qkv + (s0 + k0 + r) * ld + a.d + h * DH + c)
-                : make_uint4(0u, 0u, 0u, 0u);
-      vv.u = ok ? *reinterpret_cast<const uint4*>(qkv + (s0 + k0 + r) * ld + 2 * a.d + h * DH + c)
-                : make_uint4(0u, 0u, 0u, 0u);
+      kv[u] = k0 + r < S ? *reinterpret_cast<const uint4*>(qkv + (s0 + k0 + r) * ld + a.d + h * DH + c)
+                         : make_uint4(0u, 0u, 0u, 0u);
+    }
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        KT[c + k][r] = bf16_to_f32(kv.e[k]);
-        Vs[r][c + k] = bf16_to_f32(vv.e[k]);
+    for (int u = 0; u < 2; ++u) {
+      const int e = tid + u * NT, j = e & 31, c = (e >> 5) * 8, r = 2 * j;
+      va[u] = k0 + r < S ? *reinterpret_cast<const uint4*>(qkv + (s0 + k0 + r) * ld + 2 * a.d + h * DH + c)
+                         : make_uint4(0u, 0u, 0u, 0u);
+      vb[u] = k0 + r + 1 < S ? *reinterpret_cast<const uint4*>(qkv + (s0 + k0 + r + 1) * ld + 2 * a.d + h * DH + c)
+                             : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = tid + u * NT, r = e >> 4, c = (e & 15) * 8;
+      *reinterpret_cast<uint4*>(Ks + r * LQ + c) = kv[u];
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int e = tid + u * NT, j = e & 31, c = (e >> 5) * 8;
+      Bf8 x, y;
+      x.u = va[u];
+      y.u = vb[u];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        *reinterpret_cast<uint32_t*>(VT + (c + k) * LV + 2 * j) =
+            static_cast<uint32_t>(x.e[k]) | (static_cast<uint32_t>(y.e[k]) << 16);
+    }
+    __syncthreads();
+    // the score tile: rows 32 wi + lr (queries), columns 32 wj + lr (keys)
+    f32x16_t sc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sc[r] = 0.0f;
+#pragma unroll
+    for (int st = 0; st < DH / 16; ++st) {
+      const bf16x8_t qa = *reinterpret_cast<const bf16x8_t*>(Qs + (32 * wi + lr) * LQ + 16 * st + 8 * lh);
+      const bf16x8_t kk = *reinterpret_cast<const bf16x8_t*>(Ks + (32 * wj + lr) * LQ + 16 * st + 8 * lh);
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kk, sc, 0, 0, 0);
+    }
+    {
+      const int col = 32 * wj + lr, kj = k0 + col;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * wi + acc_row(r, lane);
+        Ss[row * LS + col] = (kj <= q0 + row && kj < S) ? sc[r] * scale : -INFINITY;
       }
     }
     __syncthreads();
-    float sc[4][4];
+    {  // row srow, keys 16 sq .. 16 sq + 15
+      float v[16];
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-      for (int y = 0; y < 4; ++y) sc[x][y] = 0.0f;
-#pragma unroll 4
-    for (int dd = 0; dd < DH; ++dd) {
-      const float4 qv = *reinterpret_cast<const float4*>(&QT[dd][4 * ti]);
-      const float4 kv = *reinterpret_cast<const float4*>(&KT[dd][4 * tj]);
-      const float qa[4] = {qv.x, qv.y, qv.z, qv.w}, ka[4] = {kv.x, kv.y, kv.z, kv.w};
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y) sc[x][y] = fmaf(qa[x], ka[y], sc[x][y]);
-    }
-    // causal mask, online softmax over this block's keys
-#pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      const int qi = q0 + 4 * ti + x;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int y = 0; y < 4; ++y) {
-        const int kj = k0 + 4 * tj + y;
-        sc[x][y] = (kj <= qi && kj < S) ? sc[x][y] * scale : -INFINITY;
-        mx = fmaxf(mx, sc[x][y]);
+      for (int k = 0; k < 16; k += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(Ss + srow * LS + 16 * sq + k);
+        v[k] = x.x;
+        v[k + 1] = x.y;
+        v[k + 2] = x.z;
+        v[k + 3] = x.w;
       }
+      float mx = v[0];
 #pragma unroll
-      for (int off = 8; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 16));
-      const float mn = fmaxf(m[x], mx);
-      const float alpha = (mn == -INFINITY || m[x] == -INFINITY) ? (mn == -INFINITY ? 1.0f : 0.0f) : __expf(m[x] - mn);
-      float rs = 0.0f;
+      for (int k = 1; k < 16; ++k) mx = fmaxf(mx, v[k]);
+      mx = fmaxf(mx, __shfl_xor(mx, 1, 4));
+      mx = fmaxf(mx, __shfl_xor(mx, 2, 4));
+      const float mo = mrow[srow], mn = fmaxf(mo, mx);
+      float sum = 0.0f;
+      Bf8 p0, p1;
 #pragma unroll
-      for (int y = 0; y < 4; ++y) {
-        const float p = mn == -INFINITY ? 0.0f : __expf(sc[x][y] - mn);
-        PT[4 * tj + y][4 * ti + x] = p;
-        rs += p;
+      for (int k = 0; k < 16; ++k) {
+        const float pv = mn == -INFINITY ? 0.0f : __expf(v[k] - mn);
+        sum += pv;
+        if (k < 8) p0.e[k] = f32_to_bf16(pv);
+        else p1.e[k - 8] = f32_to_bf16(pv);
       }
-#pragma unroll
-      for (int off = 8; off > 0; off >>= 1) rs += __shfl_xor(rs, off, 16);
-      l[x] = l[x] * alpha + rs;
-      m[x] = mn;
-#pragma unroll
-      for (int c = 0; c < 8; ++c) O[x][c] *= alpha;
+      *reinterpret_cast<uint4*>(Ps + srow * LV + 16 * sq) = p0.u;
+      *reinterpret_cast<uint4*>(Ps + srow * LV + 16 * sq + 8) = p1.u;
+      sum += __shfl_xor(sum, 1, 4);
+      sum += __shfl_xor(sum, 2, 4);
+      __syncthreads();  // every quarter has read mrow before it changes
+      if (sq == 0) {
+        const float al = mn == -INFINITY ? 1.0f : (mo == -INFINITY ? 0.0f : __expf(mo - mn));
+        lrow[srow] = lrow[srow] * al + sum;
+        mrow[srow] = mn;
+        alph[srow] = al;
+      }
     }
     __syncthreads();
-#pragma unroll 4
-    for (int j = 0; j < 64; ++j) {
-      const float4 pv = *reinterpret_cast<const float4*>(&PT[j][4 * ti]);
-      const float4 v0 = *reinterpret_cast<const float4*>(&Vs[j][8 * tj]);
-      const float4 v1 = *reinterpret_cast<const float4*>(&Vs[j][8 * tj + 4]);
-      const float pa[4] = {pv.x, pv.y, pv.z, pv.w}, va[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
-      for (int x = 0; x < 4; ++x)
+    for (int r = 0; r < 16; ++r) {
+      const float al = alph[32 * wi + acc_row(r, lane)];
+      o[0][r] *= al;
+      o[1][r] *= al;
+    }
 #pragma unroll
-        for (int c = 0; c < 8; ++c) O[x][c] = fmaf(pa[x], va[c], O[x][c]);
+    for (int st = 0; st < 4; ++st) {
+      const bf16x8_t pa = *reinterpret_cast<const bf16x8_t*>(Ps + (32 * wi + lr) * LV + 16 * st + 8 * lh);
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const bf16x8_t vb2 = *reinterpret_cast<const bf16x8_t*>(VT + (64 * wj + 32 * jj + lr) * LV + 16 * st + 8 * lh);
+        o[jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, vb2, o[jj], 0, 0, 0);
+      }
     }
   }
+  __syncthreads();
   bf16_t* out = static_cast<bf16_t*>(a.o);
 #pragma unroll
-  for (int x = 0; x < 4; ++x) {
-    const int row = q0 + 4 * ti + x;
-    if (row >= S) continue;
-    const float inv = 1.0f / l[x];
-    Bf8 o;
+  for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-    for (int c = 0; c < 8; ++c) o.e[c] = f32_to_bf16(O[x][c] * inv);
-    *reinterpret_cast<uint4*>(out + (long long)(s0 + row) * a.d + h * DH + 8 * tj) = o.u;
-  }
+    for (int r = 0; r < 16; ++r) {
+      const int row = 32 * wi + acc_row(r, lane);
+      if (q0 + row < S)
+        out[(long long)(s0 + q0 + row) * a.d + h * DH + 64 * wj + 32 * jj + lr] = f32_to_bf16(o[jj][r] / lrow[row]);
+    }
 }
 
 // act[r][i] = SiLU(gu[r][i]) * gu[r][ff + i], 8 entries per thread.
@@ -244,7 +297,7 @@ hipError_t launch_rope_qkv(const DecoderArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_attention(const DecoderArgs& a, hipStream_t s) {
-  constexpr int bytes = sizeof(float) * (2 * 128 * 68 + 64 * 132 + 64 * 68);
+  constexpr int bytes = kAttnLds;
   const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(attention_kernel),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
