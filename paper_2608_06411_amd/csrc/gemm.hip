@@ -848,6 +848,135 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
     epilogue<bf16_t>(P, bt, tm, tn, acc, L.q0, L.q1, tid, lane, wm, wn);
 }
 
+// ------------------------------------------------------------ 256 x 256 tiles
+// Launches of several waves of workgroups (the first layer over a batch of
+// images, the decoder layer's long products) run 256 x 256 tiles: per
+// product a compute unit then moves half the bytes from L2 into LDS and
+// reads half as many operand bytes from LDS as with 128 x 128 tiles, which
+// is what bounds the smaller tile.  512 threads, eight wave64s, two per
+// SIMD; wave w (group h = w / 4, (qm, qn) = ((w / 2) % 2, w % 2)) owns rows
+// 128 h + 64 qm + (0..63) and columns 128 s + 64 qn + (0..63) for s = 0, 1,
+// i.e. 2 x 4 MFMA 32x32 blocks whose two A operands serve four products.
+// Group h then holds sub-tiles (h, 0) and (h, 1) in the 128 x 128 kernel's
+// accumulator layout and finishes them with its epilogues, staging through
+// its own 64 KiB.  Two 64 KiB stages: one K slice loads while the matrix
+// cores consume the other.  Tiles are ordered in groups of kBigRows tile
+// rows, column by column inside a group, each XCD taking a contiguous range.
+constexpr int kBig = 256;
+constexpr int kBigThreads = 512;
+constexpr int kBigRows = 4;
+
+__global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch args) {
+  __shared__ uint4 bst0[2 * kBig][8], bst1[2 * kBig][8];  // per stage: A rows, then B rows
+  const int tile = xcd_remap(blockIdx.x, args.total_tiles);
+  int pi = 0;
+#pragma unroll
+  for (int q = 1; q < kMaxGemmProblems; ++q)
+    if (q < args.count && tile >= args.p[q].tile_begin) pi = q;
+  const GemmProblem& P = args.p[pi];
+  const int local = tile - P.tile_begin;
+  const int bt = local / P.tiles_per_batch, tt = local - bt * P.tiles_per_batch;
+  const int grp = tt / (kBigRows * P.tiles_n), first = grp * kBigRows;
+  const int rows = min(kBigRows, P.tiles_m - first), in = tt - grp * kBigRows * P.tiles_n;
+  const int tm = first + in % rows, tn = in / rows;
+  if (P.run_if && P.run_if[bt] == 0) return;
+  const int M = P.M, N = P.N, m0 = tm * kBig, n0 = tn * kBig;
+  const bf16_t* __restrict__ A = static_cast<const bf16_t*>(P.A) + bt * P.strideA;
+  const bf16_t* __restrict__ B = static_cast<const bf16_t*>(P.B) + bt * P.strideB;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = wave >> 2, qm = (wave >> 1) & 1, qn = wave & 1;
+  const int nk = P.K / 64;
+  // wave w loads rows 32 w .. 32 w + 31 of the A tile and of the B tile,
+  // one instruction per 8 rows (rows past the matrix read its last row)
+  const int32_t* mapA = P.mapA ? P.mapA + bt * P.mapStride : nullptr;
+  const int32_t* mapB = P.mapB ? P.mapB + bt * P.mapStride : nullptr;
+  const bf16_t* ga[4];
+  const bf16_t* gb[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = 32 * wave + 8 * j + (lane >> 3);
+    const int v = (lane & 7) ^ swz(r);
+    const int ra = min(m0 + r, M - 1), rb = min(n0 + r, N - 1);
+    ga[j] = A + (long long)(mapA ? mapA[ra] : ra) * P.lda + 8 * v;
+    gb[j] = B + (long long)(mapB ? mapB[rb] : rb) * P.ldb + 8 * v;
+  }
+  const uint32_t wrow = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave)) * 32u * 128u;
+  auto issue = [&](uint4 (*dst)[8], int kt) {
+    const int k0 = kt * 64;
+    const uint32_t m = lds_addr(&dst[0][0]) + wrow;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      dma16(ga[j] + k0, m + 1024u * j);
+      dma16(gb[j] + k0, m + kBig * 128u + 1024u * j);
+    }
+  };
+  f32x16_t acc[2][2][2];  // [s][i][j]: rows 128 h + 64 qm + 32 i, columns 128 s + 64 qn + 32 j
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[s][i][j][r] = 0.0f;
+  const int lr = lane & 31, lh = lane >> 5;
+  // One K slice: four steps of 16; the operands of step s + 1 are read
+  // before the products of step s issue.
+  auto mma = [&](const uint4 (*st)[8]) {
+    const uint4 (*As)[8] = st;
+    const uint4 (*Bs)[8] = st + kBig;
+    bf16x8_t a[2][2], b[2][4];
+    auto read = [&](int s, int buf) {
+      const int v = 2 * s + lh;  // 16-byte chunk: k = 16 s + 8 lh + (0..7)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int r = 128 * h + 64 * qm + 32 * i + lr;
+        a[buf][i] = __builtin_bit_cast(bf16x8_t, As[r][v ^ swz(r)]);
+      }
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int r = 128 * (c >> 1) + 64 * qn + 32 * (c & 1) + lr;
+        b[buf][c] = __builtin_bit_cast(bf16x8_t, Bs[r][v ^ swz(r)]);
+      }
+    };
+    read(0, 0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s < 3) read(s + 1, (s + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          acc[c >> 1][i][c & 1] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s & 1][i], b[s & 1][c], acc[c >> 1][i][c & 1], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // Step kt waits for this wave's loads of slice kt, then for every wave's
+  // at the barrier (which also means every wave is done with slice kt - 1,
+  // whose stage now receives slice kt + 1), and runs the products.
+  issue(bst0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    wait_vm_lgkm0(0);
+    __builtin_amdgcn_s_barrier();
+    if (kt + 1 < nk) issue((kt & 1) ? bst0 : bst1, kt + 1);
+    mma((kt & 1) ? bst1 : bst0);
+  }
+  __syncthreads();  // the epilogues reuse the stages: group h stages through bst<h>
+  float* stg = reinterpret_cast<float*>(h ? &bst1[0][0] : &bst0[0][0]);
+  const StagedTile L{stg, stg + 64 * BN, nullptr, nullptr};
+  const int t2 = tid & (NT - 1);
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    if (s) __syncthreads();  // the staging is read out before it is written again
+    if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS)
+      epi_bias_staged(P, bt, m0 + 128 * h, n0 + 128 * s, acc[s], L, t2, lane, qm, qn);
+    else
+      epi_direct_staged(P, bt, m0 + 128 * h, n0 + 128 * s, acc[s], L, t2, lane, qm, qn);
+  }
+}
+
 // Projection to d_p <= 128 columns with the RoPE epilogue (the keys and
 // queries of Eq. (3)): C = RoPE(A B^T + bias), A [M][K] and B [N][K] bf16.
 // With N this small a 128 x 128 tile leaves most compute units idle, each
@@ -1111,6 +1240,52 @@ bool gemm_direct_loads(map_dtype dt, const GemmBatch& g) {
   return dma;
 }
 
+// Compute units of the current device (cached per device).
+static int gemm_cus() {
+  static int cached[16] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return 256;
+  if (cached[dev] == 0) {
+    int c = 0;
+    cached[dev] = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && c > 0 ? c : 256;
+  }
+  return cached[dev];
+}
+
+// 256 x 256 tiles for a direct-load launch whose problems all have a
+// row-wise epilogue (bias, GELU, float32, GELU', product, residual) and no
+// K split, when they take fewer waves of workgroups: a wave of 256 x 256
+// tiles costs about 2.3 waves of 128 x 128 tiles (measured on the first
+// layer's and the decoder layer's shapes).
+static bool big_tiles_pay(const GemmBatch& g) {
+  if (g.norm_blocks) return false;
+  long long t128 = 0, t256 = 0;
+  for (int i = 0; i < g.count; ++i) {
+    const GemmProblem& p = g.p[i];
+    if (!(p.epi == EPI_BIAS || p.epi == EPI_BIAS_GELU || epi_direct(p.epi)) || p.ksplit > 1 || p.triangular)
+      return false;
+    t128 += (long long)((p.M + 127) / 128) * ((p.N + 127) / 128) * p.batch;
+    t256 += (long long)((p.M + kBig - 1) / kBig) * ((p.N + kBig - 1) / kBig) * p.batch;
+  }
+  const long long cus = gemm_cus();
+  return 23 * ((t256 + cus - 1) / cus) < 10 * ((t128 + cus - 1) / cus);
+}
+
+static void finalize_big(GemmBatch& g) {
+  int begin = 0;
+  for (int i = 0; i < g.count; ++i) {
+    GemmProblem& p = g.p[i];
+    p.tiles_m = (p.M + kBig - 1) / kBig;
+    p.tiles_n = (p.N + kBig - 1) / kBig;
+    p.tiles_tri = p.tiles_m * p.tiles_n;
+    p.tiles_per_batch = p.tiles_tri;
+    p.tile_begin = begin;
+    begin += p.tiles_per_batch * p.batch;
+  }
+  g.total_tiles = begin;
+  g.first_tiles = 0;
+}
+
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s) {
   if (g.total_tiles == 0) return hipSuccess;
   if (dt == MAP_BF16) {
@@ -1121,6 +1296,11 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
             (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
             p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
             k_ranges_ok(p);
+    }
+    if (dma && big_tiles_pay(g)) {
+      GemmBatch q = g;
+      finalize_big(q);
+      return launch_kernel(name, gemm_big_kernel, dim3(q.total_tiles), dim3(kBigThreads), 0, s, q);
     }
     if (dma) return launch_kernel(name, gemm_dma_kernel, dim3(g.total_tiles + g.norm_blocks), dim3(NT), 0, s, g);
     if (g.norm_blocks) return hipErrorInvalidValue;

@@ -80,6 +80,20 @@ def test_decoder_7b_shape_pruned_length():
     _run_and_check(X, pos, [0, 224], _weights(d, ff, 6), H, "7B 224")
 
 
+def test_decoder_long_sequences_large_tiles():
+    """Two sequences of 2944 and 1500 rows at d 1024 (8 heads), SwiGLU 2816:
+    the QKV and gate/up products have enough tiles for the 256 x 256
+    kernel (4444 rows: a ragged last tile row), the output and down
+    products stay on 128 x 128 tiles."""
+    d, H, ff = 1024, 8, 2816
+    announce("decoder long sequences, 4444 rows at d 1024")
+    rng = np.random.default_rng(8)
+    seq_off = [0, 2944, 4444]
+    X = f32_to_bf16_bits(rng.standard_normal((seq_off[-1], d)).astype(np.float32))
+    pos = np.concatenate([np.arange(2944), np.arange(1500) * 2]).astype(np.int32)
+    _run_and_check(X, pos, seq_off, _weights(d, ff, 9, std=0.03), H, "long")
+
+
 def test_decoder_on_the_pruned_layer0_input():
     """map_prune_assemble's output for two images is the layer's input: the
     sequences are each image's kept rows then its question rows."""

@@ -46,6 +46,9 @@ CASES = {
     # where a 10 % logit-scale error moves p_hat by more than the bf16 bar
     "peaked_bf16": ("tiny", {"dtype": "bf16", "pred": PredictorShape(weight_std=0.03)}, 2e-2),
     "peaked_f32": ("tiny", {"pred": PredictorShape(weight_std=0.03)}, 1e-5),
+    # eight images: the first layer takes the 256 x 256 tiles of large launches
+    "batch8_peaked_bf16": ("sweep", {"B": 8, "N": 2880, "M": (16, 64),
+                                     "pred": PredictorShape(D=1024, D_h=1024, d_p=128, weight_std=0.03)}, 2e-2),
 }
 
 
