@@ -60,6 +60,27 @@ def subset_tokens(cfg, setting=0):
     return nc if nc < cfg.N else 0
 
 
+def norms_in_prep(cfg, sumM, nc, cus=256):
+    """Whether map_prune's prep launch reads V for the row norms, restated
+    from the library: on the subset path (bf16) the first-layer launch forms
+    them, by its 256 x 256 tiles when those take fewer waves (a wave of them
+    costs about 2.3 waves of 128 x 128 tiles), else by workgroups on the
+    compute units its last wave of 128 x 128 tiles leaves idle (at least 16,
+    at most 128 rows each); otherwise prep does."""
+    if not nc or cfg.dtype != "bf16":
+        return True
+    H, dp = cfg.pred.D_h, cfg.pred.d_p
+
+    def tiles(t):
+        c = lambda a: -(-a // t)  # noqa: E731
+        return c(cfg.B * cfg.N) * c(H) + c(sumM) * c(H) + 2 * c(dp) * c(H)
+    t128, t256 = tiles(128), tiles(256)
+    if 23 * -(-t256 // cus) < 10 * -(-t128 // cus):
+        return False
+    idle = (cus - t128 % cus) % cus
+    return not (idle >= 16 and idle * 128 >= cfg.B * cfg.N)
+
+
 def algorithmic_work(cfg, sumM, gathered=True, nc=0):
     """Per-launch algorithmic work of each kernel: (bound, amount, unit).
     `gathered`: the selection launch also gathers the kept rows (no gather launch).
@@ -89,8 +110,9 @@ def algorithmic_work(cfg, sumM, gathered=True, nc=0):
         "gemm_proj_rope": ("mfma", 2.0 * rows * H * dp, "flop"),
         # read V, write norms, 1/norms and the cos/sin table; transpose the two
         # second-layer weights and fold the biases
-        # (on the subset path the layer-1 launch forms the norms: no V here)
-        "prep": ("hbm", (0.0 if nc else B * N * D * el + 8.0 * B * N) + 8.0 * rows * dp / 2 + 2 * 2.0 * H * H * el
+        # (on the subset path the layer-1 launch usually forms the norms: no V here)
+        "prep": ("hbm", (B * N * D * el + 8.0 * B * N if norms_in_prep(cfg, sumM, nc) else 0.0)
+                 + 8.0 * rows * dp / 2 + 2 * 2.0 * H * H * el
                  + 2 * (dp * H + H) * el + 8.0 * dp, "byte"),
         # read the selection order and the kept rows, write the rows, indices and positions
         "gather": ("hbm", 2.0 * B * K * D * el + 16.0 * B * K, "byte"),

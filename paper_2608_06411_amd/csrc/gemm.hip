@@ -920,6 +920,14 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[s][i][j][r] = 0.0f;
   const int lr = lane & 31, lh = lane >> 5;
+  // Row norms (args.norm_tiles): in the first tile column each wave also
+  // sums the squares of one of the two A operands it reads, the one of rows
+  // 128 h + 64 qm + 32 qn + (0..31) (lane l: row l & 31, the k-half l >> 5 of
+  // every 16), in float32, slice after slice; the two halves are added at
+  // the end.  (The two waves of a (h, qm) pair read the same A operands and
+  // sit on different SIMDs, so each SIMD gets an equal share.)
+  const bool sumsq = args.norm_tiles == pi + 1 && tn == 0;
+  float nacc = 0.0f;
   // One K slice: four steps of 16; the operands of step s + 1 are read
   // before the products of step s issue.
   auto mma = [&](const uint4 (*st)[8]) {
@@ -950,6 +958,15 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
         for (int c = 0; c < 4; ++c)
           acc[c >> 1][i][c & 1] =
               __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s & 1][i], b[s & 1][c], acc[c >> 1][i][c & 1], 0, 0, 0);
+      if (sumsq) {  // (vector ALU work under the products)
+        const uint4 u = __builtin_bit_cast(uint4, qn ? a[s & 1][1] : a[s & 1][0]);
+        const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const float x = __uint_as_float((k & 1) ? (wv[k >> 1] & 0xffff0000u) : (wv[k >> 1] << 16));
+          nacc = fmaf(x, x, nacc);
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -962,6 +979,15 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
     __builtin_amdgcn_s_barrier();
     if (kt + 1 < nk) issue((kt & 1) ? bst0 : bst1, kt + 1);
     mma((kt & 1) ? bst1 : bst0);
+  }
+  if (sumsq) {
+    const float t = nacc + __shfl_xor(nacc, 32);
+    const int row = m0 + 128 * h + 64 * qm + 32 * qn + lr;
+    if (lh == 0 && row < M) {
+      const float n = sqrtf(t);
+      args.norms[row] = n;
+      args.ninv[row] = n > 0.0f ? 1.0f / n : 0.0f;
+    }
   }
   __syncthreads();  // the epilogues reuse the stages: group h stages through bst<h>
   float* stg = reinterpret_cast<float*>(h ? &bst1[0][0] : &bst0[0][0]);
@@ -1259,6 +1285,7 @@ static int gemm_cus() {
 // layer's and the decoder layer's shapes).
 static bool big_tiles_pay(const GemmBatch& g) {
   if (g.norm_blocks) return false;
+  if (g.norm_tiles > 0 && (g.norm_tiles > g.count || g.p[g.norm_tiles - 1].batch != 1)) return false;
   long long t128 = 0, t256 = 0;
   for (int i = 0; i < g.count; ++i) {
     const GemmProblem& p = g.p[i];
@@ -1286,8 +1313,12 @@ static void finalize_big(GemmBatch& g) {
   g.first_tiles = 0;
 }
 
+bool gemm_big_tiles(map_dtype dt, const GemmBatch& g) { return gemm_direct_loads(dt, g) && big_tiles_pay(g); }
+
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s) {
   if (g.total_tiles == 0) return hipSuccess;
+  // the in-tile row norms exist in the 256 x 256 kernel only
+  if (g.norm_tiles > 0 && !gemm_big_tiles(dt, g)) return hipErrorInvalidValue;
   if (dt == MAP_BF16) {
     bool dma = true;  // every problem meets the direct-load requirements
     for (int i = 0; i < g.count; ++i) {

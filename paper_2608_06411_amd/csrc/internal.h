@@ -125,10 +125,15 @@ struct GemmBatch {
   int norm_rows, norm_D;
   float* norms;
   float* ninv;
+  // 256 x 256 tiles only (gemm_big_tiles): when norm_tiles = q + 1 > 0, the
+  // tiles of problem q (batch 1) in its first tile column also write the row
+  // norms of its A rows and their reciprocals (norm_blocks must be 0)
+  int norm_tiles;
 };
 
 void gemm_finalize(GemmBatch& g);  // computes the tile counts
 bool gemm_direct_loads(map_dtype dt, const GemmBatch& g);  // launch_gemm would use the direct-load kernel
+bool gemm_big_tiles(map_dtype dt, const GemmBatch& g);     // ... with 256 x 256 tiles
 hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s);
 // The projection with the RoPE epilogue (every problem EPI_ROPE, at most two):
 // a K-split kernel for bf16 and N <= 128, else launch_gemm.

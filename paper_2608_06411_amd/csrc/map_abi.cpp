@@ -296,10 +296,16 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   // the Gram matrix last: its tiles are dispatched after every tile above
   if (extra_l1) g1.p[g1.count++] = *extra_l1;
   gemm_finalize(g1);
-  // The row norms: by prep, or (norms_in_layer1) by workgroups of the
-  // layer-1 launch on the compute units its last wave of tiles leaves idle,
-  // when there are at least 16 of them and at most 128 rows each.
-  if (norms_in_layer1 && gemm_direct_loads(dt, g1) && (reinterpret_cast<uintptr_t>(V) & 15) == 0) {
+  // The row norms: by prep, or (norms_in_layer1) inside the layer-1 launch:
+  // with 256 x 256 tiles, by the first column of f_V's tiles from the
+  // operands they read; otherwise by workgroups on the compute units its
+  // last wave of tiles leaves idle, when there are at least 16 of them and
+  // at most 128 rows each.
+  if (norms_in_layer1 && gemm_big_tiles(dt, g1)) {
+    g1.norm_tiles = 1;  // problem 0: layer 1 of f_V, A = V
+    g1.norms = norms;
+    g1.ninv = ninv;
+  } else if (norms_in_layer1 && gemm_direct_loads(dt, g1) && (reinterpret_cast<uintptr_t>(V) & 15) == 0) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0) {
@@ -314,7 +320,7 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
       }
     }
   }
-  hipError_t e = launch_prep(dt, pa, norms != nullptr && g1.norm_blocks == 0, true, true, st);
+  hipError_t e = launch_prep(dt, pa, norms != nullptr && g1.norm_blocks == 0 && g1.norm_tiles == 0, true, true, st);
   if (e != hipSuccess) return e;
   if ((e = launch_gemm(dt, g1, extra_l1 ? "gemm_layer1_gram" : "gemm_layer1", st)) != hipSuccess) return e;
 

@@ -866,9 +866,19 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       const int m0 = a.q_off[b], M = a.q_off[b + 1] - m0, nq = w < M ? (M - w + G - 1) / G : 0;
       const uint4* qs = static_cast<const uint4*>(a.qT) + (long long)m0 * chunks;
       uint4* qd = dst + (long long)K * chunks;
-      for (int e = tid; e < nq * chunks; e += NT) {
-        const int j = e / chunks, c = e - j * chunks, m = w + G * j;
-        qd[(long long)m * chunks + c] = qs[(long long)m * chunks + c];
+      constexpr int QU = 4;  // loads in flight per thread
+      for (int e0 = tid; e0 < nq * chunks; e0 += QU * NT) {
+        uint4 v[QU];
+#pragma unroll
+        for (int u = 0; u < QU; ++u) {
+          const int e = min(e0 + u * NT, nq * chunks - 1), j = e / chunks, m = w + G * j;
+          v[u] = qs[(long long)m * chunks + (e - j * chunks)];
+        }
+#pragma unroll
+        for (int u = 0; u < QU; ++u) {
+          const int e = e0 + u * NT, j = e / chunks, m = w + G * j;
+          if (e < nq * chunks) qd[(long long)m * chunks + (e - j * chunks)] = v[u];
+        }
       }
       for (int j = tid; j < nq; j += NT) a.gpos_out[orow + K + w + G * j] = a.qpos[m0 + w + G * j];
     }
