@@ -427,16 +427,24 @@ struct StagedTile {
   __device__ float* col_chunk(int c, int ch) const { return (c < 64 ? t0 : t1) + (c & 63) * BM + 4 * (ch ^ (c & 31)); }
 };
 
+// The staged epilogues take the accumulators of either layout of a 128 x
+// 128 tile: J = 2, four waves (wm, wn) of 64 x 64 (2 x 2 blocks, columns
+// 64 wn + 32 j), 256 threads; J = 1, eight waves (wm, wn) of 64 x 32 (rows
+// 64 wm + 32 i, columns 32 wn), 512 threads.
+template <int J> struct EpiThreads { static constexpr int value = J == 2 ? 256 : 512; };
+
 // Bias (+ GELU) in float32, bf16 output.
+template <int J>
 __device__ __forceinline__ void epi_bias_staged(const GemmProblem& P, int bt, int m0, int n0,
-                                                f32x16_t (&acc)[2][2], const StagedTile& L, int tid,
+                                                f32x16_t (&acc)[2][J], const StagedTile& L, int tid,
                                                 int lane, int wm, int wn) {
+  constexpr int NTH = EpiThreads<J>::value;
   const int M = P.M, N = P.N;
   const bf16_t* __restrict__ bias = static_cast<const bf16_t*>(P.bias);
   const bool gelu = P.epi == EPI_BIAS_GELU;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int cl = wn * 64 + j * 32 + acc_col(lane);
+  for (int j = 0; j < J; ++j) {
+    const int cl = wn * (32 * J) + j * 32 + acc_col(lane);
     const float bv = (bias && n0 + cl < N) ? bf16_to_f32(bias[n0 + cl]) : 0.0f;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -451,7 +459,7 @@ __device__ __forceinline__ void epi_bias_staged(const GemmProblem& P, int bt, in
   bf16_t* __restrict__ C = static_cast<bf16_t*>(P.C) + bt * P.strideC;
   const bool vec = (P.ldc & 7) == 0 && (reinterpret_cast<uintptr_t>(C) & 15) == 0;
 #pragma unroll 2
-  for (int e = tid; e < BM * (BN / 8); e += NT) {  // 8 columns per item
+  for (int e = tid; e < BM * (BN / 8); e += NTH) {  // 8 columns per item
     const int r = e >> 4, c8 = (e & 15) * 8;
     const int row = m0 + r, col = n0 + c8;
     if (row >= M || col >= N) continue;
@@ -487,14 +495,16 @@ __device__ __forceinline__ uint4 pack_bf16x8(const float (&f)[8]) {
   return o;
 }
 
+template <int J>
 __device__ __forceinline__ void epi_direct_staged(const GemmProblem& P, int bt, int m0, int n0,
-                                                  f32x16_t (&acc)[2][2], const StagedTile& L, int tid,
+                                                  f32x16_t (&acc)[2][J], const StagedTile& L, int tid,
                                                   int lane, int wm, int wn) {
+  constexpr int NTH = EpiThreads<J>::value;
   const int M = P.M, N = P.N, e = P.epi;
   const bf16_t* __restrict__ bias = static_cast<const bf16_t*>(P.bias);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int cl = wn * 64 + j * 32 + acc_col(lane);
+  for (int j = 0; j < J; ++j) {
+    const int cl = wn * (32 * J) + j * 32 + acc_col(lane);
     const float bv = (e == EPI_GELU2 && bias && n0 + cl < N) ? bf16_to_f32(bias[n0 + cl]) : 0.0f;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -506,7 +516,7 @@ __device__ __forceinline__ void epi_direct_staged(const GemmProblem& P, int bt, 
   const bool vec = (P.ldc & 7) == 0 && (reinterpret_cast<uintptr_t>(P.C) & 15) == 0 &&
                    (!P.aux || (reinterpret_cast<uintptr_t>(P.aux) & 15) == 0) && (base & 7) == 0;
 #pragma unroll 2
-  for (int it = tid; it < BM * (BN / 8); it += NT) {  // 8 columns per item
+  for (int it = tid; it < BM * (BN / 8); it += NTH) {  // 8 columns per item
     const int r = it >> 4, c8 = (it & 15) * 8;
     const int row = m0 + r, col = n0 + c8;
     if (row >= M || col >= N) continue;
@@ -572,15 +582,17 @@ __device__ __forceinline__ void epi_direct_staged(const GemmProblem& P, int bt, 
 // (row, col) and (col, row) from the same float, so S is bitwise symmetric.
 // A diagonal tile takes the entries below its diagonal from the transposed
 // copy (the mirror of the entries above it).
+template <int J>
 __device__ __forceinline__ void epi_cosine_staged(const GemmProblem& P, int bt, int tm, int tn,
-                                                  f32x16_t (&acc)[2][2], const StagedTile& L,
+                                                  f32x16_t (&acc)[2][J], const StagedTile& L,
                                                   const float* rs_rows, const float* rs_cols, int tid,
                                                   int lane, int wm, int wn) {
+  constexpr int NTH = EpiThreads<J>::value;
   const int M = P.M, N = P.N, m0 = tm * BM, n0 = tn * BN;
   const bool diag = tm == tn;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int cl = wn * 64 + j * 32 + acc_col(lane);
+  for (int j = 0; j < J; ++j) {
+    const int cl = wn * (32 * J) + j * 32 + acc_col(lane);
     const float sc = rs_cols[cl];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -600,7 +612,7 @@ __device__ __forceinline__ void epi_cosine_staged(const GemmProblem& P, int bt, 
   float* __restrict__ S = static_cast<float*>(P.C) + bt * P.strideC;
   const bool vec = (P.ldc & 3) == 0;
   // S[m0 + r][n0 + 4 ch ..]: row r of the tile (the mirror below a diagonal tile's diagonal)
-  for (int e = tid; e < BM * (BN / 4); e += NT) {
+  for (int e = tid; e < BM * (BN / 4); e += NTH) {
     const int r = e >> 5, ch = e & 31;
     const int row = m0 + r, col = n0 + 4 * ch;
     if (row >= M || col >= N) continue;
@@ -622,7 +634,7 @@ __device__ __forceinline__ void epi_cosine_staged(const GemmProblem& P, int bt, 
   }
   if (diag) return;
   // S[n0 + c][m0 + 4 ch ..]: column c of the tile
-  for (int e = tid; e < BN * (BM / 4); e += NT) {
+  for (int e = tid; e < BN * (BM / 4); e += NTH) {
     const int c = e >> 5, ch = e & 31;
     const int row = n0 + c, col = m0 + 4 * ch;
     if (row >= N || col >= M) continue;
@@ -640,14 +652,17 @@ __device__ __forceinline__ void epi_cosine_staged(const GemmProblem& P, int bt, 
 // bf16 variant with a five-stage LDS ring filled by direct global->LDS loads
 // (global_load_lds_dwordx4): four K slices are in flight while the matrix
 // cores consume the fifth, with no register staging, and the five 32 KiB
-// stages fill gfx950's 160 KiB of LDS.  Each wave moves 32 rows of A and 32
-// rows of B per slice, one instruction per 8 rows: lane l lands at row
+// stages fill gfx950's 160 KiB of LDS.  Eight waves, two per SIMD (one
+// wave's products run while the other waits on LDS or at the barrier):
+// wave (wm, wn) = (w / 4, w % 4) forms 64 x 32 of the tile.  Each wave moves
+// 16 rows of A and 16 rows of B per slice, one instruction per 8 rows: lane l lands at row
 // 8j + l/8, chunk position l%8 of its instruction's 1 KiB, and fetches the
 // chunk the XOR swizzle puts there.  The stages are separate LDS arrays
 // addressed with compile-time stage numbers, so the only waits on those
 // loads are the explicit counted ones before each barrier.
 // Requirements (checked by the host): K % 256 == 0, lda and ldb multiples of
-// 8, A and B 16-byte aligned.
+// 8, A and B 16-byte aligned, a staged epilogue (bias, cosine, direct) or
+// EPI_PARTIAL.
 
 // LDS byte address of a __shared__ object (the value M0 takes for a direct load).
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
@@ -669,12 +684,44 @@ __device__ __forceinline__ void dma16(const void* gsrc, uint32_t m) {
 
 __device__ __forceinline__ void wait_vm_lgkm0(int outstanding) {
   // s_waitcnt encoding: vmcnt in bits [3:0] and [15:14], expcnt [6:4]
-  // (7 = no wait), lgkmcnt [11:8]; here vmcnt = outstanding (0, 8, 16 or
-  // 24) and lgkmcnt = 0
+  // (7 = no wait), lgkmcnt [11:8]; here vmcnt = outstanding (0, 4, 8, 12,
+  // 16 or 24; anything else waits for more) and lgkmcnt = 0
   if (outstanding >= 24) __builtin_amdgcn_s_waitcnt(0x4078);
   else if (outstanding >= 16) __builtin_amdgcn_s_waitcnt(0x4070);
+  else if (outstanding >= 12) __builtin_amdgcn_s_waitcnt(0x007c);
   else if (outstanding >= 8) __builtin_amdgcn_s_waitcnt(0x0078);
+  else if (outstanding >= 4) __builtin_amdgcn_s_waitcnt(0x0074);
   else __builtin_amdgcn_s_waitcnt(0x0070);
+}
+
+// One K slice of the eight-wave 128 x 128 tile: wave (wm, wn) forms rows
+// 64 wm + (0..63) by columns 32 wn + (0..31), two 32x32 blocks sharing the B
+// operand; the operands of step s + 1 are read before the products of
+// step s issue.
+__device__ __forceinline__ void mma_slice8(const uint4 (*As)[8], const uint4 (*Bs)[8], int wm, int wn, int lane,
+                                           f32x16_t (&acc)[2][1]) {
+  const int lr = lane & 31, lh = lane >> 5;
+  bf16x8_t a[2][2], b[2];
+  auto read = [&](int s, int buf) {
+    const int v = 2 * s + lh;  // 16-byte chunk: k = 16 s + 8 lh + (0..7)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = wm * 64 + i * 32 + lr;
+      a[buf][i] = __builtin_bit_cast(bf16x8_t, As[r][v ^ swz(r)]);
+    }
+    const int r = wn * 32 + lr;
+    b[buf] = __builtin_bit_cast(bf16x8_t, Bs[r][v ^ swz(r)]);
+  };
+  read(0, 0);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if (s < 3) read(s + 1, (s + 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s & 1][i], b[s & 1], acc[i][0], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 }
 
 // Row norms for the workgroups past the tiles: rows of one block spread over
@@ -684,10 +731,10 @@ __device__ __forceinline__ void wait_vm_lgkm0(int outstanding) {
 __device__ __forceinline__ void norm_rows(const GemmBatch& args, int blk) {
   const int rows = args.norm_rows, D = args.norm_D, nb = args.norm_blocks;
   const int per = (rows + nb - 1) / nb, r0 = blk * per, r1 = min(rows, r0 + per);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   constexpr int VEC = 8, U = 8;
   const int nchunk = D / VEC;
-  for (int r = r0 + 2 * wave; r < r1; r += 2 * (NT / 64)) {
+  for (int r = r0 + 2 * wave; r < r1; r += 2 * nw) {
     const bf16_t* row0 = static_cast<const bf16_t*>(args.norm_V) + (long long)r * D;
     const bf16_t* row1 = static_cast<const bf16_t*>(args.norm_V) + (long long)min(r + 1, r1 - 1) * D;
     float acc[2] = {0.0f, 0.0f};
@@ -726,7 +773,9 @@ __device__ __forceinline__ void norm_rows(const GemmBatch& args, int blk) {
   }
 }
 
-__global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
+constexpr int kDmaThreads = 512;
+
+__global__ __launch_bounds__(kDmaThreads) void gemm_dma_kernel(const GemmBatch args) {
   __shared__ uint4 st0[2][BM][8], st1[2][BM][8], st2[2][BM][8], st3[2][BM][8], st4[2][BM][8];  // 5 x 32 KiB
   if (static_cast<int>(blockIdx.x) >= args.total_tiles) {
     norm_rows(args, blockIdx.x - args.total_tiles);
@@ -744,58 +793,56 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
   const bf16_t* __restrict__ B = static_cast<const bf16_t*>(P.B) + bt * P.strideB + (long long)kc * kl;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave >> 2, wn = wave & 3;
   const int nk = min(kl, P.K - kc * kl) / 64;
   float rs_mine = 0.0f;  // cosine epilogue: reciprocal norm of tile row tid, or of column tid - BM
-  if (P.epi == EPI_COSINE) {
+  if (P.epi == EPI_COSINE && tid < BM + BN) {
     const float* rs = P.rs + (long long)bt * M;
     const int k = tid < BM ? m0 + tid : n0 + tid - BM;
     if (k < (tid < BM ? M : N)) rs_mine = rs[k];
   }
 
-  // Per-lane global row pointers of this wave's 4 A rows and 4 B rows
+  // Per-lane global row pointers of this wave's 2 A rows and 2 B rows
   // (rows past the matrix read its last row; they are never stored), through
   // the index maps when there are any.
   const int32_t* mapA = P.mapA ? P.mapA + bt * P.mapStride : nullptr;
   const int32_t* mapB = P.mapB ? P.mapB + bt * P.mapStride : nullptr;
-  const bf16_t* ga[4];
-  const bf16_t* gb[4];
+  const bf16_t* ga[2];
+  const bf16_t* gb[2];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int r = 32 * wave + 8 * j + (lane >> 3);
+  for (int j = 0; j < 2; ++j) {
+    const int r = 16 * wave + 8 * j + (lane >> 3);
     const int v = (lane & 7) ^ swz(r);  // the chunk the swizzle puts at position lane & 7 of row r
     const int ra = min(m0 + r, M - 1), rb = min(n0 + r, N - 1);
     ga[j] = A + (long long)(mapA ? mapA[ra] : ra) * P.lda + 8 * v;
     gb[j] = B + (long long)(mapB ? mapB[rb] : rb) * P.ldb + 8 * v;
   }
-  // this wave's first destination row inside a stage: 32 wave rows of 128 bytes
-  const uint32_t wrow = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave)) * 32u * 128u;
+  // this wave's first destination row inside a stage: 16 wave rows of 128 bytes
+  const uint32_t wrow = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(wave)) * 16u * 128u;
   auto issue = [&](uint4 (*dst)[BM][8], int kt) {
     const int k0 = kt * 64;
     const uint32_t m = lds_addr(&dst[0][0][0]) + wrow;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 2; ++j) {
       dma16(ga[j] + k0, m + 1024u * j);
       dma16(gb[j] + k0, m + BM * 128u + 1024u * j);
     }
   };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[2][1];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    for (int r = 0; r < 16; ++r) acc[i][0][r] = 0.0f;
 
   // Step kt waits for slice kt (this wave's loads, then every wave's at the
   // barrier), refills the stage every wave finished reading in the previous
   // step with slice kt + 4, and runs the matrix cores on slice kt.  Slice kt
   // sits in stage kt % 5, a compile-time constant in the unrolled body; the
   // early exits are uniform scalar branches.
-  auto mma = [&](uint4 (*cur)[BM][8]) { mma_slice<bf16_t>(cur[0], cur[1], wm, wn, lane, acc); };
+  auto mma = [&](uint4 (*cur)[BM][8]) { mma_slice8(cur[0], cur[1], wm, wn, lane, acc); };
   auto step = [&](uint4 (*cur)[BM][8], uint4 (*nxt)[BM][8], int kt) {
-    wait_vm_lgkm0(8 * min(3, nk - 1 - kt));
+    wait_vm_lgkm0(4 * min(3, nk - 1 - kt));
     __builtin_amdgcn_s_barrier();
     if (kt + 4 < nk) issue(nxt, kt + 4);
     mma(cur);
@@ -817,35 +864,34 @@ __global__ __launch_bounds__(NT) void gemm_dma_kernel(const GemmBatch args) {
     step(st0, st4, kt + 4);
   }
   if (P.epi == EPI_PARTIAL) {
-    // the raw sums of this K range: float4 q = (2 i + j) 4 + e / 4 of thread
-    // tid at q * 256 + tid (every store of a wave contiguous)
-    float4* dst = static_cast<float4*>(P.C) + (long long)local * (16 * NT);
+    // the raw sums of this K range in the four-wave layout the reductions
+    // read: entries (i, j, 4 g .. 4 g + 3) of that layout's thread t (wave
+    // 2 wm + wn / 2, j = wn % 2) as float4 q = (2 i + j) 4 + g at q * 256 + t
+    // (every store of a wave contiguous)
+    float4* dst = static_cast<float4*>(P.C) + (long long)local * (16 * 256);
+    const int t4 = (2 * wm + (wn >> 1)) * 64 + lane, j4 = wn & 1;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-          dst[((2 * i + j) * 4 + g) * NT + tid] =
-              make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+      for (int g = 0; g < 4; ++g)
+        dst[((2 * i + j4) * 4 + g) * 256 + t4] =
+            make_float4(acc[i][0][4 * g], acc[i][0][4 * g + 1], acc[i][0][4 * g + 2], acc[i][0][4 * g + 3]);
     return;
   }
   __syncthreads();  // the epilogues reuse the stage arrays
   float* rs_tile = reinterpret_cast<float*>(&st4[0][0][0]);
   if (P.epi == EPI_COSINE) {
-    rs_tile[tid] = rs_mine;
+    if (tid < BM + BN) rs_tile[tid] = rs_mine;
     __syncthreads();
   }
   const StagedTile L{reinterpret_cast<float*>(&st0[0][0][0]), reinterpret_cast<float*>(&st1[0][0][0]),
                      reinterpret_cast<float*>(&st2[0][0][0]), reinterpret_cast<float*>(&st3[0][0][0])};
   if (P.epi == EPI_COSINE)
-    epi_cosine_staged(P, bt, tm, tn, acc, L, rs_tile, rs_tile + BM, tid, lane, wm, wn);
+    epi_cosine_staged<1>(P, bt, tm, tn, acc, L, rs_tile, rs_tile + BM, tid, lane, wm, wn);
   else if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS)
-    epi_bias_staged(P, bt, m0, n0, acc, L, tid, lane, wm, wn);
-  else if (epi_direct(P.epi))
-    epi_direct_staged(P, bt, m0, n0, acc, L, tid, lane, wm, wn);
+    epi_bias_staged<1>(P, bt, m0, n0, acc, L, tid, lane, wm, wn);
   else
-    epilogue<bf16_t>(P, bt, tm, tn, acc, L.q0, L.q1, tid, lane, wm, wn);
+    epi_direct_staged<1>(P, bt, m0, n0, acc, L, tid, lane, wm, wn);
 }
 
 // ------------------------------------------------------------ 256 x 256 tiles
@@ -997,9 +1043,9 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
   for (int s = 0; s < 2; ++s) {
     if (s) __syncthreads();  // the staging is read out before it is written again
     if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS)
-      epi_bias_staged(P, bt, m0 + 128 * h, n0 + 128 * s, acc[s], L, t2, lane, qm, qn);
+      epi_bias_staged<2>(P, bt, m0 + 128 * h, n0 + 128 * s, acc[s], L, t2, lane, qm, qn);
     else
-      epi_direct_staged(P, bt, m0 + 128 * h, n0 + 128 * s, acc[s], L, t2, lane, qm, qn);
+      epi_direct_staged<2>(P, bt, m0 + 128 * h, n0 + 128 * s, acc[s], L, t2, lane, qm, qn);
   }
 }
 
@@ -1253,12 +1299,18 @@ static bool k_ranges_ok(const GemmProblem& p) {
   return p.K % p.ksplit == 0 && (p.K / p.ksplit) % 256 == 0;
 }
 
+// The epilogues of the direct-load kernel (the RoPE epilogue runs in the
+// register-staged kernel or the projection kernel).
+static bool dma_epilogue(int e) {
+  return e == EPI_BIAS_GELU || e == EPI_BIAS || e == EPI_COSINE || e == EPI_PARTIAL || epi_direct(e);
+}
+
 bool gemm_direct_loads(map_dtype dt, const GemmBatch& g) {
   if (dt != MAP_BF16) return false;
   bool dma = true;  // every problem meets the direct-load requirements
   for (int i = 0; i < g.count; ++i) {
     const GemmProblem& p = g.p[i];
-    dma = dma && (p.epi <= EPI_PARTIAL || epi_direct(p.epi)) && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+    dma = dma && dma_epilogue(p.epi) && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
           (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
           p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
           k_ranges_ok(p);
@@ -1323,7 +1375,7 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
     bool dma = true;  // every problem meets the direct-load requirements
     for (int i = 0; i < g.count; ++i) {
       const GemmProblem& p = g.p[i];
-      dma = dma && (p.epi <= EPI_PARTIAL || epi_direct(p.epi)) && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
+      dma = dma && dma_epilogue(p.epi) && p.K % 256 == 0 && p.lda % 8 == 0 && p.ldb % 8 == 0 &&
             (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 && (reinterpret_cast<uintptr_t>(p.B) & 15) == 0 &&
             p.strideA % 8 == 0 && p.strideB % 8 == 0 &&
             k_ranges_ok(p);
@@ -1333,7 +1385,8 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
       finalize_big(q);
       return launch_kernel(name, gemm_big_kernel, dim3(q.total_tiles), dim3(kBigThreads), 0, s, q);
     }
-    if (dma) return launch_kernel(name, gemm_dma_kernel, dim3(g.total_tiles + g.norm_blocks), dim3(NT), 0, s, g);
+    if (dma)
+      return launch_kernel(name, gemm_dma_kernel, dim3(g.total_tiles + g.norm_blocks), dim3(kDmaThreads), 0, s, g);
     if (g.norm_blocks) return hipErrorInvalidValue;
     for (int i = 0; i < g.count; ++i)  // index maps and K ranges exist in the direct-load kernel only
       if (g.p[i].epi == EPI_PARTIAL || g.p[i].mapA || g.p[i].mapB) return hipErrorInvalidValue;
