@@ -1051,8 +1051,9 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
 
 // Projection to d_p <= 128 columns with the RoPE epilogue (the keys and
 // queries of Eq. (3)): C = RoPE(A B^T + bias), A [M][K] and B [N][K] bf16.
-// With N this small a 128 x 128 tile leaves most compute units idle, each
-// streaming the whole K with a few slices in flight.  Here a workgroup takes
+// With N this small and rows for fewer than one wave of tiles, a 128 x 128
+// tile leaves most compute units idle, each streaming the whole K with a
+// few slices in flight.  Here a workgroup takes
 // 32 rows and one of two groups of RoPE pairs: with half = N / 2 and
 // PG = ceil(half / 2), group g holds pairs c = g PG .. (g + 1) PG - 1, i.e.
 // columns c and c + half, so every rotation is local and each workgroup
@@ -1403,7 +1404,11 @@ hipError_t launch_proj_rope(map_dtype dt, const GemmBatch& g, const char* name, 
            p.ldb % 8 == 0 && (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 &&
            (reinterpret_cast<uintptr_t>(p.B) & 15) == 0;
   }
-  if (!fits) return launch_gemm(dt, g, name, s);
+  // With enough rows for a wave of 128 x 128 tiles, the tiled kernel reads
+  // B once per tile instead of once per 32 rows.
+  long long rows = 0;
+  for (int i = 0; i < g.count; ++i) rows += g.p[i].M;
+  if (!fits || rows >= 128LL * gemm_cus()) return launch_gemm(dt, g, name, s);
   GemmBatch q = g;
   int total = 0;
   for (int i = 0; i < q.count; ++i) {
