@@ -902,22 +902,26 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   sa.clear_r0flag = sw.r0flag + B;
   if ((e = launch_subset(sa, st)) != hipSuccess) return MAP_ERR_HIP;
 
-  // cosine entries among the subset: raw sums per K range, then their
-  // ordered sum with the cosine scaling
+  // cosine entries among the subset: with tiles for a wave of workgroups,
+  // straight from the tiles' cosine epilogue; otherwise raw sums per K
+  // range, then their ordered sum with the cosine scaling
+  const bool direct = (long long)B * subset_tiles(nc) >= device_cus();
   GemmBatch g;
   memset(&g, 0, sizeof(g));
-  g.p[0] = gram(V, B, nc, w.D, u.partial, nullptr);
+  g.p[0] = gram(V, B, nc, w.D, direct ? u.SJ : u.partial, direct ? u.ninvJ : nullptr);
   g.p[0].strideA = (long long)N * w.D;
   g.p[0].strideB = (long long)N * w.D;
-  g.p[0].epi = EPI_PARTIAL;
   g.p[0].mapA = u.jmap;
   g.p[0].mapB = u.jmap;
   g.p[0].mapStride = nc;
-  g.p[0].ksplit = subset_ksplit(w.D);
+  if (!direct) {
+    g.p[0].epi = EPI_PARTIAL;
+    g.p[0].ksplit = subset_ksplit(w.D);
+  }
   g.count = 1;
   gemm_finalize(g);
   if ((e = launch_gemm(dt, g, "gemm_subset", st)) != hipSuccess) return MAP_ERR_HIP;
-  if ((e = launch_gram_reduce(g.p[0], u.SJ, nc, u.ninvJ, st)) != hipSuccess) return MAP_ERR_HIP;
+  if (!direct && (e = launch_gram_reduce(g.p[0], u.SJ, nc, u.ninvJ, st)) != hipSuccess) return MAP_ERR_HIP;
 
   int32_t* order_img = order_out ? order_out : u.order_img;
   const GatherArgs ga = gather_args(V, pos_v, order_img, sw.err, idx_out, V_out, pos_out, B, N, sp.K,
