@@ -974,57 +974,68 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
   // sit on different SIMDs, so each SIMD gets an equal share.)
   const bool sumsq = args.norm_tiles == pi + 1 && tn == 0;
   float nacc = 0.0f;
-  // One K slice: four steps of 16; the operands of step s + 1 are read
-  // before the products of step s issue.
-  auto mma = [&](const uint4 (*st)[8]) {
+  // The operands of one step of 16 (two buffers: those of the next step are
+  // read while the products of this one run), and the step's products.
+  bf16x8_t a[2][2], b[2][4];
+  auto read = [&](const uint4 (*st)[8], int s, int buf) {
     const uint4 (*As)[8] = st;
     const uint4 (*Bs)[8] = st + kBig;
-    bf16x8_t a[2][2], b[2][4];
-    auto read = [&](int s, int buf) {
-      const int v = 2 * s + lh;  // 16-byte chunk: k = 16 s + 8 lh + (0..7)
+    const int v = 2 * s + lh;  // 16-byte chunk: k = 16 s + 8 lh + (0..7)
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int r = 128 * h + 64 * qm + 32 * i + lr;
-        a[buf][i] = __builtin_bit_cast(bf16x8_t, As[r][v ^ swz(r)]);
-      }
+    for (int i = 0; i < 2; ++i) {
+      const int r = 128 * h + 64 * qm + 32 * i + lr;
+      a[buf][i] = __builtin_bit_cast(bf16x8_t, As[r][v ^ swz(r)]);
+    }
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int r = 128 * (c >> 1) + 64 * qn + 32 * (c & 1) + lr;
-        b[buf][c] = __builtin_bit_cast(bf16x8_t, Bs[r][v ^ swz(r)]);
-      }
-    };
-    read(0, 0);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      if (s < 3) read(s + 1, (s + 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-          acc[c >> 1][i][c & 1] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s & 1][i], b[s & 1][c], acc[c >> 1][i][c & 1], 0, 0, 0);
-      if (sumsq) {  // (vector ALU work under the products)
-        const uint4 u = __builtin_bit_cast(uint4, qn ? a[s & 1][1] : a[s & 1][0]);
-        const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const float x = __uint_as_float((k & 1) ? (wv[k >> 1] & 0xffff0000u) : (wv[k >> 1] << 16));
-          nacc = fmaf(x, x, nacc);
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
+    for (int c = 0; c < 4; ++c) {
+      const int r = 128 * (c >> 1) + 64 * qn + 32 * (c & 1) + lr;
+      b[buf][c] = __builtin_bit_cast(bf16x8_t, Bs[r][v ^ swz(r)]);
     }
   };
-  // Step kt waits for this wave's loads of slice kt, then for every wave's
-  // at the barrier (which also means every wave is done with slice kt - 1,
-  // whose stage now receives slice kt + 1), and runs the products.
+  auto products = [&](int buf) {
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        acc[c >> 1][i][c & 1] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b[buf][c], acc[c >> 1][i][c & 1], 0, 0, 0);
+    if (sumsq) {  // (vector ALU work under the products)
+      const uint4 u = __builtin_bit_cast(uint4, qn ? a[buf][1] : a[buf][0]);
+      const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float x = __uint_as_float((k & 1) ? (wv[k >> 1] & 0xffff0000u) : (wv[k >> 1] << 16));
+        nacc = fmaf(x, x, nacc);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Slice kt sits in stage kt % 2.  The wait for slice kt + 1 and the
+  // barrier come before the products of kt's last step, so that the next
+  // slice's first operands are read while those run; the barrier also means
+  // every wave is done reading slice kt, whose stage receives slice kt + 2
+  // at the start of the next step.
   issue(bst0, 0);
+  wait_vm_lgkm0(0);
+  __builtin_amdgcn_s_barrier();
+  read(bst0, 0, 0);
   for (int kt = 0; kt < nk; ++kt) {
-    wait_vm_lgkm0(0);
-    __builtin_amdgcn_s_barrier();
-    if (kt + 1 < nk) issue((kt & 1) ? bst0 : bst1, kt + 1);
-    mma((kt & 1) ? bst1 : bst0);
+    uint4 (*cur)[8] = (kt & 1) ? bst1 : bst0;
+    uint4 (*nxt)[8] = (kt & 1) ? bst0 : bst1;
+    if (kt + 1 < nk) issue(nxt, kt + 1);
+    read(cur, 1, 1);
+    products(0);
+    read(cur, 2, 0);
+    products(1);
+    read(cur, 3, 1);
+    products(0);
+    if (kt + 1 < nk) {
+      wait_vm_lgkm0(0);
+      __builtin_amdgcn_s_barrier();
+      read(nxt, 0, 0);
+    }
+    products(1);
   }
   if (sumsq) {
     const float t = nacc + __shfl_xor(nacc, 32);
