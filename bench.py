@@ -457,13 +457,15 @@ def measure_prune(mp, torch, dev, cfg, x, d, steps, warmup, subset=0, per_step=0
 def train_flops(cfg, sumM):
     """Algorithmic flops of one training step's matrix products: the forward
     (layer 1, the folded weights, the projection) and the backward (X = dz^T h
-    and dL/da per branch, dW1, dW_K, dW2)."""
+    and dL/da per branch; dW1 of f_V in one launch; dW1 of f_T, dW_K, dW2 in
+    another)."""
     D, H, dp = cfg.pred.D, cfg.pred.D_h, cfg.pred.d_p
     rows = cfg.B * cfg.N + sumM
     fwd = 2.0 * rows * D * H + 4.0 * dp * H * H + 2.0 * rows * H * dp
     bwd = 4.0 * dp * H * rows + 2.0 * H * D * rows + 8.0 * dp * H * H
     return {"gemm_layer1": 2.0 * rows * D * H + 4.0 * dp * H * H, "gemm_proj_rope": 2.0 * rows * H * dp,
-            "gemm_train_x_da": 4.0 * dp * H * rows, "gemm_train_dw": 2.0 * H * D * rows + 8.0 * dp * H * H,
+            "gemm_train_x_da": 4.0 * dp * H * rows, "gemm_train_dw": 2.0 * H * D * cfg.B * cfg.N,
+            "gemm_train_dw_small": 2.0 * H * D * sumM + 8.0 * dp * H * H,
             "total": fwd + bwd}
 
 

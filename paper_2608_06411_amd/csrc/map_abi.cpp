@@ -632,9 +632,17 @@ hipError_t enqueue_train(const map_weights& w, map_dtype dt, int B, int N, const
   g2.p[4] = linear(t.WKT, Dh, t.XvT, nullptr, g.w2_v, Dh, t.kdp, EPI_F32);
   g2.p[5] = linear(t.WQT, Dh, t.XtT, nullptr, g.w2_t, Dh, t.kdp, EPI_F32);
   g2.count = 6;
+  // dW1_v's 256 long tiles (K = the visual tokens) in a launch of their own,
+  // one wave over every compute unit; the five short problems after it
+  // (sharing one launch with them took 79 us against 38 + 20)
+  GemmBatch g3 = g2;
+  g2.count = 1;
   gemm_finalize(g2);
-  g2.first_tiles = g2.p[1].tile_begin;  // dW1_v's long tiles first, spread over every XCD
+  for (int i = 0; i < 5; ++i) g3.p[i] = g3.p[i + 1];
+  g3.count = 5;
+  gemm_finalize(g3);
   if ((e = launch_gemm(dt, g2, "gemm_train_dw", st)) != hipSuccess) return e;
+  if ((e = launch_gemm(dt, g3, "gemm_train_dw_small", st)) != hipSuccess) return e;
   // bias gradients and the sums of dz over tokens
   RowsumBatch rs;
   memset(&rs, 0, sizeof(rs));
