@@ -169,6 +169,13 @@ struct SubsetWs {
   int32_t* order_img;
 };
 
+int device_cus();
+
+// The subset's Gram entries come straight from the tiles' cosine epilogue
+// when the batch's tiles fill a wave of workgroups; otherwise from K-range
+// partial sums (which need the partial buffer).
+bool subset_gram_direct(int B, int nc) { return (long long)B * subset_tiles(nc) >= device_cus(); }
+
 SubsetWs carve_subset(Carver& c, int B, int K, int nc, int D) {
   SubsetWs s;
   s.jmap = c.take<int32_t>((size_t)B * nc);
@@ -178,7 +185,8 @@ SubsetWs carve_subset(Carver& c, int B, int K, int nc, int D) {
   s.hout = c.take<uint32_t>(B);
   s.uncert = c.take<int32_t>(B);
   s.SJ = c.take<float>((size_t)B * nc * nc);
-  s.partial = c.take<float>((size_t)B * subset_tiles(nc) * subset_ksplit(D) * 128 * 128);
+  s.partial = subset_gram_direct(B, nc) ? nullptr
+                                        : c.take<float>((size_t)B * subset_tiles(nc) * subset_ksplit(D) * 128 * 128);
   s.order_img = c.take<int32_t>((size_t)B * K);
   return s;
 }
@@ -913,7 +921,7 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   // cosine entries among the subset: with tiles for a wave of workgroups,
   // straight from the tiles' cosine epilogue; otherwise raw sums per K
   // range, then their ordered sum with the cosine scaling
-  const bool direct = (long long)B * subset_tiles(nc) >= device_cus();
+  const bool direct = subset_gram_direct(B, nc);
   GemmBatch g;
   memset(&g, 0, sizeof(g));
   g.p[0] = gram(V, B, nc, w.D, direct ? u.SJ : u.partial, direct ? u.ninvJ : nullptr);
