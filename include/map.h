@@ -69,8 +69,10 @@ typedef enum {
   MAP_ERR_UNSUPPORTED = 2,  /* valid request the library does not implement */
   MAP_ERR_WORKSPACE = 3,    /* ws is NULL, misaligned or smaller than needed */
   MAP_ERR_HIP = 4,          /* the HIP runtime reported an error            */
-  MAP_ERR_TOO_LARGE = 5     /* the call needs more scratch than the static
+  MAP_ERR_TOO_LARGE = 5,    /* the call needs more scratch than the static
                                buffer of map_prune_noalloc holds            */
+  MAP_ERR_NONFINITE = 6     /* the finite check (map_set_finite_check) found
+                               an infinity or a NaN in a float input        */
 } map_status;
 
 typedef enum { MAP_F32 = 0, MAP_BF16 = 1 } map_dtype;
@@ -362,6 +364,20 @@ map_status map_set_subset_tokens(int n);
  * MAP_ERR_INVALID_ARG for a null or misaligned pointer; MAP_ERR_HIP if the
  * copy cannot be enqueued. */
 map_status map_selection_status(const void* ws, int32_t* status_out, void* stream);
+
+/* map_set_finite_check -- a debugging aid, off by default.  While enabled
+ * (enable != 0), map_score, map_similarity, map_select, map_prune,
+ * map_prune_assemble, map_prune_noalloc, map_teacher, map_train_step and
+ * map_decoder_layer first scan their floating-point inputs (activations,
+ * weights, scores, similarities, attention, teacher distributions) on
+ * `stream` for infinities and NaNs, wait for the scan (the call then blocks
+ * until the stream has passed it, so it cannot be captured in a graph) and
+ * return MAP_ERR_NONFINITE, having enqueued nothing else, if it finds one.
+ * With the check off a non-finite input is not detected: the method's
+ * arithmetic then follows IEEE rules (a non-finite or negative score keys
+ * as 0 in the selection).  Process-wide; change it only between calls.
+ * Returns MAP_OK. */
+map_status map_set_finite_check(int enable);
 
 /* At most n images per persistent selection launch (n <= 0: as many as
  * can be resident at once, the default).  Larger batches then run as

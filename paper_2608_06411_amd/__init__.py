@@ -8,12 +8,12 @@ kept tokens -- as hand-written HIP kernels for gfx950 behind a C ABI
 """
 from .binding import (EXPORTS, MAP_BF16, MAP_F32, MapError, PredictorWeights, PruneWorkspace, TrainWorkspace, DecoderWeights, decoder_workspace, map_decoder_layer,
                       lib, map_assemble, map_prune, map_prune_assemble, map_score, map_train_step, map_select, map_similarity, map_teacher,
-                      selection_status, set_select_images_per_launch, set_subset_tokens,
+                      selection_status, set_finite_check, set_select_images_per_launch, set_subset_tokens,
                       timing_enable, timing_read, timing_reset)
 
 __all__ = [
     "EXPORTS", "MAP_BF16", "MAP_F32", "MapError", "PredictorWeights", "PruneWorkspace", "lib",
     "TrainWorkspace", "map_train_step", "DecoderWeights", "decoder_workspace", "map_decoder_layer", "map_assemble", "map_prune", "map_prune_assemble", "map_score", "map_select", "map_similarity", "map_teacher", "selection_status",
-    "set_select_images_per_launch", "set_subset_tokens", "timing_enable",
+    "set_finite_check", "set_select_images_per_launch", "set_subset_tokens", "timing_enable",
     "timing_read", "timing_reset",
 ]

@@ -19,7 +19,8 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmap.so")
 
-MAP_OK, MAP_ERR_INVALID_ARG, MAP_ERR_UNSUPPORTED, MAP_ERR_WORKSPACE, MAP_ERR_HIP, MAP_ERR_TOO_LARGE = range(6)
+(MAP_OK, MAP_ERR_INVALID_ARG, MAP_ERR_UNSUPPORTED, MAP_ERR_WORKSPACE, MAP_ERR_HIP, MAP_ERR_TOO_LARGE,
+ MAP_ERR_NONFINITE) = range(7)
 MAP_PRUNE_NOALLOC_MAX_BYTES = 96 << 20
 MAP_F32, MAP_BF16 = 0, 1
 MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
@@ -30,7 +31,8 @@ EXPORTS = (
     "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
     "map_prune", "map_prune_assemble", "map_prune_noalloc", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
     "map_train_workspace", "map_train_step", "map_decoder_workspace", "map_decoder_layer",
-    "map_selection_status", "map_set_select_images_per_launch", "map_timing_enable", "map_timing_read",
+    "map_selection_status", "map_set_select_images_per_launch", "map_set_finite_check", "map_timing_enable",
+    "map_timing_read",
     "map_timing_reset",
 )
 
@@ -85,6 +87,7 @@ _SIGS = {
     "map_set_subset_tokens": (_I, [_I]),
     "map_selection_status": (_I, [_P, _P, _P]),
     "map_set_select_images_per_launch": (_I, [_I]),
+    "map_set_finite_check": (_I, [_I]),
     "map_timing_enable": (_I, [_I]),
     "map_timing_read": (_I, [ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
                              ctypes.POINTER(ctypes.c_int), _I]),
@@ -613,6 +616,14 @@ def set_select_images_per_launch(n: int):
     """At most n images per persistent selection launch (n <= 0: as many as
     fit, the default).  Process-wide; for testing the multi-launch path."""
     _check(lib().map_set_select_images_per_launch(int(n)), "map_set_select_images_per_launch")
+
+
+def set_finite_check(on: bool):
+    """The library's finite check (a debugging aid, off by default): while
+    on, each call first scans its float inputs for infinities and NaNs, waits
+    for the scan and raises MapError(MAP_ERR_NONFINITE) if it finds one.
+    Process-wide."""
+    _check(lib().map_set_finite_check(1 if on else 0), "map_set_finite_check")
 
 
 def timing_enable(on: bool = True):

@@ -192,6 +192,13 @@ struct PrepArgs {
 };
 hipError_t launch_prep(map_dtype dt, const PrepArgs& a, bool norms, bool table, bool fold, hipStream_t s);
 
+// ---------------------------------------------------------------- finite check
+// The device flag of this device (nullptr on failure), and one scan that sets
+// it when `count` elements of elem_bytes (2: bf16, 4: float32) at p hold an
+// infinity or a NaN.
+int* finite_flag();
+hipError_t launch_finite_check(const void* p, long long count, int elem_bytes, int* flag, hipStream_t s);
+
 // ---------------------------------------------------------------- score
 struct ScoreArgs {
   const float* q;         // [sum_M][d_p] (after RoPE)

@@ -20,6 +20,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <initializer_list>
 #include <mutex>
 #include <vector>
 
@@ -978,6 +979,42 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   return gathered ? MAP_OK : hip_status(launch_gather(ga, st));
 }
 
+// ------------------------------------------------------------ finite check
+std::atomic<int> g_finite_check{0};
+
+struct FiniteBuf {
+  const void* p;
+  long long count;
+  int elem_bytes;
+};
+
+// With the check on: scan the buffers on `st`, wait, and report
+// MAP_ERR_NONFINITE if any holds an infinity or a NaN; MAP_OK otherwise
+// (and at once with the check off).
+map_status check_finite(hipStream_t st, std::initializer_list<FiniteBuf> bufs) {
+  if (!g_finite_check.load()) return MAP_OK;
+  int* flag = finite_flag();
+  if (!flag || hipMemsetAsync(flag, 0, sizeof(int), st) != hipSuccess) return MAP_ERR_HIP;
+  for (const FiniteBuf& f : bufs)
+    if (launch_finite_check(f.p, f.count, f.elem_bytes, flag, st) != hipSuccess) return MAP_ERR_HIP;
+  int found = 0;
+  if (hipMemcpyAsync(&found, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return MAP_ERR_HIP;
+  return found ? MAP_ERR_NONFINITE : MAP_OK;
+}
+
+// The predictor's inputs: V, T and the ten weight tensors.
+map_status check_predictor_inputs(hipStream_t st, const map_weights& w, map_dtype dt, int B, int N, const void* V,
+                                  const void* T, int sumM) {
+  const int e = static_cast<int>(elem_size(dt));
+  const long long D = w.D, H = w.D_h, dp = w.d_p;
+  return check_finite(st, {{V, (long long)B * N * D, e}, {T, (long long)sumM * D, e}, {w.w1_v, H * D, e},
+                           {w.b1_v, H, e}, {w.w2_v, H * H, e}, {w.b2_v, H, e}, {w.w_k, dp * H, e},
+                           {w.w1_t, H * D, e}, {w.b1_t, H, e}, {w.w2_t, H * H, e}, {w.b2_t, H, e},
+                           {w.w_q, dp * H, e}});
+}
+
 extern "C" {
 
 const char* map_status_string(int status) {
@@ -988,6 +1025,7 @@ const char* map_status_string(int status) {
     case MAP_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case MAP_ERR_HIP: return "HIP runtime error";
     case MAP_ERR_TOO_LARGE: return "the call needs more scratch than map_prune_noalloc's static buffer holds";
+    case MAP_ERR_NONFINITE: return "an input holds an infinity or a NaN (finite check)";
     default: return "unknown status";
   }
 }
@@ -1041,6 +1079,8 @@ map_status map_score(const map_weights* w, map_dtype dt, int B, int N, const voi
   const int sumM = t_off_host[B];
   const map_status ws_ok = check_ws(ws, ws_bytes, score_ws_bytes(dt, B, N, sumM, *w));
   if (ws_ok != MAP_OK) return ws_ok;
+  const map_status fin = check_predictor_inputs(static_cast<hipStream_t>(stream), *w, dt, B, N, V, T, sumM);
+  if (fin != MAP_OK) return fin;
   Carver c(ws);
   const ScoreWs s = carve_score(c, dt, B, N, sumM, *w);
   return hip_status(enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p_out, s, nullptr,
@@ -1053,6 +1093,8 @@ map_status map_similarity(map_dtype dt, int B, int N, int D, const void* V, floa
   const map_status ws_ok = check_ws(ws, ws_bytes, map_similarity_workspace(dt, B, N, D));
   if (ws_ok != MAP_OK) return ws_ok;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const map_status fin = check_finite(st, {{V, (long long)B * N * D, static_cast<int>(elem_size(dt))}});
+  if (fin != MAP_OK) return fin;
   Carver c(ws);
   float* ninv = c.take<float>((size_t)B * N);
   PrepArgs pa;
@@ -1080,6 +1122,9 @@ map_status map_select(int B, int N, const float* p, const float* S, const float*
     return MAP_ERR_INVALID_ARG;
   const map_status ws_ok = check_ws(ws, ws_bytes, select_ws_bytes(B, N, sp.K));
   if (ws_ok != MAP_OK) return ws_ok;
+  const map_status fin = check_finite(static_cast<hipStream_t>(stream),
+                                      {{p, (long long)B * N, 4}, {S, (long long)B * N * N, 4}, {norms, (long long)B * N, 4}});
+  if (fin != MAP_OK) return fin;
   Carver c(ws);
   int32_t* status = carve_status(c);
   SelectWs w = carve_select(c, B, N, sp.K);
@@ -1101,6 +1146,8 @@ static map_status prune_impl(const map_weights* w, map_dtype dt, int B, int N, c
   const map_status ws_ok = check_ws(ws, ws_bytes, map_prune_workspace(dt, B, N, sumM, w, sp.K));
   if (ws_ok != MAP_OK) return ws_ok;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  const map_status fin = check_predictor_inputs(st, *w, dt, B, N, V, T, sumM);
+  if (fin != MAP_OK) return fin;
   Carver c(ws);
   int32_t* status = carve_status(c);
   const ScoreWs s = carve_score(c, dt, B, N, sumM, *w);
@@ -1244,6 +1291,13 @@ map_status map_teacher(map_dtype dt, int B, int L, int H, int N, const void* A, 
     return MAP_ERR_INVALID_ARG;
   if (!ws || (reinterpret_cast<uintptr_t>(ws) & 15) || ws_bytes < map_teacher_workspace(B, L, N))
     return MAP_ERR_WORKSPACE;
+  {
+    const int e = static_cast<int>(elem_size(dt));
+    const map_status fin = check_finite(static_cast<hipStream_t>(stream),
+                                        {{A, (long long)L * H * m_off_host[B] * N, e},
+                                         {A_ref, (long long)B * L * H * M_ref * N, e}});
+    if (fin != MAP_OK) return fin;
+  }
   TeacherArgs a;
   memset(&a, 0, sizeof(a));
   a.A = A;
@@ -1284,6 +1338,9 @@ map_status map_train_step(const map_weights* w, map_dtype dt, int B, int N, cons
   const int sumM = t_off_host[B];
   const map_status ws_ok = check_ws(ws, ws_bytes, train_ws_bytes(dt, B, N, sumM, *w));
   if (ws_ok != MAP_OK) return ws_ok;
+  map_status fin = check_predictor_inputs(static_cast<hipStream_t>(stream), *w, dt, B, N, V, T, sumM);
+  if (fin == MAP_OK) fin = check_finite(static_cast<hipStream_t>(stream), {{p_teacher, (long long)B * N, 4}});
+  if (fin != MAP_OK) return fin;
   Carver c(ws);
   const TrainWs t = carve_train(c, dt, B, N, sumM, *w);
   return hip_status(enqueue_train(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p_teacher, loss_out,
@@ -1307,9 +1364,22 @@ map_status map_decoder_layer(const map_decoder_weights* w, map_dtype dt, int B, 
   const int R = seq_off_host[B], cus = device_cus();
   const map_status ws_ok = check_ws(ws, ws_bytes, map_decoder_workspace(R, w));
   if (ws_ok != MAP_OK) return ws_ok;
+  {
+    const long long d = w->d, ff = w->ff;
+    const map_status fin = check_finite(static_cast<hipStream_t>(stream),
+                                        {{X, (long long)R * d, 2}, {w->attn_norm, d, 2}, {w->w_qkv, 3 * d * d, 2},
+                                         {w->w_o, d * d, 2}, {w->ffn_norm, d, 2}, {w->w_gate_up, 2 * ff * d, 2},
+                                         {w->w_down, d * ff, 2}});
+    if (fin != MAP_OK) return fin;
+  }
   Carver c(ws);
   const DecoderWs t = carve_decoder(c, R, *w, cus);
   return hip_status(enqueue_decoder(*w, B, X, pos, seq_off_host, Y, t, cus, static_cast<hipStream_t>(stream)));
+}
+
+map_status map_set_finite_check(int enable) {
+  g_finite_check.store(enable != 0 ? 1 : 0);
+  return MAP_OK;
 }
 
 map_status map_set_subset_tokens(int n) {

@@ -29,6 +29,7 @@ def test_header_declarations_are_exported(L, repo_root):
 def test_status_strings_and_version(L):
     assert L.map_status_string(0) == b"ok"
     assert b"workspace" in L.map_status_string(3)
+    assert b"infinity or a NaN" in L.map_status_string(6)
     assert L.map_status_string(99) == b"unknown status"
     assert L.map_version() >= 100
 
