@@ -119,6 +119,11 @@ size_t map_score_workspace(map_dtype dt, int B, int N, int sum_M, const map_weig
 size_t map_similarity_workspace(map_dtype dt, int B, int N, int D);
 size_t map_select_workspace(int B, int N, int K);
 size_t map_prune_workspace(map_dtype dt, int B, int N, int sum_M, const map_weights* w, int K);
+/* One workspace size that serves map_score, map_similarity, map_select and
+ * map_prune alike for these sizes: the largest of the four (map_score and
+ * map_prune left out when w is NULL).  D must equal w->D when w is given;
+ * 0 if the sizes are invalid. */
+size_t map_workspace_bytes(int B, int N, int D, int sum_M, int K, const map_weights* w, map_dtype dt);
 
 /* map_score -- predicted attention, Eq. (3):
  *   p_hat[b][n] = (1/M_b) sum_m softmax_n( <q_m, k_n> / sqrt(d_p) ),

@@ -28,7 +28,7 @@ MAP_MAX_BATCH, MAP_MAX_N, MAP_MAX_K = 64, 16384, 1024
 # Every symbol include/map.h declares.
 EXPORTS = (
     "map_status_string", "map_version", "map_score_workspace", "map_similarity_workspace",
-    "map_select_workspace", "map_prune_workspace", "map_score", "map_similarity", "map_select",
+    "map_select_workspace", "map_prune_workspace", "map_workspace_bytes", "map_score", "map_similarity", "map_select",
     "map_prune", "map_prune_assemble", "map_prune_noalloc", "map_assemble", "map_teacher_workspace", "map_teacher", "map_set_subset_tokens",
     "map_train_workspace", "map_train_step", "map_decoder_workspace", "map_decoder_layer",
     "map_selection_status", "map_set_select_images_per_launch", "map_set_finite_check", "map_timing_enable",
@@ -66,6 +66,7 @@ _SIGS = {
     "map_score_workspace": (_SZ, [_I, _I, _I, _I, ctypes.POINTER(map_weights)]),
     "map_similarity_workspace": (_SZ, [_I, _I, _I, _I]),
     "map_select_workspace": (_SZ, [_I, _I, _I]),
+    "map_workspace_bytes": (_SZ, [_I, _I, _I, _I, _I, ctypes.POINTER(map_weights), _I]),
     "map_prune_workspace": (_SZ, [_I, _I, _I, _I, ctypes.POINTER(map_weights), _I]),
     "map_score": (_I, [ctypes.POINTER(map_weights), _I, _I, _I, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "map_similarity": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _SZ, _P]),

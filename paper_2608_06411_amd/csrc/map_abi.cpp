@@ -1069,6 +1069,19 @@ size_t map_prune_workspace(map_dtype dt, int B, int N, int sum_M, const map_weig
          align_up((size_t)B * N * N * sizeof(float)) + 3 * align_up((size_t)B * N * sizeof(float)) + sub;
 }
 
+size_t map_workspace_bytes(int B, int N, int D, int sum_M, int K, const map_weights* w, map_dtype dt) {
+  if (w && w->D != D) return 0;
+  const size_t sim = map_similarity_workspace(dt, B, N, D), sel = map_select_workspace(B, N, K);
+  if (!sim || !sel) return 0;
+  size_t need = std::max(sim, sel);
+  if (w) {
+    const size_t sc = map_score_workspace(dt, B, N, sum_M, w), pr = map_prune_workspace(dt, B, N, sum_M, w, K);
+    if (!sc || !pr) return 0;
+    need = std::max(need, std::max(sc, pr));
+  }
+  return need;
+}
+
 map_status map_score(const map_weights* w, map_dtype dt, int B, int N, const void* V,
                      const int32_t* pos_v, const void* T, const int32_t* pos_t,
                      const int32_t* t_off_host, float* p_out, void* ws, size_t ws_bytes,

@@ -63,6 +63,14 @@ def test_workspace_sizes(L):
     bad = _fake_weights()
     bad.w_q = None
     assert L.map_score_workspace(bd.MAP_F32, 1, 100, 5, ctypes.byref(bad)) == 0
+    # one size for all four calls: their maximum
+    each = [L.map_score_workspace(bd.MAP_BF16, 2, 100, 10, ctypes.byref(w)),
+            L.map_similarity_workspace(bd.MAP_BF16, 2, 100, 64), L.map_select_workspace(2, 100, 10),
+            L.map_prune_workspace(bd.MAP_BF16, 2, 100, 10, ctypes.byref(w), 10)]
+    assert L.map_workspace_bytes(2, 100, 64, 10, 10, ctypes.byref(w), bd.MAP_BF16) == max(each)
+    assert L.map_workspace_bytes(2, 100, 64, 10, 10, None, bd.MAP_BF16) == max(each[1:3])
+    assert L.map_workspace_bytes(2, 100, 32, 10, 10, ctypes.byref(w), bd.MAP_BF16) == 0  # D != w.D
+    assert L.map_workspace_bytes(2, 100, 64, 10, 101, ctypes.byref(w), bd.MAP_BF16) == 0  # K > N
 
 
 P = ctypes.c_void_p
