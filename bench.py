@@ -407,7 +407,27 @@ def _time_steps(torch, dev, run, steps, warmup, per_step=0):
     return res
 
 
-def measure_prune(mp, torch, dev, cfg, x, d, steps, warmup, subset=0, per_step=0, workload_key=None):
+def cold_steps(torch, dev, run, n, evict_mib=512):
+    """Median, p10 and p90 of n individually timed calls, each after a write
+    of evict_mib MiB of scratch memory (outside the timed region) that evicts
+    the inputs from the Infinity Cache and the L2s: the step as it runs when
+    its image arrives fresh in HBM."""
+    scratch = torch.empty(evict_mib << 18, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in ev:
+        scratch.fill_(1.0)
+        a.record(stream)
+        run()
+        b.record(stream)
+    torch.cuda.synchronize()
+    us = np.array([1e3 * a.elapsed_time(b) for a, b in ev])
+    del scratch
+    return {"median": float(np.median(us)), "p10": float(np.percentile(us, 10)),
+            "p90": float(np.percentile(us, 90)), "samples": n, "evict_mib_between_steps": evict_mib}
+
+
+def measure_prune(mp, torch, dev, cfg, x, d, steps, warmup, subset=0, per_step=0, workload_key=None, cold=0):
     """One workload's map_prune: throughput, per-kernel times and rooflines.
     Returns (result dict, output tensors)."""
     t_off = x["t_off"]
@@ -420,6 +440,8 @@ def measure_prune(mp, torch, dev, cfg, x, d, steps, warmup, subset=0, per_step=0
                      workspace=ws)
 
     tm = _time_steps(torch, dev, step, steps, warmup, per_step)
+    if cold:
+        tm["step_us_cold"] = cold_steps(torch, dev, step, cold)
     kern = _kernel_table(mp, torch, step, steps)
     sumM = int(t_off[-1])
     nc = subset_tokens(cfg, subset) if "subset" in kern else 0
@@ -614,6 +636,8 @@ def main():
     ap.add_argument("--no-train", action="store_true", help="skip the training-step measurement")
     ap.add_argument("--percentile-steps", type=int, default=200,
                     help="individually timed steps for the median / p10 / p90 (0: none)")
+    ap.add_argument("--cold-steps", type=int, default=50,
+                    help="individually timed steps after a 512 MiB scratch write each (cold caches; 0: none)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run a plain float32 copy kernel over this many MiB (three times), "
                          "the reference dispatch for calibrating HBM byte counters")
@@ -644,7 +668,7 @@ def main():
         del src, dst
 
     head, out = measure_prune(mp, torch, dev, cfg, x, d, args.steps, args.warmup, subset=args.subset,
-                              per_step=args.percentile_steps, workload_key=args.workload)
+                              per_step=args.percentile_steps, workload_key=args.workload, cold=args.cold_steps)
     sumM = int(x["t_off"][-1])
     line = {
         "metric": METRIC, "value": head["value"], "unit": "images/s", "n_gpus": 1,
@@ -653,7 +677,8 @@ def main():
         "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic (seeded mixture, random-init predictor)",
         "config": {"workload": head["workload"], "global_batch": cfg.B, "seq_len": cfg.N,
                    "parallelism": "single GPU", "subset_tokens": head["subset_tokens"]},
-        "wall_s_timed": head["wall_s_timed"], "step_us": head.get("step_us"), "kernels": head["kernels"],
+        "wall_s_timed": head["wall_s_timed"], "step_us": head.get("step_us"),
+        "step_us_cold": head.get("step_us_cold"), "kernels": head["kernels"],
         "dominant_kernel": head["dominant_kernel"], "roofline": head["roofline"],
         "roofline_mfma": head["roofline_mfma"], "hbm_stages": head["hbm_stages"],
     }
