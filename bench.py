@@ -427,6 +427,54 @@ def cold_steps(torch, dev, run, n, evict_mib=512):
             "p90": float(np.percentile(us, 90)), "samples": n, "evict_mib_between_steps": evict_mib}
 
 
+def concurrent_streams(mp, torch, dev, cfg, x, d, steps, warmup, n):
+    """Images/s when n streams each run map_prune calls on the workload back
+    to back (same batch size, own workspaces and outputs): one call's
+    selection, which keeps a few compute units busy, runs beside another
+    call's matrix products.  A serving context for the headline, not
+    `value`; the outputs are checked equal to the single-stream ones."""
+    t_off = x["t_off"]
+    streams = [torch.cuda.Stream(dev) for _ in range(n)]
+    wss = [mp.PruneWorkspace(d["w"], d["V"], t_off, cfg.K) for _ in streams]
+    outs = []
+    for st, ws in zip(streams, wss):
+        with torch.cuda.stream(st):
+            outs.append(mp.map_prune(d["w"], d["V"], d["pos_v"], d["T"], d["pos_t"], t_off, cfg.K, cfg.K0, cfg.tau,
+                                     workspace=ws))
+
+    def run(i):
+        with torch.cuda.stream(streams[i]):
+            mp.map_prune(d["w"], d["V"], d["pos_v"], d["T"], d["pos_t"], t_off, cfg.K, cfg.K0, cfg.tau,
+                         out=outs[i], workspace=wss[i])
+
+    for _ in range(warmup):
+        for i in range(n):
+            run(i)
+    torch.cuda.synchronize()
+    main = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(main)
+    for st in streams:
+        st.wait_event(e0)
+    for _ in range(steps):
+        for i in range(n):
+            run(i)
+    for st in streams:
+        done = torch.cuda.Event()
+        done.record(st)
+        main.wait_event(done)
+    e1.record(main)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    ref = mp.map_prune(d["w"], d["V"], d["pos_v"], d["T"], d["pos_t"], t_off, cfg.K, cfg.K0, cfg.tau)
+    torch.cuda.synchronize()
+    same = all(torch.equal(o["idx"], ref["idx"]) and torch.equal(o["V_out"].view(torch.int16),
+                                                                  ref["V_out"].view(torch.int16)) for o in outs)
+    images = n * steps * cfg.B
+    return {"streams": n, "value": images / (ms * 1e-3), "unit": "images/s", "us_per_image": 1e3 * ms / images,
+            "calls_per_stream": steps, "outputs_equal_single_stream": bool(same)}
+
+
 def measure_prune(mp, torch, dev, cfg, x, d, steps, warmup, subset=0, per_step=0, workload_key=None, cold=0):
     """One workload's map_prune: throughput, per-kernel times and rooflines.
     Returns (result dict, output tensors)."""
@@ -636,6 +684,7 @@ def main():
     ap.add_argument("--no-train", action="store_true", help="skip the training-step measurement")
     ap.add_argument("--percentile-steps", type=int, default=200,
                     help="individually timed steps for the median / p10 / p90 (0: none)")
+    ap.add_argument("--no-streams", action="store_true", help="skip the concurrent-stream throughput")
     ap.add_argument("--cold-steps", type=int, default=50,
                     help="individually timed steps after a 512 MiB scratch write each (cold caches; 0: none)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -683,6 +732,9 @@ def main():
         "roofline_mfma": head["roofline_mfma"], "hbm_stages": head["hbm_stages"],
     }
     line["assembly"] = assembly_bench(args, mp, torch, dev, out, d["T"], d["pos_t"], x["t_off"], cfg)
+    if not args.no_streams:
+        line["concurrent_streams"] = [concurrent_streams(mp, torch, dev, cfg, x, d, args.steps, args.warmup, n)
+                                      for n in (2, 3, 4)]
     if not args.no_train:
         line["training_step"] = train_bench(mp, torch, dev, cfg, x, d, min(args.steps, 20), min(args.warmup, 5))
     if not args.no_context:
