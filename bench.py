@@ -81,10 +81,13 @@ def norms_in_prep(cfg, sumM, nc, cus=256):
     return not (idle >= 16 and idle * 128 >= cfg.B * cfg.N)
 
 
-def algorithmic_work(cfg, sumM, gathered=True, nc=0):
+def algorithmic_work(cfg, sumM, gathered=True, nc=0, chunks=None):
     """Per-launch algorithmic work of each kernel: (bound, amount, unit).
     `gathered`: the selection launch also gathers the kept rows (no gather launch).
-    `nc`: tokens per image of the candidate subset the selection runs on (0: all N)."""
+    `nc`: tokens per image of the candidate subset the selection runs on (0: all N).
+    `chunks`: the images' chunks of 16 question tokens (default: one image)."""
+    if chunks is None:
+        chunks = -(-sumM // 16)
     B, N, K, K0 = cfg.B, cfg.N, cfg.K, cfg.K0
     K0f = K0 if 0 < K0 <= R0_FACTOR_MAX else 0  # picks placed by the R0 kernel
     D, H, dp = cfg.pred.D, cfg.pred.D_h, cfg.pred.d_p
@@ -120,6 +123,11 @@ def algorithmic_work(cfg, sumM, gathered=True, nc=0):
         "logits": ("hbm", 4.0 * (B * N + sumM) * dp + 4.0 * sumM * N + 8.0 * sumM * ((N + 63) // 64), "byte"),
         # read logits and partials, write p
         "softmax_mean": ("hbm", 4.0 * sumM * N + 8.0 * sumM * ((N + 63) // 64) + 4.0 * B * N, "byte"),
+        # both in one launch: read keys and queries; the per-block (max, sum of
+        # exp) pairs and each question chunk's share of p written and read once;
+        # write p
+        "score": ("hbm", 4.0 * (B * N + sumM) * dp + 16.0 * sumM * ((N + 63) // 64) + 8.0 * chunks * N
+                  + 4.0 * B * N, "byte"),
         # R0 (K0 <= 128): p, the norms and the K0 similarity rows of R0 in; the
         # K0 coefficient rows of every token, r^2, order and gain out
         "select_r0": ("hbm", B * (12.0 * Ns + 8.0 * K0 * Ns + 8.0 * K0), "byte"),
@@ -149,6 +157,7 @@ KERNEL_SOURCES = {
     "gemm_proj_rope": ("gemm.hip", "internal.h"),
     "logits": ("score.hip", "internal.h"),
     "softmax_mean": ("score.hip", "internal.h"),
+    "score": ("score.hip", "internal.h"),
     "select_r0": ("select.hip", "internal.h"),
     "select": ("select.hip", "internal.h"),
     "gather": ("gather.hip", "internal.h"),
@@ -493,7 +502,8 @@ def measure_prune(mp, torch, dev, cfg, x, d, steps, warmup, subset=0, per_step=0
     kern = _kernel_table(mp, torch, step, steps)
     sumM = int(t_off[-1])
     nc = subset_tokens(cfg, subset) if "subset" in kern else 0
-    work = algorithmic_work(cfg, sumM, gathered="gather" not in kern, nc=nc)
+    chunks = sum(-(-(int(t_off[b + 1]) - int(t_off[b])) // 16) for b in range(cfg.B))
+    work = algorithmic_work(cfg, sumM, gathered="gather" not in kern, nc=nc, chunks=chunks)
     # (the full-path launches behind a subset do work only for images the
     # subset cannot certify: they are never the dominant kernel)
     dominant = max((k for k in kern if not k.endswith("_full")),

@@ -189,6 +189,8 @@ struct PrepArgs {
   const void* fb[2];
   float* fout[2];
   int frows, fcols;
+  uint64_t* clear[2];     // optional: arrays zeroed by the launch (the scoring's exchange words)
+  long long nclear[2];
 };
 hipError_t launch_prep(map_dtype dt, const PrepArgs& a, bool norms, bool table, bool fold, hipStream_t s);
 
@@ -203,14 +205,24 @@ hipError_t launch_finite_check(const void* p, long long count, int elem_bytes, i
 struct ScoreArgs {
   const float* q;         // [sum_M][d_p] (after RoPE)
   const float* k;         // [B][N][d_p]  (after RoPE)
-  float* logits;          // [sum_M][N]
+  float* logits;          // [sum_M][N]: written by the two-launch form, and by the
+                          // one-launch form when store_logits (the training step)
   float2* partial;        // [sum_M][nblk] (running max, sum of exp) per key block
   unsigned int* clear_bar; // optional: selection barrier counters [B] to zero
-  int32_t* clear_err;      // optional: selection error flag to zero
+  int32_t* clear_err;      // optional: selection error flag to zero (set when the
+                           // one-launch form's barrier gives up)
   float* p_out;           // [B][N]
+  // the one-launch form (null pp: the two-launch form) exchanges the pairs
+  // in `partial` and each question chunk's share of p in `pp` as 64-bit
+  // words; both arrays are zeroed before the launch (prep does it)
+  uint64_t* pp;           // [q_off[B]][N], rows q_off[b] + chunk
+  int store_logits;
   int B, N, d_p, nblk;
   int t_off[MAP_MAX_BATCH + 1];
+  int q_off[MAP_MAX_BATCH + 1];  // chunks of 16 queries before image b (set by launch_score)
 };
+// Rows of ScoreArgs::pp a call with these question lengths needs at most.
+inline long long score_pp_rows(int B, int sumM) { return (sumM + 15) / 16 + B; }
 hipError_t launch_score(const ScoreArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- select

@@ -98,6 +98,8 @@ struct ScoreWs {
   float *bc_v, *bc_t;   // folded W_K b2, W_Q b2 [d_p]
   float *k, *q, *logits;
   float2* partial;
+  uint64_t* pp;  // the one-launch scoring's shares of p
+  long long pp_words;
 };
 
 ScoreWs carve_score(Carver& c, map_dtype dt, int B, int N, int sumM, const map_weights& w) {
@@ -118,6 +120,8 @@ ScoreWs carve_score(Carver& c, map_dtype dt, int B, int N, int sumM, const map_w
   s.q = c.take<float>((size_t)sumM * w.d_p);
   s.logits = c.take<float>((size_t)sumM * N);
   s.partial = c.take<float2>((size_t)sumM * nblk);
+  s.pp_words = score_pp_rows(B, sumM) * N;
+  s.pp = c.take<uint64_t>((size_t)s.pp_words);
   return s;
 }
 
@@ -290,6 +294,10 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   pa.fout[1] = s.bc_t;
   pa.frows = w.d_p;
   pa.fcols = w.D_h;
+  pa.clear[0] = reinterpret_cast<uint64_t*>(s.partial);
+  pa.nclear[0] = (long long)sumM * ((N + 63) / 64);
+  pa.clear[1] = s.pp;
+  pa.nclear[1] = s.pp_words;
   GemmBatch g1;
   memset(&g1, 0, sizeof(g1));
   g1.p[0] = linear(V, rowsV, w.w1_v, w.b1_v, s.h1_v, w.D_h, w.D, EPI_BIAS_GELU);
@@ -350,7 +358,9 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   sa.q = s.q;
   sa.k = s.k;
   sa.logits = s.logits;
+  sa.store_logits = gprime_v != nullptr;  // the training step's backward reads them
   sa.partial = s.partial;
+  sa.pp = s.pp;
   sa.clear_bar = clear_bar;
   sa.clear_err = clear_err;
   sa.p_out = p_out;

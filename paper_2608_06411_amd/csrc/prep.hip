@@ -25,6 +25,10 @@ constexpr int kRowsPerBlock = 4;
 template <typename T>
 __global__ __launch_bounds__(256) void prep_kernel(const PrepArgs a, int norm_blocks, int table_blocks,
                                                    int tr_blocks) {
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+    if (a.clear[c])
+      for (long long i = blockIdx.x * 256ll + threadIdx.x; i < a.nclear[c]; i += 256ll * gridDim.x) a.clear[c][i] = 0ull;
   int bid = static_cast<int>(blockIdx.x) - norm_blocks - table_blocks;
   if (bid >= 0) {
     if (bid < tr_blocks) {  // transpose tile (ti, tj) of matrix s, 16-byte pieces both ways

@@ -1,17 +1,27 @@
 // Predicted attention, Eq. (3): logits, softmax over the visual tokens and
 // the mean over the question tokens.
 //
-// logits_kernel: one workgroup per (block of 64 visual tokens, chunk of 16
-// question tokens, image).  Each wave forms a 16 x 16 tile of q.k / sqrt(d_p)
-// on float32 matrix cores from operands read straight from global memory, and
-// the workgroup also emits each query's (max, sum of exp) over its 64 logits,
-// so that no pass over a whole logits row is needed later.
+// score_kernel (one launch): one workgroup per (block of 64 visual tokens,
+// chunk of 16 question tokens, image).  Each wave forms a 16 x 16 tile of
+// q.k / sqrt(d_p) on float32 matrix cores from operands read straight from
+// global memory and keeps it in registers; the workgroup publishes each
+// query's (max, sum of exp) over its 64 logits as one 64-bit word.  Each
+// workgroup then waits for the words of its 16 queries from every token
+// block of the image, folds them into the row statistics (max_m, sum_m),
+// and publishes its 64 tokens' share sum_m exp(l_mn - max_m) / sum_m over
+// those queries, again as 64-bit words; the workgroup of the image's first
+// chunk waits for the other chunks' shares of its tokens, adds them in
+// chunk order and divides by M.  A published word is never zero (a sum of
+// exp includes exp(0) = 1; a share word carries a marker in its high half),
+// and prep zeroes both arrays before the launch, so a nonzero word is a
+// complete one: the exchange needs no counters and no cache flushes, only
+// agent-scope atomic 64-bit stores and loads.  Every sum runs in a fixed
+// order, so the result is bitwise reproducible.  The host launches it only
+// for groups of images whose workgroups can all be resident at once.
 //
-// softmax_mean_kernel: one workgroup per (block of 64 visual tokens, image).
-// Each workgroup folds the per-block partials of its image into the row
-// statistics (max_m, sum_m), four threads per row with all loads in flight,
-// then for its 64 tokens averages exp(l_mn - max_m) / sum_m over m.  The sums
-// run in a fixed order, so the result is bitwise reproducible.
+// logits_kernel + softmax_mean_kernel: the same in two launches, for
+// questions too long for the one-launch form: the first writes the logits
+// and the per-block pairs, the second folds the pairs and averages over m.
 #include "internal.h"
 
 namespace mapk {
@@ -23,14 +33,26 @@ constexpr int QB = 16;    // question tokens per workgroup
 
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
-__global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
-  __shared__ float wmax[4][QB];
-  __shared__ float wsum[4][QB];
-  const int blk = blockIdx.x, q0 = blockIdx.y * QB, b = blockIdx.z, tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+__device__ __forceinline__ uint64_t load_word(const uint64_t* p) {
+  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_word(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 word_pair(uint64_t w) {
+  return make_float2(__uint_as_float(static_cast<uint32_t>(w)), __uint_as_float(static_cast<uint32_t>(w >> 32)));
+}
+
+
+// The 16 x 64 tile (queries q0 .., keys 64 blk ..) of image b: out[i] is the
+// scaled logit of query q0 + 4 (lane >> 4) + i and key 64 blk + 16 wave +
+// (lane & 15).  The logits are stored when `store`; each query's (max, sum
+// of exp) over the 64 keys goes to a.partial.
+__device__ __forceinline__ void logits_tile(const ScoreArgs& a, int b, int blk, int q0, bool store, float (&out)[4],
+                                            float (*wmax)[QB], float (*wsum)[QB], bool words) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n0 = blk * KB, dp = a.d_p;
   const int mb = a.t_off[b], M = a.t_off[b + 1] - mb;
-  if (q0 >= M) return;
   // Wave w forms the 16 x 16 tile (queries q0 .. q0 + 15) x (keys n0 + 16 w ..)
   // on float32 16 x 16 x 4 matrix cores.  Lane l supplies query row l & 15
   // and key row l & 15 at d = 16 t + 4 (l >> 4) + e to the e-th product of
@@ -65,10 +87,10 @@ __global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
   float mx[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    acc[i] *= scale;
+    out[i] = acc[i] * scale;
     const int m = q0 + 4 * g + i;
-    if (m < M && nok) a.logits[(long long)(mb + m) * a.N + n] = acc[i];
-    mx[i] = nok ? acc[i] : -INFINITY;
+    if (store && m < M && nok) a.logits[(long long)(mb + m) * a.N + n] = out[i];
+    mx[i] = nok ? out[i] : -INFINITY;
   }
   // per query: the maximum over the block's 64 keys (the 16 lanes of a group
   // hold one query's 16 keys of this wave), then the sum of exp in a fixed order
@@ -85,8 +107,7 @@ __global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
   for (int i = 0; i < 4; ++i) {
     const int qi = 4 * g + i;
     const float bm = fmaxf(fmaxf(wmax[0][qi], wmax[1][qi]), fmaxf(wmax[2][qi], wmax[3][qi]));
-    mx[i] = bm;
-    sm[i] = nok ? expf(acc[i] - bm) : 0.0f;
+    sm[i] = nok ? expf(out[i] - bm) : 0.0f;
   }
 #pragma unroll
   for (int off = 8; off > 0; off >>= 1)
@@ -96,10 +117,144 @@ __global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) wsum[wave][4 * g + i] = sm[i];
   __syncthreads();
-  if (tid < QB && q0 + tid < M)
-    a.partial[(long long)(mb + q0 + tid) * a.nblk + blk] =
-        make_float2(fmaxf(fmaxf(wmax[0][tid], wmax[1][tid]), fmaxf(wmax[2][tid], wmax[3][tid])),
-                    (wsum[0][tid] + wsum[1][tid]) + (wsum[2][tid] + wsum[3][tid]));
+  if (tid < QB && q0 + tid < M) {
+    const float bm = fmaxf(fmaxf(wmax[0][tid], wmax[1][tid]), fmaxf(wmax[2][tid], wmax[3][tid]));
+    const float bs = (wsum[0][tid] + wsum[1][tid]) + (wsum[2][tid] + wsum[3][tid]);
+    float2* dst = a.partial + (long long)(mb + q0 + tid) * a.nblk + blk;
+    if (words)
+      store_word(reinterpret_cast<uint64_t*>(dst),
+                 (static_cast<uint64_t>(__float_as_uint(bs)) << 32) | __float_as_uint(bm));
+    else
+      *dst = make_float2(bm, bs);
+  }
+}
+
+// (max, sum of exp) pairs combined: lo is the pair of the lower lane (or the
+// running pair), so every lane of a butterfly gets the same bits.
+__device__ __forceinline__ float2 merge_pair(float2 lo, float2 hi) {
+  const float nm = fmaxf(lo.x, hi.x);
+  return make_float2(nm, (lo.x == -INFINITY ? 0.0f : lo.y * expf(lo.x - nm)) +
+                             (hi.x == -INFINITY ? 0.0f : hi.y * expf(hi.x - nm)));
+}
+
+__device__ __forceinline__ void clear_selection_counters(const ScoreArgs& a) {
+  for (int i = threadIdx.x; i < a.B; i += 256) a.clear_bar[i] = 0u;
+  if (threadIdx.x == 0) *a.clear_err = 0;
+}
+
+constexpr unsigned kScoreSpinLimit = 1u << 20;  // polls of one word set (each sleeps about 64 clocks)
+
+__global__ __launch_bounds__(256) void score_kernel(const ScoreArgs a, int b0) {
+  __shared__ float wmax[4][QB];
+  __shared__ float wsum[4][QB];
+  __shared__ float2 stats[QB];
+  const int blk = blockIdx.x, qc = blockIdx.y, b = b0 + blockIdx.z, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int mb = a.t_off[b], M = a.t_off[b + 1] - mb, q0 = qc * QB;
+  if (a.clear_bar && blk == 0 && qc == 0 && blockIdx.z == 0) clear_selection_counters(a);
+  if (q0 >= M) return;
+  float l[4];
+  // the tile; its (max, sum) pairs go out as words (x in the low half)
+  logits_tile(a, b, blk, q0, a.store_logits != 0, l, wmax, wsum, true);
+
+  // row statistics of the 16 queries: 16 threads per query, thread j waiting
+  // for the words of blocks j, j + 16, ... (all polled at once), then folding
+  // them in block order and a butterfly over the 16 in a fixed pairing
+  bool ok = true;
+  {
+    constexpr int PW = 16;  // blocks per thread (nblk <= 256)
+    const int qi = tid >> 4, j = tid & 15, m = min(q0 + qi, M - 1);
+    const uint64_t* pr = reinterpret_cast<const uint64_t*>(a.partial) + (long long)(mb + m) * a.nblk;
+    uint64_t w[PW];
+#pragma unroll
+    for (int u = 0; u < PW; ++u) w[u] = j + 16 * u < a.nblk ? load_word(pr + j + 16 * u) : 1ull;
+    for (unsigned spins = 0;; ++spins) {
+      bool all = true;
+#pragma unroll
+      for (int u = 0; u < PW; ++u) all = all && w[u] != 0ull;
+      if (all) break;
+      if (spins > kScoreSpinLimit) {  // not every workgroup was resident
+        ok = false;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+      for (int u = 0; u < PW; ++u)
+        if (w[u] == 0ull) w[u] = load_word(pr + j + 16 * u);
+    }
+    float2 run = make_float2(-INFINITY, 0.0f);
+#pragma unroll
+    for (int u = 0; u < PW; ++u)
+      if (j + 16 * u < a.nblk) run = merge_pair(run, word_pair(w[u]));
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const float2 o = make_float2(__shfl_xor(run.x, off, 16), __shfl_xor(run.y, off, 16));
+      run = (j & off) ? merge_pair(o, run) : merge_pair(run, o);
+    }
+    if (j == 0) stats[qi] = make_float2(run.x, 1.0f / run.y);
+  }
+  ok = __syncthreads_and(ok);
+  if (!ok && tid == 0 && a.clear_err) atomicExch(a.clear_err, 1);
+
+  // this chunk's share of the mean for the 64 tokens: lane (g, r) of wave w
+  // sums its four queries, then the four groups g are added
+  const int r = lane & 15, g = lane >> 4, n = blk * KB + 16 * wave + r;
+  float v = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int qi = 4 * g + i;
+    if (q0 + qi < M) v += expf(l[i] - stats[qi].x) * stats[qi].y;
+  }
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 32);
+  if (!ok) v = NAN;
+  uint64_t* pp = a.pp + (long long)a.q_off[b] * a.N;
+  if (qc > 0) {
+    if (g == 0 && n < a.N) store_word(pp + (long long)qc * a.N + n, (1ull << 32) | __float_as_uint(v));
+    return;
+  }
+  // the first chunk's workgroup adds the other chunks' shares in chunk order
+  const int nq = (M + QB - 1) / QB;
+  if (g == 0 && n < a.N) {
+    float s = v;
+    constexpr int CW = 8;  // chunks polled at once
+    for (int c0 = 1; c0 < nq; c0 += CW) {
+      uint64_t x[CW];
+#pragma unroll
+      for (int u = 0; u < CW; ++u) x[u] = c0 + u < nq ? load_word(pp + (long long)(c0 + u) * a.N + n) : 1ull;
+      for (unsigned spins = 0;; ++spins) {
+        bool all = true;
+#pragma unroll
+        for (int u = 0; u < CW; ++u) all = all && x[u] != 0ull;
+        if (all) break;
+        if (spins > kScoreSpinLimit) {
+#pragma unroll
+          for (int u = 0; u < CW; ++u)
+            if (x[u] == 0ull) x[u] = (1ull << 32) | __float_as_uint(NAN);
+          if (a.clear_err) atomicExch(a.clear_err, 1);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+        for (int u = 0; u < CW; ++u)
+          if (x[u] == 0ull) x[u] = load_word(pp + (long long)(c0 + u) * a.N + n);
+      }
+#pragma unroll
+      for (int u = 0; u < CW; ++u)
+        if (c0 + u < nq) s += __uint_as_float(static_cast<uint32_t>(x[u]));
+    }
+    a.p_out[(long long)b * a.N + n] = s / static_cast<float>(M);
+  }
+}
+
+__global__ __launch_bounds__(256) void logits_kernel(const ScoreArgs a) {
+  __shared__ float wmax[4][QB];
+  __shared__ float wsum[4][QB];
+  const int blk = blockIdx.x, q0 = blockIdx.y * QB, b = blockIdx.z;
+  const int M = a.t_off[b + 1] - a.t_off[b];
+  if (q0 >= M) return;
+  float l[4];
+  logits_tile(a, b, blk, q0, true, l, wmax, wsum, false);
 }
 
 __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
@@ -107,10 +262,7 @@ __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
   __shared__ float part[4][KB];
   const int blk = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
   const int mb = a.t_off[b], M = a.t_off[b + 1] - mb;
-  if (a.clear_bar && blk == 0 && b == 0) {  // the selection that follows starts from zero
-    for (int i = tid; i < a.B; i += 256) a.clear_bar[i] = 0u;
-    if (tid == 0) *a.clear_err = 0;
-  }
+  if (a.clear_bar && blk == 0 && b == 0) clear_selection_counters(a);  // the selection starts from zero
   // the first LU logits of this thread's token (question tokens g, g + 4,
   // ...) are loaded now, at clamped addresses, so that they arrive while the
   // row statistics are formed
@@ -193,9 +345,53 @@ __global__ __launch_bounds__(256) void softmax_mean_kernel(const ScoreArgs a) {
 
 }  // namespace
 
-hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
+// Workgroups of score_kernel that can be resident at once on the current
+// device (cached per device; 0 when unknown).
+static int score_capacity() {
+  static int cached[16] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 16) return 0;
+  if (cached[dev] == 0) {
+    int cus = 0, per = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, score_kernel, 256, 0) != hipSuccess || cus <= 0 || per <= 0)
+      return 0;
+    cached[dev] = cus * per;
+  }
+  return cached[dev];
+}
+
+hipError_t launch_score(const ScoreArgs& a0, hipStream_t s) {
+  ScoreArgs a = a0;
   int maxM = 0;
-  for (int b = 0; b < a.B; ++b) maxM = a.t_off[b + 1] - a.t_off[b] > maxM ? a.t_off[b + 1] - a.t_off[b] : maxM;
+  a.q_off[0] = 0;
+  for (int b = 0; b < a.B; ++b) {
+    const int M = a.t_off[b + 1] - a.t_off[b];
+    maxM = M > maxM ? M : maxM;
+    a.q_off[b + 1] = a.q_off[b] + (M + QB - 1) / QB;
+  }
+  // one launch per group of images whose workgroups all fit on the device
+  const int cap = a.pp && a.nblk <= 256 ? score_capacity() : 0;
+  bool fits = cap > 0;
+  for (int b = 0; b < a.B && fits; ++b) fits = (long long)a.nblk * (a.q_off[b + 1] - a.q_off[b]) <= cap;
+  if (fits) {
+    for (int b0 = 0; b0 < a.B;) {
+      int b1 = b0, mq = 0;
+      long long wgs = 0;
+      while (b1 < a.B && wgs + (long long)a.nblk * (a.q_off[b1 + 1] - a.q_off[b1]) <= cap) {
+        const int nq = a.q_off[b1 + 1] - a.q_off[b1];
+        wgs += (long long)a.nblk * nq;
+        mq = nq > mq ? nq : mq;
+        ++b1;
+      }
+      const hipError_t e = launch_kernel("score", score_kernel, dim3(a.nblk, mq, b1 - b0), dim3(256), 0, s, a, b0);
+      if (e != hipSuccess) return e;
+      a.clear_bar = nullptr;  // cleared by the first launch
+      a.clear_err = nullptr;
+      b0 = b1;
+    }
+    return hipSuccess;
+  }
   const hipError_t e =
       launch_kernel("logits", logits_kernel, dim3(a.nblk, (maxM + QB - 1) / QB, a.B), dim3(256), 0, s, a);
   if (e != hipSuccess) return e;
