@@ -53,6 +53,8 @@ def subset_tokens(cfg, setting=0):
         return 0
     nc = setting
     if setting == 0:
+        if 12 * cfg.K > cfg.N:
+            return 0
         nc = (cfg.K0 + max(2 * (cfg.K - cfg.K0), cfg.N // 4) + 63) // 64 * 64
         if 4 * nc > 3 * cfg.N:
             return 0

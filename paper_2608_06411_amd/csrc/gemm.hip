@@ -586,12 +586,12 @@ template <int J>
 __device__ __forceinline__ void epi_cosine_staged(const GemmProblem& P, int bt, int tm, int tn,
                                                   f32x16_t (&acc)[2][J], const StagedTile& L,
                                                   const float* rs_rows, const float* rs_cols, int tid,
-                                                  int lane, int wm, int wn) {
+                                                  int lane, int wm, int wn, bool active = true) {
   constexpr int NTH = EpiThreads<J>::value;
   const int M = P.M, N = P.N, m0 = tm * BM, n0 = tn * BN;
   const bool diag = tm == tn;
 #pragma unroll
-  for (int j = 0; j < J; ++j) {
+  for (int j = 0; active && j < J; ++j) {
     const int cl = wn * (32 * J) + j * 32 + acc_col(lane);
     const float sc = rs_cols[cl];
 #pragma unroll
@@ -609,6 +609,7 @@ __device__ __forceinline__ void epi_cosine_staged(const GemmProblem& P, int bt, 
       }
   }
   __syncthreads();
+  if (!active) return;  // (a workgroup's other half: only the barrier above)
   float* __restrict__ S = static_cast<float*>(P.C) + bt * P.strideC;
   const bool vec = (P.ldc & 3) == 0;
   // S[m0 + r][n0 + 4 ch ..]: row r of the tile (the mirror below a diagonal tile's diagonal)
@@ -917,15 +918,21 @@ __global__ __launch_bounds__(kDmaThreads) void gemm_dma_kernel(const GemmBatch a
 // i.e. 2 x 4 MFMA 32x32 blocks whose two A operands serve four products.
 // Group h then holds sub-tiles (h, 0) and (h, 1) in the 128 x 128 kernel's
 // accumulator layout and finishes them with its epilogues, staging through
-// its own 64 KiB.  Two 64 KiB stages: one K slice loads while the matrix
-// cores consume the other.  Tiles are ordered in groups of kBigRows tile
-// rows, column by column inside a group, each XCD taking a contiguous range.
+// its own 64 KiB; the cosine epilogue (a Gram matrix's upper triangle of
+// tiles, mirrored) needs 128 KiB per sub-tile, so the two groups take turns
+// there, sub-tile by sub-tile, and a diagonal tile's sub-tile below the
+// diagonal is the mirror of the one above it.  Two 64 KiB stages: one K
+// slice loads while the matrix cores consume the other.  Tiles are ordered
+// in groups of kBigRows tile rows, column by column inside a group (a
+// triangular problem: its upper triangle row by row), each XCD taking a
+// contiguous range.
 constexpr int kBig = 256;
 constexpr int kBigThreads = 512;
 constexpr int kBigRows = 4;
 
 __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch args) {
   __shared__ uint4 bst0[2 * kBig][8], bst1[2 * kBig][8];  // per stage: A rows, then B rows
+  __shared__ float rs_big[2 * kBig];                       // cosine: 1/norm of the tile's rows, then columns
   const int tile = xcd_remap(blockIdx.x, args.total_tiles);
   int pi = 0;
 #pragma unroll
@@ -933,10 +940,18 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
     if (q < args.count && tile >= args.p[q].tile_begin) pi = q;
   const GemmProblem& P = args.p[pi];
   const int local = tile - P.tile_begin;
-  const int bt = local / P.tiles_per_batch, tt = local - bt * P.tiles_per_batch;
-  const int grp = tt / (kBigRows * P.tiles_n), first = grp * kBigRows;
-  const int rows = min(kBigRows, P.tiles_m - first), in = tt - grp * kBigRows * P.tiles_n;
-  const int tm = first + in % rows, tn = in / rows;
+  const int bt = local / P.tiles_per_batch;
+  int tt = local - bt * P.tiles_per_batch, tm, tn;
+  if (P.triangular) {  // upper triangle, row by row: row tm holds tiles_n - tm tiles
+    tm = 0;
+    while (tt >= P.tiles_n - tm) { tt -= P.tiles_n - tm; ++tm; }
+    tn = tm + tt;
+  } else {
+    const int grp = tt / (kBigRows * P.tiles_n), first = grp * kBigRows;
+    const int rows = min(kBigRows, P.tiles_m - first), in = tt - grp * kBigRows * P.tiles_n;
+    tm = first + in % rows;
+    tn = in / rows;
+  }
   if (P.run_if && P.run_if[bt] == 0) return;
   const int M = P.M, N = P.N, m0 = tm * kBig, n0 = tn * kBig;
   const bf16_t* __restrict__ A = static_cast<const bf16_t*>(P.A) + bt * P.strideA;
@@ -944,6 +959,11 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = wave >> 2, qm = (wave >> 1) & 1, qn = wave & 1;
   const int nk = P.K / 64;
+  float rs_mine = 0.0f;  // cosine epilogue: 1/norm of tile row tid, or of column tid - 256
+  if (P.epi == EPI_COSINE) {
+    const int k = tid < kBig ? m0 + tid : n0 + tid - kBig;
+    if (k < (tid < kBig ? M : N)) rs_mine = P.rs[(long long)bt * M + k];
+  }
   // wave w loads rows 32 w .. 32 w + 31 of the A tile and of the B tile,
   // one instruction per 8 rows (rows past the matrix read its last row)
   const int32_t* mapA = P.mapA ? P.mapA + bt * P.mapStride : nullptr;
@@ -1059,6 +1079,22 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
     }
   }
   __syncthreads();  // the epilogues reuse the stages: group h stages through bst<h>
+  if (P.epi == EPI_COSINE) {
+    rs_big[tid] = rs_mine;
+    const StagedTile LC{reinterpret_cast<float*>(&bst0[0][0]), reinterpret_cast<float*>(&bst0[0][0]) + 64 * BN,
+                        reinterpret_cast<float*>(&bst1[0][0]), reinterpret_cast<float*>(&bst1[0][0]) + 64 * BM};
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int TM = 2 * tm + hh, TN = 2 * tn + s;  // the sub-tile in 128 x 128 tiles
+        if (TM > TN || TM * BM >= M || TN * BN >= N) continue;  // (uniform over the workgroup)
+        __syncthreads();  // the staging is free (and rs_big written)
+        epi_cosine_staged<2>(P, bt, TM, TN, acc[s], LC, rs_big + 128 * hh, rs_big + kBig + 128 * s,
+                             tid & (NT - 1), lane, qm, qn, h == hh);
+      }
+    return;
+  }
   float* stg = reinterpret_cast<float*>(h ? &bst1[0][0] : &bst0[0][0]);
   const StagedTile L{stg, stg + 64 * BN, nullptr, nullptr};
   const int t2 = tid & (NT - 1);
@@ -1355,8 +1391,9 @@ static int gemm_cus() {
 }
 
 // 256 x 256 tiles for a direct-load launch whose problems all have a
-// row-wise epilogue (bias, GELU, float32, GELU', product, residual) and no
-// K split, when they take fewer waves of workgroups: a wave of 256 x 256
+// row-wise epilogue (bias, GELU, float32, GELU', product, residual) or are a
+// Gram matrix's upper triangle (cosine), and no K split, when they take
+// fewer waves of workgroups: a wave of 256 x 256
 // tiles costs about 2.3 waves of 128 x 128 tiles (measured on the first
 // layer's and the decoder layer's shapes).
 static bool big_tiles_pay(const GemmBatch& g) {
@@ -1365,10 +1402,14 @@ static bool big_tiles_pay(const GemmBatch& g) {
   long long t128 = 0, t256 = 0;
   for (int i = 0; i < g.count; ++i) {
     const GemmProblem& p = g.p[i];
-    if (!(p.epi == EPI_BIAS || p.epi == EPI_BIAS_GELU || epi_direct(p.epi)) || p.ksplit > 1 || p.triangular)
+    const bool gram = p.epi == EPI_COSINE && p.triangular && p.M == p.N;
+    if (!(p.epi == EPI_BIAS || p.epi == EPI_BIAS_GELU || epi_direct(p.epi) || gram) || p.ksplit > 1 ||
+        (p.triangular && !gram))
       return false;
-    t128 += (long long)((p.M + 127) / 128) * ((p.N + 127) / 128) * p.batch;
-    t256 += (long long)((p.M + kBig - 1) / kBig) * ((p.N + kBig - 1) / kBig) * p.batch;
+    const long long a = (p.M + 127) / 128, b = (p.N + 127) / 128;
+    const long long c = (p.M + kBig - 1) / kBig, d = (p.N + kBig - 1) / kBig;
+    t128 += (gram ? a * (a + 1) / 2 : a * b) * p.batch;
+    t256 += (gram ? c * (c + 1) / 2 : c * d) * p.batch;
   }
   const long long cus = gemm_cus();
   return 23 * ((t256 + cus - 1) / cus) < 10 * ((t128 + cus - 1) / cus);
@@ -1380,7 +1421,7 @@ static void finalize_big(GemmBatch& g) {
     GemmProblem& p = g.p[i];
     p.tiles_m = (p.M + kBig - 1) / kBig;
     p.tiles_n = (p.N + kBig - 1) / kBig;
-    p.tiles_tri = p.tiles_m * p.tiles_n;
+    p.tiles_tri = p.triangular ? p.tiles_m * (p.tiles_m + 1) / 2 : p.tiles_m * p.tiles_n;
     p.tiles_per_batch = p.tiles_tri;
     p.tile_begin = begin;
     begin += p.tiles_per_batch * p.batch;

@@ -148,6 +148,10 @@ int subset_size(map_dtype dt, int N, int D, const map_select_params& sp) {
   if (o < 0 || dt != MAP_BF16 || D % 256 != 0 || N > kSubsetMaxN) return 0;
   int nc = o;
   if (o == 0) {
+    // Past K = N / 12 the greedy picks' scores fall into the bulk of the
+    // bounds and the certificate needs nearly every token (K = N / 9: 80-95 %
+    // of them on the retention sweep's images), so the subset cannot pay.
+    if (12 * sp.K > N) return 0;
     nc = (sp.K0 + std::max(2 * (sp.K - sp.K0), N / 4) + 63) & ~63;
     if (4 * nc > 3 * N) return 0;  // too close to N to pay
   }

@@ -123,8 +123,12 @@ def test_sweep_retention_budgets(sweep, K):
     x, d, p_ref = sweep
     cfg = x["cfg"]
     K0, tau = K // 2, cfg.tau
-    announce(f"sweep B={cfg.B} K={K} subset auto")
-    auto = _prune(x, d, K, K0, tau, subset=0)
+    # past K = N / 12 the automatic rule takes the full path at once; a
+    # subset of N / 3 forced there still runs the subset, which flags the
+    # images it cannot certify for the full selection behind it
+    subset = 0 if 12 * K <= cfg.N else cfg.N // 3
+    announce(f"sweep B={cfg.B} K={K} subset {subset or 'auto'}")
+    auto = _prune(x, d, K, K0, tau, subset=subset)
     _check_structure(x, auto, K, p_ref, 2e-2)
     replayed = list(range(cfg.B)) if K <= 160 else [0, cfg.B - 1]
     reps = _replay(x, auto, K, K0, tau, replayed)

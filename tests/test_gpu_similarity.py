@@ -30,6 +30,9 @@ def _tokens(seed, B, N, D, dtype):
 @pytest.mark.parametrize("dtype,B,N,D", [
     ("f32", 1, 576, 256), ("bf16", 2, 300, 512), ("bf16", 1, 1, 64), ("f32", 1, 130, 4096),
     ("bf16", 1, 257, 4096), ("bf16", 3, 129, 3584),
+    # enough tiles for the 256 x 256 kernel (its last tile row and column
+    # partial): the cosine epilogue's sub-tiles and their mirrors
+    ("bf16", 2, 4500, 3584),
 ])
 def test_similarity_matches_oracle(dtype, B, N, D):
     from paper_2608_06411_amd import map_similarity
