@@ -212,7 +212,8 @@ struct ScoreArgs {
   int32_t* clear_err;      // optional: selection error flag to zero (set when the
                            // one-launch form's barrier gives up)
   float* p_out;           // [B][N]
-  // the one-launch form (null pp: the two-launch form) exchanges the pairs
+  // the one-launch form (null pp, or score_one_launch false: the two-launch
+  // form) exchanges the pairs
   // in `partial` and each question chunk's share of p in `pp` as 64-bit
   // words; both arrays are zeroed before the launch (prep does it)
   uint64_t* pp;           // [q_off[B]][N], rows q_off[b] + chunk
@@ -224,6 +225,9 @@ struct ScoreArgs {
 // Rows of ScoreArgs::pp a call with these question lengths needs at most.
 inline long long score_pp_rows(int B, int sumM) { return (sumM + 15) / 16 + B; }
 hipError_t launch_score(const ScoreArgs& a, hipStream_t s);
+// Whether launch_score takes the one-launch form for these question lengths
+// (t_off host, [B + 1]); its exchange arrays must then be zeroed first.
+bool score_one_launch(int B, int N, const int32_t* t_off);
 
 // ---------------------------------------------------------------- select
 struct SelectArgs {

@@ -298,10 +298,13 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   pa.fout[1] = s.bc_t;
   pa.frows = w.d_p;
   pa.fcols = w.D_h;
-  pa.clear[0] = reinterpret_cast<uint64_t*>(s.partial);
-  pa.nclear[0] = (long long)sumM * ((N + 63) / 64);
-  pa.clear[1] = s.pp;
-  pa.nclear[1] = s.pp_words;
+  const bool one_launch = score_one_launch(B, N, t_off);  // the scoring's exchange arrays, zeroed here
+  if (one_launch) {
+    pa.clear[0] = reinterpret_cast<uint64_t*>(s.partial);
+    pa.nclear[0] = (long long)sumM * ((N + 63) / 64);
+    pa.clear[1] = s.pp;
+    pa.nclear[1] = s.pp_words;
+  }
   GemmBatch g1;
   memset(&g1, 0, sizeof(g1));
   g1.p[0] = linear(V, rowsV, w.w1_v, w.b1_v, s.h1_v, w.D_h, w.D, EPI_BIAS_GELU);
@@ -364,7 +367,7 @@ hipError_t enqueue_score(const map_weights& w, map_dtype dt, int B, int N, const
   sa.logits = s.logits;
   sa.store_logits = gprime_v != nullptr;  // the training step's backward reads them
   sa.partial = s.partial;
-  sa.pp = s.pp;
+  sa.pp = one_launch ? s.pp : nullptr;
   sa.clear_bar = clear_bar;
   sa.clear_err = clear_err;
   sa.p_out = p_out;
