@@ -695,29 +695,35 @@ __device__ __forceinline__ void wait_vm_lgkm0(int outstanding) {
   else __builtin_amdgcn_s_waitcnt(0x0070);
 }
 
-// The eight-wave 128 x 128 tile's operands and products: wave (wm, wn) forms
-// rows 64 wm + (0..63) by columns 32 wn + (0..31), two 32x32 blocks sharing
-// the B operand.  One register buffer per k-step of a slice (four of them),
-// so the operands of step s + 2 are read while the products of step s run.
-struct Mma8 {
-  bf16x8_t a[4][2], b[4];
-  int wm, wn, lane;
-  __device__ __forceinline__ void read(const uint4 (*As)[8], const uint4 (*Bs)[8], int s) {
-    const int lr = lane & 31, v = 2 * s + (lane >> 5);  // 16-byte chunk: k = 16 s + 8 (lane >> 5) + (0..7)
+// One K slice of the eight-wave 128 x 128 tile: wave (wm, wn) forms rows
+// 64 wm + (0..63) by columns 32 wn + (0..31), two 32x32 blocks sharing the B
+// operand; the operands of step s + 1 are read before the products of
+// step s issue.
+__device__ __forceinline__ void mma_slice8(const uint4 (*As)[8], const uint4 (*Bs)[8], int wm, int wn, int lane,
+                                           f32x16_t (&acc)[2][1]) {
+  const int lr = lane & 31, lh = lane >> 5;
+  bf16x8_t a[2][2], b[2];
+  auto read = [&](int s, int buf) {
+    const int v = 2 * s + lh;  // 16-byte chunk: k = 16 s + 8 lh + (0..7)
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int r = wm * 64 + i * 32 + lr;
-      a[s][i] = __builtin_bit_cast(bf16x8_t, As[r][v ^ swz(r)]);
+      a[buf][i] = __builtin_bit_cast(bf16x8_t, As[r][v ^ swz(r)]);
     }
     const int r = wn * 32 + lr;
-    b[s] = __builtin_bit_cast(bf16x8_t, Bs[r][v ^ swz(r)]);
-  }
-  __device__ __forceinline__ void mfma(int s, f32x16_t (&acc)[2][1]) {
+    b[buf] = __builtin_bit_cast(bf16x8_t, Bs[r][v ^ swz(r)]);
+  };
+  read(0, 0);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if (s < 3) read(s + 1, (s + 1) & 1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s][i], b[s], acc[i][0], 0, 0, 0);
+      acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s & 1][i], b[s & 1], acc[i][0], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
-};
+}
 
 // Row norms for the workgroups past the tiles: rows of one block spread over
 // its waves, two rows per wave at a time.  Each row is summed as prep sums
@@ -771,7 +777,7 @@ __device__ __forceinline__ void norm_rows(const GemmBatch& args, int blk) {
 constexpr int kDmaThreads = 512;
 
 __global__ __launch_bounds__(kDmaThreads) void gemm_dma_kernel(const GemmBatch args) {
-  __shared__ uint4 stg[5][2][BM][8];  // 5 stages of 32 KiB: A rows, then B rows
+  __shared__ uint4 st0[2][BM][8], st1[2][BM][8], st2[2][BM][8], st3[2][BM][8], st4[2][BM][8];  // 5 x 32 KiB
   if (static_cast<int>(blockIdx.x) >= args.total_tiles) {
     norm_rows(args, blockIdx.x - args.total_tiles);
     return;
@@ -830,51 +836,33 @@ __global__ __launch_bounds__(kDmaThreads) void gemm_dma_kernel(const GemmBatch a
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[i][0][r] = 0.0f;
 
-  // Slice kt sits in stage kt % 5.  Step kt refills the stage every wave finished reading in step
-  // kt - 1 with slice kt + 4, runs the products of slice kt's first two
-  // k-steps (the operands of its last two read meanwhile), then waits for
-  // slice kt + 1 (this wave's loads, then every wave's at the barrier) and
-  // reads its first two k-steps' operands while slice kt's last two
-  // products run.
-  Mma8 mm;
-  mm.wm = wm;
-  mm.wn = wn;
-  mm.lane = lane;
-  auto step = [&](uint4 (*cur)[BM][8], uint4 (*nxt)[BM][8], uint4 (*fill)[BM][8], int kt) {
-    if (kt + 4 < nk) issue(fill, kt + 4);
-    mm.read(cur[0], cur[1], 2);
-    __builtin_amdgcn_sched_barrier(0);
-    mm.mfma(0, acc);
-    __builtin_amdgcn_sched_barrier(0);
-    mm.read(cur[0], cur[1], 3);
-    __builtin_amdgcn_sched_barrier(0);
-    mm.mfma(1, acc);
-    __builtin_amdgcn_sched_barrier(0);
-    if (kt + 1 < nk) {
-      wait_vm_lgkm0(4 * min(3, nk - 2 - kt));
-      __builtin_amdgcn_s_barrier();
-      mm.read(nxt[0], nxt[1], 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    mm.mfma(2, acc);
-    __builtin_amdgcn_sched_barrier(0);
-    if (kt + 1 < nk) mm.read(nxt[0], nxt[1], 1);
-    __builtin_amdgcn_sched_barrier(0);
-    mm.mfma(3, acc);
-    __builtin_amdgcn_sched_barrier(0);
+  // Step kt waits for slice kt (this wave's loads, then every wave's at the
+  // barrier), refills the stage every wave finished reading in the previous
+  // step with slice kt + 4, and runs the matrix cores on slice kt.  Slice kt
+  // sits in stage kt % 5, a compile-time constant in the unrolled body; the
+  // early exits are uniform scalar branches.
+  auto mma = [&](uint4 (*cur)[BM][8]) { mma_slice8(cur[0], cur[1], wm, wn, lane, acc); };
+  auto step = [&](uint4 (*cur)[BM][8], uint4 (*nxt)[BM][8], int kt) {
+    wait_vm_lgkm0(4 * min(3, nk - 1 - kt));
+    __builtin_amdgcn_s_barrier();
+    if (kt + 4 < nk) issue(nxt, kt + 4);
+    mma(cur);
   };
-  issue(stg[0], 0);
-  if (nk > 1) issue(stg[1], 1);
-  if (nk > 2) issue(stg[2], 2);
-  if (nk > 3) issue(stg[3], 3);
-  wait_vm_lgkm0(4 * min(3, nk - 1));
-  __builtin_amdgcn_s_barrier();
-  mm.read(stg[0][0], stg[0][1], 0);
-  mm.read(stg[0][0], stg[0][1], 1);
-  for (int kt = 0, cur = 0; kt < nk; ++kt) {
-    const int nxt = cur == 4 ? 0 : cur + 1, fill = cur == 0 ? 4 : cur - 1;
-    step(stg[cur], stg[nxt], stg[fill], kt);
-    cur = nxt;
+  issue(st0, 0);
+  issue(st1, 1);
+  issue(st2, 2);
+  issue(st3, 3);
+  step(st0, st4, 0);
+  for (int kt = 1; kt < nk; kt += 5) {
+    step(st1, st0, kt);
+    if (kt + 1 >= nk) break;
+    step(st2, st1, kt + 1);
+    if (kt + 2 >= nk) break;
+    step(st3, st2, kt + 2);
+    if (kt + 3 >= nk) break;
+    step(st4, st3, kt + 3);
+    if (kt + 4 >= nk) break;
+    step(st0, st4, kt + 4);
   }
   if (P.epi == EPI_PARTIAL) {
     // the raw sums of this K range in the four-wave layout the reductions
@@ -892,13 +880,13 @@ __global__ __launch_bounds__(kDmaThreads) void gemm_dma_kernel(const GemmBatch a
     return;
   }
   __syncthreads();  // the epilogues reuse the stage arrays
-  float* rs_tile = reinterpret_cast<float*>(&stg[4][0][0][0]);
+  float* rs_tile = reinterpret_cast<float*>(&st4[0][0][0]);
   if (P.epi == EPI_COSINE) {
     if (tid < BM + BN) rs_tile[tid] = rs_mine;
     __syncthreads();
   }
-  const StagedTile L{reinterpret_cast<float*>(&stg[0][0][0][0]), reinterpret_cast<float*>(&stg[1][0][0][0]),
-                     reinterpret_cast<float*>(&stg[2][0][0][0]), reinterpret_cast<float*>(&stg[3][0][0][0])};
+  const StagedTile L{reinterpret_cast<float*>(&st0[0][0][0]), reinterpret_cast<float*>(&st1[0][0][0]),
+                     reinterpret_cast<float*>(&st2[0][0][0]), reinterpret_cast<float*>(&st3[0][0][0])};
   if (P.epi == EPI_COSINE)
     epi_cosine_staged<1>(P, bt, tm, tn, acc, L, rs_tile, rs_tile + BM, tid, lane, wm, wn);
   else if (P.epi == EPI_BIAS_GELU || P.epi == EPI_BIAS)
