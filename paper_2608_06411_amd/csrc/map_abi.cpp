@@ -986,7 +986,10 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   full.run_if = u.uncert;
   full.Ng = N;
   full.fallback = 1;
-  full.no_r0_kernel = 1;  // (R0 in its own rounds: slower, and only for a flagged image)
+  // R0 of a flagged image: at one image in the selection's own rounds (slower,
+  // but a certified image then pays no launch for it); for a batch by
+  // r0_kernel, gated like the rest
+  full.no_r0_kernel = B == 1;
   bool gathered = false;
   SelectWs sw2 = sw;
   sw2.bar = sw.bar + B;

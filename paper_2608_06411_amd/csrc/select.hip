@@ -1716,7 +1716,8 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
                                                hipFuncAttributeMaxDynamicSharedMemorySize, rb);
       if (e != hipSuccess) return e;
     }
-    const hipError_t e = launch_kernel("select_r0", r0_kernel, dim3((a.N + 63) / 64, a.B), dim3(NT),
+    const hipError_t e = launch_kernel(a.fallback ? "select_r0_full" : "select_r0", r0_kernel,
+                                       dim3((a.N + 63) / 64, a.B), dim3(NT),
                                        static_cast<size_t>(rb), s, a);
     if (e != hipSuccess) return e;
   }
