@@ -1210,6 +1210,7 @@ __global__ __launch_bounds__(kPW * 64) void proj_rope_kernel(const GemmBatch arg
 __global__ __launch_bounds__(NT) void gram_reduce_kernel(const GemmProblem P, float* out, int ldc,
                                                          const float* rs_all) {
   const int bt = blockIdx.y, t = blockIdx.x >> 4, q = blockIdx.x & 15;
+  if (P.run_if && P.run_if[bt] == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int ks = P.ksplit > 1 ? P.ksplit : 1;
@@ -1317,9 +1318,10 @@ hipError_t launch_splitk_resid(const GemmProblem& P, const void* res, void* out,
                        static_cast<const bf16_t*>(res), static_cast<bf16_t*>(out), ldc);
 }
 
-hipError_t launch_gram_reduce(const GemmProblem& partial, float* out, int ldc, const float* rs, hipStream_t s) {
+hipError_t launch_gram_reduce(const GemmProblem& partial, float* out, int ldc, const float* rs, hipStream_t s,
+                              const char* name) {
   if (partial.tiles_tri == 0 || partial.batch == 0) return hipSuccess;
-  return launch_kernel("gram_reduce", gram_reduce_kernel, dim3(partial.tiles_tri * 16, partial.batch), dim3(NT), 0,
+  return launch_kernel(name, gram_reduce_kernel, dim3(partial.tiles_tri * 16, partial.batch), dim3(NT), 0,
                        s, partial, out, ldc, rs);
 }
 

@@ -141,7 +141,8 @@ hipError_t launch_proj_rope(map_dtype dt, const GemmBatch& g, const char* name, 
 // The split-K sums of an EPI_PARTIAL problem (finalized, ksplit > 1) in a
 // fixed order, then the cosine epilogue into out (symmetric, ldc, rs as in
 // EPI_COSINE).
-hipError_t launch_gram_reduce(const GemmProblem& partial, float* out, int ldc, const float* rs, hipStream_t s);
+hipError_t launch_gram_reduce(const GemmProblem& partial, float* out, int ldc, const float* rs, hipStream_t s,
+                              const char* name = "gram_reduce");
 
 // ---------------------------------------------------------------- subset
 // The candidate subset J of map_prune (R0 plus the largest score bounds),
@@ -158,6 +159,10 @@ struct SubsetArgs {
   int32_t* uncert;      // [B] cleared here; set by the selection when a pick is not certified
   unsigned int* clear_bar;  // [B] barrier counters of the full selection behind the subset, cleared here
   int32_t* clear_r0flag;    // [B] its R0 flags, cleared here (it places R0 in its own rounds)
+  // optional (a second, larger subset): image b is taken only when
+  // run_if[b] != 0; the others get uncert = 0 and nothing else
+  const int32_t* run_if;
+  int tier2;                // timing names of the second subset's launches
   int B, N, Nc, K0;
   float tau2;
 };
@@ -266,6 +271,7 @@ struct SelectArgs {
   const int32_t* run_if;  // [B] images whose flag is 0 are skipped (null: none)
   int Ng;
   int fallback;           // the launches are the full selection behind a subset (timing names)
+  int tier2;              // the launches select on the second, larger subset (timing names)
   int no_r0_kernel;       // R0 is placed by the selection's own rounds (r0flag must read 0)
   int B, N, K, K0, G, ch, pcap;
   float tau2;

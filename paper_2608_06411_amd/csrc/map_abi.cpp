@@ -159,6 +159,18 @@ int subset_size(map_dtype dt, int N, int D, const map_select_params& sp) {
   return nc < N ? nc : 0;
 }
 
+// The second, larger subset behind the first for a batch (0: none): twice
+// the first, if that stays below 3N/4.  Images the first cannot certify
+// (correlated frames need more of their tokens: 1567-1820 of 4608 on the
+// eight-frame batch against a first subset of 1280) are selected on it
+// before the full path; at one image its launches would only add dispatch
+// time to the headline call.
+int subset_tier2_size(int B, int N, int nc) {
+  if (B < 2 || nc <= 0) return 0;
+  const int nc2 = (2 * nc + 63) & ~63;
+  return 4 * nc2 <= 3 * N ? nc2 : 0;
+}
+
 int subset_ksplit(int D) { return D % 512 == 0 ? D / 512 : D / 256; }
 
 int subset_tiles(int nc) {
@@ -205,11 +217,11 @@ SelectWs carve_select(Carver& c, int B, int N, int K) {
   s.C = c.take<float>((size_t)B * N * ((K + 3) & ~3));  // token-major, rows of K rounded up to 4
   s.r2 = c.take<float>((size_t)B * N);
   s.pub = c.take<uint64_t>((size_t)B * 2 * 128 * (kPub + 1));
-  s.bar = c.take<unsigned int>(2 * (size_t)B);  // the second B: the full selection behind a subset
+  s.bar = c.take<unsigned int>(3 * (size_t)B);  // then the full selection behind a subset, then its second subset
   s.err = nullptr;  // the status word at the workspace's start (see carve_status)
   s.order = c.take<int32_t>((size_t)B * K);
   s.gain = c.take<float>((size_t)B * K);
-  s.r0flag = c.take<int32_t>(2 * (size_t)B);  // the second B: the full selection behind a subset
+  s.r0flag = c.take<int32_t>(3 * (size_t)B);  // as the barriers
   return s;
 }
 
@@ -394,6 +406,7 @@ struct SubsetSel {
   int Ng;
   int fallback;
   int no_r0_kernel;
+  int tier2;
 };
 
 hipError_t enqueue_select(int B, int N, const float* p, const float* S, const float* norms,
@@ -412,6 +425,7 @@ hipError_t enqueue_select(int B, int N, const float* p, const float* S, const fl
     a.run_if = sub->run_if;
     a.Ng = sub->Ng;
     a.fallback = sub->fallback;
+    a.tier2 = sub->tier2;
     a.no_r0_kernel = sub->no_r0_kernel;
   }
   a.p = p;
@@ -907,15 +921,17 @@ GatherArgs gather_args(const void* V, const int32_t* pos_v, const int32_t* order
 
 // map_prune on a candidate subset (see subset.hip), with the full
 // selection behind it for the images whose picks it cannot certify.
-map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, const void* V, const int32_t* pos_v,
-                           const void* T, const int32_t* pos_t, const int32_t* t_off_host,
-                           const map_select_params& sp, int32_t* idx_out, void* V_out, int32_t* pos_out, float* p,
-                           int32_t* order_out, float* gain_out, const ScoreWs& s, const SelectWs& sw, float* S,
-                           float* norms, float* ninv, const SubsetWs& u, int nc, hipStream_t st,
-                           const Layer0* l0) {
-  hipError_t e =
-      enqueue_score(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, nullptr, norms, ninv, st, sw.bar, sw.err, true);
-  if (e != hipSuccess) return MAP_ERR_HIP;
+// One subset tier: J, its cosine matrix and the selection on it with the
+// certificate check.  run_if (null: every image) limits it to the images an
+// earlier tier flagged.  Its subset kernel zeroes clear_bar and
+// clear_r0flag for the images it takes: the full selection's counters and
+// R0 flags for the first tier (the scoring kernel zeroes the first tier's
+// own), the second tier's own for the second.
+hipError_t subset_tier(const map_weights& w, map_dtype dt, int B, int N, const void* V,
+                       const map_select_params& sp, int32_t* idx_out, float* p, float* norms, float* ninv,
+                       float* gain_out, const SelectWs& sw, const SubsetWs& u, int nc, int32_t* order_img,
+                       const int32_t* run_if, unsigned int* clear_bar, int32_t* clear_r0flag, bool tier2,
+                       hipStream_t st) {
   SubsetArgs sa;
   memset(&sa, 0, sizeof(sa));
   sa.p = p;
@@ -932,9 +948,12 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   sa.Nc = nc;
   sa.K0 = sp.K0;
   sa.tau2 = sp.tau * sp.tau;
-  sa.clear_bar = sw.bar + B;
-  sa.clear_r0flag = sw.r0flag + B;
-  if ((e = launch_subset(sa, st)) != hipSuccess) return MAP_ERR_HIP;
+  sa.clear_bar = clear_bar;
+  sa.clear_r0flag = clear_r0flag;
+  sa.run_if = run_if;
+  sa.tier2 = tier2;
+  hipError_t e = launch_subset(sa, st);
+  if (e != hipSuccess) return e;
 
   // cosine entries among the subset: with tiles for a wave of workgroups,
   // straight from the tiles' cosine epilogue; otherwise raw sums per K
@@ -948,53 +967,84 @@ map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, con
   g.p[0].mapA = u.jmap;
   g.p[0].mapB = u.jmap;
   g.p[0].mapStride = nc;
+  g.p[0].run_if = run_if;
   if (!direct) {
     g.p[0].epi = EPI_PARTIAL;
     g.p[0].ksplit = subset_ksplit(w.D);
   }
   g.count = 1;
   gemm_finalize(g);
-  if ((e = launch_gemm(dt, g, "gemm_subset", st)) != hipSuccess) return MAP_ERR_HIP;
-  if (!direct && (e = launch_gram_reduce(g.p[0], u.SJ, nc, u.ninvJ, st)) != hipSuccess) return MAP_ERR_HIP;
+  if ((e = launch_gemm(dt, g, tier2 ? "gemm_subset_t2" : "gemm_subset", st)) != hipSuccess) return e;
+  if (!direct &&
+      (e = launch_gram_reduce(g.p[0], u.SJ, nc, u.ninvJ, st, tier2 ? "gram_reduce_t2" : "gram_reduce")) != hipSuccess)
+    return e;
 
-  int32_t* order_img = order_out ? order_out : u.order_img;
-  const GatherArgs ga = gather_args(V, pos_v, order_img, sw.err, idx_out, V_out, pos_out, B, N, sp.K,
-                                    static_cast<int>(w.D * elem_size(dt)), l0);
   SubsetSel sub;
   memset(&sub, 0, sizeof(sub));
   sub.jmap = u.jmap;
   sub.order_map = order_img;
   sub.hout = u.hout;
   sub.uncert = u.uncert;
+  sub.run_if = run_if;
   sub.Ng = N;
-  e = enqueue_select(B, nc, u.pJ, u.SJ, u.nJ, sp, idx_out, sw.order, gain_out, sw, st, true, nullptr, nullptr, &sub);
+  sub.tier2 = tier2;
+  return enqueue_select(B, nc, u.pJ, u.SJ, u.nJ, sp, idx_out, sw.order, gain_out, sw, st, true, nullptr, nullptr, &sub);
+}
+
+// map_prune on a candidate subset (see subset.hip), for a batch with a
+// second, larger subset behind it, and the full selection behind those for
+// the images whose picks they cannot certify.  The selection's barrier
+// counters and R0 flags come in three sets of B: the first subset's, the full
+// selection's, the second subset's.
+map_status prune_on_subset(const map_weights& w, map_dtype dt, int B, int N, const void* V, const int32_t* pos_v,
+                           const void* T, const int32_t* pos_t, const int32_t* t_off_host,
+                           const map_select_params& sp, int32_t* idx_out, void* V_out, int32_t* pos_out, float* p,
+                           int32_t* order_out, float* gain_out, const ScoreWs& s, const SelectWs& sw, float* S,
+                           float* norms, float* ninv, const SubsetWs& u, int nc, const SubsetWs& u2, int nc2,
+                           hipStream_t st, const Layer0* l0) {
+  hipError_t e =
+      enqueue_score(w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, nullptr, norms, ninv, st, sw.bar, sw.err, true);
   if (e != hipSuccess) return MAP_ERR_HIP;
+  int32_t* order_img = order_out ? order_out : u.order_img;
+  SelectWs sw_full = sw, sw_t2 = sw;
+  sw_full.bar = sw.bar + B;
+  sw_full.r0flag = sw.r0flag + B;
+  sw_t2.bar = sw.bar + 2 * B;
+  sw_t2.r0flag = sw.r0flag + 2 * B;
+  e = subset_tier(w, dt, B, N, V, sp, idx_out, p, norms, ninv, gain_out, sw, u, nc, order_img, nullptr, sw_full.bar,
+                  sw_full.r0flag, false, st);
+  if (e != hipSuccess) return MAP_ERR_HIP;
+  const int32_t* flagged = u.uncert;
+  if (nc2 > 0) {
+    e = subset_tier(w, dt, B, N, V, sp, idx_out, p, norms, ninv, gain_out, sw_t2, u2, nc2, order_img, u.uncert,
+                    sw_t2.bar, sw_t2.r0flag, true, st);
+    if (e != hipSuccess) return MAP_ERR_HIP;
+    flagged = u2.uncert;
+  }
 
   // the images whose picks were not certified: the full Gram matrix and
-  // selection (its barrier counters are the second set, which the subset
-  // kernel cleared); the workgroups of a certified image only gather its
-  // kept rows, from the order the subset's selection wrote as image tokens
+  // selection; the workgroups of a certified image only gather its kept
+  // rows, from the order the subset's selection wrote as image tokens
+  const GatherArgs ga = gather_args(V, pos_v, order_img, sw.err, idx_out, V_out, pos_out, B, N, sp.K,
+                                    static_cast<int>(w.D * elem_size(dt)), l0);
   GemmBatch gf;
   memset(&gf, 0, sizeof(gf));
   gf.p[0] = gram(V, B, N, w.D, S, ninv);
-  gf.p[0].run_if = u.uncert;
+  gf.p[0].run_if = flagged;
   gf.count = 1;
   gemm_finalize(gf);
   if ((e = launch_gemm(dt, gf, "gemm_gram_full", st)) != hipSuccess) return MAP_ERR_HIP;
   SubsetSel full;
   memset(&full, 0, sizeof(full));
-  full.run_if = u.uncert;
+  full.run_if = flagged;
   full.Ng = N;
   full.fallback = 1;
-  // R0 of a flagged image: at one image in the selection's own rounds (slower,
-  // but a certified image then pays no launch for it); for a batch by
-  // r0_kernel, gated like the rest
-  full.no_r0_kernel = B == 1;
+  // R0 of a flagged image in the selection's own rounds (slower than
+  // r0_kernel, but a certified image then pays no launch for it); r0_kernel
+  // (gated like the rest) only for a batch without a second subset
+  full.no_r0_kernel = B == 1 || nc2 > 0;
   bool gathered = false;
-  SelectWs sw2 = sw;
-  sw2.bar = sw.bar + B;
-  sw2.r0flag = sw.r0flag + B;
-  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_img, gain_out, sw2, st, true, &ga, &gathered, &full);
+  e = enqueue_select(B, N, p, S, norms, sp, idx_out, order_img, gain_out, sw_full, st, true, &ga, &gathered, &full);
   if (e != hipSuccess) return MAP_ERR_HIP;
   return gathered ? MAP_OK : hip_status(launch_gather(ga, st));
 }
@@ -1082,6 +1132,8 @@ size_t map_prune_workspace(map_dtype dt, int B, int N, int sum_M, const map_weig
     if (nc > 0) {
       Carver c(nullptr);
       carve_subset(c, B, K, nc, w->D);
+      const int nc2 = subset_tier2_size(B, N, nc);
+      if (nc2 > 0) carve_subset(c, B, K, nc2, w->D);
       sub = std::max(sub, c.off);
     }
   }
@@ -1193,9 +1245,13 @@ static map_status prune_impl(const map_weights* w, map_dtype dt, int B, int N, c
   const int nc = subset_size(dt, N, w->D, sp);
   Layer0 l0{T, pos_t, t_off_host};
   const Layer0* l0p = layer0 ? &l0 : nullptr;
-  if (nc > 0) return prune_on_subset(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, sp, idx_out, V_out, pos_out,
-                                     p, order_out, gain_out, s, sw, S, norms, ninv, carve_subset(c, B, sp.K, nc, w->D),
-                                     nc, st, l0p);
+  if (nc > 0) {
+    const SubsetWs u = carve_subset(c, B, sp.K, nc, w->D);
+    const int nc2 = subset_tier2_size(B, N, nc);
+    const SubsetWs u2 = nc2 > 0 ? carve_subset(c, B, sp.K, nc2, w->D) : SubsetWs{};
+    return prune_on_subset(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, sp, idx_out, V_out, pos_out, p, order_out,
+                           gain_out, s, sw, S, norms, ninv, u, nc, u2, nc2, st, l0p);
+  }
   const GemmProblem g = gram(V, B, N, w->D, S, ninv);
   hipError_t e =
       enqueue_score(*w, dt, B, N, V, pos_v, T, pos_t, t_off_host, p, s, &g, norms, ninv, st, sw.bar, sw.err);

@@ -1716,7 +1716,7 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
                                                hipFuncAttributeMaxDynamicSharedMemorySize, rb);
       if (e != hipSuccess) return e;
     }
-    const hipError_t e = launch_kernel(a.fallback ? "select_r0_full" : "select_r0", r0_kernel,
+    const hipError_t e = launch_kernel(a.fallback ? "select_r0_full" : a.tier2 ? "select_r0_t2" : "select_r0", r0_kernel,
                                        dim3((a.N + 63) / 64, a.B), dim3(NT),
                                        static_cast<size_t>(rb), s, a);
     if (e != hipSuccess) return e;
@@ -1724,9 +1724,11 @@ hipError_t launch_select(SelectArgs& a, hipStream_t s) {
   for (int b0 = 0; b0 < a.B; b0 += per_launch) {
     const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
     const hipError_t e =
-        chosen_pipe ? launch_kernel(a.fallback ? "select_full" : "select", select_kernel<true>, dim3(nb * chosen_G),
+        chosen_pipe ? launch_kernel(a.fallback ? "select_full" : a.tier2 ? "select_t2" : "select", select_kernel<true>,
+                                    dim3(nb * chosen_G),
                                     dim3(NT), static_cast<size_t>(chosen_bytes), s, a, b0)
-                    : launch_kernel(a.fallback ? "select_full" : "select", select_kernel<false>, dim3(nb * chosen_G),
+                    : launch_kernel(a.fallback ? "select_full" : a.tier2 ? "select_t2" : "select", select_kernel<false>,
+                                    dim3(nb * chosen_G),
                                     dim3(NT), static_cast<size_t>(chosen_bytes), s, a, b0);
     if (e != hipSuccess) return e;
   }

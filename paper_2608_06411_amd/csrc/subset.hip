@@ -183,6 +183,10 @@ __global__ __launch_bounds__(NT) void subset_kernel(const SubsetArgs a) {
   __shared__ int hist[kBins];
   __shared__ BlockScratch s;
   const int b = blockIdx.x, N = a.N, Nc = a.Nc, K0 = a.K0, tid = threadIdx.x;
+  if (a.run_if && a.run_if[b] == 0) {  // (certified by the first subset)
+    if (tid == 0) a.uncert[b] = 0;
+    return;
+  }
   float* nv = pv + N;
   float* iv = nv + N;
   unsigned char* member = reinterpret_cast<unsigned char*>(iv + N);
@@ -309,7 +313,7 @@ hipError_t launch_subset_kpt(const SubsetArgs& a, hipStream_t s) {
                                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(bytes));
     if (e != hipSuccess) return e;
   }
-  return launch_kernel("subset", subset_kernel<KPT>, dim3(a.B), dim3(NT), bytes, s, a);
+  return launch_kernel(a.tier2 ? "subset_t2" : "subset", subset_kernel<KPT>, dim3(a.B), dim3(NT), bytes, s, a);
 }
 
 hipError_t launch_subset(const SubsetArgs& a, hipStream_t s) {
