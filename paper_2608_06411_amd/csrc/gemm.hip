@@ -1097,7 +1097,8 @@ __global__ __launch_bounds__(kBigThreads) void gemm_big_kernel(const GemmBatch a
 }
 
 // Projection to d_p <= 128 columns with the RoPE epilogue (the keys and
-// queries of Eq. (3)): C = RoPE(A B^T + bias), A [M][K] and B [N][K] bf16.
+// queries of Eq. (3)): C = RoPE(A B^T + bias), A [M][K] and B [N][K] bf16
+// (float32 inputs: the same with 32 x 32 x 2 float32 products).
 // With N this small and rows for fewer than one wave of tiles, a 128 x 128
 // tile leaves most compute units idle, each streaming the whole K with a
 // few slices in flight.  Here a workgroup takes
@@ -1117,6 +1118,9 @@ constexpr int kPW = 8;    // waves per workgroup
 constexpr int kPG = 2;    // groups of RoPE pairs per row block
 constexpr int kPS = 68;   // LDS row stride of the partial tiles (floats)
 
+typedef __attribute__((ext_vector_type(4))) float float4v;
+
+template <typename T>
 __global__ __launch_bounds__(kPW * 64) void proj_rope_kernel(const GemmBatch args) {
   __shared__ float part[kPW][kPR][kPS];
   const int t0 = args.p[0].tiles_m, pi = blockIdx.x < t0 ? 0 : 1;
@@ -1127,19 +1131,48 @@ __global__ __launch_bounds__(kPW * 64) void proj_rope_kernel(const GemmBatch arg
   const int PG = (half + kPG - 1) / kPG, c0 = g * PG, npg = min(PG, half - c0);
   if (npg <= 0) return;  // a group without pairs (half = 1)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const bf16_t* __restrict__ A = static_cast<const bf16_t*>(P.A);
-  const bf16_t* __restrict__ B = static_cast<const bf16_t*>(P.B);
+  const T* __restrict__ A = static_cast<const T*>(P.A);
+  const T* __restrict__ B = static_cast<const T*>(P.B);
 
   const int r = lane & 31, h = lane >> 5;
-  const bf16_t* arow = A + (long long)min(m0 + r, M - 1) * P.lda;
+  const T* arow = A + (long long)min(m0 + r, M - 1) * P.lda;
   const int pr = c0 + min(r, npg - 1);  // the pair of tile column r (32 + r: its partner)
-  const bf16_t* brow[2] = {B + (long long)pr * P.ldb, B + (long long)(pr + half) * P.ldb};
+  const T* brow[2] = {B + (long long)pr * P.ldb, B + (long long)(pr + half) * P.ldb};
   f32x16_t acc[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j)
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[j][e] = 0.0f;
   const int nchunk = (K + 63) >> 6;
+  if constexpr (sizeof(T) == 4) {
+    // float32: per 64-wide chunk lane l holds 32 contiguous k of its row
+    // (half h = l >> 5 of the chunk), for A and B alike; the 32 x 32 x 2
+    // products pair k = s of the first half with k = 32 + s of the second
+    // (any common order of k gives the same sum)
+    for (int kc = wave; kc < nchunk; kc += kPW) {
+      const int kb = 64 * kc + 32 * h;
+      float4v av[8], bv[2][8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int k = kb + 4 * q;
+        const int off = k < K ? k : 0;  // past K: a valid address, zeroed below
+        av[q] = *reinterpret_cast<const float4v*>(arow + off);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) bv[j][q] = *reinterpret_cast<const float4v*>(brow[j] + off);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of the products
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float4v z = {0.0f, 0.0f, 0.0f, 0.0f};
+        const float4v a = kb + 4 * q < K ? av[q] : z;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], bv[j][q][e], acc[j], 0, 0, 0);
+      }
+    }
+  } else
   for (int kc = wave; kc < nchunk; kc += 2 * kPW) {  // two chunks per pass, every load issued first
     uint4 av[2][4], bv[2][2][4];
 #pragma unroll
@@ -1451,11 +1484,12 @@ hipError_t launch_gemm(map_dtype dt, const GemmBatch& g, const char* name, hipSt
 }
 
 hipError_t launch_proj_rope(map_dtype dt, const GemmBatch& g, const char* name, hipStream_t s) {
-  bool fits = dt == MAP_BF16 && g.count >= 1 && g.count <= 2;
+  bool fits = (dt == MAP_BF16 || dt == MAP_F32) && g.count >= 1 && g.count <= 2;
+  const int vec = dt == MAP_F32 ? 4 : 8;  // elements per 16-byte load
   for (int i = 0; fits && i < g.count; ++i) {
     const GemmProblem& p = g.p[i];
-    fits = p.epi == EPI_ROPE && p.batch == 1 && p.N <= 128 && p.N % 2 == 0 && p.K % 8 == 0 && p.lda % 8 == 0 &&
-           p.ldb % 8 == 0 && (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 &&
+    fits = p.epi == EPI_ROPE && p.batch == 1 && p.N <= 128 && p.N % 2 == 0 && p.K % vec == 0 &&
+           p.lda % vec == 0 && p.ldb % vec == 0 && (reinterpret_cast<uintptr_t>(p.A) & 15) == 0 &&
            (reinterpret_cast<uintptr_t>(p.B) & 15) == 0;
   }
   // With enough rows for a wave of 128 x 128 tiles, the tiled kernel reads
@@ -1472,7 +1506,8 @@ hipError_t launch_proj_rope(map_dtype dt, const GemmBatch& g, const char* name, 
   if (q.count == 1) q.p[1].tiles_m = 0;
   q.total_tiles = total;
   if (total == 0) return hipSuccess;
-  return launch_kernel(name, proj_rope_kernel, dim3(total), dim3(kPW * 64), 0, s, q);
+  if (dt == MAP_F32) return launch_kernel(name, proj_rope_kernel<float>, dim3(total), dim3(kPW * 64), 0, s, q);
+  return launch_kernel(name, proj_rope_kernel<bf16_t>, dim3(total), dim3(kPW * 64), 0, s, q);
 }
 
 }  // namespace mapk
