@@ -346,11 +346,13 @@ map_status map_decoder_layer(const map_decoder_weights* w, map_dtype dt, int B, 
 /* map_prune's candidate subset.  A greedy pick of Eq. (4) scores
  * p_i n_i r_i <= p_i n_i, so map_prune may run the selection on a subset J
  * of each image's tokens: R0 plus the tokens with the largest bounds
- * p_i n_i, about K0 + max(2 (K - K0), N / 4) of them (bf16, N <= 8192).  It
- * forms the cosine similarity only among J, and keeps J's selection when
- * every greedy pick scores above the largest bound left out.  Otherwise that
- * image is selected again over all its tokens.  Either way the result is
- * the selection over all tokens; only the time differs.
+ * p_i n_i, about K0 + max(2 (K - K0), N / 4) of them (bf16, N <= 8192, K
+ * at most N / 12).  It forms the cosine similarity only among J, and keeps
+ * J's selection when every greedy pick scores above the largest bound left
+ * out.  Otherwise, for a batch (B >= 2), that image is selected again on a
+ * subset twice the size (when that stays below 3N / 4), and an image neither
+ * subset certifies is selected over all its tokens.  Either way the result
+ * is the selection over all tokens; only the time differs.
  *   n < 0: never use a subset; n = 0: automatic (the default); n > 0: a
  *   subset of max(n, K) tokens whenever that is fewer than N.
  * The setting is process-wide and read by map_prune_workspace and map_prune
