@@ -1116,12 +1116,13 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       npub[0] = 0;
       npub[4] = 0;
     }
-    if (PIPE && t > 0 && pn > 0) {
+    if (t > 0 && pn > 0) {
       // The pool's residual Gram matrix, one float32 matrix-core product over
       // the t rows so far (columns t .. tk - 1 are zero):
       //   Rm[m][j] -= sum_l c_{l,m} c_{l,j}
-      // Wave w computes the 32 x 32 tile (w >> 1, w & 1); the own tokens'
-      // part (D) is computed by waves 1 to 3 while wave 0 picks.
+      // Wave w computes the 32 x 32 tile (w >> 1, w & 1); in the pipelined
+      // variant the own tokens' part (D) is computed by waves 1 to 3 while
+      // wave 0 picks.
       const int tr = wave >> 1, tc = wave & 1, r = lane & 31, h = lane >> 5;
       float cur[16];  // current entries of this lane's results, read ahead
 #pragma unroll
@@ -1134,60 +1135,6 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       for (int e = 0; e < 16; ++e) {
         const int m = 32 * tr + 8 * (e >> 2) + 4 * h + (e & 3), j = 32 * tc + r;
         if (m < pn && j < pn) Rm[m * rs + j] = cur[e] - acc[e];
-      }
-    }
-    // Rm -= P P^T over the t rows so far.  With R = ceil(pn / 4), tile
-    // (bi, bj), bi <= bj, covers rows bi + R x and columns bj + R y; lanes
-    // with consecutive tiles read consecutive rows (distinct bank groups) or
-    // share a row (broadcast).  Off-diagonal tiles also write the mirror.
-    if (!PIPE && t > 0) {
-      const int R = (pn + 3) >> 2;
-      const int ntile = R * (R + 1) / 2;
-      const int t4 = t & ~3;
-      for (int e = tid; e < ntile; e += NT) {
-        int bi = 0, rem = e;
-        while (rem >= R - bi) { rem -= R - bi; ++bi; }
-        const int bj = bi + rem;
-        float acc[4][4] = {};
-        const float* pa[4];
-        const float* pb[4];
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          pa[x] = pcol + min(bi + R * x, pn - 1) * cs;
-          pb[x] = pcol + min(bj + R * x, pn - 1) * cs;
-        }
-        for (int l = 0; l < t4; l += 4) {
-          float4 xa[4], xb[4];
-#pragma unroll
-          for (int x = 0; x < 4; ++x) {
-            xa[x] = *reinterpret_cast<const float4*>(pa[x] + l);
-            xb[x] = *reinterpret_cast<const float4*>(pb[x] + l);
-          }
-#pragma unroll
-          for (int x = 0; x < 4; ++x)
-#pragma unroll
-            for (int y = 0; y < 4; ++y) {
-              acc[x][y] = fmaf(xa[x].x, xb[y].x, acc[x][y]);
-              acc[x][y] = fmaf(xa[x].y, xb[y].y, acc[x][y]);
-              acc[x][y] = fmaf(xa[x].z, xb[y].z, acc[x][y]);
-              acc[x][y] = fmaf(xa[x].w, xb[y].w, acc[x][y]);
-            }
-        }
-        for (int l = t4; l < t; ++l)
-#pragma unroll
-          for (int x = 0; x < 4; ++x)
-#pragma unroll
-            for (int y = 0; y < 4; ++y) acc[x][y] = fmaf(pa[x][l], pb[y][l], acc[x][y]);
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-          for (int y = 0; y < 4; ++y) {
-            const int m1 = bi + R * x, m2 = bj + R * y;
-            if (m1 < pn && m2 < pn) {
-              Rm[m1 * rs + m2] -= acc[x][y];
-              if (bi != bj) Rm[m2 * rs + m1] -= acc[x][y];
-            }
-          }
       }
     }
     __syncthreads();
@@ -1456,59 +1403,75 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
     }
     __syncthreads();
-    if (t0 > 0) {
-      // dense part: 4 picks x 4 own tokens per thread; own columns stream
-      // from global memory (next chunk prefetched), pick columns from LDS
-      const int nbj = (np + 3) >> 2, nbc = (cnt + 3) >> 2;
-      const int t4 = t0 & ~3;
-      for (int blk = tid; blk < nbj * nbc; blk += NT) {
-        const int bj = blk / nbc, bc = blk - bj * nbc;
-        float acc[4][4] = {};
-        const float* pj[4];
-        const float* oc[4];
+    if (t0 > 0 && np > 0) {
+      // dense part on matrix cores: 32 x 32 tiles (picks by own tokens), wave
+      // w taking tiles w, w + 4, ...  The pick rows come from LDS (through
+      // pslot), the own rows from global memory, each lane's piece loaded PF
+      // steps of eight columns ahead so that the products run under the
+      // loads.  Steps past the last whole one take a zero pick operand (the
+      // own rows' reads stay at valid addresses); the last t0 % 8 columns are
+      // added with vector FMAs.
+      constexpr int PF = 8;
+      const int r = lane & 31, h = lane >> 5;
+      const int nti = (np + 31) >> 5, ntj = (cnt + 31) >> 5;
+      const int tk8 = t0 & ~7, ns = tk8 >> 3;
+      for (int tile = wave; tile < nti * ntj; tile += NT / 64) {
+        const int ti = tile / ntj, tj = tile - ti * ntj;
+        const float* arow = pcol + pslot[min(32 * ti + r, np - 1)] * cs + 4 * h;
+        const float* brow = Ct + (long long)(c0 + min(32 * tj + r, cnt - 1)) * Kp + 4 * h;
+        f32x16_t acc;
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          pj[x] = pcol + pslot[min(4 * bj + x, np - 1)] * cs;
-          oc[x] = Ct + (long long)(c0 + min(4 * bc + x, cnt - 1)) * Kp;
-        }
-        float4 xo[4], xn[4];
+        for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+        if (ns > 0) {
+          // groups of PF steps in two register buffers: a group's own-row
+          // pieces are all loaded before the previous group's products (the
+          // scheduling barriers keep the loads there)
+          auto load = [&](f32x4_t (&bq)[PF], int s0) {
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          xo[x] = t4 > 0 ? *reinterpret_cast<const float4*>(oc[x]) : make_float4(0.f, 0.f, 0.f, 0.f);
-          xn[x] = xo[x];
-        }
-        for (int l = 0; l < t4; l += 4) {
-          if (l + 4 < t4) {
+            for (int q = 0; q < PF; ++q) bq[q] = *reinterpret_cast<const f32x4_t*>(brow + 8 * min(s0 + q, ns - 1));
+          };
+          auto run = [&](const f32x4_t (&bq)[PF], int s0) {
 #pragma unroll
-            for (int x = 0; x < 4; ++x) xn[x] = *reinterpret_cast<const float4*>(oc[x] + l + 4);
-          }
-          float4 xj[4];
-#pragma unroll
-          for (int x = 0; x < 4; ++x) xj[x] = *reinterpret_cast<const float4*>(pj[x] + l);
-#pragma unroll
-          for (int x = 0; x < 4; ++x)
-#pragma unroll
-            for (int y = 0; y < 4; ++y) {
-              acc[x][y] = fmaf(xj[x].x, xo[y].x, acc[x][y]);
-              acc[x][y] = fmaf(xj[x].y, xo[y].y, acc[x][y]);
-              acc[x][y] = fmaf(xj[x].z, xo[y].z, acc[x][y]);
-              acc[x][y] = fmaf(xj[x].w, xo[y].w, acc[x][y]);
+            for (int q = 0; q < PF; ++q) {
+              const int st = s0 + q;
+              const f32x4_t z = {0.0f, 0.0f, 0.0f, 0.0f};
+              const f32x4_t av = *reinterpret_cast<const f32x4_t*>(arow + 8 * min(st, ns - 1));
+              const f32x4_t a4 = st < ns ? av : z;
+              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, bq[q].x, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, bq[q].y, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, bq[q].z, acc, 0, 0, 0);
+              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, bq[q].w, acc, 0, 0, 0);
             }
-#pragma unroll
-          for (int x = 0; x < 4; ++x) xo[x] = xn[x];
-        }
-        for (int l = t4; l < t0; ++l)
-#pragma unroll
-          for (int x = 0; x < 4; ++x)
-#pragma unroll
-            for (int y = 0; y < 4; ++y) acc[x][y] = fmaf(pj[x][l], oc[y][l], acc[x][y]);
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-          for (int y = 0; y < 4; ++y) {
-            const int jj = 4 * bj + x, c = 4 * bc + y;
-            if (jj < np && c < cnt) W[jj * wsd + c] -= acc[x][y];
+          };
+          f32x4_t bx[PF], by[PF];
+          load(bx, 0);
+          for (int s0 = 0; s0 < ns; s0 += 2 * PF) {
+            load(by, s0 + PF);
+            __builtin_amdgcn_sched_barrier(0);
+            run(bx, s0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (s0 + PF >= ns) break;
+            load(bx, s0 + 2 * PF);
+            __builtin_amdgcn_sched_barrier(0);
+            run(by, s0 + PF);
+            __builtin_amdgcn_sched_barrier(0);
           }
+        }
+        // entry e of this lane: pick row 32 ti + 8 (e >> 2) + 4 h + (e & 3), own token 32 tj + r
+        const float* orow = brow - 4 * h;
+        for (int l = tk8; l < t0; ++l) {
+          const float o = orow[l];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int m = min(32 * ti + 8 * (e >> 2) + 4 * h + (e & 3), np - 1);
+            acc[e] = fmaf(pcol[pslot[m] * cs + l], o, acc[e]);
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = 32 * ti + 8 * (e >> 2) + 4 * h + (e & 3), c = 32 * tj + r;
+          if (m < np && c < cnt) W[m * wsd + c] -= acc[e];
+        }
       }
       __syncthreads();
     }
