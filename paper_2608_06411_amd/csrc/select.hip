@@ -185,9 +185,10 @@ __host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap, bool p
   L.pslot = take(4 * pcap);
   L.pr = take(4 * pcap);
   L.pgain = take(4 * pcap);
-  // pipelined: once the round's products are done the same space holds
-  // this round's coefficients of the own tokens [ch][us]
-  L.pcol = take(4 * (pipe ? max(pcap * L.cs, ch * L.us) : pcap * L.cs));
+  // pipelined: the pool members' coefficient rows, and once the round's
+  // products are done this round's coefficients of the own tokens [ch][us];
+  // the non-pipelined variant reads the members' rows from global memory
+  L.pcol = take(4 * (pipe ? max(pcap * L.cs, ch * L.us) : 0));
   L.U = take(4 * pcap * L.us);
   const int rbytes = 4 * pcap * L.rs, wbytes = 4 * pcap * L.ws;
   L.RW = take(rbytes > wbytes ? rbytes : wbytes);
@@ -722,6 +723,62 @@ __device__ __forceinline__ void tile_product(const float* arow, const float* bro
   out = acc[0] + acc[1];
 }
 
+// The same tile with both operands in global memory: acc[e] += sum over
+// l < t of A[row][l] B[col][l], arow and brow pointing at this lane's rows
+// (rows of at least kp floats, kp a multiple of 4 and at least t).  The
+// lane's pieces (columns 8 s + 4 h .. of step s) are loaded a group of PF
+// steps ahead, in two register buffers used in turn; a read past the row
+// stays at a valid address, and in the last step the columns at or past t
+// are zero in both operands (entries past t may hold anything).
+template <int PF>
+__device__ __forceinline__ void gtile_product(const float* arow, const float* brow, int t, int kp, int h,
+                                              f32x16_t& acc) {
+  const int ns = (t + 7) >> 3;  // steps of eight columns, the last possibly partial
+  auto load = [&](f32x4_t (&av)[PF], f32x4_t (&bv)[PF], int s0) {
+#pragma unroll
+    for (int q = 0; q < PF; ++q) {
+      const int c = min(8 * (s0 + q) + 4 * h, kp - 4);
+      av[q] = *reinterpret_cast<const f32x4_t*>(arow + c);
+      bv[q] = *reinterpret_cast<const f32x4_t*>(brow + c);
+    }
+  };
+  auto run = [&](const f32x4_t (&av)[PF], const f32x4_t (&bv)[PF], int s0) {
+#pragma unroll
+    for (int q = 0; q < PF; ++q) {
+      const int st = s0 + q;
+      if (st < ns) {  // (uniform)
+        f32x4_t a4 = av[q], b4 = bv[q];
+        if (st == ns - 1 && (t & 7)) {
+          const int c = 8 * st + 4 * h;
+          const f32x4_t z = {0.0f, 0.0f, 0.0f, 0.0f};
+          a4.x = c < t ? a4.x : z.x; b4.x = c < t ? b4.x : z.x;
+          a4.y = c + 1 < t ? a4.y : z.y; b4.y = c + 1 < t ? b4.y : z.y;
+          a4.z = c + 2 < t ? a4.z : z.z; b4.z = c + 2 < t ? b4.z : z.z;
+          a4.w = c + 3 < t ? a4.w : z.w; b4.w = c + 3 < t ? b4.w : z.w;
+        }
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, b4.x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, b4.y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, b4.z, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, b4.w, acc, 0, 0, 0);
+      }
+    }
+  };
+  if (ns == 0) return;
+  f32x4_t ax[PF], bx[PF], ay[PF], by[PF];
+  load(ax, bx, 0);
+  for (int s0 = 0; s0 < ns; s0 += 2 * PF) {
+    load(ay, by, s0 + PF);
+    __builtin_amdgcn_sched_barrier(0);
+    run(ax, bx, s0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (s0 + PF >= ns) break;
+    load(ax, bx, s0 + 2 * PF);
+    __builtin_amdgcn_sched_barrier(0);
+    run(ay, by, s0 + PF);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // Global C is token-major: Ct[i][l] = c_{l,i}, rows of Kp floats (Kp = K
 // rounded up to 4), so one token's coefficients are contiguous.
 template <bool PIPE>
@@ -1054,9 +1111,10 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       const int mq = tid >> 2;
       const float* csrc = Ct + (long long)midx[min(mq, pn - 1)] * Kp;
       f32x4_t cv[CB];
+      if (PIPE)
 #pragma unroll
-      for (int u = 0; u < CB; ++u)
-        cv[u] = *reinterpret_cast<const f32x4_t*>(csrc + 4 * min((tid & 3) + 4 * u, max(tq - 1, 0)));
+        for (int u = 0; u < CB; ++u)
+          cv[u] = *reinterpret_cast<const f32x4_t*>(csrc + 4 * min((tid & 3) + 4 * u, max(tq - 1, 0)));
       // S among the members: rows m1 = 16 wave + q, column m2 = lane
       constexpr int QMAX = kMaxPool / 4;
       float sv[QMAX];
@@ -1077,7 +1135,7 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
         mqn[tid] = pc * ni;
         mr2[tid] = t == 0 ? (ni > 0.0f ? 1.0f : 0.0f) : r2m;
       }
-      if (mq < pn) {
+      if (PIPE && mq < pn) {
         auto put = [&](int q, f32x4_t v) {  // piece q, zero at and past column t
           const int l = 4 * q;
           v.x = l < t ? v.x : 0.0f;
@@ -1129,8 +1187,15 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       for (int e = 0; e < 16; ++e)
         cur[e] = Rm[min(32 * tr + 8 * (e >> 2) + 4 * h + (e & 3), pn - 1) * rs + min(32 * tc + r, pn - 1)];
       f32x16_t acc;
-      tile_product(pcol + min(32 * tr + r, pn - 1) * cs + 4 * h, pcol + min(32 * tc + r, pn - 1) * cs + 4 * h,
-                   (t + 7) & ~7, acc);
+      if (PIPE) {
+        tile_product(pcol + min(32 * tr + r, pn - 1) * cs + 4 * h, pcol + min(32 * tc + r, pn - 1) * cs + 4 * h,
+                     (t + 7) & ~7, acc);
+      } else {  // the members' rows in global C (written before the last image barrier)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+        gtile_product<4>(Ct + (long long)midx[min(32 * tr + r, pn - 1)] * Kp,
+                         Ct + (long long)midx[min(32 * tc + r, pn - 1)] * Kp, t, Kp, h, acc);
+      }
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int m = 32 * tr + 8 * (e >> 2) + 4 * h + (e & 3), j = 32 * tc + r;
@@ -1405,68 +1470,18 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     __syncthreads();
     if (t0 > 0 && np > 0) {
       // dense part on matrix cores: 32 x 32 tiles (picks by own tokens), wave
-      // w taking tiles w, w + 4, ...  The pick rows come from LDS (through
-      // pslot), the own rows from global memory, each lane's piece loaded PF
-      // steps of eight columns ahead so that the products run under the
-      // loads.  Steps past the last whole one take a zero pick operand (the
-      // own rows' reads stay at valid addresses); the last t0 % 8 columns are
-      // added with vector FMAs.
-      constexpr int PF = 8;
+      // w taking tiles w, w + 4, ...; the picks' and the own tokens' rows
+      // both come from global C
       const int r = lane & 31, h = lane >> 5;
       const int nti = (np + 31) >> 5, ntj = (cnt + 31) >> 5;
-      const int tk8 = t0 & ~7, ns = tk8 >> 3;
       for (int tile = wave; tile < nti * ntj; tile += NT / 64) {
         const int ti = tile / ntj, tj = tile - ti * ntj;
-        const float* arow = pcol + pslot[min(32 * ti + r, np - 1)] * cs + 4 * h;
-        const float* brow = Ct + (long long)(c0 + min(32 * tj + r, cnt - 1)) * Kp + 4 * h;
         f32x16_t acc;
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-        if (ns > 0) {
-          // groups of PF steps in two register buffers: a group's own-row
-          // pieces are all loaded before the previous group's products (the
-          // scheduling barriers keep the loads there)
-          auto load = [&](f32x4_t (&bq)[PF], int s0) {
-#pragma unroll
-            for (int q = 0; q < PF; ++q) bq[q] = *reinterpret_cast<const f32x4_t*>(brow + 8 * min(s0 + q, ns - 1));
-          };
-          auto run = [&](const f32x4_t (&bq)[PF], int s0) {
-#pragma unroll
-            for (int q = 0; q < PF; ++q) {
-              const int st = s0 + q;
-              const f32x4_t z = {0.0f, 0.0f, 0.0f, 0.0f};
-              const f32x4_t av = *reinterpret_cast<const f32x4_t*>(arow + 8 * min(st, ns - 1));
-              const f32x4_t a4 = st < ns ? av : z;
-              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.x, bq[q].x, acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.y, bq[q].y, acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.z, bq[q].z, acc, 0, 0, 0);
-              acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a4.w, bq[q].w, acc, 0, 0, 0);
-            }
-          };
-          f32x4_t bx[PF], by[PF];
-          load(bx, 0);
-          for (int s0 = 0; s0 < ns; s0 += 2 * PF) {
-            load(by, s0 + PF);
-            __builtin_amdgcn_sched_barrier(0);
-            run(bx, s0);
-            __builtin_amdgcn_sched_barrier(0);
-            if (s0 + PF >= ns) break;
-            load(bx, s0 + 2 * PF);
-            __builtin_amdgcn_sched_barrier(0);
-            run(by, s0 + PF);
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        }
-        // entry e of this lane: pick row 32 ti + 8 (e >> 2) + 4 h + (e & 3), own token 32 tj + r
-        const float* orow = brow - 4 * h;
-        for (int l = tk8; l < t0; ++l) {
-          const float o = orow[l];
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int m = min(32 * ti + 8 * (e >> 2) + 4 * h + (e & 3), np - 1);
-            acc[e] = fmaf(pcol[pslot[m] * cs + l], o, acc[e]);
-          }
-        }
+        gtile_product<4>(Ct + (long long)midx[pslot[min(32 * ti + r, np - 1)]] * Kp,
+                         Ct + (long long)(c0 + min(32 * tj + r, cnt - 1)) * Kp, t0, Kp, h, acc);
+        // entry e of this lane: pick 32 ti + 8 (e >> 2) + 4 h + (e & 3), own token 32 tj + r
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int m = 32 * ti + 8 * (e >> 2) + 4 * h + (e & 3), c = 32 * tj + r;
