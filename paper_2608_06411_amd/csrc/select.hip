@@ -165,7 +165,8 @@ struct Lds {
 
 // RW holds the pool's residual Gram matrix during the picks and the own
 // tokens' new rows (W) during the update; the two never live together.
-// mr2 and mkey are double-buffered by pick parity.
+// mr2 holds the members' r^2 at the round start; the mkey space is not
+// read (the picking wave keeps the keys in registers).
 __host__ __device__ inline Lds lds_layout(int K, int G, int ch, int pcap, bool pipe) {
   Lds L;
   int o = 0;
@@ -796,7 +797,6 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
   float* mn = reinterpret_cast<float*>(lds + L.mn);
   float* mqn = reinterpret_cast<float*>(lds + L.mqn);
   float* mr2 = reinterpret_cast<float*>(lds + L.mr2);     // [2][pcap]
-  uint64_t* mkey = reinterpret_cast<uint64_t*>(lds + L.mkey);  // [2][pcap]
   int* pslot = reinterpret_cast<int*>(lds + L.pslot);
   float* prr = reinterpret_cast<float*>(lds + L.pr);     // 1 / r of each pick (0: no basis vector)
   uint32_t* pgain = reinterpret_cast<uint32_t*>(lds + L.pgain);  // p (forced) or the key's high word, as bits
