@@ -1523,7 +1523,8 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       }
       __syncthreads();
       if (j0 + nb < np) {
-        for (int c = lane; c < cnt; c += 64) {
+        if (ch == 64) {  // one token per lane
+          const int c = lane;
           float x[TB];
 #pragma unroll
           for (int q = 0; q < TB; ++q) x[q] = q < nb ? W[(j0 + q) * wsd + c] : 0.0f;
@@ -1547,7 +1548,46 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u)
-              if (j2 + (NT / 64) * u < np) W[(j2 + (NT / 64) * u) * wsd + c] = v[u];
+              if (j2 + (NT / 64) * u < np && c < cnt) W[(j2 + (NT / 64) * u) * wsd + c] = v[u];
+          }
+        } else {
+          // lane l serves own tokens l, l + 64, ... (CP at most); the block's
+          // solved rows at those tokens stay in registers, and each group of
+          // four later rows is read from U once for all of them
+          constexpr int CP = 4;  // 256 own tokens at most
+          float x[CP][TB];
+#pragma unroll
+          for (int pc = 0; pc < CP; ++pc)
+#pragma unroll
+            for (int q = 0; q < TB; ++q)
+              x[pc][q] = (64 * pc < cnt && q < nb) ? W[(j0 + q) * wsd + min(lane + 64 * pc, ch - 1)] : 0.0f;
+          for (int j2 = j0 + nb + wave; j2 < np; j2 += 4 * (NT / 64)) {
+            float4 l0[4], l1[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int jr = min(j2 + (NT / 64) * u, np - 1);
+              const float* lr = U + pslot[jr] * us + j0;
+              l0[u] = *reinterpret_cast<const float4*>(lr);
+              l1[u] = *reinterpret_cast<const float4*>(lr + 4);
+            }
+#pragma unroll
+            for (int pc = 0; pc < CP; ++pc) {
+              if (64 * pc >= cnt) break;  // (uniform)
+              const int c = lane + 64 * pc;  // past cnt (the last pass): computed from valid entries, not stored
+              float v[4];
+#pragma unroll
+              for (int u = 0; u < 4; ++u) v[u] = W[min(j2 + (NT / 64) * u, np - 1) * wsd + c];
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                const float lq[TB] = {l0[u].x, l0[u].y, l0[u].z, l0[u].w, l1[u].x, l1[u].y, l1[u].z, l1[u].w};
+#pragma unroll
+                for (int q = 0; q < TB; ++q)
+                  if (q < nb) v[u] = fmaf(-lq[q], x[pc][q], v[u]);
+              }
+#pragma unroll
+              for (int u = 0; u < 4; ++u)
+                if (j2 + (NT / 64) * u < np && c < cnt) W[(j2 + (NT / 64) * u) * wsd + c] = v[u];
+            }
           }
         }
         __syncthreads();
