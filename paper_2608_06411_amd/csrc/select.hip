@@ -1449,23 +1449,30 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
     }
     if (!PIPE) {
     // W rows: S rows of the picks at the own tokens; row j = wave + 4 u,
-    // token c = lane + 64 h; up to 32 loads in flight per thread
-    {
-      const int nh = (cnt + 63) >> 6;
-      for (int h = 0; h < nh; ++h) {
-        const int c = lane + 64 * h;
-        float v[kMaxPool / 4];
+    // token c = lane + 64 h.  Every load of a thread (at most 4 x 16, at
+    // clamped valid addresses) is issued before its first store: one memory
+    // round trip
+    if (np > 0) {
+      constexpr int HP = 4;  // 256 own tokens at most
+      int row[kMaxPool / 4];
 #pragma unroll
-        for (int u = 0; u < kMaxPool / 4; ++u) {
-          const int j = wave + 4 * u;
-          v[u] = (j < np && c < cnt) ? S[(long long)midx[pslot[j]] * N + c0 + c] : 0.0f;
-        }
+      for (int u = 0; u < kMaxPool / 4; ++u) row[u] = midx[pslot[min(wave + 4 * u, np - 1)]];
+      float v[HP][kMaxPool / 4];
 #pragma unroll
-        for (int u = 0; u < kMaxPool / 4; ++u) {
-          const int j = wave + 4 * u;
-          if (j < np && c < cnt) W[j * wsd + c] = v[u];
-        }
-      }
+      for (int h = 0; h < HP; ++h)
+        if (64 * h < cnt)  // (uniform)
+#pragma unroll
+          for (int u = 0; u < kMaxPool / 4; ++u)
+            if (wave + 4 * u < np)  // (uniform)
+              v[h][u] = S[(long long)row[u] * N + c0 + min(lane + 64 * h, cnt - 1)];
+#pragma unroll
+      for (int h = 0; h < HP; ++h)
+        if (64 * h < cnt)
+#pragma unroll
+          for (int u = 0; u < kMaxPool / 4; ++u) {
+            const int j = wave + 4 * u, c = lane + 64 * h;
+            if (j < np && c < cnt) W[j * wsd + c] = v[h][u];
+          }
     }
     __syncthreads();
     if (t0 > 0 && np > 0) {
