@@ -1093,16 +1093,18 @@ __global__ __launch_bounds__(NT) void select_kernel(const SelectArgs a, int b_be
       for (int q = 0; q < NT / 64; ++q) beta = bndk[NT / 64 + q] > beta ? bndk[NT / 64 + q] : beta;
     }
     __syncthreads();
-    // members: state, columns (rows < t, written by their owners before the
-    // barrier) and their block of S.  Every global load of a thread is issued,
-    // at clamped (valid) addresses, before its first LDS store, so the phase
-    // costs about one memory round trip.
+    // members: state, their block of S and (pipelined variant) their
+    // columns (rows < t, written by their owners before the barrier; the
+    // other variant reads them from global memory where it needs them).
+    // Every global load of a thread is issued, at clamped (valid) addresses,
+    // before its first LDS store, so the phase costs about one memory round
+    // trip.
     if (pn > 0) {
       constexpr int CB = 12;  // column pieces per thread per batch
-      // member (tid >> 2) is loaded by four threads, float4 pieces q = (tid & 3) + 4 u;
-      // pieces up to column tk = t rounded up to 8 are written, with the
-      // columns at or past t set to zero (the round-start product then needs
-      // no masks)
+      // pipelined: member (tid >> 2) is loaded by four threads, float4 pieces
+      // q = (tid & 3) + 4 u; pieces up to column tk = t rounded up to 8 are
+      // written, with the columns at or past t set to zero (the round-start
+      // product then needs no masks)
       const int tq = (t + 3) >> 2, tk4 = ((t + 7) & ~7) >> 2;
       // scalars of member tid
       const int ms = min(tid, pn - 1), is = midx[ms];
