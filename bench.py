@@ -707,8 +707,9 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: the pruning stage is per image with no exchange, "
-              "and this build runs on a single MI355X (use --gpus 1).", file=sys.stderr)
+        print("bench.py measures one GPU only: the pruning stage is per image with no exchange "
+              "between GPUs, so several GPUs would each run the same kernels on their share of "
+              "the images (use --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch
